@@ -1,0 +1,67 @@
+"""Planted mistakes in the oracle must be caught by its pins (CPU only).
+
+Each case compiles a copy of the oracle source with one plausible mistake (a
+dropped term, a wrong sign, a transposed operand, a wrong index or bound) into
+a temporary library and runs the pin tests against it in a subprocess; the pins
+must fail.  The real oracle is never modified.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "scn_oracle.cpp")
+
+MUTANTS = [
+    ("fwd_drop_bias",
+     "for (int co = 0; co < Cout; ++co) yo[co] = bias ? bias[co] : 0.0;",
+     "for (int co = 0; co < Cout; ++co) yo[co] = 0.0;"),
+    ("fwd_inactive_is_zero",
+     "q[ci] = r >= 0 ? x[(int64_t)r * Cin + ci] : g_in[ci];\n      for (int ci = 0; ci < Cin; ++ci)\n        for",
+     "q[ci] = r >= 0 ? x[(int64_t)r * Cin + ci] : 0.0;\n      for (int ci = 0; ci < Cin; ++ci)\n        for"),
+    ("offset_axes_swapped",
+     "*kx = k % f;\n    *ky = (k / f) % f;\n    *kz = k / (f * f);",
+     "*kz = k % f;\n    *ky = (k / f) % f;\n    *kx = k / (f * f);"),
+    ("bwd_dW_drops_ground_term", "gW[w] += g_in[ci] * dgb[co];", "gW[w] += 0.0;"),
+    ("bwd_dg_drops_inactive_term", "          gg[ci] += back;", "          gg[ci] += 0.0;"),
+    ("pool_keeps_last_max", "if (bk < 0 || v > best)", "if (bk < 0 || v >= best)"),
+    ("pool_bwd_drops_ground", "        gg[c] += dy[o * C + c];", "        gg[c] += 0.0;"),
+    ("extent_off_by_one", "return m >= f ? (m - f) / s + 1 : 0;", "return m >= f ? (m - f) / s : 0;"),
+    ("fwd_W_transposed",
+     "yo[co] += q[ci] * W[((int64_t)k * Cin + ci) * Cout + co];",
+     "yo[co] += q[ci] * W[((int64_t)k * Cout + co) * Cin + ci];"),
+    ("ground_state_sign",
+     "gpre[co] += g_in[ci] * W[((int64_t)k * Cin + ci) * Cout + co];",
+     "gpre[co] -= g_in[ci] * W[((int64_t)k * Cin + ci) * Cout + co];"),
+    ("duplicates_accepted",
+     "if (!rb->H_in.emplace(key, static_cast<int32_t>(r)).second) {",
+     "if (!rb->H_in.emplace(key, static_cast<int32_t>(r)).second && false) {"),
+    ("range_check_off_by_one", "c[1] < 0 || c[1] >= g.mx", "c[1] < 0 || c[1] > g.mx"),
+    ("stride_divisibility_dropped",
+     "ok = ok && d[a] >= 0 && d[a] % s == 0 && d[a] / s < m[a];",
+     "ok = ok && d[a] >= 0 && d[a] / s < m[a];"),
+    ("bwd_relu_mask_dropped", "dyb[co] = (relu && !(pre[co] > 0.0)) ? 0.0 : d;", "dyb[co] = d;"),
+    ("bwd_dbias_drops_ground", "for (int co = 0; co < Cout; ++co) gB[co] += dgb[co];",
+     "for (int co = 0; co < Cout; ++co) gB[co] += 0.0;"),
+    ("rules_not_ordered_by_output",
+     "rb->lists[k].emplace_back(r, static_cast<int32_t>(o));",
+     "rb->lists[k].insert(rb->lists[k].begin(), {r, static_cast<int32_t>(o)});"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(name, old, new, tmp_path):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique/present"
+    mut = tmp_path / "mut.cpp"
+    mut.write_text(src.replace(old, new))
+    lib = tmp_path / "libmut.so"
+    subprocess.run(["g++", "-O1", "-std=c++17", "-shared", "-fPIC", str(mut), "-o", str(lib)],
+                   check=True)
+    env = dict(os.environ, SCN_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       env=env, capture_output=True, text=True, cwd=ROOT, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
