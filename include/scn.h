@@ -1,0 +1,220 @@
+/*
+ * scn.h -- C ABI of the sparse 3D convolution library for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The library implements the sparse operations of Graham, "Sparse 3D
+ * convolutional neural networks" (section 1.3, "Sparse operations"): the
+ * active-site rules, the per-layer ground state, the three-step sparse
+ * convolution (active output set and hash H_out; the matrix Q; Q W + B) and
+ * sparse max-pooling, plus their gradients (the paper trains these networks but
+ * does not spell out the backward pass; the gradients here are those of the
+ * dense-equivalent function, see scn_conv_bwd).
+ *
+ * Conventions for every call:
+ *  - Lattice: cubic, 3D.  A site is (b, x, y, z) with b the sample in the batch.
+ *    Its key is ((b*mz + z)*my + y)*mx + x for a grid (B, mx, my, mz).
+ *  - Output extent of a filter (or pooling window) of size f and stride s is
+ *    "valid": m_out = floor((m - f)/s) + 1 per axis (0 if m < f), as in the
+ *    worked example of Figure 3 (a 2x2 filter on a 6x6 grid gives 5x5).
+ *    Output site o sees input sites s*o + (kx, ky, kz), k in [0, f)^3; the
+ *    offset index is k = (kz*f + ky)*f + kx.
+ *  - Active sites: the inputs are the caller's list of sites (each listed site
+ *    is active).  An output site is active iff some active input site lies in
+ *    its window (second active-site rule of section 1.3).  Output rows are
+ *    numbered 0..a_out-1 in ascending key order.
+ *  - Feature matrices are fp32, row-major [rows][channels], channels innermost,
+ *    one row per active site (the matrix M of section 1.3).  Weights are fp32
+ *    [K][Cin][Cout] with K = f^3, i.e. the (f^3 n_in) x n_out matrix W of
+ *    section 1.3 with row k*Cin + ci.
+ *  - Ground state: every inactive site of a layer holds the same vector g
+ *    (section 1.3).  The input layer's ground state is normally 0.
+ *  - All pointers named x, y, W, g_*, d*, coords, argmax are DEVICE pointers
+ *    owned by the caller and never retained.  Host pointers are marked "host".
+ *  - Calls are asynchronous on the given HIP stream unless stated otherwise;
+ *    only scn_rulebook_build synchronises (once, to read back the sizes).
+ *  - No call allocates the caller's outputs.  Status codes are returned; no
+ *    exception crosses the ABI.  scn_last_error() gives a message for the last
+ *    failing call on the calling thread.
+ *  - A rulebook is immutable after it is built and may be used from several
+ *    streams; the caller orders its free after all work that uses it.
+ */
+#ifndef SCN_H_
+#define SCN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum scn_status {
+  SCN_OK = 0,
+  SCN_ERR_INVALID = 1,     /* null pointer, negative size, bad filter/stride/channels */
+  SCN_ERR_RANGE = 2,       /* an input site outside its grid (or b outside [0, B)) */
+  SCN_ERR_DUPLICATE = 3,   /* the same site listed twice */
+  SCN_ERR_OVERFLOW = 4,    /* a count exceeds INT32_MAX, or a key exceeds 64 bits */
+  SCN_ERR_UNSUPPORTED = 5, /* valid request outside what this version implements */
+  SCN_ERR_WORKSPACE = 6,   /* workspace pointer null or smaller than required */
+  SCN_ERR_HIP = 7,         /* a HIP runtime call failed */
+  SCN_ERR_NOMEM = 8        /* device allocation failed */
+} scn_status;
+
+/* flags of scn_conv_fwd / scn_conv_bwd */
+#define SCN_RELU 1u /* y = max(pre, 0) on active rows and on the ground state */
+
+typedef struct scn_rulebook scn_rulebook;
+
+typedef struct scn_rulebook_info {
+  int64_t a_in;        /* active input sites */
+  int64_t a_out;       /* active output sites */
+  int64_t n_pairs;     /* P = total (input row, output row) incidences */
+  int32_t K;           /* f^3 filter offsets */
+  int32_t filter;      /* f */
+  int32_t stride;      /* s */
+  int32_t input_sorted;/* 1 if the caller's rows were already in ascending key order */
+  int64_t in_grid[4];  /* B, mx, my, mz */
+  int64_t out_grid[4]; /* B, floor((m-f)/s)+1 per axis */
+} scn_rulebook_info;
+
+/*
+ * Step 1 of the sparse convolution (section 1.3): build the map H_in from
+ * active input site to row, find the active output sites of a filter of size
+ * `filter` and stride `stride` and number them (H_out), and list for every
+ * filter offset k which active input feeds which active output (the rulebook:
+ * the blocks of the matrix Q of step 2 that are not the ground state).  The
+ * same rulebook serves max-pooling when filter == stride.
+ *
+ *  coords  device int32[n][4] rows (b, x, y, z); row i is row i of the
+ *          layer's feature matrix.  Not retained.
+ *  n       number of active input sites (>= 0; 0 gives an empty rulebook).
+ *  grid    host int64[4] = (B, mx, my, mz), all >= 1.
+ *  filter  f in {1, 2, 3};  stride s >= 1 (s <= f not required).
+ *  stream  HIP stream for all device work; the call synchronises it once.
+ *  out     receives a library-owned rulebook, freed by scn_rulebook_free.
+ *
+ * Output ordering is canonical: output rows ascend by key, and each
+ * per-offset pair list ascends by output row (hence also by input key), so the
+ * result is deterministic and independent of the input row order.
+ * Errors: SCN_ERR_INVALID, SCN_ERR_RANGE, SCN_ERR_DUPLICATE, SCN_ERR_OVERFLOW,
+ * SCN_ERR_UNSUPPORTED (f > 3, or an occupancy bitmap of the input or output
+ * grid above 2^26 32-bit words, i.e. B*my*mz*ceil(mx/32) > 2^26), SCN_ERR_NOMEM,
+ * SCN_ERR_HIP.  coords must be 16-byte aligned.  On error *out is NULL.
+ */
+scn_status scn_rulebook_build(const int32_t* coords, int64_t n, const int64_t* grid,
+                              int32_t filter, int32_t stride, hipStream_t stream,
+                              scn_rulebook** out);
+
+/* Sizes and grids of a rulebook (host struct).  SCN_ERR_INVALID on null. */
+scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info);
+
+/* Device int32[a_out][4] (b, x, y, z) of the active output sites, ascending by
+ * key: the input coordinates of the next layer.  Owned by rb. */
+const int32_t* scn_rulebook_out_coords(const scn_rulebook* rb);
+
+/* Device int32[n_pairs]: the per-offset pair lists, concatenated in offset
+ * order; list k occupies [offsets[k], offsets[k+1]).  Owned by rb. */
+const int32_t* scn_rulebook_in_rows(const scn_rulebook* rb);
+const int32_t* scn_rulebook_out_rows(const scn_rulebook* rb);
+
+/* Host int64[K+1] list boundaries.  Owned by rb. */
+const int64_t* scn_rulebook_offsets(const scn_rulebook* rb);
+
+/* Copies the active output sites and the pair lists into caller device
+ * buffers (each may be NULL): out_coords int32[a_out][4], in_rows and out_rows
+ * int32[n_pairs].  Asynchronous on `stream`.  Errors: SCN_ERR_INVALID, SCN_ERR_HIP. */
+scn_status scn_rulebook_export(const scn_rulebook* rb, int32_t* out_coords, int32_t* in_rows,
+                               int32_t* out_rows, hipStream_t stream);
+
+/* Frees a rulebook (stream-ordered on the stream it was built on). NULL is a no-op. */
+void scn_rulebook_free(scn_rulebook* rb);
+
+/*
+ * Sparse convolution forward, steps 2 and 3 of section 1.3 (M_out = Q W + B)
+ * over the rulebook rb, together with the output ground state.
+ *   g_out = act(B + sum_k g_in W_k)               (the "pre-computed" g, section 1.3)
+ *   y[o]  = act(B + sum_k v_k(o) W_k),  v_k(o) = x[row of s*o+k] if that site is
+ *           active, else g_in
+ * computed as y[o] = act(g_pre + sum_{pairs (r,o) of offset k} (x[r] - g_in) W_k),
+ * which is the same sum regrouped.  act is ReLU if (flags & SCN_RELU), else
+ * the identity.
+ *
+ *  x     [a_in][Cin];  g_in [Cin];  W [K][Cin][Cout];  bias [Cout] or NULL (= 0)
+ *  y     [a_out][Cout] (written);  g_out [Cout] (written)
+ * Errors: SCN_ERR_INVALID (null, Cin or Cout < 1, rb NULL), SCN_ERR_HIP.
+ */
+scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_in,
+                        const float* W, const float* bias, int32_t Cin, int32_t Cout,
+                        uint32_t flags, float* y, float* g_out, hipStream_t stream);
+
+/* Bytes of device workspace scn_conv_bwd needs for this rulebook and shape. */
+size_t scn_conv_bwd_workspace_bytes(const scn_rulebook* rb, int32_t Cin, int32_t Cout,
+                                    uint32_t flags);
+
+/*
+ * Gradients of scn_conv_fwd for the loss L = sum_o <dy[o], y[o]> + <dg_out, g_out>
+ * (derivative of the dense-equivalent function; ReLU'(0) = 0).  With
+ * dȳ = dy * [y > 0] and dḡ = dg_out * [g_out > 0] under ReLU (else dy, dg_out):
+ *   dx[r]    = sum_{pairs (r,o) of k} dȳ[o] W_k^T
+ *   dW_k     = sum_{pairs (r,o) of k} (x[r] - g_in)^T dȳ[o] + g_in^T (S + dḡ),  S = sum_o dȳ[o]
+ *   dbias    = S + dḡ
+ *   dg_in    = sum_k W_k (S - T_k + dḡ)^T,  T_k = sum_{pairs (r,o) of k} dȳ[o]
+ * Outputs are overwritten (not accumulated); a NULL output is not computed.
+ *  x [a_in][Cin], g_in [Cin], W [K][Cin][Cout], y [a_out][Cout] and g_out
+ *  [Cout] (post-activation; read only under SCN_RELU, may be NULL otherwise),
+ *  dy [a_out][Cout], dg_out [Cout] or NULL (= 0).
+ *  dx [a_in][Cin], dg_in [Cin], dW [K][Cin][Cout], dbias [Cout].
+ *  ws/ws_bytes: device workspace of at least scn_conv_bwd_workspace_bytes().
+ * Errors: SCN_ERR_INVALID, SCN_ERR_WORKSPACE, SCN_ERR_HIP.  Deterministic:
+ * every reduction runs in a fixed order, so repeated calls are bitwise equal.
+ */
+scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_in,
+                        const float* W, const float* y, const float* g_out, const float* dy,
+                        const float* dg_out, int32_t Cin, int32_t Cout, uint32_t flags,
+                        float* dx, float* dg_in, float* dW, float* dbias, void* ws,
+                        size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Sparse max-pooling forward (section 1.3, end: pooling "is similar" to the
+ * convolution).  rb must have filter == stride (non-overlapping windows).
+ * For each active output o and channel c, y[o][c] is the maximum over the f^3
+ * positions of the window, an active position holding x[row][c] and an
+ * inactive one g_in[c]; ties keep the first position in ascending k.
+ * argmax[o][c] receives that k.  g_out = g_in.
+ *  x [a_in][C], g_in [C] -> y [a_out][C], g_out [C], argmax uint8 [a_out][C].
+ * Errors: SCN_ERR_INVALID, SCN_ERR_UNSUPPORTED (filter != stride), SCN_ERR_HIP.
+ */
+scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* g_in,
+                           int32_t C, float* y, float* g_out, uint8_t* argmax,
+                           hipStream_t stream);
+
+/* Bytes of device workspace scn_maxpool_bwd needs. */
+size_t scn_maxpool_bwd_workspace_bytes(const scn_rulebook* rb, int32_t C);
+
+/*
+ * Gradient of scn_maxpool_fwd: dy[o][c] flows to the winning position; a
+ * winning inactive position passes it to the ground state, and g_out = g_in
+ * passes dg_out through:
+ *   dx[r][c] = dy[o][c] if r is the active position argmax[o][c] of window o, else 0
+ *   dg_in[c] = dg_out[c] + sum_{o: argmax[o][c] inactive} dy[o][c]
+ *  argmax [a_out][C] from scn_maxpool_fwd, dy [a_out][C], dg_out [C] or NULL.
+ *  dx [a_in][C] (every row written), dg_in [C] (NULL: not computed).
+ * Errors: SCN_ERR_INVALID, SCN_ERR_UNSUPPORTED, SCN_ERR_WORKSPACE, SCN_ERR_HIP.
+ */
+scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const float* dy,
+                           const float* dg_out, int32_t C, float* dx, float* dg_in, void* ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/* Message describing the last failing call on this thread ("" if none). */
+const char* scn_last_error(void);
+
+/* Library version string. */
+const char* scn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCN_H_ */

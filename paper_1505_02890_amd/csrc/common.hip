@@ -1,0 +1,41 @@
+// Error reporting, stream-ordered allocation and version string.
+#include <cstdarg>
+#include <cstdio>
+
+#include "scn_internal.h"
+
+namespace scn {
+
+static thread_local char g_err[512] = {0};
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+
+void clear_error() { g_err[0] = 0; }
+
+scn_status dalloc(void** p, size_t bytes, hipStream_t s) {
+  *p = nullptr;
+  if (bytes == 0) return SCN_OK;
+  hipError_t e = hipMallocAsync(p, bytes, s);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    set_error("device allocation of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+    return SCN_ERR_NOMEM;
+  }
+  return SCN_OK;
+}
+
+void dfree(void* p, hipStream_t s) {
+  if (p) (void)hipFreeAsync(p, s);
+}
+
+}  // namespace scn
+
+extern "C" const char* scn_last_error(void) { return scn::g_err; }
+
+extern "C" const char* scn_version(void) { return "scn-mi355x 0.1 (gfx950)"; }

@@ -1,0 +1,627 @@
+// Rulebook construction on the GPU: step 1 of the sparse convolution of
+// section 1.3 (iterate over H_in, find and number the active output sites,
+// H_out) and the per-offset (input row, output row) lists that stand for the
+// non-ground-state blocks of the matrix Q of step 2.
+//
+// Data structure.  The paper keeps H_in / H_out as a map or hash table from
+// site to row.  Here the grids are bounded, so the map is an occupancy bitmap
+// (one bit per lattice site, x-rows padded to whole 32-bit words) plus an
+// exclusive prefix sum of the word popcounts: the rank of an active site in
+// key order is prefix[word] + popcount(word & bits below it).  This is a
+// minimal perfect hash of the active set that is ordered by key, so the output
+// numbering (ascending key) needs no sort, no hash probing and no atomics on
+// the output side, and every result is deterministic.
+//
+// Phases (one stream, two host synchronisations):
+//   1 mark inputs            bitmap OR per input; range / duplicate checks
+//   2 scan input words       rank of every input site
+//   3 rank -> caller row     perm[rank] = row
+//   4 dilate                 output word = OR over the window of input bits
+//                            (second active-site rule of section 1.3)
+//   5 scan output words      a_out and output numbering          [sync 1]
+//   6 output sites           coordinates and K-bit neighbour mask per output
+//   7 tile counts            pairs per (offset, tile of 64 outputs)
+//   8 scan of tile counts    list boundaries and per-tile pair ranges
+//   9 emit pairs             in_row / out_row (+ rank; pool maps)
+//  10 input-tile ranges      per (offset, tile of 64 input ranks)   [sync 2]
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+
+#include "scan.h"
+#include "scn_internal.h"
+
+namespace scn {
+namespace {
+
+enum : uint32_t { F_RANGE = 1, F_DUP = 2, F_UNSORTED = 4 };
+
+struct GridDev {
+  int32_t B, mx, my, mz;  // grid extents
+  int32_t rw;             // 32-bit words per x-row
+};
+
+__device__ inline uint64_t site_key(const GridDev& g, int64_t b, int64_t x, int64_t y,
+                                    int64_t z) {
+  return (uint64_t)(((b * g.mz + z) * g.my + y) * g.mx + x);
+}
+
+__device__ inline int64_t row_base(const GridDev& g, int64_t b, int64_t y, int64_t z) {
+  return ((b * g.mz + z) * g.my + y) * g.rw;
+}
+
+// 32 bits of an x-row starting at bit position p (bits past the row read 0).
+__device__ inline uint32_t extract32(const uint32_t* __restrict__ bm, int64_t base, int rw,
+                                     int64_t p) {
+  const int64_t w = p >> 5;
+  const int sh = (int)(p & 31);
+  const uint32_t lo = w < rw ? bm[base + w] : 0u;
+  if (sh == 0) return lo;
+  const uint32_t hi = w + 1 < rw ? bm[base + w + 1] : 0u;
+  return (lo >> sh) | (hi << (32 - sh));
+}
+
+__device__ inline uint32_t lane_rank(uint64_t ballot) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(ballot >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)ballot, 0u));
+}
+
+// even bits of a 64-bit word packed into 32 bits
+__device__ inline uint32_t compress_even(uint64_t x) {
+  x &= 0x5555555555555555ull;
+  x = (x | (x >> 1)) & 0x3333333333333333ull;
+  x = (x | (x >> 2)) & 0x0F0F0F0F0F0F0F0Full;
+  x = (x | (x >> 4)) & 0x00FF00FF00FF00FFull;
+  x = (x | (x >> 8)) & 0x0000FFFF0000FFFFull;
+  x = (x | (x >> 16)) & 0x00000000FFFFFFFFull;
+  return (uint32_t)x;
+}
+
+// ---- phase 1: mark the input sites ----------------------------------------
+__global__ void __launch_bounds__(256) mark_inputs_kernel(const int32_t* __restrict__ coords,
+                                                          int64_t n, GridDev g,
+                                                          uint32_t* __restrict__ bm,
+                                                          uint32_t* __restrict__ flags) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  uint32_t f = 0;
+  if (i < n) {
+    const int4 c = reinterpret_cast<const int4*>(coords)[i];
+    const bool ok = c.x >= 0 && c.x < g.B && c.y >= 0 && c.y < g.mx && c.z >= 0 &&
+                    c.z < g.my && c.w >= 0 && c.w < g.mz;
+    if (!ok) {
+      f |= F_RANGE;
+    } else {
+      const int64_t w = row_base(g, c.x, c.z, c.w) + (c.y >> 5);
+      const uint32_t bit = 1u << (c.y & 31);
+      const uint32_t old = atomicOr(&bm[w], bit);
+      if (old & bit) f |= F_DUP;
+      if (i > 0) {
+        const int4 p = reinterpret_cast<const int4*>(coords)[i - 1];
+        // an out-of-range predecessor is reported by its own thread
+        if (site_key(g, c.x, c.y, c.z, c.w) <= site_key(g, p.x, p.y, p.z, p.w)) f |= F_UNSORTED;
+      }
+    }
+  }
+  // one atomic per block at most
+  __shared__ uint32_t sf;
+  if (threadIdx.x == 0) sf = 0;
+  __syncthreads();
+  if (f) atomicOr(&sf, f);
+  __syncthreads();
+  if (threadIdx.x == 0 && sf) atomicOr(flags, sf);
+}
+
+struct PopcountLoad {
+  const uint32_t* bm;
+  __device__ uint32_t operator()(int64_t i) const { return (uint32_t)__popc(bm[i]); }
+};
+
+template <typename T>
+struct PlainLoad {
+  const T* v;
+  __device__ T operator()(int64_t i) const { return v[i]; }
+};
+
+// ---- phase 3: rank -> caller row ------------------------------------------
+__global__ void __launch_bounds__(256) perm_kernel(const int32_t* __restrict__ coords, int64_t n,
+                                                   GridDev g, const uint32_t* __restrict__ bm,
+                                                   const uint32_t* __restrict__ pref,
+                                                   int32_t* __restrict__ perm) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int4 c = reinterpret_cast<const int4*>(coords)[i];
+  const int64_t w = row_base(g, c.x, c.z, c.w) + (c.y >> 5);
+  const uint32_t below = (1u << (c.y & 31)) - 1u;
+  const uint32_t rank = pref[w] + (uint32_t)__popc(bm[w] & below);
+  perm[rank] = (int32_t)i;
+}
+
+// ---- phase 4: output occupancy (dilation of the input bitmap) -------------
+__global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict__ inb, GridDev gi,
+                                                     uint32_t* __restrict__ outb, GridDev go,
+                                                     int64_t nw_out, int f, int s) {
+  const int64_t wo = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (wo >= nw_out) return;
+  const int wx = (int)(wo % go.rw);
+  int64_t r = wo / go.rw;
+  const int64_t y = r % go.my;
+  r /= go.my;
+  const int64_t z = r % go.mz;
+  const int64_t b = r / go.mz;
+  const int x0 = wx * 32;
+  const int nvalid = min(32, go.mx - x0);
+  const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+  uint32_t v = 0;
+  for (int kz = 0; kz < f; ++kz)
+    for (int ky = 0; ky < f; ++ky) {
+      const int64_t base = row_base(gi, b, s * y + ky, s * z + kz);
+      if (s == 1) {
+        for (int kx = 0; kx < f; ++kx) v |= extract32(inb, base, gi.rw, (int64_t)x0 + kx);
+      } else if (s == 2) {
+        const int64_t p = 2 * (int64_t)x0;  // multiple of 64
+        const uint64_t lo = extract32(inb, base, gi.rw, p);
+        const uint64_t hi = extract32(inb, base, gi.rw, p + 32);
+        const uint64_t w64 = lo | (hi << 32);
+        uint64_t t = w64;
+        if (f >= 2) t |= w64 >> 1;
+        if (f >= 3) {
+          const uint64_t nx = extract32(inb, base, gi.rw, p + 64) & 1u;
+          t |= (w64 >> 2) | (nx << 62);
+        }
+        v |= compress_even(t);
+      } else {
+        const uint32_t fm = (1u << f) - 1u;
+        for (int j = 0; j < nvalid; ++j)
+          if (extract32(inb, base, gi.rw, (int64_t)s * (x0 + j)) & fm) v |= 1u << j;
+      }
+    }
+  outb[wo] = v & valid;
+}
+
+// ---- phase 6: output coordinates and neighbour masks ----------------------
+__global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restrict__ inb, GridDev gi,
+                                                        const uint32_t* __restrict__ outb,
+                                                        const uint32_t* __restrict__ opref,
+                                                        GridDev go, int64_t nw_out, int f, int s,
+                                                        int32_t* __restrict__ out_coords,
+                                                        uint32_t* __restrict__ masks) {
+  const int64_t wo = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (wo >= nw_out) return;
+  uint32_t v = outb[wo];
+  if (!v) return;
+  const int wx = (int)(wo % go.rw);
+  int64_t r = wo / go.rw;
+  const int64_t y = r % go.my;
+  r /= go.my;
+  const int64_t z = r % go.mz;
+  const int64_t b = r / go.mz;
+  const int x0 = wx * 32;
+  const int K = f * f * f;
+  uint32_t rank = opref[wo];
+  if (s == 1) {
+    // E[k] bit j: input site (x0 + j + kx, y + ky, z + kz) is active
+    uint32_t E[MAX_K];
+    for (int kz = 0; kz < f; ++kz)
+      for (int ky = 0; ky < f; ++ky) {
+        const int64_t base = row_base(gi, b, y + ky, z + kz);
+        for (int kx = 0; kx < f; ++kx)
+          E[(kz * f + ky) * f + kx] = extract32(inb, base, gi.rw, (int64_t)x0 + kx);
+      }
+    while (v) {
+      const int j = __builtin_ctz(v);
+      v &= v - 1;
+      uint32_t m = 0;
+      for (int k = 0; k < K; ++k) m |= ((E[k] >> j) & 1u) << k;
+      reinterpret_cast<int4*>(out_coords)[rank] =
+          make_int4((int)b, x0 + j, (int)y, (int)z);
+      masks[rank] = m;
+      ++rank;
+    }
+  } else {
+    while (v) {
+      const int j = __builtin_ctz(v);
+      v &= v - 1;
+      const int64_t xi = (int64_t)s * (x0 + j);
+      uint32_t m = 0;
+      for (int kz = 0; kz < f; ++kz)
+        for (int ky = 0; ky < f; ++ky) {
+          const int64_t base = row_base(gi, b, s * y + ky, s * z + kz);
+          const uint32_t bits = extract32(inb, base, gi.rw, xi);
+          for (int kx = 0; kx < f; ++kx) m |= ((bits >> kx) & 1u) << ((kz * f + ky) * f + kx);
+        }
+      reinterpret_cast<int4*>(out_coords)[rank] =
+          make_int4((int)b, x0 + j, (int)y, (int)z);
+      masks[rank] = m;
+      ++rank;
+    }
+  }
+}
+
+// ---- phase 7: pairs per (offset, output tile) ------------------------------
+// one wave per tile of 64 output rows; cnt[k * nt + t]
+__global__ void __launch_bounds__(256) tile_count_kernel(const uint32_t* __restrict__ masks,
+                                                         int64_t a_out, int64_t nt, int K,
+                                                         uint64_t* __restrict__ cnt) {
+  const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t t = o >> 6;
+  const uint32_t m = o < a_out ? masks[o] : 0u;
+  const int lane = threadIdx.x & 63;
+  for (int k = 0; k < K; ++k) {
+    const uint64_t bal = __ballot((m >> k) & 1u);
+    if (lane == 0 && t < nt) cnt[k * nt + t] = (uint64_t)__popcll(bal);
+  }
+}
+
+// ---- phase 8b: list boundaries off[k] = position of (k, tile 0) -----------
+__global__ void list_offsets_kernel(const uint64_t* __restrict__ pos, int64_t nt, int K,
+                                    int64_t* __restrict__ off) {
+  const int k = threadIdx.x;
+  if (k <= K) off[k] = (int64_t)pos[(int64_t)k * nt];
+}
+
+// ---- phase 9: emit the pair lists ------------------------------------------
+__global__ void __launch_bounds__(256) emit_pairs_kernel(
+    const uint32_t* __restrict__ masks, const int32_t* __restrict__ out_coords, int64_t a_out,
+    int64_t nt, int f, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
+    GridDev gi, const int32_t* __restrict__ perm, const uint64_t* __restrict__ pos,
+    int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows, int32_t* __restrict__ in_rank,
+    int32_t* __restrict__ nbr, int32_t* __restrict__ inv) {
+  const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t t = o >> 6;
+  const bool live = o < a_out;
+  const uint32_t m = live ? masks[o] : 0u;
+  int4 c = make_int4(0, 0, 0, 0);
+  if (live) c = reinterpret_cast<const int4*>(out_coords)[o];
+  const int K = f * f * f;
+  for (int k = 0; k < K; ++k) {
+    const bool bit = (m >> k) & 1u;
+    const uint64_t bal = __ballot(bit);
+    if (!live) continue;
+    if (bit) {
+      const int kx = k % f, ky = (k / f) % f, kz = k / (f * f);
+      const int64_t xi = (int64_t)s * c.y + kx;
+      const int64_t w = row_base(gi, c.x, (int64_t)s * c.z + ky, (int64_t)s * c.w + kz) + (xi >> 5);
+      const uint32_t rank = ipref[w] + (uint32_t)__popc(inb[w] & ((1u << (xi & 31)) - 1u));
+      const int32_t row = perm[rank];
+      const uint64_t p = pos[(int64_t)k * nt + t] + lane_rank(bal);
+      in_rows[p] = row;
+      out_rows[p] = (int32_t)o;
+      if (in_rank) in_rank[p] = (int32_t)rank;
+      if (nbr) {
+        nbr[o * K + k] = row;
+        inv[row] = (int32_t)(o * K + k);
+      }
+    } else if (nbr) {
+      nbr[o * K + k] = -1;
+    }
+  }
+}
+
+__global__ void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// ---- phase 10: pair ranges per tile of input ranks -------------------------
+// itile[k * nit + t] = first position p in list k with rank[p] >= t * TILE;
+// ranks ascend along each list (the window map preserves key order).
+__global__ void __launch_bounds__(256) in_tiles_kernel(const int32_t* __restrict__ rank,
+                                                       const int64_t* __restrict__ off, int K,
+                                                       int64_t nit,
+                                                       int64_t* __restrict__ itile) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)K * nit + 1) return;
+  if (i == (int64_t)K * nit) {
+    itile[i] = off[K];
+    return;
+  }
+  const int k = (int)(i / nit);
+  const int64_t t = i % nit;
+  const int64_t target = t * TILE;
+  int64_t lo = off[k], hi = off[k + 1];
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if ((int64_t)rank[mid] < target)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  itile[i] = lo;
+}
+
+inline unsigned blocks_for(int64_t n, int threads) {
+  return (unsigned)std::max<int64_t>(1, ceil_div(n, threads));
+}
+
+struct Temps {
+  hipStream_t s;
+  void* p[12] = {nullptr};
+  int n = 0;
+  explicit Temps(hipStream_t st) : s(st) {}
+  template <typename T>
+  scn_status get(T** out, size_t count) {
+    void* q = nullptr;
+    scn_status st = dalloc(&q, std::max<size_t>(count, 1) * sizeof(T), s);
+    if (st != SCN_OK) return st;
+    p[n++] = q;
+    *out = static_cast<T*>(q);
+    return SCN_OK;
+  }
+  ~Temps() {
+    for (int i = 0; i < n; ++i) dfree(p[i], s);
+  }
+};
+
+scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f, int32_t s,
+                 hipStream_t st, scn_rulebook** out) {
+  if (!out) {
+    set_error("scn_rulebook_build: out is NULL");
+    return SCN_ERR_INVALID;
+  }
+  *out = nullptr;
+  if (!grid || n < 0 || (n > 0 && !coords) || f < 1 || s < 1 ||
+      (reinterpret_cast<uintptr_t>(coords) & 15) != 0) {
+    set_error("scn_rulebook_build: invalid argument (n=%lld f=%d s=%d)", (long long)n, f, s);
+    return SCN_ERR_INVALID;
+  }
+  for (int a = 0; a < 4; ++a)
+    if (grid[a] < 1 || grid[a] > INT32_MAX) {
+      set_error("scn_rulebook_build: grid extent %d is %lld", a, (long long)grid[a]);
+      return SCN_ERR_INVALID;
+    }
+  if (f > 3) {
+    set_error("scn_rulebook_build: filter %d > 3 is not supported", f);
+    return SCN_ERR_UNSUPPORTED;
+  }
+  if (n > INT32_MAX) {
+    set_error("scn_rulebook_build: %lld sites exceed INT32_MAX", (long long)n);
+    return SCN_ERR_OVERFLOW;
+  }
+  const int K = f * f * f;
+  int64_t go4[4] = {grid[0], 0, 0, 0};
+  for (int a = 1; a < 4; ++a) go4[a] = grid[a] >= f ? (grid[a] - f) / s + 1 : 0;
+  // bitmap words of each grid; bound them (2^26 words = 2^31 sites each)
+  const int64_t rw_in = ceil_div(grid[1], 32), rw_out = ceil_div(std::max<int64_t>(go4[1], 1), 32);
+  const double nwi_d = (double)grid[0] * grid[3] * grid[2] * rw_in;
+  const double nwo_d = (double)go4[0] * go4[3] * go4[2] * rw_out;
+  const double LIMW = (double)(int64_t(1) << 26);
+  if (nwi_d > LIMW || nwo_d > LIMW) {
+    set_error("scn_rulebook_build: grid too large for the occupancy bitmap (%.3g / %.3g words)",
+              nwi_d, nwo_d);
+    return SCN_ERR_UNSUPPORTED;
+  }
+  const int64_t nw_in = (int64_t)nwi_d, nw_out = (int64_t)nwo_d;
+  GridDev gi{(int32_t)grid[0], (int32_t)grid[1], (int32_t)grid[2], (int32_t)grid[3],
+             (int32_t)rw_in};
+  GridDev go{(int32_t)go4[0], (int32_t)std::max<int64_t>(go4[1], 0), (int32_t)go4[2],
+             (int32_t)go4[3], (int32_t)rw_out};
+
+  Temps tmp(st);
+  scn_status rc;
+  uint32_t *inb, *ipref, *outb, *opref, *flags;
+  uint32_t* sc32;  // scan block sums
+  const int64_t nsb = std::max(scan_blocks(nw_in), scan_blocks(nw_out));
+  if ((rc = tmp.get(&inb, nw_in)) || (rc = tmp.get(&ipref, nw_in + 1)) ||
+      (rc = tmp.get(&outb, nw_out)) || (rc = tmp.get(&opref, nw_out + 1)) ||
+      (rc = tmp.get(&flags, 4)) || (rc = tmp.get(&sc32, nsb)))
+    return rc;
+  SCN_HIP(hipMemsetAsync(inb, 0, std::max<int64_t>(nw_in, 1) * 4, st));
+  SCN_HIP(hipMemsetAsync(flags, 0, 16, st));
+
+  // host-pinned readback area
+  struct Readback {
+    uint32_t flags, a_in, a_out, pad;
+    int64_t off[MAX_K + 1];
+  };
+  // one pinned readback area per host thread, kept for the life of the process
+  static thread_local Readback* hb = nullptr;
+  if (!hb) SCN_HIP(hipHostMalloc((void**)&hb, sizeof(Readback), hipHostMallocDefault));
+  std::memset(hb, 0, sizeof(Readback));
+
+  // phases 1-5
+  if (n > 0) {
+    hipLaunchKernelGGL(mark_inputs_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n,
+                       gi, inb, flags);
+    SCN_LAUNCH_CHECK();
+  }
+  if ((rc = exclusive_scan<uint32_t>(PopcountLoad{inb}, nw_in, ipref, ipref + nw_in, sc32, st)))
+    return rc;
+  hipLaunchKernelGGL(dilate_kernel, dim3(blocks_for(nw_out, 256)), dim3(256), 0, st, inb, gi,
+                     outb, go, nw_out, f, s);
+  SCN_LAUNCH_CHECK();
+  if ((rc = exclusive_scan<uint32_t>(PopcountLoad{outb}, nw_out, opref, opref + nw_out, sc32,
+                                     st)))
+    return rc;
+  SCN_HIP(hipMemcpyAsync(&hb->flags, flags, 4, hipMemcpyDeviceToHost, st));
+  SCN_HIP(hipMemcpyAsync(&hb->a_in, ipref + nw_in, 4, hipMemcpyDeviceToHost, st));
+  SCN_HIP(hipMemcpyAsync(&hb->a_out, opref + nw_out, 4, hipMemcpyDeviceToHost, st));
+  SCN_HIP(hipStreamSynchronize(st));
+  if (hb->flags & F_RANGE) {
+    set_error("scn_rulebook_build: a site lies outside the grid (%lld,%lld,%lld,%lld)",
+              (long long)grid[0], (long long)grid[1], (long long)grid[2], (long long)grid[3]);
+    return SCN_ERR_RANGE;
+  }
+  if ((hb->flags & F_DUP) || (int64_t)hb->a_in != n) {
+    set_error("scn_rulebook_build: duplicate site in the input list");
+    return SCN_ERR_DUPLICATE;
+  }
+  const int64_t a_out = hb->a_out;
+  const bool sorted = !(hb->flags & F_UNSORTED);
+  const bool pool = (f == s);
+  const int64_t nt = std::max<int64_t>(1, ceil_div(a_out, TILE));
+  const int64_t nit = std::max<int64_t>(1, ceil_div(n, TILE));
+  const int64_t pmax = std::min<int64_t>(n, a_out) * K;
+  if (pool && a_out * K > INT32_MAX) {
+    set_error("scn_rulebook_build: %lld pooling windows exceed the supported count",
+              (long long)a_out);
+    return SCN_ERR_OVERFLOW;
+  }
+
+  // persistent rulebook storage in one block
+  auto al = [](int64_t bytes) { return (bytes + 255) & ~int64_t(255); };
+  const int64_t sz_oc = al(a_out * 16), sz_pair = al(pmax * 4), sz_perm = al(n * 4),
+                sz_off = al((K + 1) * 8), sz_ot = al((K * nt + 1) * 8),
+                sz_it = al((K * nit + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
+                sz_inv = pool ? al(n * 4) : 0;
+  const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair) + sz_perm + sz_off + sz_ot +
+                        sz_it + sz_nbr + sz_inv;
+  scn_rulebook* rb = new scn_rulebook();
+  struct Guard {
+    scn_rulebook* rb;
+    hipStream_t s;
+    bool keep = false;
+    ~Guard() {
+      if (!keep && rb) {
+        dfree(rb->block, s);
+        delete rb;
+      }
+    }
+  } guard{rb, st};
+  if ((rc = dalloc(&rb->block, (size_t)total, st))) return rc;
+  char* cur = static_cast<char*>(rb->block);
+  auto take = [&](int64_t bytes) {
+    char* p = bytes ? cur : nullptr;
+    cur += bytes;
+    return p;
+  };
+  rb->out_coords = (int32_t*)take(sz_oc);
+  rb->in_rows = (int32_t*)take(sz_pair);
+  rb->out_rows = (int32_t*)take(sz_pair);
+  rb->in_rank = sorted ? rb->in_rows : (int32_t*)take(sz_pair);
+  rb->perm = (int32_t*)take(sz_perm);
+  rb->off_dev = (int64_t*)take(sz_off);
+  rb->otile = (int64_t*)take(sz_ot);
+  rb->itile = (int64_t*)take(sz_it);
+  rb->nbr = pool ? (int32_t*)take(sz_nbr) : nullptr;
+  rb->inv = pool ? (int32_t*)take(sz_inv) : nullptr;
+  rb->f = f;
+  rb->s = s;
+  rb->K = K;
+  for (int a = 0; a < 4; ++a) {
+    rb->gin[a] = grid[a];
+    rb->gout[a] = go4[a];
+  }
+  rb->a_in = n;
+  rb->a_out = a_out;
+  rb->input_sorted = sorted ? 1 : 0;
+  rb->stream = st;
+  rb->n_otiles = nt;
+  rb->n_itiles = nit;
+
+  uint32_t* masks;
+  uint64_t *cnt, *sc64;
+  const int64_t ncnt = K * nt;
+  if ((rc = tmp.get(&masks, a_out)) || (rc = tmp.get(&cnt, ncnt)) ||
+      (rc = tmp.get(&sc64, scan_blocks(ncnt))))
+    return rc;
+
+  if (n > 0) {
+    hipLaunchKernelGGL(perm_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n, gi,
+                       inb, ipref, rb->perm);
+    SCN_LAUNCH_CHECK();
+  }
+  if (a_out > 0) {
+    hipLaunchKernelGGL(out_sites_kernel, dim3(blocks_for(nw_out, 256)), dim3(256), 0, st, inb,
+                       gi, outb, opref, go, nw_out, f, s, rb->out_coords, masks);
+    SCN_LAUNCH_CHECK();
+  }
+  hipLaunchKernelGGL(tile_count_kernel, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st, masks,
+                     a_out, nt, K, cnt);
+  SCN_LAUNCH_CHECK();
+  // positions: otile[k*nt + t] = off[k] + pairs of list k in tiles < t
+  if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, ncnt, (uint64_t*)rb->otile,
+                                     (uint64_t*)rb->otile + ncnt, sc64, st)))
+    return rc;
+  hipLaunchKernelGGL(list_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)rb->otile,
+                     nt, K, rb->off_dev);
+  SCN_LAUNCH_CHECK();
+  if (pool && n > 0) {
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, rb->inv, n,
+                       -1);
+    SCN_LAUNCH_CHECK();
+  }
+  if (a_out > 0) {
+    hipLaunchKernelGGL(emit_pairs_kernel, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st,
+                       masks, rb->out_coords, a_out, nt, f, s, inb, ipref, gi, rb->perm,
+                       (const uint64_t*)rb->otile, rb->in_rows, rb->out_rows,
+                       sorted ? nullptr : rb->in_rank, rb->nbr, rb->inv);
+    SCN_LAUNCH_CHECK();
+  }
+  hipLaunchKernelGGL(in_tiles_kernel, dim3(blocks_for(K * nit + 1, 256)), dim3(256), 0, st,
+                     rb->in_rank, rb->off_dev, K, nit, rb->itile);
+  SCN_LAUNCH_CHECK();
+  SCN_HIP(hipMemcpyAsync(hb->off, rb->off_dev, (K + 1) * 8, hipMemcpyDeviceToHost, st));
+  SCN_HIP(hipStreamSynchronize(st));
+  rb->n_pairs = hb->off[K];
+  if (rb->n_pairs > INT32_MAX || rb->n_pairs > pmax) {
+    set_error("scn_rulebook_build: %lld pairs exceed the supported count", (long long)rb->n_pairs);
+    return SCN_ERR_OVERFLOW;
+  }
+  for (int k = 0; k <= K; ++k) rb->off_host[k] = hb->off[k];
+  guard.keep = true;
+  *out = rb;
+  return SCN_OK;
+}
+
+}  // namespace
+}  // namespace scn
+
+extern "C" {
+
+scn_status scn_rulebook_build(const int32_t* coords, int64_t n, const int64_t* grid,
+                              int32_t filter, int32_t stride, hipStream_t stream,
+                              scn_rulebook** out) {
+  scn::clear_error();
+  return scn::build(coords, n, grid, filter, stride, stream, out);
+}
+
+scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info) {
+  if (!rb || !info) {
+    scn::set_error("scn_rulebook_get_info: NULL argument");
+    return SCN_ERR_INVALID;
+  }
+  info->a_in = rb->a_in;
+  info->a_out = rb->a_out;
+  info->n_pairs = rb->n_pairs;
+  info->K = rb->K;
+  info->filter = rb->f;
+  info->stride = rb->s;
+  info->input_sorted = rb->input_sorted;
+  for (int a = 0; a < 4; ++a) {
+    info->in_grid[a] = rb->gin[a];
+    info->out_grid[a] = rb->gout[a];
+  }
+  return SCN_OK;
+}
+
+const int32_t* scn_rulebook_out_coords(const scn_rulebook* rb) { return rb ? rb->out_coords : nullptr; }
+const int32_t* scn_rulebook_in_rows(const scn_rulebook* rb) { return rb ? rb->in_rows : nullptr; }
+const int32_t* scn_rulebook_out_rows(const scn_rulebook* rb) { return rb ? rb->out_rows : nullptr; }
+const int64_t* scn_rulebook_offsets(const scn_rulebook* rb) { return rb ? rb->off_host : nullptr; }
+
+scn_status scn_rulebook_export(const scn_rulebook* rb, int32_t* out_coords, int32_t* in_rows,
+                               int32_t* out_rows, hipStream_t stream) {
+  scn::clear_error();
+  if (!rb) {
+    scn::set_error("scn_rulebook_export: rb is NULL");
+    return SCN_ERR_INVALID;
+  }
+  if (out_coords && rb->a_out > 0)
+    SCN_HIP(hipMemcpyAsync(out_coords, rb->out_coords, rb->a_out * 16, hipMemcpyDeviceToDevice,
+                           stream));
+  if (in_rows && rb->n_pairs > 0)
+    SCN_HIP(hipMemcpyAsync(in_rows, rb->in_rows, rb->n_pairs * 4, hipMemcpyDeviceToDevice, stream));
+  if (out_rows && rb->n_pairs > 0)
+    SCN_HIP(hipMemcpyAsync(out_rows, rb->out_rows, rb->n_pairs * 4, hipMemcpyDeviceToDevice,
+                           stream));
+  return SCN_OK;
+}
+
+void scn_rulebook_free(scn_rulebook* rb) {
+  if (!rb) return;
+  scn::dfree(rb->block, rb->stream);
+  delete rb;
+}
+
+}  // extern "C"

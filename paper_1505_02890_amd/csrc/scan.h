@@ -1,0 +1,111 @@
+// Device-wide exclusive prefix sum (reduce, scan of block totals, downsweep).
+// Deterministic: integer sums, fixed partition.  Used by the rulebook builder
+// to number active sites (popcounts of occupancy words) and to place pair
+// lists (per-tile pair counts).
+#pragma once
+
+#include "scn_internal.h"
+
+namespace scn {
+
+constexpr int SCAN_THREADS = 256;
+constexpr int SCAN_ITEMS = 16;  // consecutive elements per thread
+constexpr int SCAN_BLOCK = SCAN_THREADS * SCAN_ITEMS;
+
+template <typename T>
+__device__ inline T block_exclusive_scan(T v, T* total) {
+  // 256 threads = 4 waves of 64
+  __shared__ T wsum[SCAN_THREADS / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  T inc = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    T t = __shfl_up(inc, d, 64);
+    if (lane >= d) inc += t;
+  }
+  if (lane == 63) wsum[w] = inc;
+  __syncthreads();
+  T before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < SCAN_THREADS / 64; ++i) {
+    if (i < w) before += wsum[i];
+    all += wsum[i];
+  }
+  __syncthreads();
+  *total = all;
+  return before + inc - v;
+}
+
+// Load functor: T operator()(int64_t i) const, valid for i < n.
+template <typename T, class Load>
+__global__ void __launch_bounds__(SCAN_THREADS) scan_reduce_kernel(Load ld, int64_t n,
+                                                                   T* block_sums) {
+  const int64_t base = (int64_t)blockIdx.x * SCAN_BLOCK + (int64_t)threadIdx.x * SCAN_ITEMS;
+  T s = 0;
+#pragma unroll
+  for (int j = 0; j < SCAN_ITEMS; ++j)
+    if (base + j < n) s += ld(base + j);
+  T tot;
+  block_exclusive_scan<T>(s, &tot);
+  if (threadIdx.x == 0) block_sums[blockIdx.x] = tot;
+}
+
+// One block: exclusive scan of nb block totals in place; grand total to *total.
+template <typename T>
+__global__ void __launch_bounds__(SCAN_THREADS) scan_top_kernel(T* sums, int64_t nb, T* total) {
+  T carry = 0;
+  for (int64_t c = 0; c < nb; c += SCAN_THREADS) {
+    const int64_t i = c + threadIdx.x;
+    T v = i < nb ? sums[i] : T(0);
+    T tot;
+    T ex = block_exclusive_scan<T>(v, &tot);
+    if (i < nb) sums[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) *total = carry;
+}
+
+template <typename T, class Load>
+__global__ void __launch_bounds__(SCAN_THREADS) scan_down_kernel(Load ld, int64_t n,
+                                                                 const T* block_off, T* out) {
+  const int64_t base = (int64_t)blockIdx.x * SCAN_BLOCK + (int64_t)threadIdx.x * SCAN_ITEMS;
+  T v[SCAN_ITEMS];
+  T s = 0;
+#pragma unroll
+  for (int j = 0; j < SCAN_ITEMS; ++j) {
+    v[j] = base + j < n ? ld(base + j) : T(0);
+    s += v[j];
+  }
+  T tot;
+  T ex = block_exclusive_scan<T>(s, &tot) + block_off[blockIdx.x];
+#pragma unroll
+  for (int j = 0; j < SCAN_ITEMS; ++j) {
+    if (base + j < n) out[base + j] = ex;
+    ex += v[j];
+  }
+}
+
+inline int64_t scan_blocks(int64_t n) { return n > 0 ? ceil_div(n, SCAN_BLOCK) : 1; }
+
+// out[i] = sum_{j<i} ld(j) for i < n; *total = sum of all (device).  tmp holds
+// scan_blocks(n) elements of T.
+template <typename T, class Load>
+scn_status exclusive_scan(Load ld, int64_t n, T* out, T* total, T* tmp, hipStream_t s) {
+  const int64_t nb = scan_blocks(n);
+  if (n > 0) {
+    hipLaunchKernelGGL((scan_reduce_kernel<T, Load>), dim3((unsigned)nb), dim3(SCAN_THREADS), 0,
+                       s, ld, n, tmp);
+    SCN_LAUNCH_CHECK();
+  }
+  hipLaunchKernelGGL((scan_top_kernel<T>), dim3(1), dim3(SCAN_THREADS), 0, s, tmp,
+                     n > 0 ? nb : 0, total);
+  SCN_LAUNCH_CHECK();
+  if (n > 0) {
+    hipLaunchKernelGGL((scan_down_kernel<T, Load>), dim3((unsigned)nb), dim3(SCAN_THREADS), 0,
+                       s, ld, n, (const T*)tmp, out);
+    SCN_LAUNCH_CHECK();
+  }
+  return SCN_OK;
+}
+
+}  // namespace scn

@@ -1,0 +1,88 @@
+// Internal definitions shared by the library's translation units (never by the
+// CPU oracle).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/scn.h"
+
+namespace scn {
+
+// Rows of a rulebook tile: pair ranges are stored per (offset, tile of TILE
+// output rows) and per (offset, tile of TILE input ranks).
+constexpr int TILE = 64;
+constexpr int MAX_K = 27;  // f <= 3
+
+void set_error(const char* fmt, ...);
+void clear_error();
+
+struct DeviceBuffer {
+  void* p = nullptr;
+};
+
+// Stream-ordered allocation from the device's default memory pool.
+scn_status dalloc(void** p, size_t bytes, hipStream_t s);
+void dfree(void* p, hipStream_t s);
+
+#define SCN_HIP(call)                                                                  \
+  do {                                                                                 \
+    hipError_t e_ = (call);                                                            \
+    if (e_ != hipSuccess) {                                                            \
+      ::scn::set_error("%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), __FILE__, \
+                       __LINE__);                                                      \
+      return SCN_ERR_HIP;                                                              \
+    }                                                                                  \
+  } while (0)
+
+#define SCN_LAUNCH_CHECK()                                                             \
+  do {                                                                                 \
+    hipError_t e_ = hipGetLastError();                                                 \
+    if (e_ != hipSuccess) {                                                            \
+      ::scn::set_error("kernel launch failed: %s (%s:%d)", hipGetErrorString(e_),      \
+                       __FILE__, __LINE__);                                            \
+      return SCN_ERR_HIP;                                                              \
+    }                                                                                  \
+  } while (0)
+
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace scn
+
+// Device layout of a rulebook.  All arrays are owned by the rulebook.
+struct scn_rulebook {
+  int32_t f = 0, s = 0, K = 0;
+  int64_t gin[4] = {0, 0, 0, 0};   // B, mx, my, mz
+  int64_t gout[4] = {0, 0, 0, 0};
+  int64_t a_in = 0, a_out = 0, n_pairs = 0;
+  int32_t input_sorted = 0;
+  hipStream_t stream = nullptr;    // stream the rulebook was built on (frees go there)
+
+  int64_t off_host[scn::MAX_K + 1] = {0};  // list boundaries (host copy)
+
+  int32_t* out_coords = nullptr;  // [a_out][4]
+  int32_t* in_rows = nullptr;     // [P] caller row of the input of each pair
+  int32_t* out_rows = nullptr;    // [P] output row of each pair
+  int32_t* in_rank = nullptr;     // [P] rank of the input in key order (== in_rows if sorted)
+  int32_t* perm = nullptr;        // [a_in] rank -> caller row
+  int64_t* off_dev = nullptr;     // [K+1] list boundaries (device copy)
+
+  // Pair ranges per tile.  otile[k*n_otiles + t] = global position of the first
+  // pair of list k whose output row is >= t*TILE (t in [0, n_otiles]); the last
+  // entry of list k equals the start of list k+1.  Length K*n_otiles + 1.
+  int64_t n_otiles = 0;
+  int64_t* otile = nullptr;
+  // Same per tile of TILE input ranks (for the input-gradient pass).
+  int64_t n_itiles = 0;
+  int64_t* itile = nullptr;
+
+  // Pool helpers (filter == stride only): nbr[o*K + k] = input row at s*o+k or -1;
+  // inv[r] = o*K + k of the unique window containing input r, or -1.
+  int32_t* nbr = nullptr;
+  int32_t* inv = nullptr;
+
+  void* block = nullptr;  // single allocation holding all arrays above
+};
