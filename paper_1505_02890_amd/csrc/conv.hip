@@ -8,15 +8,17 @@
 //     g_pre   = B + sum_k g_in W_k,
 // so only the active blocks are gathered and multiplied.
 //
-// Gather kernel (forward and input gradient).  A work-group owns a tile of
-// accumulator rows (output rows for the forward, input ranks for the input
-// gradient) and 64 columns; the accumulators live in LDS.  For each offset k
-// the tile's pairs form one contiguous range of list k (lists ascend by output
-// row and by input key), so the work-group stages up to 64 gathered rows in
-// LDS, each wave multiplies them by its 16 columns of W_k with MFMA and adds
-// the 16x16 results into the accumulator rows named by the pairs.  A wave is
-// the only writer of its columns and pair rows are distinct within an offset,
-// so the scatter needs no atomics and the summation order is fixed.
+// Gather kernel (forward and input gradient).  A work-group of four waves owns
+// a tile of accumulator rows (output rows for the forward, input ranks for the
+// input gradient) and 64 columns; the accumulators live in LDS.  Each wave owns
+// 16 of the columns.  For each offset k the tile's pairs form one contiguous
+// range of list k (lists ascend by output row and by input key).  A wave walks
+// that range 32 pairs at a time: it loads the 32 gathered rows straight into
+// MFMA A-fragments (the next 32 are already in flight), multiplies them by its
+// slice of W_k and adds the two 16x16 results into the LDS rows named by the
+// pairs.  A wave is the only writer of its columns and pair rows are distinct
+// within an offset, so the main loop has no barrier, the scatter needs no
+// atomics between waves, and the summation order is fixed.
 //
 // Weight gradient.  dW_k = X_k^T dY_k over the P_k pairs of offset k is a
 // contraction along the pair axis: split into fixed chunks, each chunk's
@@ -35,25 +37,74 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int NT = 256;     // threads per work-group (4 waves)
 constexpr int CB = 64;      // columns per work-group
-constexpr int CH = 64;      // gathered rows per stage
-constexpr int ACC_LD = CB + 16;
+constexpr int ACC_LD = CB + 4;
 
 __device__ inline v4f mfma4(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// Work-groups are dispatched round-robin over the 8 XCDs; give each XCD a
+// contiguous range of work items so neighbouring tiles share its L2.
+__device__ inline int64_t xcd_remap(int64_t b, int64_t n) {
+  const int64_t x = b & 7, j = b >> 3, base = n >> 3, rem = n & 7;
+  return x * base + min(x, rem) + j;
+}
+
 // ---------------------------------------------------------------------------
-// Ground state of the convolution output: g_pre = B + sum_k g_in W_k
+// Ground-state terms of the convolution.
+//   gw[k][co]  = sum_ci g_in[ci] W[k][ci][co]       (what an inactive site at
+//                offset k contributes; subtracted per pair in the residual form)
+//   g_pre[co]  = B[co] + sum_k gw[k][co]
 // ---------------------------------------------------------------------------
-__global__ void ground_pre_kernel(const float* __restrict__ g_in, const float* __restrict__ W,
-                                  const float* __restrict__ bias, int K, int Cin, int Cout,
+__global__ void __launch_bounds__(256) ground_w_kernel(const float* __restrict__ g_in,
+                                                       const float* __restrict__ W, int K, int Cin,
+                                                       int Cout, int ld, float* __restrict__ gw) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)K * ld) return;
+  const int k = (int)(i / ld), co = (int)(i - (int64_t)k * ld);
+  float s = 0.f;
+  if (co < Cout) {
+    const float* wp = W + (int64_t)k * Cin * Cout + co;
+    for (int ci = 0; ci < Cin; ++ci) s = fmaf(g_in[ci], wp[(int64_t)ci * Cout], s);
+  }
+  gw[i] = s;
+}
+
+__global__ void ground_pre_kernel(const float* __restrict__ gw, int ld,
+                                  const float* __restrict__ bias, int K, int Cout,
                                   float* __restrict__ g_pre) {
   const int co = blockIdx.x * blockDim.x + threadIdx.x;
   if (co >= Cout) return;
-  float acc = bias ? bias[co] : 0.f;
-  for (int k = 0; k < K; ++k)
-    for (int ci = 0; ci < Cin; ++ci) acc = fmaf(g_in[ci], W[((int64_t)k * Cin + ci) * Cout + co], acc);
-  g_pre[co] = acc;
+  float s = bias ? bias[co] : 0.f;
+  for (int k = 0; k < K; ++k) s += gw[(int64_t)k * ld + co];
+  g_pre[co] = s;
+}
+
+__global__ void zero_kernel(float* __restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0.f;
+}
+
+// Packed weights for the gather kernel: Wp[k][n][j] = W_k(j, n) with the
+// reduction index j contiguous, zero-padded to RkP rows and NcP columns.
+//   forward:        W_k(j = ci, n = co) = W[k][ci][co]   (transpose)
+//   input gradient: W_k(j = co, n = ci) = W[k][ci][co]   (copy with padding)
+__global__ void __launch_bounds__(256) pack_w_kernel(const float* __restrict__ W, int K, int Cin,
+                                                     int Cout, int transpose, int RkP, int NcP,
+                                                     float* __restrict__ Wp) {
+  const int Nc = transpose ? Cout : Cin, Rk = transpose ? Cin : Cout;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)K * NcP * RkP) return;
+  const int j = (int)(i % RkP);
+  const int64_t kn = i / RkP;
+  const int n = (int)(kn % NcP);
+  const int64_t k = kn / NcP;
+  float v = 0.f;
+  if (j < Rk && n < Nc) {
+    const int ci = transpose ? j : n, co = transpose ? n : j;
+    v = W[(k * Cin + ci) * Cout + co];
+  }
+  Wp[i] = v;
 }
 
 __global__ void relu_vec_kernel(float* __restrict__ v, int n) {
@@ -70,148 +121,292 @@ struct GatherArgs {
   const int32_t* aidx;   // per pair: accumulator row
   const int64_t* tpos;   // [K*ntile + 1] pair ranges per tile of TILE accumulator rows
   int64_t ntile;
-  const float* W;        // B(j, n) = W[k*ks + j*sj + n*sn]
-  int64_t ks, sj, sn;
+  const float* Wp;       // W_k(j, n) = Wp[(k*NcP + n)*RkP + j], zero-padded (RkP = 16*ceil(Rk/16))
+  const float* gwp;      // [K][NcP] subtracted from every pair's product (zeros if none)
+  int NcP;               // Nc rounded up to 64
   int Rk;                // reduction length (channels of src)
-  int RkP;               // Rk rounded up to 16
   int Nc;                // output columns
-  const float* sub;      // [Rk] subtracted from gathered rows, or null
   const float* add;      // [Nc] added to every accumulator row, or null
   int relu;
   float* dst;            // [nrows][Nc]
   const int32_t* wmap;   // dst row of accumulator row r (null = identity)
   int64_t nrows;
   int K;
-  int TM;                // tiles of TILE rows per work-group
-  int vec_ok;            // rows of src are 16-byte aligned (float4 gathers)
+  int vec_ok;            // rows of src are 16-byte aligned and Rk % 4 == 0
+  int dvec_ok;           // rows of dst are 16-byte aligned and Nc % 4 == 0
 };
 
-__global__ void __launch_bounds__(NT) gather_mfma_kernel(GatherArgs a) {
-  extern __shared__ float smem[];
-  const int T = a.TM * TILE;
-  const int XS_LD = a.RkP + 4;
-  float* acc = smem;                                  // [T][ACC_LD]
-  float* xs = acc + (size_t)T * ACC_LD;               // [CH][XS_LD]
-  int* ids = reinterpret_cast<int*>(xs + (size_t)CH * XS_LD);  // [CH]
+// One pipeline stage covers 32 consecutive pairs of one offset: two 16-pair
+// blocks.  Lane (n16, q) gathers channels 16t + 4q .. +3 of pair n16 of each
+// block, which is the B-operand layout of v_mfma_f32_16x16x4f32 when the
+// contraction is computed transposed (R^T = W_k^T X^T): the result then holds
+// pair n16, output columns 4q .. 4q+3 of the wave's 16 in one lane, so the
+// lane scatters one contiguous float4 into its own pair's accumulator row.
+template <int NKT>
+struct XFrag {
+  float4 x0[NKT], x1[NKT];
+};
 
+template <int NKT>
+struct WFrag {
+  float4 w[NKT];  // W_k(j = 16t + 4q + 0..3, column 16w + n16)
+  float4 g;       // gw[k][16w + 4q .. +3]
+};
+
+// Indices of lane n16's pair in each block.  Positions past the range are
+// clamped to the range's last pair, so loads are unconditional and in bounds;
+// the scatter skips those rows.  No loaded value is masked, so loads stay in
+// flight until their use one stage later.
+struct Idx {
+  int g0, g1;  // gathered row
+  int i0, i1;  // tile-local accumulator row
+};
+
+__device__ inline Idx load_idx(const GatherArgs& a, int64_t p, int64_t e, int64_t row0, int n16) {
+  Idx r;
+  const int64_t c0 = min(p + n16, e - 1), c1 = min(p + 16 + n16, e - 1);
+  r.g0 = a.gidx[c0];
+  r.g1 = a.gidx[c1];
+  r.i0 = (int)(a.aidx[c0] - row0);
+  r.i1 = (int)(a.aidx[c1] - row0);
+  return r;
+}
+
+// Reduction slots j >= Rk read some channel of the same row; the matching W
+// entries are zero.
+template <int NKT, bool VEC>
+__device__ inline void load_x(const GatherArgs& a, const Idx& ix, int q, XFrag<NKT>& f) {
+  const float* p0 = a.src + (int64_t)ix.g0 * a.Rk;
+  const float* p1 = a.src + (int64_t)ix.g1 * a.Rk;
+#pragma unroll
+  for (int t = 0; t < NKT; ++t) {
+    const int c = 16 * t + 4 * q;
+    if (VEC) {
+      const int cc = c < a.Rk ? c : 0;
+      f.x0[t] = *reinterpret_cast<const float4*>(p0 + cc);
+      f.x1[t] = *reinterpret_cast<const float4*>(p1 + cc);
+    } else {
+      float e0[4], e1[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int cc = c + u < a.Rk ? c + u : 0;
+        e0[u] = p0[cc];
+        e1[u] = p1[cc];
+      }
+      f.x0[t] = make_float4(e0[0], e0[1], e0[2], e0[3]);
+      f.x1[t] = make_float4(e1[0], e1[1], e1[2], e1[3]);
+    }
+  }
+}
+
+// W_k(j, n) = Wp[(k*NcP + n)*RkP + j], zero-padded to RkP = 16*NKT rows and
+// NcP = 64*ceil(Nc/64) columns; gw is padded the same way.
+template <int NKT>
+__device__ inline void load_w(const GatherArgs& a, int k, int col, int cq, int q, WFrag<NKT>& f) {
+  const float* wp = a.Wp + ((int64_t)k * a.NcP + col) * (16 * NKT) + 4 * q;
+#pragma unroll
+  for (int t = 0; t < NKT; ++t) f.w[t] = *reinterpret_cast<const float4*>(wp + 16 * t);
+  f.g = *reinterpret_cast<const float4*>(a.gwp + (int64_t)k * a.NcP + cq);
+}
+
+template <int NKT>
+__device__ inline void mfma_scatter(const XFrag<NKT>& X, const WFrag<NKT>& B, const Idx& ix,
+                                    int64_t p, int64_t e, float* acc, int cq, int n16) {
+  v4f c0v = {0.f, 0.f, 0.f, 0.f}, c1v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < NKT; ++t) {
+    c0v = mfma4(B.w[t].x, X.x0[t].x, c0v);
+    c1v = mfma4(B.w[t].x, X.x1[t].x, c1v);
+    c0v = mfma4(B.w[t].y, X.x0[t].y, c0v);
+    c1v = mfma4(B.w[t].y, X.x1[t].y, c1v);
+    c0v = mfma4(B.w[t].z, X.x0[t].z, c0v);
+    c1v = mfma4(B.w[t].z, X.x1[t].z, c1v);
+    c0v = mfma4(B.w[t].w, X.x0[t].w, c0v);
+    c1v = mfma4(B.w[t].w, X.x1[t].w, c1v);
+  }
+  // lane holds pair n16 of each block, columns cq .. cq+3 (tile-local)
+  if (p + n16 < e) {
+    float4* r = reinterpret_cast<float4*>(&acc[ix.i0 * ACC_LD + cq]);
+    float4 v = *r;
+    v.x += c0v[0] - B.g.x;
+    v.y += c0v[1] - B.g.y;
+    v.z += c0v[2] - B.g.z;
+    v.w += c0v[3] - B.g.w;
+    *r = v;
+  }
+  if (p + 16 + n16 < e) {
+    float4* r = reinterpret_cast<float4*>(&acc[ix.i1 * ACC_LD + cq]);
+    float4 v = *r;
+    v.x += c1v[0] - B.g.x;
+    v.y += c1v[1] - B.g.y;
+    v.z += c1v[2] - B.g.z;
+    v.w += c1v[3] - B.g.w;
+    *r = v;
+  }
+}
+
+// Next stage after (k, p) within the tile: same offset 32 pairs on, else the
+// first pair of the next non-empty offset; k == K when there is none.
+__device__ inline void advance(const GatherArgs& a, int64_t t0, int64_t t1, int& k, int64_t& p,
+                               int64_t& e) {
+  p += 32;
+  if (p < e) return;
+  for (++k; k < a.K; ++k) {
+    p = a.tpos[(int64_t)k * a.ntile + t0];
+    e = a.tpos[(int64_t)k * a.ntile + t1];
+    if (p < e) return;
+  }
+}
+
+template <int NKT, bool VEC, int TM, int MINB>
+__global__ void __launch_bounds__(NT, MINB) gather_mfma_kernel(GatherArgs a) {
+  extern __shared__ float acc[];  // [TM*TILE][ACC_LD]
+  constexpr int T = TM * TILE;
   const int tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int n16 = lane & 15, q = lane >> 4;
-  const int64_t t0 = (int64_t)blockIdx.x * a.TM;
-  const int64_t t1 = min(t0 + a.TM, a.ntile);
+  const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t t0 = tile * TM;
+  const int64_t t1 = min(t0 + TM, a.ntile);
   const int64_t row0 = t0 * TILE;
   const int c0 = blockIdx.y * CB;
-  const int col = c0 + 16 * w + n16;     // this lane's output column in MFMA results
-  const bool wave_live = c0 + 16 * w < a.Nc;
-  const int nkt = a.RkP >> 4;            // 16-wide reduction steps
+  const int col = c0 + 16 * w + n16;  // W column this lane feeds into the A operand
+  const int cq = 16 * w + 4 * q;      // tile-local columns this lane accumulates
+  const bool live = c0 + 16 * w < a.Nc;  // wave-uniform
 
-  for (int i = tid; i < T * ACC_LD; i += NT) acc[i] = 0.f;
+  for (int i = tid; i < T * ACC_LD / 4; i += NT)
+    reinterpret_cast<float4*>(acc)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  __syncthreads();
 
-  const int vec_ok = a.vec_ok;
-  for (int k = 0; k < a.K; ++k) {
-    const int64_t p_begin = a.tpos[(int64_t)k * a.ntile + t0];
-    const int64_t p_end = a.tpos[(int64_t)k * a.ntile + t1];
-    if (p_begin >= p_end) continue;   // uniform across the work-group
-    // B fragments of W_k for this wave's 16 columns: b[t][e] = B(16t + 4q + e, col)
-    float b[64];
-#pragma unroll
-    for (int t = 0; t < 16; ++t)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int j = 16 * t + 4 * q + e;
-        float v = 0.f;
-        if (t < nkt && j < a.Rk && col < a.Nc) v = a.W[(int64_t)k * a.ks + j * a.sj + col * a.sn];
-        b[4 * t + e] = v;
-      }
-    for (int64_t p0 = p_begin; p0 < p_end; p0 += CH) {
-      const int n = (int)min<int64_t>(CH, p_end - p0);
-      __syncthreads();  // previous stage fully consumed
-      if (tid < CH) ids[tid] = tid < n ? (int)(a.aidx[p0 + tid] - row0) : 0;
-      // gather n rows (zero rows up to the next multiple of 16 and zero padding columns)
-      const int nr = (n + 15) & ~15;
-      const int q4 = a.RkP >> 2;  // float4 per staged row
-      for (int i = tid; i < nr * q4; i += NT) {
-        const int r = i / q4, c4 = (i - r * q4) * 4;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (r < n) {
-          const int64_t srow = a.gidx[p0 + r];
-          const float* sp = a.src + srow * a.Rk;
-          if (vec_ok && c4 + 3 < a.Rk) {
-            v = *reinterpret_cast<const float4*>(sp + c4);
-          } else {
-            if (c4 + 0 < a.Rk) v.x = sp[c4 + 0];
-            if (c4 + 1 < a.Rk) v.y = sp[c4 + 1];
-            if (c4 + 2 < a.Rk) v.z = sp[c4 + 2];
-            if (c4 + 3 < a.Rk) v.w = sp[c4 + 3];
-          }
-          if (a.sub) {
-            if (c4 + 0 < a.Rk) v.x -= a.sub[c4 + 0];
-            if (c4 + 1 < a.Rk) v.y -= a.sub[c4 + 1];
-            if (c4 + 2 < a.Rk) v.z -= a.sub[c4 + 2];
-            if (c4 + 3 < a.Rk) v.w -= a.sub[c4 + 3];
-          }
-        }
-        *reinterpret_cast<float4*>(xs + r * XS_LD + c4) = v;
-      }
-      __syncthreads();
-      if (!wave_live) continue;
-      for (int rb = 0; rb < nr; rb += 16) {
-        v4f c = {0.f, 0.f, 0.f, 0.f};
-        const float* arow = xs + (rb + n16) * XS_LD + 4 * q;
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-          if (t < nkt) {
-            const float4 av = *reinterpret_cast<const float4*>(arow + 16 * t);
-            c = mfma4(av.x, b[4 * t + 0], c);
-            c = mfma4(av.y, b[4 * t + 1], c);
-            c = mfma4(av.z, b[4 * t + 2], c);
-            c = mfma4(av.w, b[4 * t + 3], c);
-          }
-        }
-        // lane holds rows rb + 4q + v, column col
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int r = rb + 4 * q + v;
-          if (r < n) {
-            float* ap = acc + ids[r] * ACC_LD + 16 * w + n16;
-            *ap += c[v];
-          }
-        }
+  if (live) {
+    // first non-empty offset
+    int k = -1;
+    int64_t p = 0, e = 0;
+    advance(a, t0, t1, k, p, e);  // p = 32 >= e = 0 -> scans from k = 0
+    if (k < a.K) {
+      // pipeline: indices two stages ahead, gathered rows and W one stage
+      // ahead; past the last stage the loads repeat the last stage
+      int k1 = k;
+      int64_t p1 = p, e1 = e;
+      advance(a, t0, t1, k1, p1, e1);
+      Idx ix0 = load_idx(a, p, e, row0, n16);
+      Idx ix1 = k1 < a.K ? load_idx(a, p1, e1, row0, n16) : ix0;
+      XFrag<NKT> X;
+      WFrag<NKT> B;
+      load_x<NKT, VEC>(a, ix0, q, X);
+      load_w<NKT>(a, k, col, c0 + cq, q, B);
+      while (true) {
+        int k2 = k1;
+        int64_t p2 = p1, e2 = e1;
+        if (k1 < a.K) advance(a, t0, t1, k2, p2, e2);
+        const bool more = k1 < a.K, more2 = k2 < a.K;
+        const Idx ix2 = load_idx(a, more2 ? p2 : p, more2 ? e2 : e, row0, n16);
+        XFrag<NKT> Xn;
+        WFrag<NKT> Bn;
+        load_x<NKT, VEC>(a, ix1, q, Xn);
+        load_w<NKT>(a, more ? k1 : k, col, c0 + cq, q, Bn);
+        mfma_scatter<NKT>(X, B, ix0, p, e, acc, cq, n16);
+        if (!more) break;
+        X = Xn;
+        B = Bn;
+        ix0 = ix1;
+        ix1 = ix2;
+        k = k1;
+        p = p1;
+        e = e1;
+        k1 = k2;
+        p1 = p2;
+        e1 = e2;
       }
     }
   }
   __syncthreads();
   // epilogue: dst[row] = act(acc + add)
   const int ncols = min(CB, a.Nc - c0);
-  for (int i = tid; i < T * CB; i += NT) {
-    const int r = i / CB, cc = i - r * CB;
+  for (int i = tid; i < T * (CB / 4); i += NT) {
+    const int r = i / (CB / 4), cc = (i - r * (CB / 4)) * 4;
     const int64_t grow = row0 + r;
     if (cc >= ncols || grow >= a.nrows) continue;
-    float v = acc[r * ACC_LD + cc];
-    if (a.add) v += a.add[c0 + cc];
-    if (a.relu) v = v > 0.f ? v : 0.f;
+    float4 v = *reinterpret_cast<const float4*>(&acc[r * ACC_LD + cc]);
+    float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (a.add && cc + u < ncols) e[u] += a.add[c0 + cc + u];
+      if (a.relu) e[u] = e[u] > 0.f ? e[u] : 0.f;
+    }
     const int64_t drow = a.wmap ? (int64_t)a.wmap[grow] : grow;
-    a.dst[drow * a.Nc + c0 + cc] = v;
+    float* dp = a.dst + drow * a.Nc + c0 + cc;
+    if (a.dvec_ok && cc + 3 < ncols) {
+      *reinterpret_cast<float4*>(dp) = make_float4(e[0], e[1], e[2], e[3]);
+    } else {
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (cc + u < ncols) dp[u] = e[u];
+    }
   }
 }
 
-size_t gather_smem_bytes(int TM, int RkP) {
-  return ((size_t)TM * TILE * ACC_LD + (size_t)CH * (RkP + 4)) * sizeof(float) + CH * sizeof(int);
+typedef void (*GatherFn)(GatherArgs);
+
+template <int NKT>
+GatherFn pick_gather(int TM, bool vec) {
+  if (NKT > 4 || TM == 8) return vec ? gather_mfma_kernel<NKT, true, 8, 1>
+                                     : gather_mfma_kernel<NKT, false, 8, 1>;
+  if (TM == 2) return vec ? gather_mfma_kernel<NKT, true, 2, 4> : gather_mfma_kernel<NKT, false, 2, 4>;
+  return vec ? gather_mfma_kernel<NKT, true, 4, 2> : gather_mfma_kernel<NKT, false, 4, 2>;
+}
+
+GatherFn gather_fn(int nkt, int TM, bool vec) {
+  switch (nkt) {
+    case 1: return pick_gather<1>(TM, vec);
+    case 2: return pick_gather<2>(TM, vec);
+    case 3: return pick_gather<3>(TM, vec);
+    case 4: return pick_gather<4>(TM, vec);
+    case 5: return pick_gather<5>(TM, vec);
+    case 6: return pick_gather<6>(TM, vec);
+    case 7: return pick_gather<7>(TM, vec);
+    case 8: return pick_gather<8>(TM, vec);
+    case 9: return pick_gather<9>(TM, vec);
+    case 10: return pick_gather<10>(TM, vec);
+    case 11: return pick_gather<11>(TM, vec);
+    case 12: return pick_gather<12>(TM, vec);
+    case 13: return pick_gather<13>(TM, vec);
+    case 14: return pick_gather<14>(TM, vec);
+    case 15: return pick_gather<15>(TM, vec);
+    default: return pick_gather<16>(TM, vec);
+  }
+}
+
+int gather_tm() {
+  static int tm = -1;
+  if (tm < 0) {
+    const char* e = getenv("SCN_GATHER_TM");
+    const int v = e ? atoi(e) : 4;
+    tm = (v == 2 || v == 8) ? v : 4;
+  }
+  return tm;
 }
 
 scn_status launch_gather(GatherArgs a, hipStream_t st) {
   if (a.nrows <= 0) return SCN_OK;
   a.vec_ok = ((a.Rk & 3) == 0) && ((reinterpret_cast<uintptr_t>(a.src) & 15) == 0);
-  const int64_t nwg = ceil_div(a.ntile, a.TM);
+
+  a.dvec_ok = ((a.Nc & 3) == 0) && ((reinterpret_cast<uintptr_t>(a.dst) & 15) == 0);
+  const int nkt = (int)ceil_div(a.Rk, 16);
+  const int TM = nkt > 4 ? 8 : gather_tm();
+  const int64_t nwg = ceil_div(a.ntile, TM);
   const unsigned ncb = (unsigned)ceil_div(a.Nc, CB);
-  const size_t smem = gather_smem_bytes(a.TM, a.RkP);
-  static bool attr_set = false;
-  if (!attr_set) {
-    SCN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(gather_mfma_kernel),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024));
-    attr_set = true;
+  const size_t smem = (size_t)TM * TILE * ACC_LD * sizeof(float);
+  const bool vec = a.vec_ok;
+  GatherFn fn = gather_fn(nkt, TM, vec);
+  static bool attr_done[9][2][17] = {};
+  bool& done = attr_done[TM][vec][nkt];
+  if (!done) {
+    SCN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
+    done = true;
   }
-  hipLaunchKernelGGL(gather_mfma_kernel, dim3((unsigned)nwg, ncb), dim3(NT), smem, st, a);
+  hipLaunchKernelGGL(fn, dim3((unsigned)nwg, ncb), dim3(NT), smem, st, a);
   SCN_LAUNCH_CHECK();
   return SCN_OK;
 }
@@ -251,23 +446,34 @@ __global__ void __launch_bounds__(NT) colsum_kernel(const float* __restrict__ dy
   }
 }
 
-// S, dḡ, dbias; u0 = S + dḡ
-__global__ void finish_vec_kernel(const float* __restrict__ partS, int64_t nblk, int C,
-                                  const float* __restrict__ g_out, const float* __restrict__ dg_out,
-                                  int relu, float* __restrict__ S, float* __restrict__ u0,
-                                  float* __restrict__ dbias) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
+// S, dḡ, dbias; u0 = S + dḡ.  One block of 1024 threads per 64 columns.
+__global__ void __launch_bounds__(1024) finish_vec_kernel(const float* __restrict__ partS,
+                                                          int64_t nblk, int C,
+                                                          const float* __restrict__ g_out,
+                                                          const float* __restrict__ dg_out,
+                                                          int relu, float* __restrict__ S,
+                                                          float* __restrict__ u0,
+                                                          float* __restrict__ dbias) {
+  __shared__ float red[1024];
+  const int cl = threadIdx.x & 63, rg = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + cl;
   float s = 0.f;
-  for (int64_t b = 0; b < nblk; ++b) s += partS[b * C + c];
-  float dg = dg_out ? dg_out[c] : 0.f;
-  if (relu && dg_out) dg = g_out[c] > 0.f ? dg : 0.f;
-  S[c] = s;
-  u0[c] = s + dg;
-  if (dbias) dbias[c] = s + dg;
+  if (c < C)
+    for (int64_t b = rg; b < nblk; b += 16) s += partS[b * C + c];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  if (rg == 0 && c < C) {
+    float t = 0.f;
+    for (int i = 0; i < 16; ++i) t += red[i * 64 + cl];
+    float dg = dg_out ? dg_out[c] : 0.f;
+    if (relu && dg_out) dg = g_out[c] > 0.f ? dg : 0.f;
+    S[c] = t;
+    u0[c] = t + dg;
+    if (dbias) dbias[c] = t + dg;
+  }
 }
 
-// Weight gradient partials.  grid (chunk, k, cin-block * n_co_blocks + co-block)
+// Weight gradient partials.
 constexpr int DW_SC = 64;          // pairs per stage
 constexpr int DW_LD = DW_SC + 4;
 
@@ -278,73 +484,112 @@ struct DwArgs {
   const int32_t* in_rows;
   const int32_t* out_rows;
   const int64_t* off;    // [K+1]
+  int K;
   int Cin, Cout;
+  int nco;               // 64-column blocks of Cout
+  int nblk;              // (Cin blocks) * nco
   int64_t chp;           // pairs per chunk
   int64_t maxc;          // chunks per offset (slot count)
+  int vec_ok;            // x and dyb rows 16-byte aligned, Cin and Cout % 4 == 0
   float* part;           // [K][maxc][Cin][Cout]
   float* partT;          // [K][maxc][Cout]
 };
 
+// Rows of one stage: thread (pair pr = tid & 63, quads c4 = 4*(w + 4*i), i < 4)
+struct DwRegs {
+  float4 x[4], d[4];
+};
+
+__device__ inline void dw_load(const DwArgs& a, int64_t p0, int n, int ci0, int co0, int pr, int w,
+                               DwRegs& R) {
+  const bool v = pr < n;
+  const int64_t ri = v ? a.in_rows[p0 + pr] : 0, ro = v ? a.out_rows[p0 + pr] : 0;
+  const float* xp = a.x + ri * a.Cin + ci0;
+  const float* dp = a.dyb + ro * a.Cout + co0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c4 = 4 * (w + 4 * i);
+    float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), dv = xv;
+    if (v) {
+      if (a.vec_ok && ci0 + c4 + 3 < a.Cin) {
+        xv = *reinterpret_cast<const float4*>(xp + c4);
+      } else {
+        float e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) e[u] = ci0 + c4 + u < a.Cin ? xp[c4 + u] : 0.f;
+        xv = make_float4(e[0], e[1], e[2], e[3]);
+      }
+      if (a.vec_ok && co0 + c4 + 3 < a.Cout) {
+        dv = *reinterpret_cast<const float4*>(dp + c4);
+      } else {
+        float e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) e[u] = co0 + c4 + u < a.Cout ? dp[c4 + u] : 0.f;
+        dv = make_float4(e[0], e[1], e[2], e[3]);
+      }
+    }
+    R.x[i] = xv;
+    R.d[i] = dv;
+  }
+}
+
 __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
   __shared__ float xsT[64 * DW_LD];  // [ci][pair]
   __shared__ float dsT[64 * DW_LD];  // [co][pair]
-  const int k = blockIdx.y;
-  const int64_t c = blockIdx.x;
+  __shared__ float gsub[64];
+  // flattened (chunk, offset, block) work item, offsets fastest, XCD-contiguous
+  const int64_t item = xcd_remap(blockIdx.x, gridDim.x);
+  const int blk = (int)(item % a.nblk);
+  const int64_t ck = item / a.nblk;
+  const int k = (int)(ck % a.K);
+  const int64_t c = ck / a.K;
   const int64_t lb = a.off[k], le = a.off[k + 1];
   const int64_t p_begin = lb + c * a.chp;
   if (p_begin >= le) return;
   const int64_t p_end = min(le, p_begin + a.chp);
-  const int nco = (a.Cout + 63) / 64;
-  const int ci0 = (blockIdx.z / nco) * 64, co0 = (blockIdx.z % nco) * 64;
+  const int ci0 = (blk / a.nco) * 64, co0 = (blk % a.nco) * 64;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n16 = lane & 15, q = lane >> 4;
+  if (tid < 64) gsub[tid] = ci0 + tid < a.Cin ? a.g_in[ci0 + tid] : 0.f;
 
   v4f acc[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
-  float tsum = 0.f;  // column sum of dyb over this lane's quarter of every stage
+  float tsum = 0.f;
   const int tcol = 16 * w + n16;
+  const int pr = tid & 63;
 
-  // gather mapping: lane -> (pair = i16 + 16*rep, channel quad)
+  DwRegs R;
+  dw_load(a, p_begin, (int)min<int64_t>(DW_SC, p_end - p_begin), ci0, co0, pr, w, R);
+  __syncthreads();  // gsub ready
   for (int64_t p0 = p_begin; p0 < p_end; p0 += DW_SC) {
     const int n = (int)min<int64_t>(DW_SC, p_end - p0);
-    __syncthreads();
-    // 64 pairs x 16 quads = 1024 items, 4 per thread; consecutive lanes = consecutive pairs
-    for (int it = tid; it < DW_SC * 16; it += NT) {
-      const int pr = it & 63, c4 = (it >> 6) * 4;
-      float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), dv = xv;
-      if (pr < n) {
-        const int64_t ri = a.in_rows[p0 + pr], ro = a.out_rows[p0 + pr];
-        const float* xp = a.x + ri * a.Cin + ci0;
-        const float* dp = a.dyb + ro * a.Cout + co0;
-        float xe[4], de[4];
+    // registers -> LDS (transposed); x rows shifted by the ground state
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int ci = ci0 + c4 + e, co = co0 + c4 + e;
-          xe[e] = ci < a.Cin ? xp[c4 + e] - a.g_in[ci] : 0.f;
-          de[e] = co < a.Cout ? dp[c4 + e] : 0.f;
-        }
-        xv = make_float4(xe[0], xe[1], xe[2], xe[3]);
-        dv = make_float4(de[0], de[1], de[2], de[3]);
-      }
-      xsT[(c4 + 0) * DW_LD + pr] = xv.x;
-      xsT[(c4 + 1) * DW_LD + pr] = xv.y;
-      xsT[(c4 + 2) * DW_LD + pr] = xv.z;
-      xsT[(c4 + 3) * DW_LD + pr] = xv.w;
-      dsT[(c4 + 0) * DW_LD + pr] = dv.x;
-      dsT[(c4 + 1) * DW_LD + pr] = dv.y;
-      dsT[(c4 + 2) * DW_LD + pr] = dv.z;
-      dsT[(c4 + 3) * DW_LD + pr] = dv.w;
+    for (int i = 0; i < 4; ++i) {
+      const int c4 = 4 * (w + 4 * i);
+      const bool v = pr < n;
+      xsT[(c4 + 0) * DW_LD + pr] = v ? R.x[i].x - gsub[c4 + 0] : 0.f;
+      xsT[(c4 + 1) * DW_LD + pr] = v ? R.x[i].y - gsub[c4 + 1] : 0.f;
+      xsT[(c4 + 2) * DW_LD + pr] = v ? R.x[i].z - gsub[c4 + 2] : 0.f;
+      xsT[(c4 + 3) * DW_LD + pr] = v ? R.x[i].w - gsub[c4 + 3] : 0.f;
+      dsT[(c4 + 0) * DW_LD + pr] = R.d[i].x;
+      dsT[(c4 + 1) * DW_LD + pr] = R.d[i].y;
+      dsT[(c4 + 2) * DW_LD + pr] = R.d[i].z;
+      dsT[(c4 + 3) * DW_LD + pr] = R.d[i].w;
     }
     __syncthreads();
-    // A(m = ci, kk = pair) = xsT[16w + m][pair];  B(kk = pair, n = co) = dsT[16j + n][pair]
+    // prefetch the next stage into registers while the matrix cores work
+    const int64_t pn = p0 + DW_SC;
+    if (pn < p_end) dw_load(a, pn, (int)min<int64_t>(DW_SC, p_end - pn), ci0, co0, pr, w, R);
     const float* ar = xsT + (16 * w + n16) * DW_LD + 4 * q;
 #pragma unroll
     for (int t = 0; t < DW_SC / 16; ++t) {
       const float4 av = *reinterpret_cast<const float4*>(ar + 16 * t);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float4 bv = *reinterpret_cast<const float4*>(dsT + (16 * j + n16) * DW_LD + 4 * q + 16 * t);
+        const float4 bv =
+            *reinterpret_cast<const float4*>(dsT + (16 * j + n16) * DW_LD + 4 * q + 16 * t);
         acc[j] = mfma4(av.x, bv.x, acc[j]);
         acc[j] = mfma4(av.y, bv.y, acc[j]);
         acc[j] = mfma4(av.z, bv.z, acc[j]);
@@ -360,6 +605,7 @@ __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
         tsum += ((v.x + v.y) + v.z) + v.w;
       }
     }
+    __syncthreads();
   }
   // write partial dW: lane holds rows 4q + v (ci), column n16 of tile j (co)
   float* out = a.part + ((int64_t)k * a.maxc + c) * a.Cin * a.Cout;
@@ -408,17 +654,27 @@ __global__ void dw_reduce_kernel(const float* __restrict__ part, const float* __
   }
 }
 
-// dg_in[ci] = sum_k sum_co W[k][ci][co] * (u0[co] - T[k][co])
-__global__ void dgin_kernel(const float* __restrict__ W, const float* __restrict__ u0,
-                            const float* __restrict__ T, int K, int Cin, int Cout,
-                            float* __restrict__ dg_in) {
-  const int ci = blockIdx.x * blockDim.x + threadIdx.x;
-  if (ci >= Cin) return;
+// dg_in[ci] = sum_k sum_co W[k][ci][co] * (u0[co] - T[k][co]); one block per ci,
+// fixed-order tree over the block.
+__global__ void __launch_bounds__(256) dgin_kernel(const float* __restrict__ W,
+                                                   const float* __restrict__ u0,
+                                                   const float* __restrict__ T, int K, int Cin,
+                                                   int Cout, float* __restrict__ dg_in) {
+  __shared__ float red[256];
+  const int ci = blockIdx.x;
+  const int64_t n = (int64_t)K * Cout;
   float s = 0.f;
-  for (int k = 0; k < K; ++k)
-    for (int co = 0; co < Cout; ++co)
-      s = fmaf(W[((int64_t)k * Cin + ci) * Cout + co], u0[co] - T[(int64_t)k * Cout + co], s);
-  dg_in[ci] = s;
+  for (int64_t i = threadIdx.x; i < n; i += 256) {
+    const int k = (int)(i / Cout), co = (int)(i - (int64_t)k * Cout);
+    s = fmaf(W[((int64_t)k * Cin + ci) * Cout + co], u0[co] - T[i], s);
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) dg_in[ci] = red[0];
 }
 
 inline int64_t dw_chunk(int64_t P) {
@@ -428,7 +684,7 @@ inline int64_t dw_chunk(int64_t P) {
 
 struct BwdLayout {
   int64_t chp, maxc, nblk;
-  size_t o_dyb, o_part, o_partT, o_partS, o_S, o_u0, o_T, total;
+  size_t o_dyb, o_part, o_partT, o_partS, o_S, o_u0, o_T, o_wp, o_gz, total;
 };
 
 BwdLayout bwd_layout(const scn_rulebook* rb, int Cin, int Cout, uint32_t flags) {
@@ -454,11 +710,13 @@ BwdLayout bwd_layout(const scn_rulebook* rb, int Cin, int Cout, uint32_t flags) 
   cur += al((size_t)Cout * 4);
   L.o_T = cur;
   cur += al((size_t)rb->K * Cout * 4);
+  L.o_wp = cur;
+  cur += al((size_t)rb->K * ceil_div(Cin, 64) * 64 * ceil_div(Cout, 16) * 16 * 4);
+  L.o_gz = cur;
+  cur += al((size_t)rb->K * ceil_div(Cin, 64) * 64 * 4);
   L.total = cur;
   return L;
 }
-
-constexpr int pick_tm() { return 2; }
 
 }  // namespace
 }  // namespace scn
@@ -481,8 +739,27 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
     return SCN_ERR_UNSUPPORTED;
   }
   const int relu = (flags & SCN_RELU) ? 1 : 0;
-  hipLaunchKernelGGL(ground_pre_kernel, dim3((unsigned)ceil_div(Cout, 64)), dim3(64), 0, st, g_in,
-                     W, bias, rb->K, Cin, Cout, g_out);
+  // scratch: gw [K][NcP] and the packed weights [K][NcP][RkP]
+  const int RkP = (int)ceil_div(Cin, 16) * 16, NcP = (int)ceil_div(Cout, 64) * 64;
+  const size_t gw_bytes = ((size_t)rb->K * NcP * sizeof(float) + 255) & ~size_t(255);
+  float* gw = nullptr;
+  scn_status rc = dalloc(reinterpret_cast<void**>(&gw),
+                         gw_bytes + (size_t)rb->K * NcP * RkP * sizeof(float), st);
+  if (rc) return rc;
+  struct Free {
+    float* p;
+    hipStream_t s;
+    ~Free() { dfree(p, s); }
+  } free_gw{gw, st};
+  float* Wp = reinterpret_cast<float*>(reinterpret_cast<char*>(gw) + gw_bytes);
+  hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)ceil_div((int64_t)rb->K * NcP * RkP, 256)),
+                     dim3(256), 0, st, W, rb->K, Cin, Cout, 1, RkP, NcP, Wp);
+  SCN_LAUNCH_CHECK();
+  hipLaunchKernelGGL(ground_w_kernel, dim3((unsigned)ceil_div((int64_t)rb->K * NcP, 256)),
+                     dim3(256), 0, st, g_in, W, rb->K, Cin, Cout, NcP, gw);
+  SCN_LAUNCH_CHECK();
+  hipLaunchKernelGGL(ground_pre_kernel, dim3((unsigned)ceil_div(Cout, 64)), dim3(64), 0, st, gw,
+                     NcP, bias, rb->K, Cout, g_out);
   SCN_LAUNCH_CHECK();
   GatherArgs a{};
   a.src = x;
@@ -490,22 +767,18 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
   a.aidx = rb->out_rows;
   a.tpos = rb->otile;
   a.ntile = rb->n_otiles;
-  a.W = W;
-  a.ks = (int64_t)Cin * Cout;
-  a.sj = Cout;
-  a.sn = 1;
+  a.Wp = Wp;
+  a.gwp = gw;
+  a.NcP = NcP;
   a.Rk = Cin;
-  a.RkP = (int)ceil_div(Cin, 16) * 16;
   a.Nc = Cout;
-  a.sub = g_in;
   a.add = g_out;  // holds g_pre until the ReLU below
   a.relu = relu;
   a.dst = y;
   a.wmap = nullptr;
   a.nrows = rb->a_out;
   a.K = rb->K;
-  a.TM = pick_tm();
-  scn_status rc = launch_gather(a, st);
+  rc = launch_gather(a, st);
   if (rc) return rc;
   if (relu) {
     hipLaunchKernelGGL(relu_vec_kernel, dim3((unsigned)ceil_div(Cout, 256)), dim3(256), 0, st,
@@ -550,6 +823,8 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
   float* S = reinterpret_cast<float*>(base + L.o_S);
   float* u0 = reinterpret_cast<float*>(base + L.o_u0);
   float* T = reinterpret_cast<float*>(base + L.o_T);
+  float* wpack = reinterpret_cast<float*>(base + L.o_wp);
+  float* gzero = reinterpret_cast<float*>(base + L.o_gz);
   const int K = rb->K;
 
   // dȳ and S (column sums over active outputs)
@@ -558,7 +833,7 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
                        rb->a_out, Cout, dyb, partS);
     SCN_LAUNCH_CHECK();
   }
-  hipLaunchKernelGGL(finish_vec_kernel, dim3((unsigned)ceil_div(Cout, 64)), dim3(64), 0, st,
+  hipLaunchKernelGGL(finish_vec_kernel, dim3((unsigned)ceil_div(Cout, 64)), dim3(1024), 0, st,
                      partS, rb->a_out > 0 ? L.nblk : 0, Cout, g_out, dg_out, relu, S, u0, dbias);
   SCN_LAUNCH_CHECK();
 
@@ -570,21 +845,24 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
     a.aidx = rb->in_rank;
     a.tpos = rb->itile;
     a.ntile = rb->n_itiles;
-    a.W = W;
-    a.ks = (int64_t)Cin * Cout;
-    a.sj = 1;      // reduction index j = output channel
-    a.sn = Cout;   // result column n = input channel
+    const int RkP = (int)ceil_div(Cout, 16) * 16, NcP = (int)ceil_div(Cin, 64) * 64;
+    hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)ceil_div((int64_t)K * NcP * RkP, 256)),
+                       dim3(256), 0, st, W, K, Cin, Cout, 0, RkP, NcP, wpack);
+    SCN_LAUNCH_CHECK();
+    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)ceil_div((int64_t)K * NcP, 256)), dim3(256), 0,
+                       st, gzero, (int64_t)K * NcP);
+    SCN_LAUNCH_CHECK();
+    a.Wp = wpack;  // W_k(j = output channel, n = input channel) = W[k][n][j]
+    a.gwp = gzero;
+    a.NcP = NcP;
     a.Rk = Cout;
-    a.RkP = (int)ceil_div(Cout, 16) * 16;
     a.Nc = Cin;
-    a.sub = nullptr;
     a.add = nullptr;
     a.relu = 0;
     a.dst = dx;
     a.wmap = rb->input_sorted ? nullptr : rb->perm;
     a.nrows = rb->a_in;
     a.K = K;
-    a.TM = pick_tm();
     scn_status rc = launch_gather(a, st);
     if (rc) return rc;
   }
@@ -598,16 +876,21 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
     d.in_rows = rb->in_rows;
     d.out_rows = rb->out_rows;
     d.off = rb->off_dev;
+    d.K = K;
     d.Cin = Cin;
     d.Cout = Cout;
+    d.nco = (int)ceil_div(Cout, 64);
+    d.nblk = (int)ceil_div(Cin, 64) * d.nco;
     d.chp = L.chp;
     d.maxc = L.maxc;
+    d.vec_ok = ((Cin & 3) == 0) && ((Cout & 3) == 0) &&
+               ((reinterpret_cast<uintptr_t>(x) & 15) == 0) &&
+               ((reinterpret_cast<uintptr_t>(dyb) & 15) == 0);
     d.part = part;
     d.partT = partT;
     if (rb->n_pairs > 0) {
-      const unsigned nz = (unsigned)(ceil_div(Cin, 64) * ceil_div(Cout, 64));
-      hipLaunchKernelGGL(dw_partial_kernel, dim3((unsigned)L.maxc, (unsigned)K, nz), dim3(NT), 0,
-                         st, d);
+      const int64_t nwg = L.maxc * K * d.nblk;
+      hipLaunchKernelGGL(dw_partial_kernel, dim3((unsigned)nwg), dim3(NT), 0, st, d);
       SCN_LAUNCH_CHECK();
     }
     const int64_t nred = std::max<int64_t>((int64_t)K * Cin * Cout, (int64_t)K * Cout);
@@ -615,8 +898,8 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
                        part, partT, rb->off_dev, K, Cin, Cout, L.chp, L.maxc, g_in, u0, dW, T);
     SCN_LAUNCH_CHECK();
     if (dg_in) {
-      hipLaunchKernelGGL(dgin_kernel, dim3((unsigned)ceil_div(Cin, 64)), dim3(64), 0, st, W, u0,
-                         T, K, Cin, Cout, dg_in);
+      hipLaunchKernelGGL(dgin_kernel, dim3((unsigned)Cin), dim3(256), 0, st, W, u0, T, K, Cin,
+                         Cout, dg_in);
       SCN_LAUNCH_CHECK();
     }
   }

@@ -8,7 +8,7 @@
 #include <cstdio>
 #include <string>
 
-#include "../../include/scn.h"
+#include "scn.h"
 
 namespace scn {
 
