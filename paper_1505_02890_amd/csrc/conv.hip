@@ -136,68 +136,22 @@ struct GatherArgs {
   int dvec_ok;           // rows of dst are 16-byte aligned and Nc % 4 == 0
 };
 
-// One pipeline stage covers 32 consecutive pairs of one offset: two 16-pair
-// blocks.  Lane (n16, q) gathers channels 16t + 4q .. +3 of pair n16 of each
-// block, which is the B-operand layout of v_mfma_f32_16x16x4f32 when the
-// contraction is computed transposed (R^T = W_k^T X^T): the result then holds
-// pair n16, output columns 4q .. 4q+3 of the wave's 16 in one lane, so the
-// lane scatters one contiguous float4 into its own pair's accumulator row.
-template <int NKT>
-struct XFrag {
-  float4 x0[NKT], x1[NKT];
-};
+// One pipeline stage covers 32 consecutive pairs of one offset (two 16-pair
+// blocks).  The work-group gathers the stage's 32 rows once into an LDS
+// buffer (8 threads per row, float4 loads, issued one stage ahead); each wave
+// then reads MFMA fragments from LDS: lane (n16, q) takes channels
+// 16t + 4q .. +3 of pair n16 of each block, which is the B-operand layout of
+// v_mfma_f32_16x16x4f32 when the contraction is computed transposed
+// (R^T = W_k^T X^T).  The result holds pair n16, output columns 4q .. 4q+3 of
+// the wave's 16 in one lane, so the lane adds one contiguous float4 into its
+// pair's accumulator row.
+constexpr int SROWS = 32;  // pairs per stage
 
 template <int NKT>
 struct WFrag {
   float4 w[NKT];  // W_k(j = 16t + 4q + 0..3, column 16w + n16)
   float4 g;       // gw[k][16w + 4q .. +3]
 };
-
-// Indices of lane n16's pair in each block.  Positions past the range are
-// clamped to the range's last pair, so loads are unconditional and in bounds;
-// the scatter skips those rows.  No loaded value is masked, so loads stay in
-// flight until their use one stage later.
-struct Idx {
-  int g0, g1;  // gathered row
-  int i0, i1;  // tile-local accumulator row
-};
-
-__device__ inline Idx load_idx(const GatherArgs& a, int64_t p, int64_t e, int64_t row0, int n16) {
-  Idx r;
-  const int64_t c0 = min(p + n16, e - 1), c1 = min(p + 16 + n16, e - 1);
-  r.g0 = a.gidx[c0];
-  r.g1 = a.gidx[c1];
-  r.i0 = (int)(a.aidx[c0] - row0);
-  r.i1 = (int)(a.aidx[c1] - row0);
-  return r;
-}
-
-// Reduction slots j >= Rk read some channel of the same row; the matching W
-// entries are zero.
-template <int NKT, bool VEC>
-__device__ inline void load_x(const GatherArgs& a, const Idx& ix, int q, XFrag<NKT>& f) {
-  const float* p0 = a.src + (int64_t)ix.g0 * a.Rk;
-  const float* p1 = a.src + (int64_t)ix.g1 * a.Rk;
-#pragma unroll
-  for (int t = 0; t < NKT; ++t) {
-    const int c = 16 * t + 4 * q;
-    if (VEC) {
-      const int cc = c < a.Rk ? c : 0;
-      f.x0[t] = *reinterpret_cast<const float4*>(p0 + cc);
-      f.x1[t] = *reinterpret_cast<const float4*>(p1 + cc);
-    } else {
-      float e0[4], e1[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int cc = c + u < a.Rk ? c + u : 0;
-        e0[u] = p0[cc];
-        e1[u] = p1[cc];
-      }
-      f.x0[t] = make_float4(e0[0], e0[1], e0[2], e0[3]);
-      f.x1[t] = make_float4(e1[0], e1[1], e1[2], e1[3]);
-    }
-  }
-}
 
 // W_k(j, n) = Wp[(k*NcP + n)*RkP + j], zero-padded to RkP = 16*NKT rows and
 // NcP = 64*ceil(Nc/64) columns; gw is padded the same way.
@@ -209,24 +163,77 @@ __device__ inline void load_w(const GatherArgs& a, int k, int col, int cq, int q
   f.g = *reinterpret_cast<const float4*>(a.gwp + (int64_t)k * a.NcP + cq);
 }
 
+// Per-thread share of a stage's gather: row tid/8, channel quads
+// (tid%8) + 8u.  Positions past the range are clamped to the range's last
+// pair (loads stay in bounds; those rows are never scattered).  Reduction
+// slots j >= Rk read some channel of the row; the matching W entries are zero.
 template <int NKT>
-__device__ inline void mfma_scatter(const XFrag<NKT>& X, const WFrag<NKT>& B, const Idx& ix,
-                                    int64_t p, int64_t e, float* acc, int cq, int n16) {
+struct RowRegs {
+  static constexpr int NQ = (4 * NKT + 7) / 8;  // float4 per thread
+  float4 v[NQ];
+};
+
+template <int NKT, bool VEC>
+__device__ inline RowRegs<NKT> load_rows(const GatherArgs& a, int gi, int tid) {
+  RowRegs<NKT> R;
+  const float* rp = a.src + (int64_t)gi * a.Rk;
+  const int part = tid & 7;
+#pragma unroll
+  for (int u = 0; u < RowRegs<NKT>::NQ; ++u) {
+    const int c = 4 * (part + 8 * u);
+    if (VEC) {
+      const int cc = c < a.Rk ? c : 0;
+      R.v[u] = *reinterpret_cast<const float4*>(rp + cc);
+    } else {
+      float e[4];
+#pragma unroll
+      for (int z = 0; z < 4; ++z) e[z] = rp[c + z < a.Rk ? c + z : 0];
+      R.v[u] = make_float4(e[0], e[1], e[2], e[3]);
+    }
+  }
+  return R;
+}
+
+template <int NKT>
+__device__ inline void store_rows(float* xs, int tid, const RowRegs<NKT>& R) {
+  const int row = tid >> 3, part = tid & 7;
+#pragma unroll
+  for (int u = 0; u < RowRegs<NKT>::NQ; ++u) {
+    const int quad = part + 8 * u;
+    if (quad < 4 * NKT)
+      *reinterpret_cast<float4*>(xs + row * (16 * NKT + 4) + 4 * quad) = R.v[u];
+  }
+}
+
+template <int NKT, bool TWO>
+__device__ inline void mfma_scatter(const float* xs, const WFrag<NKT>& B, int i0, int i1,
+                                    int64_t p, int64_t e, float* acc, int cq, int n16, int q) {
+  constexpr int XLD = 16 * NKT + 4;
+  const float* r0 = xs + n16 * XLD + 4 * q;
+  const float* r1 = xs + (16 + n16) * XLD + 4 * q;
   v4f c0v = {0.f, 0.f, 0.f, 0.f}, c1v = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int t = 0; t < NKT; ++t) {
-    c0v = mfma4(B.w[t].x, X.x0[t].x, c0v);
-    c1v = mfma4(B.w[t].x, X.x1[t].x, c1v);
-    c0v = mfma4(B.w[t].y, X.x0[t].y, c0v);
-    c1v = mfma4(B.w[t].y, X.x1[t].y, c1v);
-    c0v = mfma4(B.w[t].z, X.x0[t].z, c0v);
-    c1v = mfma4(B.w[t].z, X.x1[t].z, c1v);
-    c0v = mfma4(B.w[t].w, X.x0[t].w, c0v);
-    c1v = mfma4(B.w[t].w, X.x1[t].w, c1v);
+    const float4 x0 = *reinterpret_cast<const float4*>(r0 + 16 * t);
+    c0v = mfma4(B.w[t].x, x0.x, c0v);
+    if (TWO) {
+      const float4 x1 = *reinterpret_cast<const float4*>(r1 + 16 * t);
+      c1v = mfma4(B.w[t].x, x1.x, c1v);
+      c0v = mfma4(B.w[t].y, x0.y, c0v);
+      c1v = mfma4(B.w[t].y, x1.y, c1v);
+      c0v = mfma4(B.w[t].z, x0.z, c0v);
+      c1v = mfma4(B.w[t].z, x1.z, c1v);
+      c0v = mfma4(B.w[t].w, x0.w, c0v);
+      c1v = mfma4(B.w[t].w, x1.w, c1v);
+    } else {
+      c0v = mfma4(B.w[t].y, x0.y, c0v);
+      c0v = mfma4(B.w[t].z, x0.z, c0v);
+      c0v = mfma4(B.w[t].w, x0.w, c0v);
+    }
   }
   // lane holds pair n16 of each block, columns cq .. cq+3 (tile-local)
   if (p + n16 < e) {
-    float4* r = reinterpret_cast<float4*>(&acc[ix.i0 * ACC_LD + cq]);
+    float4* r = reinterpret_cast<float4*>(&acc[i0 * ACC_LD + cq]);
     float4 v = *r;
     v.x += c0v[0] - B.g.x;
     v.y += c0v[1] - B.g.y;
@@ -234,8 +241,8 @@ __device__ inline void mfma_scatter(const XFrag<NKT>& X, const WFrag<NKT>& B, co
     v.w += c0v[3] - B.g.w;
     *r = v;
   }
-  if (p + 16 + n16 < e) {
-    float4* r = reinterpret_cast<float4*>(&acc[ix.i1 * ACC_LD + cq]);
+  if (TWO && p + 16 + n16 < e) {
+    float4* r = reinterpret_cast<float4*>(&acc[i1 * ACC_LD + cq]);
     float4 v = *r;
     v.x += c1v[0] - B.g.x;
     v.y += c1v[1] - B.g.y;
@@ -245,23 +252,32 @@ __device__ inline void mfma_scatter(const XFrag<NKT>& X, const WFrag<NKT>& B, co
   }
 }
 
-// Next stage after (k, p) within the tile: same offset 32 pairs on, else the
+// A stage position: offset k, pairs [p, min(p + 32, e)) of list k.
+struct Pos {
+  int k;
+  int64_t p, e;
+};
+
+// Next stage after `s` within the tile: same offset 32 pairs on, else the
 // first pair of the next non-empty offset; k == K when there is none.
-__device__ inline void advance(const GatherArgs& a, int64_t t0, int64_t t1, int& k, int64_t& p,
-                               int64_t& e) {
-  p += 32;
-  if (p < e) return;
-  for (++k; k < a.K; ++k) {
-    p = a.tpos[(int64_t)k * a.ntile + t0];
-    e = a.tpos[(int64_t)k * a.ntile + t1];
-    if (p < e) return;
+__device__ inline Pos advance(const GatherArgs& a, int64_t t0, int64_t t1, Pos s) {
+  s.p += SROWS;
+  if (s.p < s.e) return s;
+  for (++s.k; s.k < a.K; ++s.k) {
+    s.p = a.tpos[(int64_t)s.k * a.ntile + t0];
+    s.e = a.tpos[(int64_t)s.k * a.ntile + t1];
+    if (s.p < s.e) return s;
   }
+  return s;
 }
 
 template <int NKT, bool VEC, int TM, int MINB>
 __global__ void __launch_bounds__(NT, MINB) gather_mfma_kernel(GatherArgs a) {
-  extern __shared__ float acc[];  // [TM*TILE][ACC_LD]
+  extern __shared__ float smem[];
   constexpr int T = TM * TILE;
+  constexpr int XLD = 16 * NKT + 4;
+  float* acc = smem;                      // [T][ACC_LD]
+  float* xsb = smem + T * ACC_LD;         // [2][SROWS][XLD]
   const int tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int n16 = lane & 15, q = lane >> 4;
@@ -272,52 +288,67 @@ __global__ void __launch_bounds__(NT, MINB) gather_mfma_kernel(GatherArgs a) {
   const int c0 = blockIdx.y * CB;
   const int col = c0 + 16 * w + n16;  // W column this lane feeds into the A operand
   const int cq = 16 * w + 4 * q;      // tile-local columns this lane accumulates
-  const bool live = c0 + 16 * w < a.Nc;  // wave-uniform
+  const int lrow = tid >> 3;          // stage row this thread gathers
 
   for (int i = tid; i < T * ACC_LD / 4; i += NT)
     reinterpret_cast<float4*>(acc)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-  __syncthreads();
 
-  if (live) {
-    // first non-empty offset
-    int k = -1;
-    int64_t p = 0, e = 0;
-    advance(a, t0, t1, k, p, e);  // p = 32 >= e = 0 -> scans from k = 0
-    if (k < a.K) {
-      // pipeline: indices two stages ahead, gathered rows and W one stage
-      // ahead; past the last stage the loads repeat the last stage
-      int k1 = k;
-      int64_t p1 = p, e1 = e;
-      advance(a, t0, t1, k1, p1, e1);
-      Idx ix0 = load_idx(a, p, e, row0, n16);
-      Idx ix1 = k1 < a.K ? load_idx(a, p1, e1, row0, n16) : ix0;
-      XFrag<NKT> X;
-      WFrag<NKT> B;
-      load_x<NKT, VEC>(a, ix0, q, X);
-      load_w<NKT>(a, k, col, c0 + cq, q, B);
-      while (true) {
-        int k2 = k1;
-        int64_t p2 = p1, e2 = e1;
-        if (k1 < a.K) advance(a, t0, t1, k2, p2, e2);
-        const bool more = k1 < a.K, more2 = k2 < a.K;
-        const Idx ix2 = load_idx(a, more2 ? p2 : p, more2 ? e2 : e, row0, n16);
-        XFrag<NKT> Xn;
-        WFrag<NKT> Bn;
-        load_x<NKT, VEC>(a, ix1, q, Xn);
-        load_w<NKT>(a, more ? k1 : k, col, c0 + cq, q, Bn);
-        mfma_scatter<NKT>(X, B, ix0, p, e, acc, cq, n16);
-        if (!more) break;
-        X = Xn;
-        B = Bn;
-        ix0 = ix1;
-        ix1 = ix2;
-        k = k1;
-        p = p1;
-        e = e1;
-        k1 = k2;
-        p1 = p2;
-        e1 = e2;
-      }
+  // Work-group-uniform stage positions s .. s+3.  Loads for a position past
+  // the last stage use the last real stage instead (in bounds, never used).
+  Pos s0 = advance(a, t0, t1, Pos{-1, 0, 0});
+  if (s0.k < a.K) {
+    Pos s1 = advance(a, t0, t1, s0);
+    Pos s2 = s1.k < a.K ? advance(a, t0, t1, s1) : s1;
+    Pos last = s0;                             // last real stage seen so far
+    auto real = [&](const Pos x) -> Pos { return x.k < a.K ? x : last; };
+    if (s1.k < a.K) last = s1;
+    if (s2.k < a.K) last = s2;
+    auto gidx_of = [&](const Pos x) { const Pos r = real(x); return a.gidx[min(r.p + lrow, r.e - 1)]; };
+    auto aidx_of = [&](const Pos x, int off) {
+      const Pos r = real(x);
+      return (int)(a.aidx[min(r.p + off + n16, r.e - 1)] - row0);
+    };
+    int g2 = gidx_of(s2);                      // index of stage s+2's row
+    int i0 = aidx_of(s0, 0), j0 = aidx_of(s0, 16);
+    int i1 = aidx_of(s1, 0), j1 = aidx_of(s1, 16);
+    store_rows<NKT>(xsb, tid, load_rows<NKT, VEC>(a, gidx_of(s0), tid));
+    RowRegs<NKT> R = load_rows<NKT, VEC>(a, gidx_of(s1), tid);  // stage s+1 rows in flight
+    WFrag<NKT> B;
+    load_w<NKT>(a, s0.k, col, c0 + cq, q, B);
+    __syncthreads();
+    int buf = 0;
+    while (true) {
+      const bool more1 = s1.k < a.K;
+      const Pos s3 = s2.k < a.K ? advance(a, t0, t1, s2) : s2;
+      if (s3.k < a.K) last = s3;
+      float* xs_cur = xsb + buf * SROWS * XLD;
+      float* xs_nxt = xsb + (buf ^ 1) * SROWS * XLD;
+      // stage s+1 rows (loaded one step ago) -> the other LDS buffer
+      if (more1) store_rows<NKT>(xs_nxt, tid, R);
+      // issue: index of stage s+3, accumulator rows of stage s+2, rows of stage s+2
+      const int g3 = gidx_of(s3);
+      const int i2 = aidx_of(s2, 0), j2 = aidx_of(s2, 16);
+      R = load_rows<NKT, VEC>(a, g2, tid);
+      WFrag<NKT> Bn;
+      const bool kchange = more1 && s1.k != s0.k;
+      if (kchange) load_w<NKT>(a, s1.k, col, c0 + cq, q, Bn);
+      // a stage with at most 16 live pairs multiplies one block only
+      if (s0.e - s0.p > 16)
+        mfma_scatter<NKT, true>(xs_cur, B, i0, j0, s0.p, s0.e, acc, cq, n16, q);
+      else
+        mfma_scatter<NKT, false>(xs_cur, B, i0, j0, s0.p, s0.e, acc, cq, n16, q);
+      if (!more1) break;
+      if (kchange) B = Bn;
+      __syncthreads();
+      buf ^= 1;
+      g2 = g3;
+      i0 = i1;
+      j0 = j1;
+      i1 = i2;
+      j1 = j2;
+      s0 = s1;
+      s1 = s2;
+      s2 = s3;
     }
   }
   __syncthreads();
@@ -348,11 +379,15 @@ __global__ void __launch_bounds__(NT, MINB) gather_mfma_kernel(GatherArgs a) {
 
 typedef void (*GatherFn)(GatherArgs);
 
+// Tile rows (TM * 64) and work-groups per CU: the accumulators and the two
+// stage buffers must fit the 160 KB of LDS.  Reductions over more than 64
+// channels use 256-row tiles, one work-group per CU.
 template <int NKT>
 GatherFn pick_gather(int TM, bool vec) {
-  if (NKT > 4 || TM == 8) return vec ? gather_mfma_kernel<NKT, true, 8, 1>
-                                     : gather_mfma_kernel<NKT, false, 8, 1>;
+  if (NKT > 4) return vec ? gather_mfma_kernel<NKT, true, 4, 1> : gather_mfma_kernel<NKT, false, 4, 1>;
+  if (TM == 8) return vec ? gather_mfma_kernel<NKT, true, 8, 1> : gather_mfma_kernel<NKT, false, 8, 1>;
   if (TM == 2) return vec ? gather_mfma_kernel<NKT, true, 2, 4> : gather_mfma_kernel<NKT, false, 2, 4>;
+  if (TM == 1) return vec ? gather_mfma_kernel<NKT, true, 1, 4> : gather_mfma_kernel<NKT, false, 1, 4>;
   return vec ? gather_mfma_kernel<NKT, true, 4, 2> : gather_mfma_kernel<NKT, false, 4, 2>;
 }
 
@@ -381,8 +416,8 @@ int gather_tm() {
   static int tm = -1;
   if (tm < 0) {
     const char* e = getenv("SCN_GATHER_TM");
-    const int v = e ? atoi(e) : 4;
-    tm = (v == 2 || v == 8) ? v : 4;
+    const int v = e ? atoi(e) : 2;
+    tm = (v == 1 || v == 2 || v == 8) ? v : 4;
   }
   return tm;
 }
@@ -393,10 +428,11 @@ scn_status launch_gather(GatherArgs a, hipStream_t st) {
 
   a.dvec_ok = ((a.Nc & 3) == 0) && ((reinterpret_cast<uintptr_t>(a.dst) & 15) == 0);
   const int nkt = (int)ceil_div(a.Rk, 16);
-  const int TM = nkt > 4 ? 8 : gather_tm();
+  const int TM = nkt > 4 ? 4 : gather_tm();
   const int64_t nwg = ceil_div(a.ntile, TM);
   const unsigned ncb = (unsigned)ceil_div(a.Nc, CB);
-  const size_t smem = (size_t)TM * TILE * ACC_LD * sizeof(float);
+  const size_t smem =
+      ((size_t)TM * TILE * ACC_LD + 2 * (size_t)SROWS * (16 * nkt + 4)) * sizeof(float);
   const bool vec = a.vec_ok;
   GatherFn fn = gather_fn(nkt, TM, vec);
   static bool attr_done[9][2][17] = {};
