@@ -40,13 +40,35 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    p.add_argument("--cpu-sites", type=int, default=16000,
+    p.add_argument("--cpu-sites", type=int, default=60000,
                    help="input sites of the bounded CPU-oracle sample")
     return p.parse_args()
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def measured_traffic():
+    """HBM bytes per launch of the forward contraction from the committed
+    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, each scaled by the
+    same counter's reading for a device copy of known size), or None when the
+    kernel source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gather_fwd_1M_traffic.txt")
+    src = os.path.join(ROOT, "paper_1505_02890_amd", "csrc", "conv.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if line.startswith("#") or ":" not in line:
+            continue
+        k, v = line.split(":", 1)
+        kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if kv.get("conv_hip_sha256") != sha:
+        return None
+    return float(kv["traffic_bytes"])
 
 
 def cpu_baseline(cfg, n_sites: int):
@@ -185,7 +207,7 @@ def main():
     pool_bwd_bytes = 5.0 * prb.a_out * C + 4.0 * prb.a_in * C + 8.0 * prb.n_pairs
 
     # a plain device copy of known size (calibrates the HBM byte counters)
-    cal = torch.empty(64 << 20, dtype=torch.float32, device=dev)
+    cal = torch.full((64 << 20,), 1.0, dtype=torch.float32, device=dev)
     cal2 = torch.empty_like(cal)
     cal2.copy_(cal)
     torch.cuda.synchronize()
@@ -223,7 +245,7 @@ def main():
             "peak": MFMA_FP32_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_FP32_PEAK_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(),
         },
         "pool": {
             "a_in": prb.a_in, "a_out": prb.a_out, "channels": C,
