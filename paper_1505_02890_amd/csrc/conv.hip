@@ -509,9 +509,16 @@ __global__ void __launch_bounds__(1024) finish_vec_kernel(const float* __restric
   }
 }
 
-// Weight gradient partials.
+// Weight gradient partials.  A work-group accumulates one 64x64 block of
+// dW_k = sum_pairs (x[r] - g_in)^T dy[o] over a fixed chunk of list k, 64 pairs
+// per stage.  The stage is stored transposed in LDS ([channel][pair]) so that
+// MFMA fragments along the pair axis are single ds_read_b128s.  Thread
+// (channel c = tid % 64, pair quad group w = tid / 64) loads channel c of 16
+// pairs: every wave-wide load reads 64 consecutive channels of one row (two
+// cache lines), and each 4 pairs of one channel leave as one ds_write_b128.
+// Pair indices are staged through LDS two stages ahead, rows one stage ahead.
 constexpr int DW_SC = 64;          // pairs per stage
-constexpr int DW_LD = DW_SC + 4;
+constexpr int DW_LD = DW_SC + 4;   // pitch of a channel row (floats)
 
 struct DwArgs {
   const float* x;        // [a_in][Cin]
@@ -526,54 +533,33 @@ struct DwArgs {
   int nblk;              // (Cin blocks) * nco
   int64_t chp;           // pairs per chunk
   int64_t maxc;          // chunks per offset (slot count)
-  int vec_ok;            // x and dyb rows 16-byte aligned, Cin and Cout % 4 == 0
   float* part;           // [K][maxc][Cin][Cout]
   float* partT;          // [K][maxc][Cout]
 };
 
-// Rows of one stage: thread (pair pr = tid & 63, quads c4 = 4*(w + 4*i), i < 4)
-struct DwRegs {
-  float4 x[4], d[4];
+// channel c of pairs 4*(w + 4v) + u, v < 4, u < 4 of a stage
+struct DwRows {
+  float x[16], d[16];
 };
 
-__device__ inline void dw_load(const DwArgs& a, int64_t p0, int n, int ci0, int co0, int pr, int w,
-                               DwRegs& R) {
-  const bool v = pr < n;
-  const int64_t ri = v ? a.in_rows[p0 + pr] : 0, ro = v ? a.out_rows[p0 + pr] : 0;
-  const float* xp = a.x + ri * a.Cin + ci0;
-  const float* dp = a.dyb + ro * a.Cout + co0;
+__device__ inline void dw_rows(const DwArgs& a, const int* ix, const int* io, int cx, int cd,
+                               int w, DwRows& R) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c4 = 4 * (w + 4 * i);
-    float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), dv = xv;
-    if (v) {
-      if (a.vec_ok && ci0 + c4 + 3 < a.Cin) {
-        xv = *reinterpret_cast<const float4*>(xp + c4);
-      } else {
-        float e[4];
+  for (int v = 0; v < 4; ++v)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) e[u] = ci0 + c4 + u < a.Cin ? xp[c4 + u] : 0.f;
-        xv = make_float4(e[0], e[1], e[2], e[3]);
-      }
-      if (a.vec_ok && co0 + c4 + 3 < a.Cout) {
-        dv = *reinterpret_cast<const float4*>(dp + c4);
-      } else {
-        float e[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) e[u] = co0 + c4 + u < a.Cout ? dp[c4 + u] : 0.f;
-        dv = make_float4(e[0], e[1], e[2], e[3]);
-      }
+    for (int u = 0; u < 4; ++u) {
+      const int pr = 4 * (w + 4 * v) + u;
+      R.x[4 * v + u] = a.x[(int64_t)ix[pr] * a.Cin + cx];
+      R.d[4 * v + u] = a.dyb[(int64_t)io[pr] * a.Cout + cd];
     }
-    R.x[i] = xv;
-    R.d[i] = dv;
-  }
 }
 
 __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
-  __shared__ float xsT[64 * DW_LD];  // [ci][pair]
+  __shared__ float xsT[64 * DW_LD];  // [ci][pair], x - g_in
   __shared__ float dsT[64 * DW_LD];  // [co][pair]
-  __shared__ float gsub[64];
-  // flattened (chunk, offset, block) work item, offsets fastest, XCD-contiguous
+  __shared__ int idx[2][2][DW_SC];   // [buffer][input row, output row][pair]
+  // flattened (chunk, offset, block) work item, blocks then offsets fastest,
+  // contiguous per XCD
   const int64_t item = xcd_remap(blockIdx.x, gridDim.x);
   const int blk = (int)(item % a.nblk);
   const int64_t ck = item / a.nblk;
@@ -586,38 +572,55 @@ __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
   const int ci0 = (blk / a.nco) * 64, co0 = (blk % a.nco) * 64;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n16 = lane & 15, q = lane >> 4;
-  if (tid < 64) gsub[tid] = ci0 + tid < a.Cin ? a.g_in[ci0 + tid] : 0.f;
+  // this thread's channel of each operand (clamped into the layer; zeroed on store)
+  const int ch = lane;
+  const bool xin = ci0 + ch < a.Cin, din = co0 + ch < a.Cout;
+  const int cx = xin ? ci0 + ch : 0, cd = din ? co0 + ch : 0;
+  const float gsub = xin ? a.g_in[cx] : 0.f;
+
+  // index loaders: threads 0..63 input rows, 64..127 output rows of one stage
+  auto load_index = [&](int64_t p0) -> int {
+    const int64_t pp = min(p0 + (tid & 63), p_end - 1);
+    return tid < 64 ? a.in_rows[pp] : a.out_rows[pp];
+  };
+  if (tid < 128) {
+    idx[0][tid >> 6][tid & 63] = load_index(p_begin);
+    idx[1][tid >> 6][tid & 63] = load_index(p_begin + DW_SC);
+  }
+  __syncthreads();
+  DwRows R;
+  dw_rows(a, idx[0][0], idx[0][1], cx, cd, w, R);
 
   v4f acc[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = (v4f){0.f, 0.f, 0.f, 0.f};
   float tsum = 0.f;
   const int tcol = 16 * w + n16;
-  const int pr = tid & 63;
 
-  DwRegs R;
-  dw_load(a, p_begin, (int)min<int64_t>(DW_SC, p_end - p_begin), ci0, co0, pr, w, R);
-  __syncthreads();  // gsub ready
+  int buf = 0;
   for (int64_t p0 = p_begin; p0 < p_end; p0 += DW_SC) {
     const int n = (int)min<int64_t>(DW_SC, p_end - p0);
-    // registers -> LDS (transposed); x rows shifted by the ground state
+    // stage rows -> LDS, transposed; pairs past the chunk and channels past
+    // the layer are zero; x is shifted by the ground state
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c4 = 4 * (w + 4 * i);
-      const bool v = pr < n;
-      xsT[(c4 + 0) * DW_LD + pr] = v ? R.x[i].x - gsub[c4 + 0] : 0.f;
-      xsT[(c4 + 1) * DW_LD + pr] = v ? R.x[i].y - gsub[c4 + 1] : 0.f;
-      xsT[(c4 + 2) * DW_LD + pr] = v ? R.x[i].z - gsub[c4 + 2] : 0.f;
-      xsT[(c4 + 3) * DW_LD + pr] = v ? R.x[i].w - gsub[c4 + 3] : 0.f;
-      dsT[(c4 + 0) * DW_LD + pr] = R.d[i].x;
-      dsT[(c4 + 1) * DW_LD + pr] = R.d[i].y;
-      dsT[(c4 + 2) * DW_LD + pr] = R.d[i].z;
-      dsT[(c4 + 3) * DW_LD + pr] = R.d[i].w;
+    for (int v = 0; v < 4; ++v) {
+      const int pb = 4 * (w + 4 * v);
+      float xe[4], de[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool live = pb + u < n;
+        xe[u] = (live && xin) ? R.x[4 * v + u] - gsub : 0.f;
+        de[u] = (live && din) ? R.d[4 * v + u] : 0.f;
+      }
+      *reinterpret_cast<float4*>(&xsT[ch * DW_LD + pb]) = make_float4(xe[0], xe[1], xe[2], xe[3]);
+      *reinterpret_cast<float4*>(&dsT[ch * DW_LD + pb]) = make_float4(de[0], de[1], de[2], de[3]);
     }
+    int nidx = 0;
+    if (tid < 128) nidx = load_index(p0 + 2 * DW_SC);  // stage s+2 indices in flight
     __syncthreads();
-    // prefetch the next stage into registers while the matrix cores work
-    const int64_t pn = p0 + DW_SC;
-    if (pn < p_end) dw_load(a, pn, (int)min<int64_t>(DW_SC, p_end - pn), ci0, co0, pr, w, R);
+    // stage s+1 rows while the matrix cores work on stage s
+    dw_rows(a, idx[buf ^ 1][0], idx[buf ^ 1][1], cx, cd, w, R);
+    // A(m = ci, kk = pair) = xsT[16w + m][pair];  B(kk = pair, n = co) = dsT[16j + n][pair]
     const float* ar = xsT + (16 * w + n16) * DW_LD + 4 * q;
 #pragma unroll
     for (int t = 0; t < DW_SC / 16; ++t) {
@@ -641,6 +644,8 @@ __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
         tsum += ((v.x + v.y) + v.z) + v.w;
       }
     }
+    if (tid < 128) idx[buf][tid >> 6][tid & 63] = nidx;  // stage s's slot is free
+    buf ^= 1;
     __syncthreads();
   }
   // write partial dW: lane holds rows 4q + v (ci), column n16 of tile j (co)
@@ -919,9 +924,6 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
     d.nblk = (int)ceil_div(Cin, 64) * d.nco;
     d.chp = L.chp;
     d.maxc = L.maxc;
-    d.vec_ok = ((Cin & 3) == 0) && ((Cout & 3) == 0) &&
-               ((reinterpret_cast<uintptr_t>(x) & 15) == 0) &&
-               ((reinterpret_cast<uintptr_t>(dyb) & 15) == 0);
     d.part = part;
     d.partT = partT;
     if (rb->n_pairs > 0) {
