@@ -31,7 +31,8 @@
  *  - All pointers named x, y, W, g_*, d*, coords, argmax are DEVICE pointers
  *    owned by the caller and never retained.  Host pointers are marked "host".
  *  - Calls are asynchronous on the given HIP stream unless stated otherwise;
- *    only scn_rulebook_build synchronises (once, to read back the sizes).
+ *    only scn_rulebook_build synchronises (twice: to read back the number of
+ *    output sites, then the per-offset list boundaries).
  *  - No call allocates the caller's outputs.  Status codes are returned; no
  *    exception crosses the ABI.  scn_last_error() gives a message for the last
  *    failing call on the calling thread.
@@ -92,7 +93,7 @@ typedef struct scn_rulebook_info {
  *  n       number of active input sites (>= 0; 0 gives an empty rulebook).
  *  grid    host int64[4] = (B, mx, my, mz), all >= 1.
  *  filter  f in {1, 2, 3};  stride s >= 1 (s <= f not required).
- *  stream  HIP stream for all device work; the call synchronises it once.
+ *  stream  HIP stream for all device work; the call synchronises it twice.
  *  out     receives a library-owned rulebook, freed by scn_rulebook_free.
  *
  * Output ordering is canonical: output rows ascend by key, and each

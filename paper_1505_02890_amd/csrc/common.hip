@@ -17,9 +17,27 @@ void set_error(const char* fmt, ...) {
 
 void clear_error() { g_err[0] = 0; }
 
+// The default stream-ordered pool returns freed memory to the driver at every
+// synchronisation unless its release threshold is raised; the rulebook build
+// synchronises, so without this every build would re-allocate from scratch.
+// Memory freed into the pool stays reserved for the process's later calls.
+static void keep_pool_memory() {
+  static bool done[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64 || done[dev]) return;
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+    uint64_t keep = UINT64_MAX;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+  }
+  (void)hipGetLastError();
+  done[dev] = true;
+}
+
 scn_status dalloc(void** p, size_t bytes, hipStream_t s) {
   *p = nullptr;
   if (bytes == 0) return SCN_OK;
+  keep_pool_memory();
   hipError_t e = hipMallocAsync(p, bytes, s);
   if (e != hipSuccess) {
     (void)hipGetLastError();

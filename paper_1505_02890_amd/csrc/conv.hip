@@ -380,46 +380,39 @@ __global__ void __launch_bounds__(NT, MINB) gather_mfma_kernel(GatherArgs a) {
 typedef void (*GatherFn)(GatherArgs);
 
 // Tile rows (TM * 64) and work-groups per CU: the accumulators and the two
-// stage buffers must fit the 160 KB of LDS.  Reductions over more than 64
-// channels use 256-row tiles, one work-group per CU.
+// stage buffers must fit the 160 KB of LDS.  Reductions over up to 64
+// channels use 128-row tiles (several work-groups per CU hide the gather
+// latency); longer reductions use 256-row tiles, one work-group per CU.
 template <int NKT>
-GatherFn pick_gather(int TM, bool vec) {
-  if (NKT > 4) return vec ? gather_mfma_kernel<NKT, true, 4, 1> : gather_mfma_kernel<NKT, false, 4, 1>;
-  if (TM == 8) return vec ? gather_mfma_kernel<NKT, true, 8, 1> : gather_mfma_kernel<NKT, false, 8, 1>;
-  if (TM == 2) return vec ? gather_mfma_kernel<NKT, true, 2, 4> : gather_mfma_kernel<NKT, false, 2, 4>;
-  if (TM == 1) return vec ? gather_mfma_kernel<NKT, true, 1, 4> : gather_mfma_kernel<NKT, false, 1, 4>;
-  return vec ? gather_mfma_kernel<NKT, true, 4, 2> : gather_mfma_kernel<NKT, false, 4, 2>;
+constexpr int gather_tm() {
+  return NKT > 4 ? 4 : 2;
 }
 
-GatherFn gather_fn(int nkt, int TM, bool vec) {
+template <int NKT>
+GatherFn pick_gather(bool vec) {
+  constexpr int TM = gather_tm<NKT>(), MINB = NKT > 4 ? 1 : 4;
+  return vec ? gather_mfma_kernel<NKT, true, TM, MINB> : gather_mfma_kernel<NKT, false, TM, MINB>;
+}
+
+GatherFn gather_fn(int nkt, bool vec) {
   switch (nkt) {
-    case 1: return pick_gather<1>(TM, vec);
-    case 2: return pick_gather<2>(TM, vec);
-    case 3: return pick_gather<3>(TM, vec);
-    case 4: return pick_gather<4>(TM, vec);
-    case 5: return pick_gather<5>(TM, vec);
-    case 6: return pick_gather<6>(TM, vec);
-    case 7: return pick_gather<7>(TM, vec);
-    case 8: return pick_gather<8>(TM, vec);
-    case 9: return pick_gather<9>(TM, vec);
-    case 10: return pick_gather<10>(TM, vec);
-    case 11: return pick_gather<11>(TM, vec);
-    case 12: return pick_gather<12>(TM, vec);
-    case 13: return pick_gather<13>(TM, vec);
-    case 14: return pick_gather<14>(TM, vec);
-    case 15: return pick_gather<15>(TM, vec);
-    default: return pick_gather<16>(TM, vec);
+    case 1: return pick_gather<1>(vec);
+    case 2: return pick_gather<2>(vec);
+    case 3: return pick_gather<3>(vec);
+    case 4: return pick_gather<4>(vec);
+    case 5: return pick_gather<5>(vec);
+    case 6: return pick_gather<6>(vec);
+    case 7: return pick_gather<7>(vec);
+    case 8: return pick_gather<8>(vec);
+    case 9: return pick_gather<9>(vec);
+    case 10: return pick_gather<10>(vec);
+    case 11: return pick_gather<11>(vec);
+    case 12: return pick_gather<12>(vec);
+    case 13: return pick_gather<13>(vec);
+    case 14: return pick_gather<14>(vec);
+    case 15: return pick_gather<15>(vec);
+    default: return pick_gather<16>(vec);
   }
-}
-
-int gather_tm() {
-  static int tm = -1;
-  if (tm < 0) {
-    const char* e = getenv("SCN_GATHER_TM");
-    const int v = e ? atoi(e) : 2;
-    tm = (v == 1 || v == 2 || v == 8) ? v : 4;
-  }
-  return tm;
 }
 
 scn_status launch_gather(GatherArgs a, hipStream_t st) {
@@ -428,15 +421,15 @@ scn_status launch_gather(GatherArgs a, hipStream_t st) {
 
   a.dvec_ok = ((a.Nc & 3) == 0) && ((reinterpret_cast<uintptr_t>(a.dst) & 15) == 0);
   const int nkt = (int)ceil_div(a.Rk, 16);
-  const int TM = nkt > 4 ? 4 : gather_tm();
+  const int TM = nkt > 4 ? gather_tm<5>() : gather_tm<1>();
   const int64_t nwg = ceil_div(a.ntile, TM);
   const unsigned ncb = (unsigned)ceil_div(a.Nc, CB);
   const size_t smem =
       ((size_t)TM * TILE * ACC_LD + 2 * (size_t)SROWS * (16 * nkt + 4)) * sizeof(float);
   const bool vec = a.vec_ok;
-  GatherFn fn = gather_fn(nkt, TM, vec);
-  static bool attr_done[9][2][17] = {};
-  bool& done = attr_done[TM][vec][nkt];
+  GatherFn fn = gather_fn(nkt, vec);
+  static bool attr_done[2][17] = {};
+  bool& done = attr_done[vec][nkt];
   if (!done) {
     SCN_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));

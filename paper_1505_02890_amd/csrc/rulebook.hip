@@ -137,41 +137,58 @@ __global__ void __launch_bounds__(256) perm_kernel(const int32_t* __restrict__ c
   perm[rank] = (int32_t)i;
 }
 
+// Output word wo of the output grid -> (b, z, y, word-in-row).  32-bit:
+// bitmaps hold at most 2^26 words.
+struct WordPos {
+  int b, z, y, wx;
+};
+
+__device__ inline WordPos word_pos(int wo, const GridDev& g) {
+  WordPos p;
+  p.wx = wo % g.rw;
+  int r = wo / g.rw;
+  p.y = r % g.my;
+  r /= g.my;
+  p.z = r % g.mz;
+  p.b = r / g.mz;
+  return p;
+}
+
 // ---- phase 4: output occupancy (dilation of the input bitmap) -------------
+// SM: 1 stride 1 (funnel shifts), 2 stride 2 (even-bit compression), 0 any.
+template <int F, int SM>
 __global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict__ inb, GridDev gi,
                                                      uint32_t* __restrict__ outb, GridDev go,
-                                                     int64_t nw_out, int f, int s) {
-  const int64_t wo = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+                                                     int nw_out, int s) {
+  const int wo = blockIdx.x * blockDim.x + threadIdx.x;
   if (wo >= nw_out) return;
-  const int wx = (int)(wo % go.rw);
-  int64_t r = wo / go.rw;
-  const int64_t y = r % go.my;
-  r /= go.my;
-  const int64_t z = r % go.mz;
-  const int64_t b = r / go.mz;
-  const int x0 = wx * 32;
+  const WordPos wp = word_pos(wo, go);
+  const int x0 = wp.wx * 32;
   const int nvalid = min(32, go.mx - x0);
   const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
   uint32_t v = 0;
-  for (int kz = 0; kz < f; ++kz)
-    for (int ky = 0; ky < f; ++ky) {
-      const int64_t base = row_base(gi, b, s * y + ky, s * z + kz);
-      if (s == 1) {
-        for (int kx = 0; kx < f; ++kx) v |= extract32(inb, base, gi.rw, (int64_t)x0 + kx);
-      } else if (s == 2) {
+#pragma unroll
+  for (int kz = 0; kz < F; ++kz)
+#pragma unroll
+    for (int ky = 0; ky < F; ++ky) {
+      const int64_t base = row_base(gi, wp.b, (int64_t)s * wp.y + ky, (int64_t)s * wp.z + kz);
+      if (SM == 1) {
+#pragma unroll
+        for (int kx = 0; kx < F; ++kx) v |= extract32(inb, base, gi.rw, (int64_t)x0 + kx);
+      } else if (SM == 2) {
         const int64_t p = 2 * (int64_t)x0;  // multiple of 64
         const uint64_t lo = extract32(inb, base, gi.rw, p);
         const uint64_t hi = extract32(inb, base, gi.rw, p + 32);
         const uint64_t w64 = lo | (hi << 32);
         uint64_t t = w64;
-        if (f >= 2) t |= w64 >> 1;
-        if (f >= 3) {
+        if (F >= 2) t |= w64 >> 1;
+        if (F >= 3) {
           const uint64_t nx = extract32(inb, base, gi.rw, p + 64) & 1u;
           t |= (w64 >> 2) | (nx << 62);
         }
         v |= compress_even(t);
       } else {
-        const uint32_t fm = (1u << f) - 1u;
+        constexpr uint32_t fm = (1u << F) - 1u;
         for (int j = 0; j < nvalid; ++j)
           if (extract32(inb, base, gi.rw, (int64_t)s * (x0 + j)) & fm) v |= 1u << j;
       }
@@ -180,41 +197,43 @@ __global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict_
 }
 
 // ---- phase 6: output coordinates and neighbour masks ----------------------
+template <int F, bool S1>
 __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restrict__ inb, GridDev gi,
                                                         const uint32_t* __restrict__ outb,
                                                         const uint32_t* __restrict__ opref,
-                                                        GridDev go, int64_t nw_out, int f, int s,
+                                                        GridDev go, int nw_out, int s,
                                                         int32_t* __restrict__ out_coords,
                                                         uint32_t* __restrict__ masks) {
-  const int64_t wo = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  constexpr int K = F * F * F;
+  const int wo = blockIdx.x * blockDim.x + threadIdx.x;
   if (wo >= nw_out) return;
   uint32_t v = outb[wo];
   if (!v) return;
-  const int wx = (int)(wo % go.rw);
-  int64_t r = wo / go.rw;
-  const int64_t y = r % go.my;
-  r /= go.my;
-  const int64_t z = r % go.mz;
-  const int64_t b = r / go.mz;
-  const int x0 = wx * 32;
-  const int K = f * f * f;
+  const WordPos wp = word_pos(wo, go);
+  const int x0 = wp.wx * 32;
   uint32_t rank = opref[wo];
-  if (s == 1) {
+  if (S1) {
     // E[k] bit j: input site (x0 + j + kx, y + ky, z + kz) is active
-    uint32_t E[MAX_K];
-    for (int kz = 0; kz < f; ++kz)
-      for (int ky = 0; ky < f; ++ky) {
-        const int64_t base = row_base(gi, b, y + ky, z + kz);
-        for (int kx = 0; kx < f; ++kx)
-          E[(kz * f + ky) * f + kx] = extract32(inb, base, gi.rw, (int64_t)x0 + kx);
+    uint32_t E[K];
+#pragma unroll
+    for (int kz = 0; kz < F; ++kz)
+#pragma unroll
+      for (int ky = 0; ky < F; ++ky) {
+        const int64_t base = row_base(gi, wp.b, wp.y + ky, wp.z + kz);
+        const int64_t w = x0 >> 5;
+        const uint32_t lo = w < gi.rw ? inb[base + w] : 0u;
+        const uint32_t hi = w + 1 < gi.rw ? inb[base + w + 1] : 0u;
+#pragma unroll
+        for (int kx = 0; kx < F; ++kx)
+          E[(kz * F + ky) * F + kx] = kx ? (lo >> kx) | (hi << (32 - kx)) : lo;
       }
     while (v) {
       const int j = __builtin_ctz(v);
       v &= v - 1;
       uint32_t m = 0;
+#pragma unroll
       for (int k = 0; k < K; ++k) m |= ((E[k] >> j) & 1u) << k;
-      reinterpret_cast<int4*>(out_coords)[rank] =
-          make_int4((int)b, x0 + j, (int)y, (int)z);
+      reinterpret_cast<int4*>(out_coords)[rank] = make_int4(wp.b, x0 + j, wp.y, wp.z);
       masks[rank] = m;
       ++rank;
     }
@@ -224,14 +243,16 @@ __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restri
       v &= v - 1;
       const int64_t xi = (int64_t)s * (x0 + j);
       uint32_t m = 0;
-      for (int kz = 0; kz < f; ++kz)
-        for (int ky = 0; ky < f; ++ky) {
-          const int64_t base = row_base(gi, b, s * y + ky, s * z + kz);
+#pragma unroll
+      for (int kz = 0; kz < F; ++kz)
+#pragma unroll
+        for (int ky = 0; ky < F; ++ky) {
+          const int64_t base = row_base(gi, wp.b, (int64_t)s * wp.y + ky, (int64_t)s * wp.z + kz);
           const uint32_t bits = extract32(inb, base, gi.rw, xi);
-          for (int kx = 0; kx < f; ++kx) m |= ((bits >> kx) & 1u) << ((kz * f + ky) * f + kx);
+#pragma unroll
+          for (int kx = 0; kx < F; ++kx) m |= ((bits >> kx) & 1u) << ((kz * F + ky) * F + kx);
         }
-      reinterpret_cast<int4*>(out_coords)[rank] =
-          make_int4((int)b, x0 + j, (int)y, (int)z);
+      reinterpret_cast<int4*>(out_coords)[rank] = make_int4(wp.b, x0 + j, wp.y, wp.z);
       masks[rank] = m;
       ++rank;
     }
@@ -240,17 +261,21 @@ __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restri
 
 // ---- phase 7: pairs per (offset, output tile) ------------------------------
 // one wave per tile of 64 output rows; cnt[k * nt + t]
+template <int K>
 __global__ void __launch_bounds__(256) tile_count_kernel(const uint32_t* __restrict__ masks,
-                                                         int64_t a_out, int64_t nt, int K,
+                                                         int64_t a_out, int64_t nt,
                                                          uint64_t* __restrict__ cnt) {
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t t = o >> 6;
   const uint32_t m = o < a_out ? masks[o] : 0u;
   const int lane = threadIdx.x & 63;
+  uint64_t c = 0;
+#pragma unroll
   for (int k = 0; k < K; ++k) {
-    const uint64_t bal = __ballot((m >> k) & 1u);
-    if (lane == 0 && t < nt) cnt[k * nt + t] = (uint64_t)__popcll(bal);
+    const uint64_t n = (uint64_t)__popcll(__ballot((m >> k) & 1u));
+    if (lane == k) c = n;
   }
+  if (lane < K && t < nt) cnt[lane * nt + t] = c;
 }
 
 // ---- phase 8b: list boundaries off[k] = position of (k, tile 0) -----------
@@ -261,41 +286,53 @@ __global__ void list_offsets_kernel(const uint64_t* __restrict__ pos, int64_t nt
 }
 
 // ---- phase 9: emit the pair lists ------------------------------------------
+// One thread per output, one wave per tile.  All K rank lookups are issued
+// before any dependent load so they overlap.
+template <int F>
 __global__ void __launch_bounds__(256) emit_pairs_kernel(
     const uint32_t* __restrict__ masks, const int32_t* __restrict__ out_coords, int64_t a_out,
-    int64_t nt, int f, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
+    int64_t nt, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
     GridDev gi, const int32_t* __restrict__ perm, const uint64_t* __restrict__ pos,
     int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows, int32_t* __restrict__ in_rank,
     int32_t* __restrict__ nbr, int32_t* __restrict__ inv) {
+  constexpr int K = F * F * F;
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t t = o >> 6;
   const bool live = o < a_out;
   const uint32_t m = live ? masks[o] : 0u;
   int4 c = make_int4(0, 0, 0, 0);
   if (live) c = reinterpret_cast<const int4*>(out_coords)[o];
-  const int K = f * f * f;
+  uint32_t rank[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int kx = k % F, ky = (k / F) % F, kz = k / (F * F);
+    const int64_t xi = (int64_t)s * c.y + kx;
+    const int64_t w = row_base(gi, c.x, (int64_t)s * c.z + ky, (int64_t)s * c.w + kz) + (xi >> 5);
+    const bool bit = (m >> k) & 1u;
+    const uint32_t pw = bit ? ipref[w] : 0u, bw = bit ? inb[w] : 0u;
+    rank[k] = pw + (uint32_t)__popc(bw & ((1u << (xi & 31)) - 1u));
+  }
+#pragma unroll
   for (int k = 0; k < K; ++k) {
     const bool bit = (m >> k) & 1u;
     const uint64_t bal = __ballot(bit);
-    if (!live) continue;
+    const int32_t row = bit ? perm[rank[k]] : -1;
     if (bit) {
-      const int kx = k % f, ky = (k / f) % f, kz = k / (f * f);
-      const int64_t xi = (int64_t)s * c.y + kx;
-      const int64_t w = row_base(gi, c.x, (int64_t)s * c.z + ky, (int64_t)s * c.w + kz) + (xi >> 5);
-      const uint32_t rank = ipref[w] + (uint32_t)__popc(inb[w] & ((1u << (xi & 31)) - 1u));
-      const int32_t row = perm[rank];
       const uint64_t p = pos[(int64_t)k * nt + t] + lane_rank(bal);
       in_rows[p] = row;
       out_rows[p] = (int32_t)o;
-      if (in_rank) in_rank[p] = (int32_t)rank;
-      if (nbr) {
-        nbr[o * K + k] = row;
-        inv[row] = (int32_t)(o * K + k);
-      }
-    } else if (nbr) {
-      nbr[o * K + k] = -1;
+      if (in_rank) in_rank[p] = (int32_t)rank[k];
+      if (nbr) inv[row] = (int32_t)(o * K + k);
     }
+    if (nbr && live) nbr[o * K + k] = row;
   }
+}
+
+// flags[1] = number of active inputs, flags[2] = number of active outputs
+__global__ void pack_totals_kernel(uint32_t* __restrict__ flags, const uint32_t* __restrict__ a_in,
+                                   const uint32_t* __restrict__ a_out) {
+  flags[1] = *a_in;
+  flags[2] = *a_out;
 }
 
 __global__ void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
@@ -427,15 +464,25 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   }
   if ((rc = exclusive_scan<uint32_t>(PopcountLoad{inb}, nw_in, ipref, ipref + nw_in, sc32, st)))
     return rc;
-  hipLaunchKernelGGL(dilate_kernel, dim3(blocks_for(nw_out, 256)), dim3(256), 0, st, inb, gi,
-                     outb, go, nw_out, f, s);
-  SCN_LAUNCH_CHECK();
+  {
+    auto dil = [&](auto fn) {
+      hipLaunchKernelGGL(fn, dim3(blocks_for(nw_out, 256)), dim3(256), 0, st, inb, gi, outb, go,
+                         (int)nw_out, s);
+    };
+    const int sm = s == 1 ? 1 : (s == 2 ? 2 : 0);
+    if (f == 1) { if (sm == 1) dil(dilate_kernel<1, 1>); else if (sm == 2) dil(dilate_kernel<1, 2>); else dil(dilate_kernel<1, 0>); }
+    else if (f == 2) { if (sm == 1) dil(dilate_kernel<2, 1>); else if (sm == 2) dil(dilate_kernel<2, 2>); else dil(dilate_kernel<2, 0>); }
+    else { if (sm == 1) dil(dilate_kernel<3, 1>); else if (sm == 2) dil(dilate_kernel<3, 2>); else dil(dilate_kernel<3, 0>); }
+    SCN_LAUNCH_CHECK();
+  }
   if ((rc = exclusive_scan<uint32_t>(PopcountLoad{outb}, nw_out, opref, opref + nw_out, sc32,
                                      st)))
     return rc;
-  SCN_HIP(hipMemcpyAsync(&hb->flags, flags, 4, hipMemcpyDeviceToHost, st));
-  SCN_HIP(hipMemcpyAsync(&hb->a_in, ipref + nw_in, 4, hipMemcpyDeviceToHost, st));
-  SCN_HIP(hipMemcpyAsync(&hb->a_out, opref + nw_out, 4, hipMemcpyDeviceToHost, st));
+  // flags and both totals in one read-back
+  hipLaunchKernelGGL(pack_totals_kernel, dim3(1), dim3(1), 0, st, flags, ipref + nw_in,
+                     opref + nw_out);
+  SCN_LAUNCH_CHECK();
+  SCN_HIP(hipMemcpyAsync(&hb->flags, flags, 12, hipMemcpyDeviceToHost, st));
   SCN_HIP(hipStreamSynchronize(st));
   if (hb->flags & F_RANGE) {
     set_error("scn_rulebook_build: a site lies outside the grid (%lld,%lld,%lld,%lld)",
@@ -522,13 +569,23 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     SCN_LAUNCH_CHECK();
   }
   if (a_out > 0) {
-    hipLaunchKernelGGL(out_sites_kernel, dim3(blocks_for(nw_out, 256)), dim3(256), 0, st, inb,
-                       gi, outb, opref, go, nw_out, f, s, rb->out_coords, masks);
+    auto os = [&](auto fn) {
+      hipLaunchKernelGGL(fn, dim3(blocks_for(nw_out, 256)), dim3(256), 0, st, inb, gi, outb, opref,
+                         go, (int)nw_out, s, rb->out_coords, masks);
+    };
+    if (f == 1) { if (s == 1) os(out_sites_kernel<1, true>); else os(out_sites_kernel<1, false>); }
+    else if (f == 2) { if (s == 1) os(out_sites_kernel<2, true>); else os(out_sites_kernel<2, false>); }
+    else { if (s == 1) os(out_sites_kernel<3, true>); else os(out_sites_kernel<3, false>); }
     SCN_LAUNCH_CHECK();
   }
-  hipLaunchKernelGGL(tile_count_kernel, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st, masks,
-                     a_out, nt, K, cnt);
-  SCN_LAUNCH_CHECK();
+  {
+    auto tc = [&](auto fn) {
+      hipLaunchKernelGGL(fn, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st, masks, a_out, nt,
+                         cnt);
+    };
+    if (f == 1) tc(tile_count_kernel<1>); else if (f == 2) tc(tile_count_kernel<8>); else tc(tile_count_kernel<27>);
+    SCN_LAUNCH_CHECK();
+  }
   // positions: otile[k*nt + t] = off[k] + pairs of list k in tiles < t
   if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, ncnt, (uint64_t*)rb->otile,
                                      (uint64_t*)rb->otile + ncnt, sc64, st)))
@@ -542,10 +599,13 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     SCN_LAUNCH_CHECK();
   }
   if (a_out > 0) {
-    hipLaunchKernelGGL(emit_pairs_kernel, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st,
-                       masks, rb->out_coords, a_out, nt, f, s, inb, ipref, gi, rb->perm,
-                       (const uint64_t*)rb->otile, rb->in_rows, rb->out_rows,
-                       sorted ? nullptr : rb->in_rank, rb->nbr, rb->inv);
+    auto em = [&](auto fn) {
+      hipLaunchKernelGGL(fn, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st, masks,
+                         rb->out_coords, a_out, nt, s, inb, ipref, gi, rb->perm,
+                         (const uint64_t*)rb->otile, rb->in_rows, rb->out_rows,
+                         sorted ? nullptr : rb->in_rank, rb->nbr, rb->inv);
+    };
+    if (f == 1) em(emit_pairs_kernel<1>); else if (f == 2) em(emit_pairs_kernel<2>); else em(emit_pairs_kernel<3>);
     SCN_LAUNCH_CHECK();
   }
   hipLaunchKernelGGL(in_tiles_kernel, dim3(blocks_for(K * nit + 1, 256)), dim3(256), 0, st,
