@@ -10,15 +10,19 @@
 //
 // Gather kernel (forward and input gradient).  A work-group of four waves owns
 // a tile of accumulator rows (output rows for the forward, input ranks for the
-// input gradient) and 64 columns; the accumulators live in LDS.  Each wave owns
-// 16 of the columns.  For each offset k the tile's pairs form one contiguous
-// range of list k (lists ascend by output row and by input key).  A wave walks
-// that range 32 pairs at a time: it loads the 32 gathered rows straight into
-// MFMA A-fragments (the next 32 are already in flight), multiplies them by its
-// slice of W_k and adds the two 16x16 results into the LDS rows named by the
-// pairs.  A wave is the only writer of its columns and pair rows are distinct
-// within an offset, so the main loop has no barrier, the scatter needs no
-// atomics between waves, and the summation order is fixed.
+// input gradient) and 64 columns; the accumulators live in LDS and each wave
+// owns 16 of the columns.  For each offset k the tile's pairs form one
+// contiguous range of list k (lists ascend by output row and by input key).
+// The tile's ranges are read once into lanes; the work-group walks them in
+// stages of 32 pairs of one offset.  Per stage it gathers the 32 rows into an
+// LDS buffer (one gather per row, shared by the four waves), each wave
+// multiplies them by its slice of W_k on the matrix cores and adds the
+// products into the LDS rows named by the pairs.  Rows, row indices and
+// weights are fetched two stages ahead, and a stage's products are added one
+// stage later, so no wave waits for memory or for its own matrix-core
+// results in steady state.  A wave is the only writer of its columns and pair
+// rows are distinct within an offset, so the scatter needs no atomics and the
+// summation order is fixed.
 //
 // Weight gradient.  dW_k = X_k^T dY_k over the P_k pairs of offset k is a
 // contraction along the pair axis: split into fixed chunks, each chunk's
@@ -85,20 +89,28 @@ __global__ void zero_kernel(float* __restrict__ p, int64_t n) {
   if (i < n) p[i] = 0.f;
 }
 
-// Packed weights for the gather kernel: Wp[k][n][j] = W_k(j, n) with the
-// reduction index j contiguous, zero-padded to RkP rows and NcP columns.
-//   forward:        W_k(j = ci, n = co) = W[k][ci][co]   (transpose)
-//   input gradient: W_k(j = co, n = ci) = W[k][ci][co]   (copy with padding)
+// Packed weights for the gather kernel, in MFMA fragment order:
+//   Wp[k][cb][w][t][lane][e] = W_k(j = 16t + 4q + e, n = 64cb + 16w + n16),
+//   lane = n16 + 16q, zero outside j < Rk, n < Nc;  RkP = 16*NKT, NcP = 64*NCB.
+//   forward:        W_k(j = ci, n = co) = W[k][ci][co]
+//   input gradient: W_k(j = co, n = ci) = W[k][ci][co]
 __global__ void __launch_bounds__(256) pack_w_kernel(const float* __restrict__ W, int K, int Cin,
                                                      int Cout, int transpose, int RkP, int NcP,
                                                      float* __restrict__ Wp) {
   const int Nc = transpose ? Cout : Cin, Rk = transpose ? Cin : Cout;
+  const int nkt = RkP / 16, ncb = NcP / 64;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= (int64_t)K * NcP * RkP) return;
-  const int j = (int)(i % RkP);
-  const int64_t kn = i / RkP;
-  const int n = (int)(kn % NcP);
-  const int64_t k = kn / NcP;
+  const int e = (int)(i & 3), ln = (int)((i >> 2) & 63);
+  const int64_t f = i >> 8;  // ((k*ncb + cb)*4 + w)*nkt + t
+  const int t = (int)(f % nkt);
+  const int64_t g = f / nkt;
+  const int wv = (int)(g & 3);
+  const int64_t h = g >> 2;
+  const int cbk = (int)(h % ncb);
+  const int64_t k = h / ncb;
+  const int j = 16 * t + 4 * (ln >> 4) + e;
+  const int n = 64 * cbk + 16 * wv + (ln & 15);
   float v = 0.f;
   if (j < Rk && n < Nc) {
     const int ci = transpose ? j : n, co = transpose ? n : j;
@@ -136,15 +148,16 @@ struct GatherArgs {
   int dvec_ok;           // rows of dst are 16-byte aligned and Nc % 4 == 0
 };
 
-// One pipeline stage covers 32 consecutive pairs of one offset (two 16-pair
-// blocks).  The work-group gathers the stage's 32 rows once into an LDS
-// buffer (8 threads per row, float4 loads, issued one stage ahead); each wave
-// then reads MFMA fragments from LDS: lane (n16, q) takes channels
-// 16t + 4q .. +3 of pair n16 of each block, which is the B-operand layout of
-// v_mfma_f32_16x16x4f32 when the contraction is computed transposed
-// (R^T = W_k^T X^T).  The result holds pair n16, output columns 4q .. 4q+3 of
-// the wave's 16 in one lane, so the lane adds one contiguous float4 into its
-// pair's accumulator row.
+// One pipeline stage covers up to 32 consecutive pairs of one offset (two
+// 16-pair blocks).  The work-group gathers the stage's rows once into an LDS
+// buffer (8 threads per row, float4 loads); each wave then reads MFMA
+// fragments from LDS: lane (n16, q) takes channels 16t + 4q .. +3 of pair n16
+// of each block, which is the B-operand layout of v_mfma_f32_16x16x4f32 when
+// the contraction is computed transposed (R^T = W_k^T X^T).  The result holds
+// pair n16, output columns 4q .. 4q+3 of the wave's 16 in one lane, so the
+// lane adds one contiguous float4 into its pair's accumulator row.  The
+// pair's accumulator row travels with its gathered row, in the padding word
+// of the LDS row.
 constexpr int SROWS = 32;  // pairs per stage
 
 template <int NKT>
@@ -153,33 +166,40 @@ struct WFrag {
   float4 g;       // gw[k][16w + 4q .. +3]
 };
 
-// W_k(j, n) = Wp[(k*NcP + n)*RkP + j], zero-padded to RkP = 16*NKT rows and
-// NcP = 64*ceil(Nc/64) columns; gw is padded the same way.
+// Weights in fragment order: Wp[k][cb][w][t][lane][e] = W_k(j = 16t + 4q + e,
+// n = 64cb + 16w + n16) with lane = n16 + 16q, zero-padded to 16*NKT rows and
+// NcP = 64*ceil(Nc/64) columns, so a wave's fragment is NKT contiguous 1 KB
+// blocks.  gw is [K][NcP].
 template <int NKT>
-__device__ inline void load_w(const GatherArgs& a, int k, int col, int cq, int q, WFrag<NKT>& f) {
-  const float* wp = a.Wp + ((int64_t)k * a.NcP + col) * (16 * NKT) + 4 * q;
+__device__ inline WFrag<NKT> load_w(const GatherArgs& a, int k, int cb, int w, int lane, int gcol) {
+  WFrag<NKT> f;
+  const float* wp =
+      a.Wp + (((int64_t)k * (a.NcP >> 6) + cb) * 4 + w) * (int64_t)(NKT * 256) + lane * 4;
 #pragma unroll
-  for (int t = 0; t < NKT; ++t) f.w[t] = *reinterpret_cast<const float4*>(wp + 16 * t);
-  f.g = *reinterpret_cast<const float4*>(a.gwp + (int64_t)k * a.NcP + cq);
+  for (int t = 0; t < NKT; ++t) f.w[t] = *reinterpret_cast<const float4*>(wp + 256 * t);
+  f.g = *reinterpret_cast<const float4*>(a.gwp + (int64_t)k * a.NcP + gcol);
+  return f;
 }
 
-// Per-thread share of a stage's gather: row tid/8, channel quads
-// (tid%8) + 8u.  Positions past the range are clamped to the range's last
-// pair (loads stay in bounds; those rows are never scattered).  Reduction
-// slots j >= Rk read some channel of the row; the matching W entries are zero.
+// Per-thread share of one stage's gather: row tid/8, channel quads
+// (tid%8) + 8u, and the row's accumulator index.  Positions past the stage's
+// pairs are clamped to its last pair (loads stay in bounds; those rows are
+// never scattered).  Reduction slots j >= Rk read some channel of the row;
+// the matching W entries are zero.
 template <int NKT>
-struct RowRegs {
+struct StageRegs {
   static constexpr int NQ = (4 * NKT + 7) / 8;  // float4 per thread
   float4 v[NQ];
+  int acc_row;
 };
 
 template <int NKT, bool VEC>
-__device__ inline RowRegs<NKT> load_rows(const GatherArgs& a, int gi, int tid) {
-  RowRegs<NKT> R;
+__device__ inline StageRegs<NKT> load_stage(const GatherArgs& a, int gi, int ai, int tid) {
+  StageRegs<NKT> R;
   const float* rp = a.src + (int64_t)gi * a.Rk;
   const int part = tid & 7;
 #pragma unroll
-  for (int u = 0; u < RowRegs<NKT>::NQ; ++u) {
+  for (int u = 0; u < StageRegs<NKT>::NQ; ++u) {
     const int c = 4 * (part + 8 * u);
     if (VEC) {
       const int cc = c < a.Rk ? c : 0;
@@ -191,93 +211,143 @@ __device__ inline RowRegs<NKT> load_rows(const GatherArgs& a, int gi, int tid) {
       R.v[u] = make_float4(e[0], e[1], e[2], e[3]);
     }
   }
+  R.acc_row = ai;
   return R;
 }
 
 template <int NKT>
-__device__ inline void store_rows(float* xs, int tid, const RowRegs<NKT>& R) {
+__device__ inline void store_stage(float* xs, int tid, const StageRegs<NKT>& R) {
+  constexpr int XLD = 16 * NKT + 4;
   const int row = tid >> 3, part = tid & 7;
 #pragma unroll
-  for (int u = 0; u < RowRegs<NKT>::NQ; ++u) {
+  for (int u = 0; u < StageRegs<NKT>::NQ; ++u) {
     const int quad = part + 8 * u;
-    if (quad < 4 * NKT)
-      *reinterpret_cast<float4*>(xs + row * (16 * NKT + 4) + 4 * quad) = R.v[u];
+    if (quad < 4 * NKT) *reinterpret_cast<float4*>(xs + row * XLD + 4 * quad) = R.v[u];
   }
+  reinterpret_cast<int*>(xs)[row * XLD + 16 * NKT] = R.acc_row;  // same value from all 8
 }
 
-template <int NKT, bool TWO>
-__device__ inline void mfma_scatter(const float* xs, const WFrag<NKT>& B, int i0, int i1,
-                                    int64_t p, int64_t e, float* acc, int cq, int n16, int q) {
+// Products of one stage held by a lane: pair n16 of each 16-pair block,
+// output columns cq .. cq+3, already offset by -gw (the accumulator starts at
+// -gw), and the accumulator rows they go to.
+struct StageOut {
+  v4f c0, c1;
+  int i0, i1;
+};
+
+// Multiply one stage (cnt live pairs, possibly none) by the wave's W_k slice.
+// Lanes past the live pairs target the spare row `spare` (never read), so
+// the code has no branch.
+template <int NKT>
+__device__ inline StageOut stage_mfma(const float* xs, const WFrag<NKT>& B, int cnt, int spare,
+                                      int n16, int q) {
   constexpr int XLD = 16 * NKT + 4;
   const float* r0 = xs + n16 * XLD + 4 * q;
   const float* r1 = xs + (16 + n16) * XLD + 4 * q;
-  v4f c0v = {0.f, 0.f, 0.f, 0.f}, c1v = {0.f, 0.f, 0.f, 0.f};
+  const int* ai = reinterpret_cast<const int*>(xs) + 16 * NKT;
+  StageOut o;
+  const int a0 = ai[n16 * XLD], a1 = ai[(16 + n16) * XLD];
+  o.i0 = n16 < cnt ? a0 : spare;
+  o.i1 = 16 + n16 < cnt ? a1 : spare;
+  v4f c0v = {-B.g.x, -B.g.y, -B.g.z, -B.g.w}, c1v = c0v;
 #pragma unroll
   for (int t = 0; t < NKT; ++t) {
     const float4 x0 = *reinterpret_cast<const float4*>(r0 + 16 * t);
+    const float4 x1 = *reinterpret_cast<const float4*>(r1 + 16 * t);
     c0v = mfma4(B.w[t].x, x0.x, c0v);
-    if (TWO) {
-      const float4 x1 = *reinterpret_cast<const float4*>(r1 + 16 * t);
-      c1v = mfma4(B.w[t].x, x1.x, c1v);
-      c0v = mfma4(B.w[t].y, x0.y, c0v);
-      c1v = mfma4(B.w[t].y, x1.y, c1v);
-      c0v = mfma4(B.w[t].z, x0.z, c0v);
-      c1v = mfma4(B.w[t].z, x1.z, c1v);
-      c0v = mfma4(B.w[t].w, x0.w, c0v);
-      c1v = mfma4(B.w[t].w, x1.w, c1v);
-    } else {
-      c0v = mfma4(B.w[t].y, x0.y, c0v);
-      c0v = mfma4(B.w[t].z, x0.z, c0v);
-      c0v = mfma4(B.w[t].w, x0.w, c0v);
-    }
+    c1v = mfma4(B.w[t].x, x1.x, c1v);
+    c0v = mfma4(B.w[t].y, x0.y, c0v);
+    c1v = mfma4(B.w[t].y, x1.y, c1v);
+    c0v = mfma4(B.w[t].z, x0.z, c0v);
+    c1v = mfma4(B.w[t].z, x1.z, c1v);
+    c0v = mfma4(B.w[t].w, x0.w, c0v);
+    c1v = mfma4(B.w[t].w, x1.w, c1v);
   }
-  // lane holds pair n16 of each block, columns cq .. cq+3 (tile-local)
-  if (p + n16 < e) {
-    float4* r = reinterpret_cast<float4*>(&acc[i0 * ACC_LD + cq]);
-    float4 v = *r;
-    v.x += c0v[0] - B.g.x;
-    v.y += c0v[1] - B.g.y;
-    v.z += c0v[2] - B.g.z;
-    v.w += c0v[3] - B.g.w;
-    *r = v;
-  }
-  if (TWO && p + 16 + n16 < e) {
-    float4* r = reinterpret_cast<float4*>(&acc[i1 * ACC_LD + cq]);
-    float4 v = *r;
-    v.x += c1v[0] - B.g.x;
-    v.y += c1v[1] - B.g.y;
-    v.z += c1v[2] - B.g.z;
-    v.w += c1v[3] - B.g.w;
-    *r = v;
-  }
+  o.c0 = c0v;
+  o.c1 = c1v;
+  return o;
 }
 
-// A stage position: offset k, pairs [p, min(p + 32, e)) of list k.
-struct Pos {
-  int k;
-  int64_t p, e;
+// Add a stage's products into its accumulator rows (columns cq .. cq+3).
+__device__ inline void stage_scatter(const StageOut& o, float* acc, int cq) {
+  float4* r = reinterpret_cast<float4*>(&acc[o.i0 * ACC_LD + cq]);
+  float4 v = *r;
+  v.x += o.c0[0];
+  v.y += o.c0[1];
+  v.z += o.c0[2];
+  v.w += o.c0[3];
+  *r = v;
+  r = reinterpret_cast<float4*>(&acc[o.i1 * ACC_LD + cq]);
+  v = *r;
+  v.x += o.c1[0];
+  v.y += o.c1[1];
+  v.z += o.c1[2];
+  v.w += o.c1[3];
+  *r = v;
+}
+
+// Stage schedule of one tile.  Lane k (< K) of every wave holds the tile's
+// pair range of list k: start P and length N (at most TM*64: one pair per
+// accumulator row and offset); `live` has bit k set when N > 0.  Stages are
+// stepped with readlane, so the main loop makes no memory access to find its
+// next stage.
+struct Sched {
+  int64_t P;
+  int N;
+  uint64_t live;
+  int K;
 };
 
-// Next stage after `s` within the tile: same offset 32 pairs on, else the
-// first pair of the next non-empty offset; k == K when there is none.
-__device__ inline Pos advance(const GatherArgs& a, int64_t t0, int64_t t1, Pos s) {
-  s.p += SROWS;
-  if (s.p < s.e) return s;
-  for (++s.k; s.k < a.K; ++s.k) {
-    s.p = a.tpos[(int64_t)s.k * a.ntile + t0];
-    s.e = a.tpos[(int64_t)s.k * a.ntile + t1];
-    if (s.p < s.e) return s;
-  }
-  return s;
+__device__ inline int64_t lane64(int64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(uint64_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
+// A stage position: offset k, pairs [p, p + min(n, 32)) of list k; k == K
+// (n == 0) past the tile's last stage.
+struct Pos {
+  int k, n;
+  int64_t p;
+};
+
+__device__ inline Pos jump(const Sched& s, uint64_t m) {
+  Pos x;
+  if (!m) {
+    x.k = s.K;
+    x.n = 0;
+    x.p = 0;
+    return x;
+  }
+  x.k = __builtin_ctzll(m);
+  x.p = lane64(s.P, x.k);
+  x.n = __builtin_amdgcn_readlane(s.N, x.k);
+  return x;
+}
+
+__device__ inline Pos next_stage(const Sched& s, Pos x) {
+  if (x.k >= s.K) return x;
+  x.p += SROWS;
+  x.n -= SROWS;
+  if (x.n > 0) return x;
+  return jump(s, s.live & ~((2ull << x.k) - 1ull));
+}
+
+// Main loop, unrolled by two so that the register sets of the software
+// pipeline keep fixed names (X = iteration parity); a tile with an odd number
+// of stages ends with one empty stage.  Iteration i computes
+// stage s_i; in flight meanwhile: the rows of s_{i+1} (landed, stored to LDS
+// at the top of the iteration), the rows of s_{i+2} and s_{i+3}, the row
+// indices of s_{i+4} and s_{i+5}, and the weights of s_{i+1} and s_{i+2}.
+// Every load of an iteration is unconditional, so each wait covers exactly the
+// loads it needs.
 template <int NKT, bool VEC, int TM, int MINB>
 __global__ void __launch_bounds__(NT, MINB) gather_mfma_kernel(GatherArgs a) {
   extern __shared__ float smem[];
   constexpr int T = TM * TILE;
   constexpr int XLD = 16 * NKT + 4;
-  float* acc = smem;                      // [T][ACC_LD]
-  float* xsb = smem + T * ACC_LD;         // [2][SROWS][XLD]
+  float* acc = smem;                      // [T + 1][ACC_LD], row T is the spare row
+  float* xsb = smem + (T + 1) * ACC_LD;   // [2][SROWS][XLD]
   const int tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int n16 = lane & 15, q = lane >> 4;
@@ -285,71 +355,93 @@ __global__ void __launch_bounds__(NT, MINB) gather_mfma_kernel(GatherArgs a) {
   const int64_t t0 = tile * TM;
   const int64_t t1 = min(t0 + TM, a.ntile);
   const int64_t row0 = t0 * TILE;
-  const int c0 = blockIdx.y * CB;
-  const int col = c0 + 16 * w + n16;  // W column this lane feeds into the A operand
+  const int cb = blockIdx.y;
+  const int c0 = cb * CB;
   const int cq = 16 * w + 4 * q;      // tile-local columns this lane accumulates
   const int lrow = tid >> 3;          // stage row this thread gathers
 
   for (int i = tid; i < T * ACC_LD / 4; i += NT)
     reinterpret_cast<float4*>(acc)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
 
-  // Work-group-uniform stage positions s .. s+3.  Loads for a position past
-  // the last stage use the last real stage instead (in bounds, never used).
-  Pos s0 = advance(a, t0, t1, Pos{-1, 0, 0});
+  Sched sc;
+  sc.K = a.K;
+  {
+    const int k = lane < a.K ? lane : 0;
+    sc.P = a.tpos[(int64_t)k * a.ntile + t0];
+    sc.N = lane < a.K ? (int)(a.tpos[(int64_t)k * a.ntile + t1] - sc.P) : 0;
+    sc.live = __ballot(sc.N > 0);
+  }
+  Pos s0 = jump(sc, sc.live);
   if (s0.k < a.K) {
-    Pos s1 = advance(a, t0, t1, s0);
-    Pos s2 = s1.k < a.K ? advance(a, t0, t1, s1) : s1;
-    Pos last = s0;                             // last real stage seen so far
-    auto real = [&](const Pos x) -> Pos { return x.k < a.K ? x : last; };
-    if (s1.k < a.K) last = s1;
-    if (s2.k < a.K) last = s2;
-    auto gidx_of = [&](const Pos x) { const Pos r = real(x); return a.gidx[min(r.p + lrow, r.e - 1)]; };
-    auto aidx_of = [&](const Pos x, int off) {
+    const Pos first = s0;
+    // loads for a position past the last stage use the first stage (in
+    // bounds, never scattered)
+    auto real = [&](const Pos x) -> Pos { return x.k < a.K ? x : first; };
+    auto gidx_of = [&](const Pos x) -> int {
       const Pos r = real(x);
-      return (int)(a.aidx[min(r.p + off + n16, r.e - 1)] - row0);
+      return a.gidx[r.p + min(lrow, r.n - 1)];
     };
-    int g2 = gidx_of(s2);                      // index of stage s+2's row
-    int i0 = aidx_of(s0, 0), j0 = aidx_of(s0, 16);
-    int i1 = aidx_of(s1, 0), j1 = aidx_of(s1, 16);
-    store_rows<NKT>(xsb, tid, load_rows<NKT, VEC>(a, gidx_of(s0), tid));
-    RowRegs<NKT> R = load_rows<NKT, VEC>(a, gidx_of(s1), tid);  // stage s+1 rows in flight
-    WFrag<NKT> B;
-    load_w<NKT>(a, s0.k, col, c0 + cq, q, B);
+    auto aidx_of = [&](const Pos x) -> int {
+      const Pos r = real(x);
+      return (int)(a.aidx[r.p + min(lrow, r.n - 1)] - row0);
+    };
+    auto wk = [&](const Pos x) { return load_w<NKT>(a, real(x).k, cb, w, lane, c0 + cq); };
+    Pos s1 = next_stage(sc, s0), s2 = next_stage(sc, s1), s3 = next_stage(sc, s2);
+    Pos s4 = next_stage(sc, s3), s5 = next_stage(sc, s4);
+
+    store_stage<NKT>(xsb, tid, load_stage<NKT, VEC>(a, gidx_of(s0), aidx_of(s0), tid));
+    StageRegs<NKT> R0 = load_stage<NKT, VEC>(a, gidx_of(s1), aidx_of(s1), tid);
+    StageRegs<NKT> R1 = load_stage<NKT, VEC>(a, gidx_of(s2), aidx_of(s2), tid);
+    int G0 = gidx_of(s3), G1 = gidx_of(s4);
+    WFrag<NKT> B0 = wk(s0), B1 = wk(s1);
+    // drain the prologue's loads once per tile, so that the wait counts in
+    // the loop follow from the loop's own loads
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    int buf = 0;
-    while (true) {
-      const bool more1 = s1.k < a.K;
-      const Pos s3 = s2.k < a.K ? advance(a, t0, t1, s2) : s2;
-      if (s3.k < a.K) last = s3;
-      float* xs_cur = xsb + buf * SROWS * XLD;
-      float* xs_nxt = xsb + (buf ^ 1) * SROWS * XLD;
-      // stage s+1 rows (loaded one step ago) -> the other LDS buffer
-      if (more1) store_rows<NKT>(xs_nxt, tid, R);
-      // issue: index of stage s+3, accumulator rows of stage s+2, rows of stage s+2
-      const int g3 = gidx_of(s3);
-      const int i2 = aidx_of(s2, 0), j2 = aidx_of(s2, 16);
-      R = load_rows<NKT, VEC>(a, g2, tid);
-      WFrag<NKT> Bn;
-      const bool kchange = more1 && s1.k != s0.k;
-      if (kchange) load_w<NKT>(a, s1.k, col, c0 + cq, q, Bn);
-      // a stage with at most 16 live pairs multiplies one block only
-      if (s0.e - s0.p > 16)
-        mfma_scatter<NKT, true>(xs_cur, B, i0, j0, s0.p, s0.e, acc, cq, n16, q);
-      else
-        mfma_scatter<NKT, false>(xs_cur, B, i0, j0, s0.p, s0.e, acc, cq, n16, q);
-      if (!more1) break;
-      if (kchange) B = Bn;
-      __syncthreads();
-      buf ^= 1;
-      g2 = g3;
-      i0 = i1;
-      j0 = j1;
-      i1 = i2;
-      j1 = j2;
+
+    // one iteration: parity X selects the register sets.  The products of
+    // s_i are added to the accumulators one iteration later, so the wave
+    // never waits for its own matrix-core results.
+    auto step = [&](StageRegs<NKT>& R, int& G, WFrag<NKT>& B, StageOut& Onew, const StageOut& Oprev,
+                    float* xs_cur, float* xs_nxt) {
+      // s_i is past the last stage (no live pairs) only in the second half
+      // of the final pair
+      Onew = stage_mfma<NKT>(xs_cur, B, min(s0.n, SROWS), T, n16, q);
+      stage_scatter(Oprev, acc, cq);
+      // rows of s_{i+1} -> the other buffer
+      store_stage<NKT>(xs_nxt, tid, R);
+      // rows of s_{i+3} (index loaded two iterations ago), index of s_{i+5}
+      R = load_stage<NKT, VEC>(a, G, aidx_of(s3), tid);
+      G = gidx_of(s5);
+      // weights of s_{i+2} into the set just used
+      B = wk(s2);
+    };
+    auto shift = [&]() {
       s0 = s1;
       s1 = s2;
       s2 = s3;
+      s3 = s4;
+      s4 = s5;
+      s5 = next_stage(sc, s5);
+    };
+    float* const xa = xsb;
+    float* const xb = xsb + SROWS * XLD;
+    // stages in pairs; the only exit is after the second of a pair, behind
+    // its barrier (every path through the loop issues the same loads)
+    StageOut O0, O1;
+    O1.c0 = v4f{0.f, 0.f, 0.f, 0.f};
+    O1.c1 = O1.c0;
+    O1.i0 = O1.i1 = T;
+    while (true) {
+      step(R0, G0, B0, O0, O1, xa, xb);
+      __syncthreads();
+      shift();
+      step(R1, G1, B1, O1, O0, xb, xa);
+      __syncthreads();
+      shift();
+      if (s0.k >= a.K) break;
     }
+    stage_scatter(O1, acc, cq);
   }
   __syncthreads();
   // epilogue: dst[row] = act(acc + add)
@@ -390,7 +482,7 @@ constexpr int gather_tm() {
 
 template <int NKT>
 GatherFn pick_gather(bool vec) {
-  constexpr int TM = gather_tm<NKT>(), MINB = NKT > 4 ? 1 : 4;
+  constexpr int TM = gather_tm<NKT>(), MINB = NKT > 4 ? 1 : 3;
   return vec ? gather_mfma_kernel<NKT, true, TM, MINB> : gather_mfma_kernel<NKT, false, TM, MINB>;
 }
 
@@ -425,7 +517,7 @@ scn_status launch_gather(GatherArgs a, hipStream_t st) {
   const int64_t nwg = ceil_div(a.ntile, TM);
   const unsigned ncb = (unsigned)ceil_div(a.Nc, CB);
   const size_t smem =
-      ((size_t)TM * TILE * ACC_LD + 2 * (size_t)SROWS * (16 * nkt + 4)) * sizeof(float);
+      ((size_t)(TM * TILE + 1) * ACC_LD + 2 * (size_t)SROWS * (16 * nkt + 4)) * sizeof(float);
   const bool vec = a.vec_ok;
   GatherFn fn = gather_fn(nkt, vec);
   static bool attr_done[2][17] = {};
