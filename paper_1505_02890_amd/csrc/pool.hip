@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <initializer_list>
 
 #include "scn_internal.h"
 
@@ -68,7 +69,115 @@ __global__ void __launch_bounds__(256) maxpool_bwd_dx_kernel(const int32_t* __re
   dx[i] = v;
 }
 
-constexpr int PB_ROWS = 1024;
+// ---- four channels per thread (C % 4 == 0, aligned rows) ------------------
+// A block holds `per` sites with nc4 = C/4 threads each; argmax bytes of four
+// channels travel as one 32-bit word (byte e = channel 4*c4 + e).
+
+template <int F>
+__global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __restrict__ x,
+                                                              const float4* __restrict__ g_in,
+                                                              const int32_t* __restrict__ nbr,
+                                                              int64_t a_out, int nc4, int per,
+                                                              float4* __restrict__ y,
+                                                              uint32_t* __restrict__ argmax) {
+  constexpr int K = F * F * F;
+  const int ol = threadIdx.x / nc4, c4 = threadIdx.x - ol * nc4;
+  const int64_t o = (int64_t)blockIdx.x * per + ol;
+  if (ol >= per || o >= a_out) return;
+  const float4 g = g_in[c4];
+  const int32_t* nb = nbr + o * K;
+  float4 v[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int32_t r = nb[k];
+    v[k] = r >= 0 ? x[(int64_t)r * nc4 + c4] : g;
+  }
+  // first strict maximum in ascending k, per channel
+  float4 best = v[0];
+  uint32_t b0 = 0, b1 = 0, b2 = 0, b3 = 0;
+#pragma unroll
+  for (int k = 1; k < K; ++k) {
+    if (v[k].x > best.x) { best.x = v[k].x; b0 = k; }
+    if (v[k].y > best.y) { best.y = v[k].y; b1 = k; }
+    if (v[k].z > best.z) { best.z = v[k].z; b2 = k; }
+    if (v[k].w > best.w) { best.w = v[k].w; b3 = k; }
+  }
+  y[o * nc4 + c4] = best;
+  argmax[o * nc4 + c4] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+}
+
+constexpr int PBV_ROWS = 256;  // outputs per block of the four-channel backward
+
+// Output-major backward: an input lies in at most one window, so each window
+// writes its inputs' dx rows (dy where the input won, else 0) and dx is
+// written once per element with no atomics (rows in no window are zeroed by
+// zero_uncovered_kernel).  A winner at an inactive
+// position sends dy to the ground state: part[blk][c] sums those, over the
+// block's outputs in a fixed order (part may be null).
+template <int F>
+__global__ void __launch_bounds__(256) maxpool_bwd_vec_kernel(const int32_t* __restrict__ nbr,
+                                                              const uint32_t* __restrict__ argmax,
+                                                              const float4* __restrict__ dy,
+                                                              int64_t a_out, int nc4,
+                                                              float4* __restrict__ dx,
+                                                              float4* __restrict__ part) {
+  constexpr int K = F * F * F;
+  __shared__ float4 red[256];
+  const int rows = 256 / nc4;  // outputs in flight per block
+  const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
+  const int64_t o0 = (int64_t)blockIdx.x * PBV_ROWS;
+  const int64_t o1 = min<int64_t>(o0 + PBV_ROWS, a_out);
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (rl < rows)
+    for (int64_t o = o0 + rl; o < o1; o += rows) {
+      const int64_t j = o * nc4 + c4;
+      const uint32_t am = argmax[j];
+      const float4 d = dy[j];
+      const uint32_t k0 = am & 255u, k1 = (am >> 8) & 255u, k2 = (am >> 16) & 255u, k3 = am >> 24;
+      const int32_t* nb = nbr + o * K;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int32_t r = nb[k];
+        const float4 v = make_float4(k0 == (uint32_t)k ? d.x : 0.f, k1 == (uint32_t)k ? d.y : 0.f,
+                                     k2 == (uint32_t)k ? d.z : 0.f, k3 == (uint32_t)k ? d.w : 0.f);
+        if (r >= 0) {
+          dx[(int64_t)r * nc4 + c4] = v;
+        } else {
+          s.x += v.x;
+          s.y += v.y;
+          s.z += v.z;
+          s.w += v.w;
+        }
+      }
+    }
+  if (!part) return;
+  red[threadIdx.x] = s;
+  __syncthreads();
+  if (rl == 0) {
+    for (int i = 1; i < rows; ++i) {
+      const float4 t = red[i * nc4 + c4];
+      s.x += t.x;
+      s.y += t.y;
+      s.z += t.z;
+      s.w += t.w;
+    }
+    part[(int64_t)blockIdx.x * nc4 + c4] = s;
+  }
+}
+
+// dx rows of inputs that lie in no window (a grid edge the windows do not
+// reach) are zero; one thread per input row
+__global__ void __launch_bounds__(256) zero_uncovered_kernel(const int32_t* __restrict__ inv,
+                                                             int64_t a_in, int nc4,
+                                                             float4* __restrict__ dx) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= a_in || inv[r] >= 0) return;
+  for (int c4 = 0; c4 < nc4; ++c4) dx[r * nc4 + c4] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+constexpr int PB_ROWS = 1024;  // outputs per block of the one-channel ground gradient
+
+// ---- any channel count (one channel per thread) -----------------------------
 
 // partial[blk][c] = sum over the block's outputs of dy[o][c] where the winner is inactive
 __global__ void __launch_bounds__(256) maxpool_bwd_ground_kernel(const int32_t* __restrict__ nbr,
@@ -96,17 +205,37 @@ __global__ void __launch_bounds__(256) maxpool_bwd_ground_kernel(const int32_t* 
   }
 }
 
-__global__ void maxpool_bwd_ground_finish(const float* __restrict__ part, int64_t nblk, int C,
-                                          const float* __restrict__ dg_out,
-                                          float* __restrict__ dg_in) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  float s = dg_out ? dg_out[c] : 0.f;
-  for (int64_t b = 0; b < nblk; ++b) s += part[b * C + c];
-  dg_in[c] = s;
+// dg_in[c] = dg_out[c] + sum_b part[b][c]; one block per channel, each thread
+// a strided share of the blocks, then a fixed-shape tree
+__global__ void __launch_bounds__(256) maxpool_bwd_ground_finish(const float* __restrict__ part,
+                                                                 int64_t nblk, int C,
+                                                                 const float* __restrict__ dg_out,
+                                                                 float* __restrict__ dg_in) {
+  __shared__ float red[256];
+  const int c = blockIdx.x;
+  float s = 0.f;
+  for (int64_t b = threadIdx.x; b < nblk; b += 256) s += part[b * C + c];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) dg_in[c] = (dg_out ? dg_out[c] : 0.f) + red[0];
 }
 
 inline unsigned nblocks(int64_t n, int t) { return (unsigned)std::max<int64_t>(1, ceil_div(n, t)); }
+
+// four-channel path: C % 4 == 0, C <= 1024, float rows 16-byte aligned, argmax
+// words 4-byte aligned
+inline bool pool_vec_ok(int C, std::initializer_list<const void*> rows, const void* argmax) {
+  if (C % 4 != 0 || C > 1024 || (reinterpret_cast<uintptr_t>(argmax) & 3) != 0) return false;
+  for (const void* p : rows)
+    if (reinterpret_cast<uintptr_t>(p) & 15) return false;
+  return true;
+}
+
+
 
 }  // namespace
 }  // namespace scn
@@ -128,8 +257,26 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
     return SCN_ERR_UNSUPPORTED;
   }
   if (rb->a_out > 0) {
-    hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(nblocks(rb->a_out * C, 256)), dim3(256), 0, st, x,
-                       g_in, rb->nbr, rb->a_out, C, rb->K, y, argmax);
+    if (pool_vec_ok(C, {x, g_in, y}, argmax)) {
+      const int nc4 = C / 4, per = 256 / nc4;
+      const dim3 grid(nblocks(rb->a_out, per));
+      const auto* x4 = reinterpret_cast<const float4*>(x);
+      const auto* g4 = reinterpret_cast<const float4*>(g_in);
+      auto* y4 = reinterpret_cast<float4*>(y);
+      auto* am4 = reinterpret_cast<uint32_t*>(argmax);
+      if (rb->f == 1)
+        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<1>, grid, dim3(256), 0, st, x4, g4, rb->nbr,
+                           rb->a_out, nc4, per, y4, am4);
+      else if (rb->f == 2)
+        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<2>, grid, dim3(256), 0, st, x4, g4, rb->nbr,
+                           rb->a_out, nc4, per, y4, am4);
+      else
+        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<3>, grid, dim3(256), 0, st, x4, g4, rb->nbr,
+                           rb->a_out, nc4, per, y4, am4);
+    } else {
+      hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(nblocks(rb->a_out * C, 256)), dim3(256), 0, st,
+                         x, g_in, rb->nbr, rb->a_out, C, rb->K, y, argmax);
+    }
     SCN_LAUNCH_CHECK();
   }
   hipLaunchKernelGGL(copy_vec_kernel, dim3(nblocks(C, 256)), dim3(256), 0, st, g_in, g_out, C);
@@ -139,7 +286,10 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
 
 size_t scn_maxpool_bwd_workspace_bytes(const scn_rulebook* rb, int32_t C) {
   if (!rb || C < 1) return 0;
-  return (size_t)std::max<int64_t>(1, ceil_div(rb->a_out, PB_ROWS)) * C * sizeof(float);
+  // enough for either path (the four-channel path uses 256-output blocks)
+  const int64_t rows = C % 4 == 0 ? PBV_ROWS : PB_ROWS;
+  return ((size_t)std::max<int64_t>(1, ceil_div(rb->a_out, rows)) * C * sizeof(float) + 15) &
+         ~size_t(15);
 }
 
 scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const float* dy,
@@ -159,20 +309,49 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
     set_error("scn_maxpool_bwd: workspace of %zu bytes needed, %zu given", need, ws_bytes);
     return SCN_ERR_WORKSPACE;
   }
-  if (rb->a_in > 0) {
-    hipLaunchKernelGGL(maxpool_bwd_dx_kernel, dim3(nblocks(rb->a_in * C, 256)), dim3(256), 0, st,
-                       rb->inv, argmax, dy, rb->a_in, C, rb->K, dx);
-    SCN_LAUNCH_CHECK();
-  }
-  if (dg_in) {
-    const int64_t nblk = std::max<int64_t>(1, ceil_div(rb->a_out, PB_ROWS));
-    float* part = static_cast<float*>(ws);
+  float* part = dg_in ? static_cast<float*>(ws) : nullptr;
+  const bool vec = pool_vec_ok(C, {dy, dx, part}, argmax);
+  int64_t nblk = 0;
+  if (vec) {
+    // one pass: dx of the inputs in windows and the ground-state partial sums
+    nblk = std::max<int64_t>(1, ceil_div(rb->a_out, PBV_ROWS));
+    if (rb->a_in > 0) {
+      hipLaunchKernelGGL(zero_uncovered_kernel, dim3(nblocks(rb->a_in, 256)), dim3(256), 0, st,
+                         rb->inv, rb->a_in, C / 4, reinterpret_cast<float4*>(dx));
+      SCN_LAUNCH_CHECK();
+    }
     if (rb->a_out > 0) {
+      const dim3 grid((unsigned)nblk);
+      const auto* am4 = reinterpret_cast<const uint32_t*>(argmax);
+      const auto* dy4 = reinterpret_cast<const float4*>(dy);
+      auto* dx4 = reinterpret_cast<float4*>(dx);
+      auto* p4 = reinterpret_cast<float4*>(part);
+      if (rb->f == 1)
+        hipLaunchKernelGGL(maxpool_bwd_vec_kernel<1>, grid, dim3(256), 0, st, rb->nbr, am4, dy4,
+                           rb->a_out, C / 4, dx4, p4);
+      else if (rb->f == 2)
+        hipLaunchKernelGGL(maxpool_bwd_vec_kernel<2>, grid, dim3(256), 0, st, rb->nbr, am4, dy4,
+                           rb->a_out, C / 4, dx4, p4);
+      else
+        hipLaunchKernelGGL(maxpool_bwd_vec_kernel<3>, grid, dim3(256), 0, st, rb->nbr, am4, dy4,
+                           rb->a_out, C / 4, dx4, p4);
+      SCN_LAUNCH_CHECK();
+    }
+  } else {
+    if (rb->a_in > 0) {
+      hipLaunchKernelGGL(maxpool_bwd_dx_kernel, dim3(nblocks(rb->a_in * C, 256)), dim3(256), 0,
+                         st, rb->inv, argmax, dy, rb->a_in, C, rb->K, dx);
+      SCN_LAUNCH_CHECK();
+    }
+    nblk = std::max<int64_t>(1, ceil_div(rb->a_out, PB_ROWS));
+    if (dg_in && rb->a_out > 0) {
       hipLaunchKernelGGL(maxpool_bwd_ground_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
                          rb->nbr, argmax, dy, rb->a_out, C, rb->K, part);
       SCN_LAUNCH_CHECK();
     }
-    hipLaunchKernelGGL(maxpool_bwd_ground_finish, dim3(nblocks(C, 64)), dim3(64), 0, st, part,
+  }
+  if (dg_in) {
+    hipLaunchKernelGGL(maxpool_bwd_ground_finish, dim3((unsigned)C), dim3(256), 0, st, part,
                        rb->a_out > 0 ? nblk : 0, C, dg_out, dg_in);
     SCN_LAUNCH_CHECK();
   }
