@@ -567,25 +567,97 @@ __global__ void __launch_bounds__(NT) colsum_kernel(const float* __restrict__ dy
   }
 }
 
-// S, dḡ, dbias; u0 = S + dḡ.  One block of 1024 threads per 64 columns.
-__global__ void __launch_bounds__(1024) finish_vec_kernel(const float* __restrict__ partS,
-                                                          int64_t nblk, int C,
-                                                          const float* __restrict__ g_out,
-                                                          const float* __restrict__ dg_out,
-                                                          int relu, float* __restrict__ S,
-                                                          float* __restrict__ u0,
-                                                          float* __restrict__ dbias) {
-  __shared__ float red[1024];
-  const int cl = threadIdx.x & 63, rg = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + cl;
-  float s = 0.f;
-  if (c < C)
-    for (int64_t b = rg; b < nblk; b += 16) s += partS[b * C + c];
+// Four channels per thread (C % 4 == 0, 16-byte aligned rows): a block reads
+// RB_ROWS rows as float4, `per` rows at a time, and combines the rows in a
+// fixed order.
+__global__ void __launch_bounds__(NT) colsum_vec_kernel(const float4* __restrict__ dy,
+                                                        const float4* __restrict__ y, int relu,
+                                                        int64_t rows, int nc4,
+                                                        float4* __restrict__ dyb,
+                                                        float4* __restrict__ partS) {
+  __shared__ float4 red[NT];
+  const int per = NT / nc4;
+  const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
+  const int64_t r0 = (int64_t)blockIdx.x * RB_ROWS;
+  const int64_t r1 = min<int64_t>(r0 + RB_ROWS, rows);
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (rl < per) {
+    int64_t r = r0 + rl;
+    // four rows in flight per thread
+    for (; r + 3 * per < r1; r += 4 * per) {
+      float4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = dy[(r + u * per) * nc4 + c4];
+      if (relu) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float4 m = y[(r + u * per) * nc4 + c4];
+          v[u].x = m.x > 0.f ? v[u].x : 0.f;
+          v[u].y = m.y > 0.f ? v[u].y : 0.f;
+          v[u].z = m.z > 0.f ? v[u].z : 0.f;
+          v[u].w = m.w > 0.f ? v[u].w : 0.f;
+          dyb[(r + u * per) * nc4 + c4] = v[u];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        s.x += v[u].x;
+        s.y += v[u].y;
+        s.z += v[u].z;
+        s.w += v[u].w;
+      }
+    }
+    for (; r < r1; r += per) {
+      float4 v = dy[r * nc4 + c4];
+      if (relu) {
+        const float4 m = y[r * nc4 + c4];
+        v.x = m.x > 0.f ? v.x : 0.f;
+        v.y = m.y > 0.f ? v.y : 0.f;
+        v.z = m.z > 0.f ? v.z : 0.f;
+        v.w = m.w > 0.f ? v.w : 0.f;
+        dyb[r * nc4 + c4] = v;
+      }
+      s.x += v.x;
+      s.y += v.y;
+      s.z += v.z;
+      s.w += v.w;
+    }
+  }
   red[threadIdx.x] = s;
   __syncthreads();
-  if (rg == 0 && c < C) {
-    float t = 0.f;
-    for (int i = 0; i < 16; ++i) t += red[i * 64 + cl];
+  if (rl == 0) {
+    for (int i = 1; i < per; ++i) {
+      const float4 t = red[i * nc4 + c4];
+      s.x += t.x;
+      s.y += t.y;
+      s.z += t.z;
+      s.w += t.w;
+    }
+    partS[(int64_t)blockIdx.x * nc4 + c4] = s;
+  }
+}
+
+// S, dḡ, dbias; u0 = S + dḡ.  One block per column: each thread sums a
+// strided share of the partials, then a fixed-shape tree.
+__global__ void __launch_bounds__(NT) finish_vec_kernel(const float* __restrict__ partS,
+                                                        int64_t nblk, int C,
+                                                        const float* __restrict__ g_out,
+                                                        const float* __restrict__ dg_out, int relu,
+                                                        float* __restrict__ S,
+                                                        float* __restrict__ u0,
+                                                        float* __restrict__ dbias) {
+  __shared__ float red[NT];
+  const int c = blockIdx.x;
+  float s = 0.f;
+  for (int64_t b = threadIdx.x; b < nblk; b += NT) s += partS[b * C + c];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int h = NT / 2; h > 0; h >>= 1) {
+    if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float t = red[0];
     float dg = dg_out ? dg_out[c] : 0.f;
     if (relu && dg_out) dg = g_out[c] > 0.f ? dg : 0.f;
     S[c] = t;
@@ -955,12 +1027,21 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
 
   // dȳ and S (column sums over active outputs)
   if (rb->a_out > 0) {
-    hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)L.nblk), dim3(NT), 0, st, dy, y, relu,
-                       rb->a_out, Cout, dyb, partS);
+    const bool v4 = (Cout % 4 == 0) && Cout <= 4 * NT &&
+                    ((reinterpret_cast<uintptr_t>(dy) | reinterpret_cast<uintptr_t>(y) |
+                      reinterpret_cast<uintptr_t>(ws)) & 15) == 0;
+    if (v4)
+      hipLaunchKernelGGL(colsum_vec_kernel, dim3((unsigned)L.nblk), dim3(NT), 0, st,
+                         reinterpret_cast<const float4*>(dy), reinterpret_cast<const float4*>(y),
+                         relu, rb->a_out, Cout / 4, reinterpret_cast<float4*>(dyb),
+                         reinterpret_cast<float4*>(partS));
+    else
+      hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)L.nblk), dim3(NT), 0, st, dy, y, relu,
+                         rb->a_out, Cout, dyb, partS);
     SCN_LAUNCH_CHECK();
   }
-  hipLaunchKernelGGL(finish_vec_kernel, dim3((unsigned)ceil_div(Cout, 64)), dim3(1024), 0, st,
-                     partS, rb->a_out > 0 ? L.nblk : 0, Cout, g_out, dg_out, relu, S, u0, dbias);
+  hipLaunchKernelGGL(finish_vec_kernel, dim3((unsigned)Cout), dim3(NT), 0, st, partS,
+                     rb->a_out > 0 ? L.nblk : 0, Cout, g_out, dg_out, relu, S, u0, dbias);
   SCN_LAUNCH_CHECK();
 
   // input gradient: accumulate over input ranks with W_k^T
