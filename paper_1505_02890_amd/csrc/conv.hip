@@ -676,6 +676,9 @@ __global__ void __launch_bounds__(NT) finish_vec_kernel(const float* __restrict_
 // Pair indices are staged through LDS two stages ahead, rows one stage ahead.
 constexpr int DW_SC = 64;          // pairs per stage
 constexpr int DW_LD = DW_SC + 4;   // pitch of a channel row (floats)
+// Pair quad p of channel row r sits at quad p ^ (r / 16) of the row: with the
+// 17-quad pitch this keeps every 16-lane group of both the transposed stores
+// and the fragment reads on 16 distinct bank groups.
 
 struct DwArgs {
   const float* x;        // [a_in][Cin]
@@ -711,6 +714,27 @@ __device__ inline void dw_rows(const DwArgs& a, const int* ix, const int* io, in
     }
 }
 
+// V4 (Cin and Cout multiples of 4, 16-byte aligned rows): thread (pair quad
+// pq = tid / 16, channel quad cq = tid % 16) loads channels 4cq .. 4cq+3 of
+// pairs 4pq .. 4pq+3 of each operand as float4 (a wave reads four whole
+// 256-byte row segments per load) and transposes the 4x4 blocks in registers.
+struct DwRows4 {
+  float4 x[4], d[4];
+};
+
+__device__ inline void dw_rows4(const DwArgs& a, const int* ix, const int* io, int cx4, int cd4,
+                                int pq, DwRows4& R) {
+  const float4* x4 = reinterpret_cast<const float4*>(a.x);
+  const float4* d4 = reinterpret_cast<const float4*>(a.dyb);
+  const int nx4 = a.Cin >> 2, nd4 = a.Cout >> 2;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    R.x[u] = x4[(int64_t)ix[4 * pq + u] * nx4 + cx4];
+    R.d[u] = d4[(int64_t)io[4 * pq + u] * nd4 + cd4];
+  }
+}
+
+template <bool V4>
 __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
   __shared__ float xsT[64 * DW_LD];  // [ci][pair], x - g_in
   __shared__ float dsT[64 * DW_LD];  // [co][pair]
@@ -729,11 +753,15 @@ __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
   const int ci0 = (blk / a.nco) * 64, co0 = (blk % a.nco) * 64;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n16 = lane & 15, q = lane >> 4;
-  // this thread's channel of each operand (clamped into the layer; zeroed on store)
-  const int ch = lane;
+  // this thread's channel (V4: channel quad) of each operand, clamped into
+  // the layer; out-of-layer channels are zeroed on store
+  const int ch = V4 ? 4 * (tid & 15) : lane;
   const bool xin = ci0 + ch < a.Cin, din = co0 + ch < a.Cout;
   const int cx = xin ? ci0 + ch : 0, cd = din ? co0 + ch : 0;
-  const float gsub = xin ? a.g_in[cx] : 0.f;
+  const float gsub = (!V4 && xin) ? a.g_in[cx] : 0.f;
+  const float4 gsub4 = (V4 && xin) ? *reinterpret_cast<const float4*>(a.g_in + cx)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+  const int pq = tid >> 4;  // V4: pair quad
 
   // index loaders: threads 0..63 input rows, 64..127 output rows of one stage
   auto load_index = [&](int64_t p0) -> int {
@@ -746,7 +774,11 @@ __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
   }
   __syncthreads();
   DwRows R;
-  dw_rows(a, idx[0][0], idx[0][1], cx, cd, w, R);
+  DwRows4 R4;
+  if (V4)
+    dw_rows4(a, idx[0][0], idx[0][1], cx >> 2, cd >> 2, pq, R4);
+  else
+    dw_rows(a, idx[0][0], idx[0][1], cx, cd, w, R);
 
   v4f acc[4];
 #pragma unroll
@@ -759,33 +791,66 @@ __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
     const int n = (int)min<int64_t>(DW_SC, p_end - p0);
     // stage rows -> LDS, transposed; pairs past the chunk and channels past
     // the layer are zero; x is shifted by the ground state
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int pb = 4 * (w + 4 * v);
-      float xe[4], de[4];
+    if (V4) {
+      const int pb = 4 * pq;
+      float xe[4][4], de[4][4];  // [channel][pair]
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const bool live = pb + u < n;
-        xe[u] = (live && xin) ? R.x[4 * v + u] - gsub : 0.f;
-        de[u] = (live && din) ? R.d[4 * v + u] : 0.f;
+        const bool lx = pb + u < n && xin, ld = pb + u < n && din;
+        xe[0][u] = lx ? R4.x[u].x - gsub4.x : 0.f;
+        xe[1][u] = lx ? R4.x[u].y - gsub4.y : 0.f;
+        xe[2][u] = lx ? R4.x[u].z - gsub4.z : 0.f;
+        xe[3][u] = lx ? R4.x[u].w - gsub4.w : 0.f;
+        de[0][u] = ld ? R4.d[u].x : 0.f;
+        de[1][u] = ld ? R4.d[u].y : 0.f;
+        de[2][u] = ld ? R4.d[u].z : 0.f;
+        de[3][u] = ld ? R4.d[u].w : 0.f;
       }
-      *reinterpret_cast<float4*>(&xsT[ch * DW_LD + pb]) = make_float4(xe[0], xe[1], xe[2], xe[3]);
-      *reinterpret_cast<float4*>(&dsT[ch * DW_LD + pb]) = make_float4(de[0], de[1], de[2], de[3]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int sq = 4 * (pq ^ ((ch + e) >> 4));  // swizzled pair quad
+        *reinterpret_cast<float4*>(&xsT[(ch + e) * DW_LD + sq]) =
+            make_float4(xe[e][0], xe[e][1], xe[e][2], xe[e][3]);
+        *reinterpret_cast<float4*>(&dsT[(ch + e) * DW_LD + sq]) =
+            make_float4(de[e][0], de[e][1], de[e][2], de[e][3]);
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int pb = 4 * (w + 4 * v);
+        float xe[4], de[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const bool live = pb + u < n;
+          xe[u] = (live && xin) ? R.x[4 * v + u] - gsub : 0.f;
+          de[u] = (live && din) ? R.d[4 * v + u] : 0.f;
+        }
+        const int sq = 4 * ((pb >> 2) ^ (ch >> 4));  // swizzled pair quad
+        *reinterpret_cast<float4*>(&xsT[ch * DW_LD + sq]) = make_float4(xe[0], xe[1], xe[2], xe[3]);
+        *reinterpret_cast<float4*>(&dsT[ch * DW_LD + sq]) = make_float4(de[0], de[1], de[2], de[3]);
+      }
     }
     int nidx = 0;
     if (tid < 128) nidx = load_index(p0 + 2 * DW_SC);  // stage s+2 indices in flight
     __syncthreads();
     // stage s+1 rows while the matrix cores work on stage s
-    dw_rows(a, idx[buf ^ 1][0], idx[buf ^ 1][1], cx, cd, w, R);
+    if (V4)
+      dw_rows4(a, idx[buf ^ 1][0], idx[buf ^ 1][1], cx >> 2, cd >> 2, pq, R4);
+    else
+      dw_rows(a, idx[buf ^ 1][0], idx[buf ^ 1][1], cx, cd, w, R);
+    // keep those loads ahead of the matrix-core section (left to itself the
+    // scheduler sinks them below it to reuse their registers, and the next
+    // stage then waits for the full memory latency)
+    __builtin_amdgcn_sched_barrier(0);
     // A(m = ci, kk = pair) = xsT[16w + m][pair];  B(kk = pair, n = co) = dsT[16j + n][pair]
-    const float* ar = xsT + (16 * w + n16) * DW_LD + 4 * q;
+    const float* ar = xsT + (16 * w + n16) * DW_LD + 4 * (q ^ w);
 #pragma unroll
     for (int t = 0; t < DW_SC / 16; ++t) {
       const float4 av = *reinterpret_cast<const float4*>(ar + 16 * t);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float4 bv =
-            *reinterpret_cast<const float4*>(dsT + (16 * j + n16) * DW_LD + 4 * q + 16 * t);
+            *reinterpret_cast<const float4*>(dsT + (16 * j + n16) * DW_LD + 4 * (q ^ j) + 16 * t);
         acc[j] = mfma4(av.x, bv.x, acc[j]);
         acc[j] = mfma4(av.y, bv.y, acc[j]);
         acc[j] = mfma4(av.z, bv.z, acc[j]);
@@ -797,7 +862,7 @@ __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
       const float* tr = dsT + tcol * DW_LD + 16 * q;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float4 v = *reinterpret_cast<const float4*>(tr + 4 * i);
+        const float4 v = *reinterpret_cast<const float4*>(tr + 4 * (i ^ w));
         tsum += ((v.x + v.y) + v.z) + v.w;
       }
     }
@@ -1094,7 +1159,13 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
     d.partT = partT;
     if (rb->n_pairs > 0) {
       const int64_t nwg = L.maxc * K * d.nblk;
-      hipLaunchKernelGGL(dw_partial_kernel, dim3((unsigned)nwg), dim3(NT), 0, st, d);
+      const bool v4 = Cin % 4 == 0 && Cout % 4 == 0 &&
+                      ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(dyb) |
+                        reinterpret_cast<uintptr_t>(g_in)) & 15) == 0;
+      if (v4)
+        hipLaunchKernelGGL(dw_partial_kernel<true>, dim3((unsigned)nwg), dim3(NT), 0, st, d);
+      else
+        hipLaunchKernelGGL(dw_partial_kernel<false>, dim3((unsigned)nwg), dim3(NT), 0, st, d);
       SCN_LAUNCH_CHECK();
     }
     const int64_t nred = std::max<int64_t>((int64_t)K * Cin * Cout, (int64_t)K * Cout);
