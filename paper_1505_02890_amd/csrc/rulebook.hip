@@ -316,7 +316,8 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
   for (int k = 0; k < K; ++k) {
     const bool bit = (m >> k) & 1u;
     const uint64_t bal = __ballot(bit);
-    const int32_t row = bit ? perm[rank[k]] : -1;
+    // sorted input: rank order is the caller's row order (no perm table)
+    const int32_t row = bit ? (perm ? perm[rank[k]] : (int32_t)rank[k]) : -1;
     if (bit) {
       const uint64_t p = pos[(int64_t)k * nt + t] + lane_rank(bal);
       in_rows[p] = row;
@@ -511,7 +512,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
                 sz_off = al((K + 1) * 8), sz_ot = al((K * nt + 1) * 8),
                 sz_it = al((K * nit + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
                 sz_inv = pool ? al(n * 4) : 0;
-  const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair) + sz_perm + sz_off + sz_ot +
+  const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair + sz_perm) + sz_off + sz_ot +
                         sz_it + sz_nbr + sz_inv;
   scn_rulebook* rb = new scn_rulebook();
   struct Guard {
@@ -536,7 +537,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   rb->in_rows = (int32_t*)take(sz_pair);
   rb->out_rows = (int32_t*)take(sz_pair);
   rb->in_rank = sorted ? rb->in_rows : (int32_t*)take(sz_pair);
-  rb->perm = (int32_t*)take(sz_perm);
+  rb->perm = sorted ? nullptr : (int32_t*)take(sz_perm);  // identity when sorted
   rb->off_dev = (int64_t*)take(sz_off);
   rb->otile = (int64_t*)take(sz_ot);
   rb->itile = (int64_t*)take(sz_it);
@@ -563,7 +564,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
       (rc = tmp.get(&sc64, scan_blocks(ncnt))))
     return rc;
 
-  if (n > 0) {
+  if (n > 0 && !sorted) {
     hipLaunchKernelGGL(perm_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n, gi,
                        inb, ipref, rb->perm);
     SCN_LAUNCH_CHECK();

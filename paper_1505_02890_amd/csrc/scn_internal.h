@@ -67,7 +67,7 @@ struct scn_rulebook {
   int32_t* in_rows = nullptr;     // [P] caller row of the input of each pair
   int32_t* out_rows = nullptr;    // [P] output row of each pair
   int32_t* in_rank = nullptr;     // [P] rank of the input in key order (== in_rows if sorted)
-  int32_t* perm = nullptr;        // [a_in] rank -> caller row
+  int32_t* perm = nullptr;        // [a_in] rank -> caller row (null when sorted: identity)
   int64_t* off_dev = nullptr;     // [K+1] list boundaries (device copy)
 
   // Pair ranges per tile.  otile[k*n_otiles + t] = global position of the first

@@ -154,10 +154,9 @@ def _sq(a):
     return None if a is None else np.asarray(a, np.float64) ** 2
 
 
-@pytest.mark.parametrize("case", CONV_CASES, ids=[str(i) for i in range(len(CONV_CASES))])
-def test_conv_fwd_bwd_parity(scn, case):
+def _conv_check(scn, case, inputs, seed):
     f, s, B, dims, n, Cin, Cout, relu = case
-    coords, grid, x, g_in, W, bias = _conv_inputs(case, 100 + CONV_CASES.index(case))
+    coords, grid, x, g_in, W, bias = inputs
     g, o = _rb_pair(scn, coords, grid, f, s)
     _check_rulebook(g, o)
     # forward
@@ -169,7 +168,7 @@ def test_conv_fwd_bwd_parity(scn, case):
     assert_close("g_out", host(god), go_ref, sig_g)
     # backward; output gradients vanish where the oracle's pre-activation sits
     # within rounding of the ReLU kink, so the mask is the same on both sides
-    rng = stream_rng(200 + CONV_CASES.index(case), 2)
+    rng = stream_rng(seed, 2)
     dy = rng.uniform(-1, 1, size=(g.a_out, Cout)).astype(np.float32)
     dg = rng.uniform(-1, 1, size=Cout).astype(np.float32)
     if relu:
@@ -183,6 +182,25 @@ def test_conv_fwd_bwd_parity(scn, case):
     out = scn.conv_bwd(g, dev(x), dev(g_in), dev(W), yd, god, dev(dy), dev(dg), relu=relu)
     for k in ("dx", "dW", "dbias", "dg_in"):
         assert_close(k, host(out[k]), ref[k], sig[k])
+    return g
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[str(i) for i in range(len(CONV_CASES))])
+def test_conv_fwd_bwd_parity(scn, case):
+    i = CONV_CASES.index(case)
+    _conv_check(scn, case, _conv_inputs(case, 100 + i), 200 + i)
+
+
+@pytest.mark.parametrize("case", [CONV_CASES[2], CONV_CASES[4], CONV_CASES[10]],
+                         ids=["f3s1", "f2s2", "f2s1-64"])
+def test_conv_sorted_input(scn, case):
+    """Sites listed in key order: the rulebook keeps no rank-to-row table and
+    the input gradient writes ranks directly."""
+    coords, grid, x, g_in, W, bias = _conv_inputs(case, 400 + CONV_CASES.index(case))
+    order = np.argsort(keys_of(coords, grid), kind="stable")
+    g = _conv_check(scn, case, (coords[order], grid, x[order], g_in, W, bias),
+                    500 + CONV_CASES.index(case))
+    assert g.input_sorted
 
 
 def test_conv_without_bias_and_partial_outputs(scn):
