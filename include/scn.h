@@ -85,8 +85,10 @@ typedef struct scn_rulebook_info {
  * active input site to row, find the active output sites of a filter of size
  * `filter` and stride `stride` and number them (H_out), and list for every
  * filter offset k which active input feeds which active output (the rulebook:
- * the blocks of the matrix Q of step 2 that are not the ground state).  The
- * same rulebook serves max-pooling when filter == stride.
+ * the blocks of the matrix Q of step 2 that are not the ground state).  A
+ * rulebook with stride >= 2 also serves max-pooling (it then keeps the
+ * window tables pooling uses: 4*K bytes per output and 4 bytes per input, 32
+ * when windows overlap).
  *
  *  coords  device int32[n][4] rows (b, x, y, z); row i is row i of the
  *          layer's feature matrix.  Not retained.
@@ -179,13 +181,14 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
 
 /*
  * Sparse max-pooling forward (section 1.3, end: pooling "is similar" to the
- * convolution).  rb must have filter == stride (non-overlapping windows).
+ * convolution).  rb must have stride >= 2; windows may overlap (filter >
+ * stride: 3 over 2, the pooling the paper's networks use) or leave gaps.
  * For each active output o and channel c, y[o][c] is the maximum over the f^3
  * positions of the window, an active position holding x[row][c] and an
  * inactive one g_in[c]; ties keep the first position in ascending k.
  * argmax[o][c] receives that k.  g_out = g_in.
  *  x [a_in][C], g_in [C] -> y [a_out][C], g_out [C], argmax uint8 [a_out][C].
- * Errors: SCN_ERR_INVALID, SCN_ERR_UNSUPPORTED (filter != stride), SCN_ERR_HIP.
+ * Errors: SCN_ERR_INVALID, SCN_ERR_UNSUPPORTED (stride 1), SCN_ERR_HIP.
  */
 scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* g_in,
                            int32_t C, float* y, float* g_out, uint8_t* argmax,
@@ -198,11 +201,15 @@ size_t scn_maxpool_bwd_workspace_bytes(const scn_rulebook* rb, int32_t C);
  * Gradient of scn_maxpool_fwd: dy[o][c] flows to the winning position; a
  * winning inactive position passes it to the ground state, and g_out = g_in
  * passes dg_out through:
- *   dx[r][c] = dy[o][c] if r is the active position argmax[o][c] of window o, else 0
+ *   dx[r][c] = sum over the windows o containing r of dy[o][c] if r is the
+ *              active position argmax[o][c] of window o (one window at most
+ *              when filter <= stride, up to 8 when 3 over 2; summed in a
+ *              fixed order)
  *   dg_in[c] = dg_out[c] + sum_{o: argmax[o][c] inactive} dy[o][c]
  *  argmax [a_out][C] from scn_maxpool_fwd, dy [a_out][C], dg_out [C] or NULL.
  *  dx [a_in][C] (every row written), dg_in [C] (NULL: not computed).
- * Errors: SCN_ERR_INVALID, SCN_ERR_UNSUPPORTED, SCN_ERR_WORKSPACE, SCN_ERR_HIP.
+ * Errors: SCN_ERR_INVALID, SCN_ERR_UNSUPPORTED (stride 1), SCN_ERR_WORKSPACE,
+ *         SCN_ERR_HIP.
  */
 scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const float* dy,
                            const float* dg_out, int32_t C, float* dx, float* dg_in, void* ws,

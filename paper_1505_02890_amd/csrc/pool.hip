@@ -141,7 +141,7 @@ __global__ void __launch_bounds__(256) maxpool_bwd_vec_kernel(const int32_t* __r
         const float4 v = make_float4(k0 == (uint32_t)k ? d.x : 0.f, k1 == (uint32_t)k ? d.y : 0.f,
                                      k2 == (uint32_t)k ? d.z : 0.f, k3 == (uint32_t)k ? d.w : 0.f);
         if (r >= 0) {
-          dx[(int64_t)r * nc4 + c4] = v;
+          if (dx) dx[(int64_t)r * nc4 + c4] = v;
         } else {
           s.x += v.x;
           s.y += v.y;
@@ -163,6 +163,58 @@ __global__ void __launch_bounds__(256) maxpool_bwd_vec_kernel(const int32_t* __r
     }
     part[(int64_t)blockIdx.x * nc4 + c4] = s;
   }
+}
+
+// Overlapping windows (filter > stride): an input lies in up to 8 windows.
+// dx[r][c] = sum over its windows (slot order 0..7, a fixed order) of
+// dy[o][c] where the input won channel c of window o.  win[r*8 + j] = o*K + k
+// or -1.
+__global__ void __launch_bounds__(256) maxpool_bwd_overlap_vec_kernel(
+    const int32_t* __restrict__ win, const uint32_t* __restrict__ argmax,
+    const float4* __restrict__ dy, int64_t a_in, int nc4, int per, int K,
+    float4* __restrict__ dx) {
+  const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
+  const int64_t r = (int64_t)blockIdx.x * per + rl;
+  if (rl >= per || r >= a_in) return;
+  int32_t t[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) t[j] = win[r * 8 + j];
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    if (t[j] < 0) continue;
+    const int32_t o = t[j] / K;
+    const uint32_t k = (uint32_t)(t[j] - o * K);
+    const int64_t jj = (int64_t)o * nc4 + c4;
+    const uint32_t am = argmax[jj];
+    const float4 d = dy[jj];
+    if ((am & 255u) == k) v.x += d.x;
+    if (((am >> 8) & 255u) == k) v.y += d.y;
+    if (((am >> 16) & 255u) == k) v.z += d.z;
+    if ((am >> 24) == k) v.w += d.w;
+  }
+  dx[r * nc4 + c4] = v;
+}
+
+__global__ void __launch_bounds__(256) maxpool_bwd_overlap_kernel(const int32_t* __restrict__ win,
+                                                                  const uint8_t* __restrict__ argmax,
+                                                                  const float* __restrict__ dy,
+                                                                  int64_t a_in, int C, int K,
+                                                                  float* __restrict__ dx) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a_in * C) return;
+  const int64_t r = i / C;
+  const int c = (int)(i - r * C);
+  float v = 0.f;
+  for (int j = 0; j < 8; ++j) {
+    const int32_t t = win[r * 8 + j];
+    if (t < 0) continue;
+    const int32_t o = t / K;
+    const int k = t - o * K;
+    const int64_t jj = (int64_t)o * C + c;
+    if (argmax[jj] == k) v += dy[jj];
+  }
+  dx[i] = v;
 }
 
 // dx rows of inputs that lie in no window (a grid edge the windows do not
@@ -252,8 +304,8 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
     set_error("scn_maxpool_fwd: invalid argument");
     return SCN_ERR_INVALID;
   }
-  if (rb->f != rb->s || !rb->nbr) {
-    set_error("scn_maxpool_fwd: only non-overlapping windows (filter == stride) are supported");
+  if (!rb->nbr) {
+    set_error("scn_maxpool_fwd: pooling needs a rulebook with stride >= 2");
     return SCN_ERR_UNSUPPORTED;
   }
   if (rb->a_out > 0) {
@@ -300,8 +352,8 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
     set_error("scn_maxpool_bwd: invalid argument");
     return SCN_ERR_INVALID;
   }
-  if (rb->f != rb->s || !rb->nbr) {
-    set_error("scn_maxpool_bwd: only non-overlapping windows (filter == stride) are supported");
+  if (!rb->nbr) {
+    set_error("scn_maxpool_bwd: pooling needs a rulebook with stride >= 2");
     return SCN_ERR_UNSUPPORTED;
   }
   const size_t need = scn_maxpool_bwd_workspace_bytes(rb, C);
@@ -311,8 +363,41 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
   }
   float* part = dg_in ? static_cast<float*>(ws) : nullptr;
   const bool vec = pool_vec_ok(C, {dy, dx, part}, argmax);
+  const bool overlap = rb->inv_slots == 8;
   int64_t nblk = 0;
-  if (vec) {
+  if (overlap) {
+    // dx per input over its (up to 8) windows, then the ground-state sums
+    // output-major
+    if (rb->a_in > 0) {
+      if (vec) {
+        const int nc4 = C / 4, per = 256 / nc4;
+        hipLaunchKernelGGL(maxpool_bwd_overlap_vec_kernel, dim3(nblocks(rb->a_in, per)), dim3(256),
+                           0, st, rb->inv, reinterpret_cast<const uint32_t*>(argmax),
+                           reinterpret_cast<const float4*>(dy), rb->a_in, nc4, per, rb->K,
+                           reinterpret_cast<float4*>(dx));
+      } else {
+        hipLaunchKernelGGL(maxpool_bwd_overlap_kernel, dim3(nblocks(rb->a_in * C, 256)), dim3(256),
+                           0, st, rb->inv, argmax, dy, rb->a_in, C, rb->K, dx);
+      }
+      SCN_LAUNCH_CHECK();
+    }
+    if (dg_in) {
+      nblk = std::max<int64_t>(1, ceil_div(rb->a_out, vec ? PBV_ROWS : PB_ROWS));
+      if (rb->a_out > 0) {
+        if (vec) {
+          // f > s only for 3 over 2
+          hipLaunchKernelGGL(maxpool_bwd_vec_kernel<3>, dim3((unsigned)nblk), dim3(256), 0, st,
+                             rb->nbr, reinterpret_cast<const uint32_t*>(argmax),
+                             reinterpret_cast<const float4*>(dy), rb->a_out, C / 4, nullptr,
+                             reinterpret_cast<float4*>(part));
+        } else {
+          hipLaunchKernelGGL(maxpool_bwd_ground_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
+                             rb->nbr, argmax, dy, rb->a_out, C, rb->K, part);
+        }
+        SCN_LAUNCH_CHECK();
+      }
+    }
+  } else if (vec) {
     // one pass: dx of the inputs in windows and the ground-state partial sums
     nblk = std::max<int64_t>(1, ceil_div(rb->a_out, PBV_ROWS));
     if (rb->a_in > 0) {

@@ -294,7 +294,7 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
     int64_t nt, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
     GridDev gi, const int32_t* __restrict__ perm, const uint64_t* __restrict__ pos,
     int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows, int32_t* __restrict__ in_rank,
-    int32_t* __restrict__ nbr, int32_t* __restrict__ inv) {
+    int32_t* __restrict__ nbr, int32_t* __restrict__ inv, int inv_slots) {
   constexpr int K = F * F * F;
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t t = o >> 6;
@@ -323,7 +323,13 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
       in_rows[p] = row;
       out_rows[p] = (int32_t)o;
       if (in_rank) in_rank[p] = (int32_t)rank[k];
-      if (nbr) inv[row] = (int32_t)(o * K + k);
+      if (nbr) {
+        // input -> its window(s): one slot, or (overlapping windows, f > s,
+        // at most two per axis) the slot picked by which of the two it is
+        const int kx = k % F, ky = (k / F) % F, kz = k / (F * F);
+        const int slot = inv_slots == 1 ? 0 : (kx >= s) | ((ky >= s) << 1) | ((kz >= s) << 2);
+        inv[(int64_t)row * inv_slots + slot] = (int32_t)(o * K + k);
+      }
     }
     if (nbr && live) nbr[o * K + k] = row;
   }
@@ -496,7 +502,9 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   }
   const int64_t a_out = hb->a_out;
   const bool sorted = !(hb->flags & F_UNSORTED);
-  const bool pool = (f == s);
+  // pooling tables (window rows per output, windows per input) for stride >= 2
+  const bool pool = s >= 2;
+  const int inv_slots = pool ? (f > s ? 8 : 1) : 0;
   const int64_t nt = std::max<int64_t>(1, ceil_div(a_out, TILE));
   const int64_t nit = std::max<int64_t>(1, ceil_div(n, TILE));
   const int64_t pmax = std::min<int64_t>(n, a_out) * K;
@@ -511,7 +519,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   const int64_t sz_oc = al(a_out * 16), sz_pair = al(pmax * 4), sz_perm = al(n * 4),
                 sz_off = al((K + 1) * 8), sz_ot = al((K * nt + 1) * 8),
                 sz_it = al((K * nit + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
-                sz_inv = pool ? al(n * 4) : 0;
+                sz_inv = pool ? al(n * 4 * inv_slots) : 0;
   const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair + sz_perm) + sz_off + sz_ot +
                         sz_it + sz_nbr + sz_inv;
   scn_rulebook* rb = new scn_rulebook();
@@ -543,6 +551,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   rb->itile = (int64_t*)take(sz_it);
   rb->nbr = pool ? (int32_t*)take(sz_nbr) : nullptr;
   rb->inv = pool ? (int32_t*)take(sz_inv) : nullptr;
+  rb->inv_slots = inv_slots;
   rb->f = f;
   rb->s = s;
   rb->K = K;
@@ -595,7 +604,8 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
                      nt, K, rb->off_dev);
   SCN_LAUNCH_CHECK();
   if (pool && n > 0) {
-    hipLaunchKernelGGL(fill_i32_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, rb->inv, n,
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(blocks_for(n * inv_slots, 256)), dim3(256), 0, st,
+                       rb->inv, n * inv_slots,
                        -1);
     SCN_LAUNCH_CHECK();
   }
@@ -604,7 +614,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
       hipLaunchKernelGGL(fn, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st, masks,
                          rb->out_coords, a_out, nt, s, inb, ipref, gi, rb->perm,
                          (const uint64_t*)rb->otile, rb->in_rows, rb->out_rows,
-                         sorted ? nullptr : rb->in_rank, rb->nbr, rb->inv);
+                         sorted ? nullptr : rb->in_rank, rb->nbr, rb->inv, inv_slots);
     };
     if (f == 1) em(emit_pairs_kernel<1>); else if (f == 2) em(emit_pairs_kernel<2>); else em(emit_pairs_kernel<3>);
     SCN_LAUNCH_CHECK();

@@ -79,10 +79,14 @@ struct scn_rulebook {
   int64_t n_itiles = 0;
   int64_t* itile = nullptr;
 
-  // Pool helpers (filter == stride only): nbr[o*K + k] = input row at s*o+k or -1;
-  // inv[r] = o*K + k of the unique window containing input r, or -1.
+  // Pool helpers (stride >= 2 only): nbr[o*K + k] = input row at s*o+k or -1;
+  // inv[r*inv_slots + j] = o*K + k of a window containing input r, or -1.  With
+  // filter <= stride an input lies in at most one window (inv_slots = 1); with
+  // filter > stride (3 over 2) in at most two per axis, slot j = sum over axes
+  // of [k_axis >= s] << axis (inv_slots = 8).
   int32_t* nbr = nullptr;
   int32_t* inv = nullptr;
+  int inv_slots = 0;
 
   void* block = nullptr;  // single allocation holding all arrays above
 };

@@ -187,18 +187,22 @@ def conv_layer_interior(scn, coords, grid, x, g_in, W, bias, f, s, relu, seed, n
     return def_oc, g.out_grid
 
 
-def pool_layer_interior(scn, coords, grid, x, g_in, f, seed, n_sub=6000):
+def pool_layer_interior(scn, coords, grid, x, g_in, f, seed, n_sub=6000, s=None):
+    """Max-pool (filter f, stride s, default s = f) at full size; outputs whose
+    window lies in an interior sub-box are compared with the oracle run on the
+    sub-box alone."""
+    s = f if s is None else s
     x = _f32(x)
     g_in = _f32(g_in)
-    g = scn.build_rulebook(dev(np.ascontiguousarray(coords, np.int32)), grid, f, f)
-    def_oc = check_rulebook_definition(g, coords, grid, f, f)
+    g = scn.build_rulebook(dev(np.ascontiguousarray(coords, np.int32)), grid, f, s)
+    def_oc = check_rulebook_definition(g, coords, grid, f, s)
     goc = host(g.out_coords())
     yd, god, am = scn.maxpool_fwd(g, dev(x), dev(g_in))
     m, b, lo, hi = subbox(coords, n_sub, seed)
     sub = np.ascontiguousarray(np.asarray(coords)[m], np.int32)
-    o = oracle.Rulebook(sub, grid, f, f)
+    o = oracle.Rulebook(sub, grid, f, s)
     oc = o.arrays().out_coords.astype(np.int64)
-    io = (oc[:, 0] == b) & np.all((f * oc[:, 1:4] >= lo) & (f * oc[:, 1:4] + f - 1 <= hi), axis=1)
+    io = (oc[:, 0] == b) & np.all((s * oc[:, 1:4] >= lo) & (s * oc[:, 1:4] + f - 1 <= hi), axis=1)
     y_ref, _, ak_ref, _ = oracle.maxpool_fwd(o, x[m], g_in)
     gr = find_rows(goc, g.out_grid, oc[io])
     assert np.array_equal(host(yd)[gr], y_ref[io].astype(np.float32))
@@ -209,9 +213,14 @@ def pool_layer_interior(scn, coords, grid, x, g_in, f, seed, n_sub=6000):
     dy_full[gr] = dy_o[io]
     dx_ref, dg_ref = oracle.maxpool_bwd(o, x[m], g_in, dy_o, None)
     dxd, dgd = scn.maxpool_bwd(g, am, dev(dy_full))
-    # every input of the cube: its window is interior (same argmax on both
-    # sides) or carries a zero output gradient on both sides
-    assert np.array_equal(host(dxd)[np.nonzero(m)[0]], dx_ref.astype(np.float32))
+    # every input of the cube: each of its windows is interior (same argmax on
+    # both sides) or carries a zero output gradient on both sides
+    rows = np.nonzero(m)[0]
+    if f <= s:
+        assert np.array_equal(host(dxd)[rows], dx_ref.astype(np.float32))
+    else:
+        sig_dx = np.sqrt(oracle.maxpool_bwd(o, x[m], g_in, _sq(dy_o), None)[0])
+        assert_close("pool dx", host(dxd)[rows], dx_ref, sig_dx)
     sig = np.sqrt(oracle.maxpool_bwd(o, x[m], g_in, _sq(dy_o), None)[1])
     assert_close("pool dg_in", host(dgd), dg_ref, sig)
     return def_oc, g.out_grid
@@ -323,6 +332,9 @@ def test_surfaces_first_levels_interior(scn):
     xp = stream_rng(cfg.seed, 9).standard_normal((len(oc), L0.cout)).astype(np.float32)
     xp[xp < 0] = 0.0  # ReLU-like zeros: many ties with the zero ground state
     pool_layer_interior(scn, oc, og, xp, np.zeros(L0.cout, np.float32), 2, seed=cfg.seed + 1)
+    # the paper's overlapping 3x3x3 stride-2 pooling on the same level
+    pool_layer_interior(scn, oc, og, xp, np.zeros(L0.cout, np.float32), 3, seed=cfg.seed + 2,
+                        s=2)
 
 
 def test_microbenchmark_interior(scn):

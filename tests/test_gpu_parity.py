@@ -268,25 +268,30 @@ def test_conv_workspace_checked(scn):
 # --------------------------------------------------------------------------
 
 POOL_CASES = [
-    # (f, B, dims, n, C, zero_frac, g_scale)
-    (2, 2, (12, 11, 10), 500, 16, 0.0, 0.5),
-    (2, 1, (9, 9, 9), 400, 1, 0.5, 0.0),     # many exact ties with g = 0
-    (2, 3, (70, 6, 7), 900, 33, 0.3, 0.0),
-    (3, 1, (13, 14, 12), 600, 8, 0.0, 2.0),  # ground state often the maximum
-    (2, 1, (8, 8, 8), 512, 64, 0.2, -0.1),   # every site active
+    # (f, s, B, dims, n, C, zero_frac, g_scale)
+    (2, 2, 2, (12, 11, 10), 500, 16, 0.0, 0.5),
+    (2, 2, 1, (9, 9, 9), 400, 1, 0.5, 0.0),     # many exact ties with g = 0
+    (2, 2, 3, (70, 6, 7), 900, 33, 0.3, 0.0),
+    (3, 3, 1, (13, 14, 12), 600, 8, 0.0, 2.0),  # ground state often the maximum
+    (2, 2, 1, (8, 8, 8), 512, 64, 0.2, -0.1),   # every site active
+    (3, 2, 1, (13, 14, 12), 600, 16, 0.0, 0.5),  # overlapping windows (MP3/2)
+    (3, 2, 2, (9, 11, 10), 500, 5, 0.3, 0.0),    # MP3/2, one channel per thread, ties
+    (3, 2, 1, (7, 7, 7), 343, 64, 0.2, 0.1),     # MP3/2, every site active
+    (3, 2, 2, (30, 9, 8), 900, 12, 0.0, 1.5),    # MP3/2, ground state often wins
+    (2, 3, 1, (14, 13, 11), 500, 8, 0.0, 0.5),   # gaps between windows
 ]
 
 
 @pytest.mark.parametrize("case", POOL_CASES, ids=[str(i) for i in range(len(POOL_CASES))])
 def test_maxpool_parity(scn, case):
-    f, B, dims, n, C, zf, gs = case
+    f, s, B, dims, n, C, zf, gs = case
     rng = stream_rng(300 + POOL_CASES.index(case), 0)
     coords = random_sites(rng, B, dims, n)
     x = rng.standard_normal((len(coords), C)).astype(np.float32)
     x[rng.random(x.shape) < zf] = 0.0
     g_in = (np.abs(rng.standard_normal(C)) * gs).astype(np.float32)
     grid = (B,) + tuple(dims)
-    g, o = _rb_pair(scn, coords, grid, f, f)
+    g, o = _rb_pair(scn, coords, grid, f, s)
     _check_rulebook(g, o)
     y_ref, go_ref, ak_ref, _ = oracle.maxpool_fwd(o, x, g_in)
     yd, god, am = scn.maxpool_fwd(g, dev(x), dev(g_in))
@@ -297,14 +302,20 @@ def test_maxpool_parity(scn, case):
     dg = rng.uniform(-1, 1, size=C).astype(np.float32)
     dx_ref, dgi_ref = oracle.maxpool_bwd(o, x, g_in, dy, dg)
     dxd, dgid = scn.maxpool_bwd(g, am, dev(dy), dev(dg))
-    assert np.array_equal(host(dxd), dx_ref.astype(np.float32))
+    if f <= s:
+        # every input has at most one window: dx is a copy of dy entries
+        assert np.array_equal(host(dxd), dx_ref.astype(np.float32))
+    else:
+        # an input sums dy over up to 8 windows (fp32, fixed order)
+        sig_dx = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), None)[0])
+        assert_close("dx", host(dxd), dx_ref, sig_dx)
     sig = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), _sq(dg))[1])
     assert_close("dg_in", host(dgid), dgi_ref, sig)
 
 
-def test_maxpool_rejects_overlapping_windows(scn):
+def test_maxpool_needs_stride_two(scn):
     coords = random_sites(stream_rng(1, 1), 1, (8, 8, 8), 50)
-    g = scn.build_rulebook(dev(coords), (1, 8, 8, 8), 3, 2)
+    g = scn.build_rulebook(dev(coords), (1, 8, 8, 8), 2, 1)
     x = dev(np.ones((50, 4), np.float32))
     with pytest.raises(scn.ScnError) as e:
         scn.maxpool_fwd(g, x, dev(np.zeros(4, np.float32)))
