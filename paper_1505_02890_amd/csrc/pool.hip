@@ -86,21 +86,31 @@ __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __re
   if (ol >= per || o >= a_out) return;
   const float4 g = g_in[c4];
   const int32_t* nb = nbr + o * K;
-  float4 v[K];
-#pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const int32_t r = nb[k];
-    v[k] = r >= 0 ? x[(int64_t)r * nc4 + c4] : g;
-  }
   // first strict maximum in ascending k, per channel
-  float4 best = v[0];
+  // (planes of a 3-wide window one by one; smaller windows all at once)
+  constexpr int PL = F == 3 ? F * F : F * F * F, NPL = K / PL;
+  float4 best = make_float4(0.f, 0.f, 0.f, 0.f);
   uint32_t b0 = 0, b1 = 0, b2 = 0, b3 = 0;
+#pragma unroll 1
+  for (int kz = 0; kz < NPL; ++kz) {
+    float4 v[PL];
 #pragma unroll
-  for (int k = 1; k < K; ++k) {
-    if (v[k].x > best.x) { best.x = v[k].x; b0 = k; }
-    if (v[k].y > best.y) { best.y = v[k].y; b1 = k; }
-    if (v[k].z > best.z) { best.z = v[k].z; b2 = k; }
-    if (v[k].w > best.w) { best.w = v[k].w; b3 = k; }
+    for (int i = 0; i < PL; ++i) {
+      const int32_t r = nb[kz * PL + i];
+      v[i] = r >= 0 ? x[(int64_t)r * nc4 + c4] : g;
+    }
+#pragma unroll
+    for (int i = 0; i < PL; ++i) {
+      const uint32_t k = kz * PL + i;
+      if (k == 0) {
+        best = v[i];
+        continue;
+      }
+      if (v[i].x > best.x) { best.x = v[i].x; b0 = k; }
+      if (v[i].y > best.y) { best.y = v[i].y; b1 = k; }
+      if (v[i].z > best.z) { best.z = v[i].z; b2 = k; }
+      if (v[i].w > best.w) { best.w = v[i].w; b3 = k; }
+    }
   }
   y[o * nc4 + c4] = best;
   argmax[o * nc4 + c4] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
@@ -176,22 +186,29 @@ __global__ void __launch_bounds__(256) maxpool_bwd_overlap_vec_kernel(
   const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
   const int64_t r = (int64_t)blockIdx.x * per + rl;
   if (rl >= per || r >= a_in) return;
-  int32_t t[8];
+  const int4 w0 = reinterpret_cast<const int4*>(win)[2 * r];
+  const int4 w1 = reinterpret_cast<const int4*>(win)[2 * r + 1];
+  const int32_t t[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+  // branch-free: an empty slot reads window 0 with an offset no argmax holds,
+  // so all slot loads are in flight together
+  uint32_t am[8];
+  float4 d[8];
+  uint32_t kk[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) t[j] = win[r * 8 + j];
+  for (int j = 0; j < 8; ++j) {
+    const int32_t o = t[j] >= 0 ? t[j] / K : 0;
+    kk[j] = t[j] >= 0 ? (uint32_t)(t[j] - o * K) : 255u;
+    const int64_t jj = (int64_t)o * nc4 + c4;
+    am[j] = argmax[jj];
+    d[j] = dy[jj];
+  }
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    if (t[j] < 0) continue;
-    const int32_t o = t[j] / K;
-    const uint32_t k = (uint32_t)(t[j] - o * K);
-    const int64_t jj = (int64_t)o * nc4 + c4;
-    const uint32_t am = argmax[jj];
-    const float4 d = dy[jj];
-    if ((am & 255u) == k) v.x += d.x;
-    if (((am >> 8) & 255u) == k) v.y += d.y;
-    if (((am >> 16) & 255u) == k) v.z += d.z;
-    if ((am >> 24) == k) v.w += d.w;
+    v.x += (am[j] & 255u) == kk[j] ? d[j].x : 0.f;
+    v.y += ((am[j] >> 8) & 255u) == kk[j] ? d[j].y : 0.f;
+    v.z += ((am[j] >> 16) & 255u) == kk[j] ? d[j].z : 0.f;
+    v.w += (am[j] >> 24) == kk[j] ? d[j].w : 0.f;
   }
   dx[r * nc4 + c4] = v;
 }
@@ -215,6 +232,46 @@ __global__ void __launch_bounds__(256) maxpool_bwd_overlap_kernel(const int32_t*
     if (argmax[jj] == k) v += dy[jj];
   }
   dx[i] = v;
+}
+
+// Ground-state partial sums alone (the overlapping case computes dx input-
+// major): part[blk][c] sums, over the block's outputs in a fixed order, dy[o][c]
+// where the winner of (o, c) is an inactive position.  Only the winners' window
+// entries are read.
+__global__ void __launch_bounds__(256) maxpool_ground_vec_kernel(const int32_t* __restrict__ nbr,
+                                                                 const uint32_t* __restrict__ argmax,
+                                                                 const float4* __restrict__ dy,
+                                                                 int64_t a_out, int nc4, int K,
+                                                                 float4* __restrict__ part) {
+  __shared__ float4 red[256];
+  const int rows = 256 / nc4;
+  const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
+  const int64_t o0 = (int64_t)blockIdx.x * PBV_ROWS;
+  const int64_t o1 = min<int64_t>(o0 + PBV_ROWS, a_out);
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (rl < rows)
+    for (int64_t o = o0 + rl; o < o1; o += rows) {
+      const int64_t j = o * nc4 + c4;
+      const uint32_t am = argmax[j];
+      const float4 d = dy[j];
+      const int32_t* nb = nbr + o * K;
+      if (nb[am & 255u] < 0) s.x += d.x;
+      if (nb[(am >> 8) & 255u] < 0) s.y += d.y;
+      if (nb[(am >> 16) & 255u] < 0) s.z += d.z;
+      if (nb[am >> 24] < 0) s.w += d.w;
+    }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  if (rl == 0) {
+    for (int i = 1; i < rows; ++i) {
+      const float4 t = red[i * nc4 + c4];
+      s.x += t.x;
+      s.y += t.y;
+      s.z += t.z;
+      s.w += t.w;
+    }
+    part[(int64_t)blockIdx.x * nc4 + c4] = s;
+  }
 }
 
 // dx rows of inputs that lie in no window (a grid edge the windows do not
@@ -385,10 +442,9 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
       nblk = std::max<int64_t>(1, ceil_div(rb->a_out, vec ? PBV_ROWS : PB_ROWS));
       if (rb->a_out > 0) {
         if (vec) {
-          // f > s only for 3 over 2
-          hipLaunchKernelGGL(maxpool_bwd_vec_kernel<3>, dim3((unsigned)nblk), dim3(256), 0, st,
+          hipLaunchKernelGGL(maxpool_ground_vec_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
                              rb->nbr, reinterpret_cast<const uint32_t*>(argmax),
-                             reinterpret_cast<const float4*>(dy), rb->a_out, C / 4, nullptr,
+                             reinterpret_cast<const float4*>(dy), rb->a_out, C / 4, rb->K,
                              reinterpret_cast<float4*>(part));
         } else {
           hipLaunchKernelGGL(maxpool_bwd_ground_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
