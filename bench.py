@@ -15,6 +15,10 @@ convolution's output, and the CPU oracle timed on a bounded sample of the same
 workload.
 
     python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--no-cpu]
+
+With --network it instead times whole-network inference of the paper's cubic
+object-recognition networks (nC2-MP3/2, scales 20/40/80) and prints one JSON
+line per network.
 """
 from __future__ import annotations
 
@@ -43,6 +47,10 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-sites", type=int, default=60000,
                    help="input sites of the bounded CPU-oracle sample")
+    p.add_argument("--network", action="store_true",
+                   help="instead: whole-network inference throughput of the paper's cubic "
+                        "object-recognition networks (scales 20/40/80), one JSON line each")
+    p.add_argument("--batch", type=int, default=64, help="samples per batch for --network")
     return p.parse_args()
 
 
@@ -117,11 +125,64 @@ def cpu_baseline(cfg, n_sites: int):
     }
 
 
+def network_bench(batch: int, reps: int, warmup: int) -> None:
+    """Inference throughput of nC2-MP3/2 networks (the object-recognition
+    experiment of section 2): each sample is one seeded shell (ellipsoid or
+    rounded-box superquadric, random rotation, semi-axes scale/2 * U(0.6, 1.0))
+    centred in the network's input grid, features 1.0 at active sites, random
+    He-scaled weights.  A batch is timed end to end (every rulebook build,
+    convolution and pooling, inputs resident in HBM); median over `reps`."""
+    import torch
+
+    from gen import shell_sites, stream_rng
+    from paper_1505_02890_amd.network import SparseNet, input_size, macs
+
+    # the paper's figures for these networks (cubic lattice, GTX 780), context only
+    paper = {20: (36, 1190), 40: (126, 794), 80: (406, 310)}
+    for scale, levels in ((20, 4), (40, 5), (80, 6)):
+        m = input_size(levels)
+        rows = []
+        for b in range(batch):
+            rng = stream_rng(150502890 + scale, b)
+            semi = [0.5 * scale * float(rng.uniform(0.6, 1.0)) for _ in range(3)]
+            power = (2, 4)[int(rng.integers(2))]
+            sh = shell_sites(rng, m, semi, [m / 2.0] * 3, power)
+            rows.append(np.concatenate([np.full((len(sh), 1), b, np.int64), sh], axis=1))
+        c = np.ascontiguousarray(np.concatenate(rows).astype(np.int32))
+        cd = torch.from_numpy(c).cuda()
+        xd = torch.ones((len(c), 1), dtype=torch.float32, device="cuda")
+        net = SparseNet(levels, seed=scale)
+        for _ in range(warmup):
+            net.forward(cd, xd, batch)
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            out, oc, rec = net.forward(cd, xd, batch)
+            torch.cuda.synchronize()
+            times.append(time.perf_counter() - t0)
+        t = float(np.median(times))
+        print(json.dumps({
+            "metric": "sparse CNN inference throughput (nC2-MP3/2 cubic network)",
+            "value": round(batch / t, 1), "unit": "tests/s", "higher_is_better": True,
+            "scale": scale, "levels": levels, "input_grid": m, "batch": batch,
+            "active_input_sites_per_sample": round(len(c) / batch, 1),
+            "macs_per_sample_millions": round(macs(rec) / batch / 1e6, 2),
+            "ms_per_batch": round(t * 1e3, 3), "final_sites": int(out.shape[0]),
+            "paper_gtx780": {"million_operations": paper[scale][0],
+                             "tests_per_s": paper[scale][1], "note": "context only"},
+            "dtype": "f32", "data": "synthetic (seeded shells)",
+        }), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
+    if args.network:
+        network_bench(args.batch, max(args.steps, 5), args.warmup)
+        return
     import torch
 
     import paper_1505_02890_amd as scn

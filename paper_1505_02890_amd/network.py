@@ -1,0 +1,103 @@
+"""Whole-network sparse CNN inference on the C ABI: the cubic networks of the
+paper's 3D object-recognition experiment (section 2, "Object recognition"),
+
+    32C2 - MP3/2 - 64C2 - MP3/2 - 96C2 - ... - output,
+
+with L levels of 3x3x3 stride-2 max-pooling.  Every convolution has a 2x2x2
+filter, stride 1, ReLU, and 32*(i+1) output channels at level i; "output" is a
+1x1x1 convolution to the class scores on the single site that remains.
+
+All padding is valid, so the input grid is the size the network reduces to one
+site: working back from 1, a C2 adds 1 and an MP3/2 maps m to 2m + 1, which
+gives 62, 126 and 254 for 4, 5 and 6 levels.
+
+Every step runs in the library's kernels (rulebook build, contraction,
+pooling); this module only sequences the calls and keeps the layer state.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import List
+
+import torch
+
+from . import _lib as scn
+
+
+def input_size(levels: int) -> int:
+    """Grid size that `levels` x (C2, MP3/2) followed by one C2 reduce to 1."""
+    m = 2  # the last C2 maps 2 -> 1
+    for _ in range(levels):
+        m = 2 * m + 1  # MP3/2: (m_in - 3) / 2 + 1 = m
+        m += 1         # C2 before it
+    return m
+
+
+@dataclass
+class Layer:
+    kind: str            # "conv" or "pool"
+    f: int
+    s: int
+    cin: int = 0
+    cout: int = 0
+    relu: bool = False
+
+
+def architecture(levels: int, classes: int = 50, width: int = 32, cin: int = 1) -> List[Layer]:
+    """nC2-MP3/2 per level (n = width, 2*width, ...), a last C2, then the 1x1x1
+    class layer."""
+    layers: List[Layer] = []
+    c = cin
+    for i in range(levels):
+        layers.append(Layer("conv", 2, 1, c, width * (i + 1), True))
+        layers.append(Layer("pool", 3, 2))
+        c = width * (i + 1)
+    layers.append(Layer("conv", 2, 1, c, width * (levels + 1), True))
+    layers.append(Layer("conv", 1, 1, width * (levels + 1), classes, False))
+    return layers
+
+
+class SparseNet:
+    """Random-initialised weights (He scaling) for `architecture(levels)`; the
+    input ground state is 0 (an empty site holds no signal)."""
+
+    def __init__(self, levels: int, classes: int = 50, width: int = 32, seed: int = 0,
+                 device: str = "cuda"):
+        self.levels = levels
+        self.layers = architecture(levels, classes, width)
+        self.m = input_size(levels)
+        g = torch.Generator().manual_seed(seed)
+        self.params = []
+        for L in self.layers:
+            if L.kind != "conv":
+                self.params.append(None)
+                continue
+            K = L.f ** 3
+            W = torch.randn(K, L.cin, L.cout, generator=g) * math.sqrt(2.0 / (K * L.cin))
+            b = torch.randn(L.cout, generator=g) * 0.05
+            self.params.append((W.to(device), b.to(device)))
+        self.device = device
+
+    def forward(self, coords: torch.Tensor, x: torch.Tensor, batch: int):
+        """coords int32 [n][4] (b, x, y, z) on the device, x [n][1].  Returns
+        (scores [a][classes], out_coords [a][4], per-layer records)."""
+        grid = (batch, self.m, self.m, self.m)
+        g = torch.zeros(x.shape[1], dtype=torch.float32, device=self.device)
+        rec = []
+        for L, p in zip(self.layers, self.params):
+            rb = scn.build_rulebook(coords, grid, L.f, L.s)
+            if L.kind == "conv":
+                W, b = p
+                x, g = scn.conv_fwd(rb, x, g, W, b, relu=L.relu)
+                rec.append(("conv", rb.a_in, rb.a_out, rb.n_pairs, L.cin, L.cout))
+            else:
+                x, g, _ = scn.maxpool_fwd(rb, x, g)
+                rec.append(("pool", rb.a_in, rb.a_out, rb.n_pairs, x.shape[1], x.shape[1]))
+            coords, grid = rb.out_coords(), tuple(rb.out_grid)
+        return x, coords, rec
+
+
+def macs(records) -> int:
+    """Multiply-accumulates of the convolutions (active pairs only)."""
+    return int(sum(P * ci * co for kind, _, _, P, ci, co in records if kind == "conv"))

@@ -1,0 +1,72 @@
+"""A whole nC2-MP3/2 network (the object-recognition networks of section 2)
+through the C ABI against the same chain of layers in the oracle.
+
+The oracle builds every layer's rulebook from its own output sites, so the
+two chains share only the seeded input and the weights."""
+from __future__ import annotations
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
+import oracle  # noqa: E402
+from gen import shell_sites, stream_rng  # noqa: E402
+from helpers import dev, host  # noqa: E402
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def scn():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1505_02890_amd as m
+    m.lib()  # raises if the HIP library is missing
+    return m
+
+
+def _batch(batch, m, scale, seed):
+    rows = []
+    for b in range(batch):
+        rng = stream_rng(seed, b)
+        semi = [0.5 * scale * float(rng.uniform(0.6, 1.0)) for _ in range(3)]
+        s = shell_sites(rng, m, semi, [m / 2.0] * 3, (2, 4)[int(rng.integers(2))])
+        rows.append(np.concatenate([np.full((len(s), 1), b, np.int64), s], axis=1))
+    return np.ascontiguousarray(np.concatenate(rows).astype(np.int32))
+
+
+@pytest.mark.parametrize("levels,width,scale", [(1, 4, 3.0), (2, 4, 6.0), (3, 3, 12.0)])
+def test_network_matches_oracle_chain(scn, levels, width, scale):
+    from paper_1505_02890_amd.network import SparseNet, input_size
+
+    batch = 3
+    m = input_size(levels)
+    coords = _batch(batch, m, scale, 4242 + levels)
+    net = SparseNet(levels, classes=5, width=width, seed=levels)
+    x = np.ones((len(coords), 1), np.float32)
+    out, oc, rec = net.forward(dev(coords, torch.int32), dev(x), batch)
+    assert [r[0] for r in rec] == [L.kind for L in net.layers]
+
+    c, grid, xr = coords, (batch, m, m, m), x.astype(np.float64)
+    g = np.zeros(1)
+    for L, p in zip(net.layers, net.params):
+        o = oracle.Rulebook(c, grid, L.f, L.s)
+        if L.kind == "conv":
+            W, b = (host(t).astype(np.float64) for t in p)
+            xr, g = oracle.conv_fwd(o, xr, g, W, b, relu=L.relu)
+        else:
+            xr, g, _, _ = oracle.maxpool_fwd(o, xr, g)
+        c, grid = o.arrays().out_coords, tuple(o.out_grid)
+
+    assert np.array_equal(host(oc), c)
+    # one final site per sample whose shell survives the network
+    assert len(c) == batch and np.array_equal(c[:, 0], np.arange(batch))
+    got = host(out).astype(np.float64)
+    scale_ref = np.sqrt(np.mean(xr ** 2)) + 1e-30
+    err = np.abs(got - xr)
+    assert np.all(err <= 1e-5 + 1e-4 * np.maximum(np.abs(xr), scale_ref)), err.max()
