@@ -50,7 +50,9 @@ def parse():
     p.add_argument("--network", action="store_true",
                    help="instead: whole-network inference throughput of the paper's cubic "
                         "object-recognition networks (scales 20/40/80), one JSON line each")
-    p.add_argument("--batch", type=int, default=64, help="samples per batch for --network")
+    p.add_argument("--batch", type=int, default=256,
+                   help="samples per batch for --network (capped per network by the "
+                        "rulebook's grid limit)")
     return p.parse_args()
 
 
@@ -141,8 +143,12 @@ def network_bench(batch: int, reps: int, warmup: int) -> None:
     paper = {20: (36, 1190), 40: (126, 794), 80: (406, 310)}
     for scale, levels in ((20, 4), (40, 5), (80, 6)):
         m = input_size(levels)
+        # the rulebook's occupancy bitmap holds at most 2^26 words per grid
+        # (the largest grid is the first convolution's output, m + 1 per axis)
+        words = (m + 1) * (m + 1) * ((m + 1 + 31) // 32)
+        batch_n = min(batch, (1 << 26) // words)
         rows = []
-        for b in range(batch):
+        for b in range(batch_n):
             rng = stream_rng(150502890 + scale, b)
             semi = [0.5 * scale * float(rng.uniform(0.6, 1.0)) for _ in range(3)]
             power = (2, 4)[int(rng.integers(2))]
@@ -153,21 +159,21 @@ def network_bench(batch: int, reps: int, warmup: int) -> None:
         xd = torch.ones((len(c), 1), dtype=torch.float32, device="cuda")
         net = SparseNet(levels, seed=scale)
         for _ in range(warmup):
-            net.forward(cd, xd, batch)
+            net.forward(cd, xd, batch_n)
         torch.cuda.synchronize()
         times = []
         for _ in range(reps):
             t0 = time.perf_counter()
-            out, oc, rec = net.forward(cd, xd, batch)
+            out, oc, rec = net.forward(cd, xd, batch_n)
             torch.cuda.synchronize()
             times.append(time.perf_counter() - t0)
         t = float(np.median(times))
         print(json.dumps({
             "metric": "sparse CNN inference throughput (nC2-MP3/2 cubic network)",
-            "value": round(batch / t, 1), "unit": "tests/s", "higher_is_better": True,
-            "scale": scale, "levels": levels, "input_grid": m, "batch": batch,
-            "active_input_sites_per_sample": round(len(c) / batch, 1),
-            "macs_per_sample_millions": round(macs(rec) / batch / 1e6, 2),
+            "value": round(batch_n / t, 1), "unit": "tests/s", "higher_is_better": True,
+            "scale": scale, "levels": levels, "input_grid": m, "batch": batch_n,
+            "active_input_sites_per_sample": round(len(c) / batch_n, 1),
+            "macs_per_sample_millions": round(macs(rec) / batch_n / 1e6, 2),
             "ms_per_batch": round(t * 1e3, 3), "final_sites": int(out.shape[0]),
             "paper_gtx780": {"million_operations": paper[scale][0],
                              "tests_per_s": paper[scale][1], "note": "context only"},
