@@ -18,5 +18,8 @@ from .synth import (  # noqa: F401
     bridge_walk,
     shell_sites,
     random_sites,
+    tetra_sites,
+    tetra_random_sites,
+    tetra_shell_sites,
     stream_rng,
 )

@@ -249,6 +249,95 @@ def random_sites(rng: np.random.Generator, batch: int, dims: Sequence[int], n: i
     return np.stack([b, x, y, z], axis=1).astype(np.int32)
 
 
+# --------------------------------------------------------------------------
+# tetrahedral lattice (skewed coordinates: the grid of size m is the sites
+# x + y + z < m; site (x, y, z) sits at x*e1 + y*e2 + z*e3 for unit vectors
+# at 60 degrees to each other, so the grid is a regular tetrahedron)
+# --------------------------------------------------------------------------
+
+_SQ3 = math.sqrt(3.0)
+_TETRA_BASIS = np.array([[1.0, 0.0, 0.0],
+                         [0.5, _SQ3 / 2.0, 0.0],
+                         [0.5, _SQ3 / 6.0, math.sqrt(2.0 / 3.0)]])   # rows e1, e2, e3
+# the twelve nearest neighbours of a site, in skewed coordinates
+_TETRA_NBRS = np.array([[1, 0, 0], [-1, 0, 0], [0, 1, 0], [0, -1, 0], [0, 0, 1], [0, 0, -1],
+                        [1, -1, 0], [-1, 1, 0], [1, 0, -1], [-1, 0, 1], [0, 1, -1], [0, -1, 1]],
+                       dtype=np.int64)
+
+
+def tetra_sites(m: int) -> np.ndarray:
+    """All sites x + y + z < m as int64[C(m+2, 3)][3] (x, y, z), z slowest."""
+    r = np.arange(max(int(m), 0))
+    z, y, x = np.meshgrid(r, r, r, indexing="ij")
+    keep = (x + y + z) < m
+    return np.stack([x[keep], y[keep], z[keep]], axis=1).astype(np.int64)
+
+
+def tetra_random_sites(rng: np.random.Generator, batch: int, m: int, n: int,
+                       shuffle: bool = True) -> np.ndarray:
+    """n distinct uniformly random sites of `batch` tetrahedral grids of size m
+    as int32[n][4] rows (b, x, y, z)."""
+    cell = tetra_sites(m)
+    vol = batch * len(cell)
+    n = min(int(n), vol)
+    flat = rng.choice(vol, size=n, replace=False)
+    if not shuffle:
+        flat = np.sort(flat)
+    b, i = flat // max(len(cell), 1), flat % max(len(cell), 1)
+    return np.concatenate([b[:, None], cell[i]], axis=1).astype(np.int32)
+
+
+def tetra_shell_sites(rng: np.random.Generator, m: int, semi: Sequence[float],
+                      power: int = 2) -> np.ndarray:
+    """The shell of `shell_sites` drawn on the tetrahedral grid of size m:
+    site p is on it iff F(p) <= 0 and one of its twelve neighbours has F > 0,
+    with F as there, evaluated at the site's position and centred on the
+    grid's centroid.  Sites outside the grid are dropped.  Returns
+    int64[n][3] (x, y, z) in skewed coordinates."""
+    assert power % 2 == 0 and power >= 2
+    R = _rotation(rng)
+    a = [float(v) for v in semi]
+    cs = (m - 1) / 4.0                       # centroid, skewed coordinates
+    reach = max(a) * (3.0 ** (0.5 - 1.0 / power)) + 2.0
+    # a skewed coordinate moves by at most sqrt(3/2) per unit of distance
+    h = int(math.ceil(reach * math.sqrt(1.5))) + 1
+    lo, hi = max(-1, int(math.floor(cs)) - h), min(m, int(math.ceil(cs)) + h)
+    r = np.arange(lo, hi + 1, dtype=np.int64)
+    E = _TETRA_BASIS
+
+    def F(pts: np.ndarray) -> np.ndarray:
+        d = pts.astype(np.float64) - cs
+        ph = [d[:, 0] * E[0][j] + d[:, 1] * E[1][j] + d[:, 2] * E[2][j] for j in range(3)]
+        out = np.full(len(pts), -1.0)
+        for j in range(3):
+            u = ph[0] * R[0][j] + ph[1] * R[1][j] + ph[2] * R[2][j]
+            t = u / a[j]
+            t2 = t * t
+            tp = t2
+            for _ in range(power // 2 - 1):
+                tp = tp * t2
+            out = out + tp
+        return out
+
+    found = []
+    for z in r:
+        yy, xx = np.meshgrid(r, r, indexing="ij")
+        pts = np.stack([xx.ravel(), yy.ravel(), np.full(xx.size, z)], axis=1)
+        pts = pts[(pts.min(axis=1) >= 0) & (pts.sum(axis=1) < m)]
+        if len(pts) == 0:
+            continue
+        pts = pts[F(pts) <= 0.0]
+        if len(pts) == 0:
+            continue
+        edge = np.zeros(len(pts), bool)
+        for d in _TETRA_NBRS:
+            edge |= F(pts + d) > 0.0
+        found.append(pts[edge])
+    if not found:
+        return np.zeros((0, 3), np.int64)
+    return np.concatenate(found, axis=0)
+
+
 def _to_coords(per_sample: List[np.ndarray], rng: Optional[np.random.Generator]) -> np.ndarray:
     rows = []
     for b, s in enumerate(per_sample):

@@ -24,6 +24,10 @@ from .build import LIB_PATH, build
 
 STATUS = {0: "ok", 1: "invalid", 2: "range", 3: "duplicate", 4: "overflow"}
 
+# section 1.2: the cubic lattice, and the tetrahedral lattice in skewed
+# coordinates (grid x + y + z < m, filter offsets kx + ky + kz < f)
+LATTICES = {"cubic": 0, "tetrahedral": 1}
+
 _lib = None
 
 
@@ -44,6 +48,8 @@ def lib():
         i64, i32 = ctypes.c_int64, ctypes.c_int32
         L.orc_rb_build.argtypes = [P, i64, P, i32, i32, ctypes.POINTER(P)]
         L.orc_rb_build.restype = ctypes.c_int
+        L.orc_rb_build_lattice.argtypes = [P, i64, P, i32, i32, i32, ctypes.POINTER(P)]
+        L.orc_rb_build_lattice.restype = ctypes.c_int
         L.orc_rb_free.argtypes = [P]
         L.orc_rb_info.argtypes = [P, P]
         L.orc_rb_offsets.argtypes = [P, P]
@@ -80,17 +86,20 @@ class RulebookArrays:
 
 
 class Rulebook:
-    """Owner of an oracle rulebook (H_in, H_out and the per-offset rule lists)."""
+    """Owner of an oracle rulebook (H_in, H_out and the per-offset rule lists)
+    on the cubic or the tetrahedral lattice."""
 
-    def __init__(self, coords: np.ndarray, grid: Sequence[int], f: int, s: int):
+    def __init__(self, coords: np.ndarray, grid: Sequence[int], f: int, s: int,
+                 lattice: str = "cubic"):
         c = np.ascontiguousarray(np.asarray(coords, dtype=np.int32).reshape(-1, 4))
         g = np.ascontiguousarray(np.asarray(grid, dtype=np.int64))
         h = ctypes.c_void_p()
-        rc = lib().orc_rb_build(_p(c), len(c), _p(g), int(f), int(s), ctypes.byref(h))
+        rc = lib().orc_rb_build_lattice(_p(c), len(c), _p(g), int(f), int(s),
+                                        LATTICES[lattice], ctypes.byref(h))
         if rc != 0:
             raise OracleError(rc)
         self._h = h
-        self.f, self.s = int(f), int(s)
+        self.f, self.s, self.lattice = int(f), int(s), lattice
         info = np.zeros(8, np.int64)
         lib().orc_rb_info(self._h, _p(info))
         self.a_in, self.a_out, self.n_pairs, self.K = (int(v) for v in info[:4])

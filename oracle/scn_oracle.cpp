@@ -13,6 +13,12 @@
 //    as in Figure 3 (a 2x2 filter on a 6x6 grid gives a 5x5 output);
 //  * output site o sees input sites s*o + k, k in [0, f)^3, offset index
 //    k = (kz*f + ky)*f + kx;
+//  * the tetrahedral lattice (section 1.2) is written in skewed integer
+//    coordinates: a grid of size m is the sites x + y + z < m (equal extents
+//    m on the three axes), a filter of size f the C(f+2, 3) offsets
+//    kx + ky + kz < f, numbered in the cubic scan order above restricted to
+//    those offsets, and output o is valid when its whole window lies in the
+//    grid, i.e. ox + oy + oz < floor((m - f) / s) + 1;
 //  * site key = ((b*mz + z)*my + y)*mx + x; output rows are numbered in
 //    ascending key order starting at 0;
 //  * W is stored offset-major: W[k][ci][co] (row k*Cin + ci of the
@@ -43,6 +49,8 @@ uint64_t key_of(const Grid& g, int64_t b, int64_t x, int64_t y, int64_t z) {
 
 struct Rulebook {
   int f = 0, s = 0, K = 0;
+  int lattice = 0;  // 0 cubic, 1 tetrahedral
+  std::vector<int> offs;  // offset k -> (kz*f + ky)*f + kx of the cube scan
   Grid gin, gout;
   int64_t a_in = 0;
   // H_in: active input location -> row of M_in (the paper's map H_in).
@@ -57,9 +65,10 @@ struct Rulebook {
 
   // offset index -> (kx, ky, kz)
   void offset(int k, int64_t* kx, int64_t* ky, int64_t* kz) const {
-    *kx = k % f;
-    *ky = (k / f) % f;
-    *kz = k / (f * f);
+    const int c = offs[k];
+    *kx = c % f;
+    *ky = (c / f) % f;
+    *kz = c / (f * f);
   }
 
   // Row of M_in at input site s*o + k for output row o, or -1 when that site
@@ -87,12 +96,15 @@ extern "C" {
 // active, the second active-site rule of section 1.3) and number them; then list,
 // per filter offset, which active input feeds which active output.  These lists
 // are the non-ground-state blocks of the matrix Q of step 2.
-int orc_rb_build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f, int32_t s,
-                 void** out) {
+int orc_rb_build_lattice(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f,
+                         int32_t s, int32_t lattice, void** out) {
   *out = nullptr;
   if (n < 0 || f < 1 || s < 1 || (n > 0 && coords == nullptr) || grid == nullptr) return INVALID;
+  if (lattice != 0 && lattice != 1) return INVALID;
   Grid g{grid[0], grid[1], grid[2], grid[3]};
   if (g.B < 1 || g.mx < 1 || g.my < 1 || g.mz < 1) return INVALID;
+  // a tetrahedral grid has one size m: the sites x + y + z < m
+  if (lattice == 1 && (g.my != g.mx || g.mz != g.mx)) return INVALID;
   const int64_t LIM = INT64_C(1) << 62;
   if (!mul_ok(g.B, g.mz, LIM) || !mul_ok(g.B * g.mz, g.my, LIM) ||
       !mul_ok(g.B * g.mz * g.my, g.mx, LIM))
@@ -102,7 +114,12 @@ int orc_rb_build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   Rulebook* rb = new Rulebook();
   rb->f = f;
   rb->s = s;
-  rb->K = f * f * f;
+  rb->lattice = lattice;
+  for (int kz = 0; kz < f; ++kz)
+    for (int ky = 0; ky < f; ++ky)
+      for (int kx = 0; kx < f; ++kx)
+        if (lattice == 0 || kx + ky + kz < f) rb->offs.push_back((kz * f + ky) * f + kx);
+  rb->K = static_cast<int>(rb->offs.size());
   rb->gin = g;
   rb->gout = Grid{g.B, out_extent(g.mx, f, s), out_extent(g.my, f, s), out_extent(g.mz, f, s)};
   rb->a_in = n;
@@ -110,7 +127,8 @@ int orc_rb_build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   for (int64_t r = 0; r < n; ++r) {
     const int32_t* c = coords + 4 * r;
     if (c[0] < 0 || c[0] >= g.B || c[1] < 0 || c[1] >= g.mx || c[2] < 0 || c[2] >= g.my ||
-        c[3] < 0 || c[3] >= g.mz) {
+        c[3] < 0 || c[3] >= g.mz ||
+        (lattice == 1 && (int64_t)c[1] + c[2] + c[3] >= g.mx)) {
       delete rb;
       return RANGE;
     }
@@ -134,6 +152,8 @@ int orc_rb_build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
       bool ok = true;
       for (int a = 0; a < 3; ++a)
         ok = ok && d[a] >= 0 && d[a] % s == 0 && d[a] / s < m[a];
+      // tetrahedral: the output grid is the sites o with ox + oy + oz < m_out
+      if (lattice == 1) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;
       if (ok) H_out.insert(key_of(go, c[0], d[0] / s, d[1] / s, d[2] / s));
     }
   }
@@ -176,6 +196,12 @@ int orc_rb_build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   }
   *out = rb;
   return OK;
+}
+
+// The cubic lattice of the recipe above.
+int orc_rb_build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f, int32_t s,
+                 void** out) {
+  return orc_rb_build_lattice(coords, n, grid, f, s, 0, out);
 }
 
 void orc_rb_free(void* h) { delete static_cast<Rulebook*>(h); }

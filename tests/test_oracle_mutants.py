@@ -22,8 +22,8 @@ MUTANTS = [
      "q[ci] = r >= 0 ? x[(int64_t)r * Cin + ci] : g_in[ci];\n      for (int ci = 0; ci < Cin; ++ci)\n        for",
      "q[ci] = r >= 0 ? x[(int64_t)r * Cin + ci] : 0.0;\n      for (int ci = 0; ci < Cin; ++ci)\n        for"),
     ("offset_axes_swapped",
-     "*kx = k % f;\n    *ky = (k / f) % f;\n    *kz = k / (f * f);",
-     "*kz = k % f;\n    *ky = (k / f) % f;\n    *kx = k / (f * f);"),
+     "*kx = c % f;\n    *ky = (c / f) % f;\n    *kz = c / (f * f);",
+     "*kz = c % f;\n    *ky = (c / f) % f;\n    *kx = c / (f * f);"),
     ("bwd_dW_drops_ground_term", "gW[w] += g_in[ci] * dgb[co];", "gW[w] += 0.0;"),
     ("bwd_dg_drops_inactive_term", "          gg[ci] += back;", "          gg[ci] += 0.0;"),
     ("pool_keeps_last_max", "if (bk < 0 || v > best)", "if (bk < 0 || v >= best)"),
@@ -51,8 +51,26 @@ MUTANTS = [
 ]
 
 
-@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_pins_catch_planted_mistake(name, old, new, tmp_path):
+# mistakes in the tetrahedral lattice (section 1.2), caught by its own pins
+LATTICE_MUTANTS = [
+    ("tetra_filter_one_too_big", "if (lattice == 0 || kx + ky + kz < f)",
+     "if (lattice == 0 || kx + ky + kz <= f)"),
+    ("tetra_output_bound_dropped", "if (lattice == 1) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;",
+     "if (lattice == 1) ok = ok;"),
+    ("tetra_output_bound_off_by_one", "if (lattice == 1) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;",
+     "if (lattice == 1) ok = ok && (d[0] + d[1] + d[2]) / s <= go.mx;"),
+    ("tetra_range_check_dropped", "(lattice == 1 && (int64_t)c[1] + c[2] + c[3] >= g.mx)",
+     "(lattice == 1 && false)"),
+    ("tetra_offsets_reversed", "rb->K = static_cast<int>(rb->offs.size());",
+     "std::reverse(rb->offs.begin(), rb->offs.end());\n  rb->K = static_cast<int>(rb->offs.size());"),
+]
+
+CASES = [m + ("test_oracle_pins.py",) for m in MUTANTS] + \
+        [m + ("test_oracle_lattice.py",) for m in LATTICE_MUTANTS]
+
+
+@pytest.mark.parametrize("name,old,new,pins", CASES, ids=[m[0] for m in CASES])
+def test_pins_catch_planted_mistake(name, old, new, pins, tmp_path):
     src = open(SRC).read()
     assert src.count(old) == 1, f"mutation site for {name} not unique/present"
     mut = tmp_path / "mut.cpp"
@@ -62,6 +80,6 @@ def test_pins_catch_planted_mistake(name, old, new, tmp_path):
                    check=True)
     env = dict(os.environ, SCN_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        os.path.join(ROOT, "tests", pins)],
                        env=env, capture_output=True, text=True, cwd=ROOT, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
