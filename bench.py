@@ -16,9 +16,9 @@ workload.
 
     python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--no-cpu]
 
-With --network it instead times whole-network inference of the paper's cubic
-object-recognition networks (nC2-MP3/2, scales 20/40/80) and prints one JSON
-line per network.
+With --network it instead times whole-network inference of the paper's
+object-recognition networks (nC2-MP3/2, scales 20/40/80, on the cubic and the
+tetrahedral lattice) and prints one JSON line per network.
 """
 from __future__ import annotations
 
@@ -48,8 +48,9 @@ def parse():
     p.add_argument("--cpu-sites", type=int, default=60000,
                    help="input sites of the bounded CPU-oracle sample")
     p.add_argument("--network", action="store_true",
-                   help="instead: whole-network inference throughput of the paper's cubic "
-                        "object-recognition networks (scales 20/40/80), one JSON line each")
+                   help="instead: whole-network inference throughput of the paper's "
+                        "object-recognition networks (scales 20/40/80, cubic and tetrahedral "
+                        "lattice), one JSON line each")
     p.add_argument("--batch", type=int, default=256,
                    help="samples per batch for --network (capped per network by the "
                         "rulebook's grid limit)")
@@ -129,19 +130,22 @@ def cpu_baseline(cfg, n_sites: int):
 
 def network_bench(batch: int, reps: int, warmup: int) -> None:
     """Inference throughput of nC2-MP3/2 networks (the object-recognition
-    experiment of section 2): each sample is one seeded shell (ellipsoid or
-    rounded-box superquadric, random rotation, semi-axes scale/2 * U(0.6, 1.0))
-    centred in the network's input grid, features 1.0 at active sites, random
-    He-scaled weights.  A batch is timed end to end (every rulebook build,
-    convolution and pooling, inputs resident in HBM); median over `reps`."""
+    experiment of section 2) on the cubic and the tetrahedral lattice: each
+    sample is one seeded shell (ellipsoid or rounded-box superquadric, random
+    rotation, semi-axes scale/2 * U(0.6, 1.0)) centred in the network's input
+    grid, features 1.0 at active sites, random He-scaled weights.  A batch is
+    timed end to end (every rulebook build, convolution and pooling, inputs
+    resident in HBM); median over `reps`."""
     import torch
 
-    from gen import shell_sites, stream_rng
+    from gen import shell_sites, stream_rng, tetra_shell_sites
     from paper_1505_02890_amd.network import SparseNet, input_size, macs
 
-    # the paper's figures for these networks (cubic lattice, GTX 780), context only
-    paper = {20: (36, 1190), 40: (126, 794), 80: (406, 310)}
-    for scale, levels in ((20, 4), (40, 5), (80, 6)):
+    # the paper's figures for these networks (GTX 780), context only
+    paper = {"cubic": {20: (36, 1190), 40: (126, 794), 80: (406, 310)},
+             "tetrahedral": {20: (9, 1133), 40: (35, 675), 80: (143, 286)}}
+    for lattice, scale, levels in [(lat, sc, lv) for lat in ("cubic", "tetrahedral")
+                                   for sc, lv in ((20, 4), (40, 5), (80, 6))]:
         m = input_size(levels)
         # the rulebook's occupancy bitmap holds at most 2^26 words per grid
         # (the largest grid is the first convolution's output, m + 1 per axis)
@@ -152,12 +156,15 @@ def network_bench(batch: int, reps: int, warmup: int) -> None:
             rng = stream_rng(150502890 + scale, b)
             semi = [0.5 * scale * float(rng.uniform(0.6, 1.0)) for _ in range(3)]
             power = (2, 4)[int(rng.integers(2))]
-            sh = shell_sites(rng, m, semi, [m / 2.0] * 3, power)
+            if lattice == "cubic":
+                sh = shell_sites(rng, m, semi, [m / 2.0] * 3, power)
+            else:
+                sh = tetra_shell_sites(rng, m, semi, power)
             rows.append(np.concatenate([np.full((len(sh), 1), b, np.int64), sh], axis=1))
         c = np.ascontiguousarray(np.concatenate(rows).astype(np.int32))
         cd = torch.from_numpy(c).cuda()
         xd = torch.ones((len(c), 1), dtype=torch.float32, device="cuda")
-        net = SparseNet(levels, seed=scale)
+        net = SparseNet(levels, seed=scale, lattice=lattice)
         for _ in range(warmup):
             net.forward(cd, xd, batch_n)
         torch.cuda.synchronize()
@@ -169,14 +176,14 @@ def network_bench(batch: int, reps: int, warmup: int) -> None:
             times.append(time.perf_counter() - t0)
         t = float(np.median(times))
         print(json.dumps({
-            "metric": "sparse CNN inference throughput (nC2-MP3/2 cubic network)",
+            "metric": f"sparse CNN inference throughput (nC2-MP3/2 {lattice} network)",
             "value": round(batch_n / t, 1), "unit": "tests/s", "higher_is_better": True,
             "scale": scale, "levels": levels, "input_grid": m, "batch": batch_n,
             "active_input_sites_per_sample": round(len(c) / batch_n, 1),
             "macs_per_sample_millions": round(macs(rec) / batch_n / 1e6, 2),
             "ms_per_batch": round(t * 1e3, 3), "final_sites": int(out.shape[0]),
-            "paper_gtx780": {"million_operations": paper[scale][0],
-                             "tests_per_s": paper[scale][1], "note": "context only"},
+            "paper_gtx780": {"million_operations": paper[lattice][scale][0],
+                             "tests_per_s": paper[lattice][scale][1], "note": "context only"},
             "dtype": "f32", "data": "synthetic (seeded shells)",
         }), flush=True)
 

@@ -11,8 +11,10 @@
  * dense-equivalent function, see scn_conv_bwd).
  *
  * Conventions for every call:
- *  - Lattice: cubic, 3D.  A site is (b, x, y, z) with b the sample in the batch.
- *    Its key is ((b*mz + z)*my + y)*mx + x for a grid (B, mx, my, mz).
+ *  - Lattice: cubic, 3D, unless a rulebook is built on the tetrahedral
+ *    lattice (scn_rulebook_build_lattice).  A site is (b, x, y, z) with b the
+ *    sample in the batch.  Its key is ((b*mz + z)*my + y)*mx + x for a grid
+ *    (B, mx, my, mz).
  *  - Output extent of a filter (or pooling window) of size f and stride s is
  *    "valid": m_out = floor((m - f)/s) + 1 per axis (0 if m < f), as in the
  *    worked example of Figure 3 (a 2x2 filter on a 6x6 grid gives 5x5).
@@ -25,7 +27,8 @@
  *  - Feature matrices are fp32, row-major [rows][channels], channels innermost,
  *    one row per active site (the matrix M of section 1.3).  Weights are fp32
  *    [K][Cin][Cout] with K = f^3, i.e. the (f^3 n_in) x n_out matrix W of
- *    section 1.3 with row k*Cin + ci.
+ *    section 1.3 with row k*Cin + ci (K = C(f+2, 3) on the tetrahedral
+ *    lattice: the rulebook's K).
  *  - Ground state: every inactive site of a layer holds the same vector g
  *    (section 1.3).  The input layer's ground state is normally 0.
  *  - All pointers named x, y, W, g_*, d*, coords, argmax are DEVICE pointers
@@ -63,6 +66,10 @@ typedef enum scn_status {
   SCN_ERR_NOMEM = 8        /* device allocation failed */
 } scn_status;
 
+/* lattices of scn_rulebook_build_lattice (section 1.2) */
+#define SCN_LATTICE_CUBIC 0
+#define SCN_LATTICE_TETRAHEDRAL 1
+
 /* flags of scn_conv_fwd / scn_conv_bwd */
 #define SCN_RELU 1u /* y = max(pre, 0) on active rows and on the ground state */
 
@@ -72,12 +79,14 @@ typedef struct scn_rulebook_info {
   int64_t a_in;        /* active input sites */
   int64_t a_out;       /* active output sites */
   int64_t n_pairs;     /* P = total (input row, output row) incidences */
-  int32_t K;           /* f^3 filter offsets */
+  int32_t K;           /* filter offsets: f^3, or C(f+2, 3) on the tetrahedral lattice */
   int32_t filter;      /* f */
   int32_t stride;      /* s */
   int32_t input_sorted;/* 1 if the caller's rows were already in ascending key order */
   int64_t in_grid[4];  /* B, mx, my, mz */
   int64_t out_grid[4]; /* B, floor((m-f)/s)+1 per axis */
+  int32_t lattice;     /* SCN_LATTICE_CUBIC or SCN_LATTICE_TETRAHEDRAL */
+  int32_t reserved;    /* 0 */
 } scn_rulebook_info;
 
 /*
@@ -109,6 +118,28 @@ typedef struct scn_rulebook_info {
 scn_status scn_rulebook_build(const int32_t* coords, int64_t n, const int64_t* grid,
                               int32_t filter, int32_t stride, hipStream_t stream,
                               scn_rulebook** out);
+
+/*
+ * scn_rulebook_build on a chosen lattice (section 1.2, "CNNs on different
+ * lattices").  SCN_LATTICE_CUBIC is scn_rulebook_build.  SCN_LATTICE_TETRAHEDRAL
+ * holds the tetrahedral lattice in skewed integer coordinates:
+ *  - the grid must have equal extents mx = my = mz = m; its sites are
+ *    x + y + z < m (a site past it is SCN_ERR_RANGE);
+ *  - a filter (or pooling region) of size f covers the C(f+2, 3) offsets
+ *    kx + ky + kz < f: 4 for f = 2, 10 for f = 3.  They are numbered in the
+ *    cubic scan order restricted to them (f = 2: (0,0,0), (1,0,0), (0,1,0),
+ *    (0,0,1)), and W of a convolution on this rulebook is [K][Cin][Cout] in
+ *    that order;
+ *  - output o exists where its whole window lies in the grid:
+ *    ox + oy + oz < floor((m - f)/s) + 1, the output grid of the same size
+ *    (out_grid holds the cube's extents, as for the cubic lattice).
+ * Convolution and pooling on such a rulebook behave as on the cubic lattice
+ * with these windows.  Another lattice value, or unequal tetrahedral extents,
+ * is SCN_ERR_INVALID; all other arguments and errors as scn_rulebook_build.
+ */
+scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const int64_t* grid,
+                                      int32_t filter, int32_t stride, int32_t lattice,
+                                      hipStream_t stream, scn_rulebook** out);
 
 /* Sizes and grids of a rulebook (host struct).  SCN_ERR_INVALID on null. */
 scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info);
@@ -183,9 +214,10 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
  * Sparse max-pooling forward (section 1.3, end: pooling "is similar" to the
  * convolution).  rb must have stride >= 2; windows may overlap (filter >
  * stride: 3 over 2, the pooling the paper's networks use) or leave gaps.
- * For each active output o and channel c, y[o][c] is the maximum over the f^3
- * positions of the window, an active position holding x[row][c] and an
- * inactive one g_in[c]; ties keep the first position in ascending k.
+ * For each active output o and channel c, y[o][c] is the maximum over the K
+ * positions of the window (f^3, or C(f+2, 3) on the tetrahedral lattice: 10
+ * for MP3/2), an active position holding x[row][c] and an inactive one
+ * g_in[c]; ties keep the first position in ascending k.
  * argmax[o][c] receives that k.  g_out = g_in.
  *  x [a_in][C], g_in [C] -> y [a_out][C], g_out [C], argmax uint8 [a_out][C].
  * Errors: SCN_ERR_INVALID, SCN_ERR_UNSUPPORTED (stride 1), SCN_ERR_HIP.

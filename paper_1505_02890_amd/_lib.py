@@ -19,11 +19,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("SCN_LIB") or os.path.join(HERE, "libscn.so")
 
 SCN_RELU = 1
+# section 1.2: the cubic lattice and the tetrahedral lattice (skewed coordinates)
+LATTICES = {"cubic": 0, "tetrahedral": 1}
 STATUS = {0: "ok", 1: "invalid", 2: "range", 3: "duplicate", 4: "overflow",
           5: "unsupported", 6: "workspace", 7: "hip", 8: "nomem"}
 
 EXPORTED = (
-    "scn_rulebook_build", "scn_rulebook_get_info", "scn_rulebook_out_coords",
+    "scn_rulebook_build", "scn_rulebook_build_lattice", "scn_rulebook_get_info", "scn_rulebook_out_coords",
     "scn_rulebook_in_rows", "scn_rulebook_out_rows", "scn_rulebook_offsets",
     "scn_rulebook_export", "scn_rulebook_free", "scn_conv_fwd",
     "scn_conv_bwd_workspace_bytes", "scn_conv_bwd", "scn_maxpool_fwd",
@@ -43,7 +45,8 @@ class _Info(ctypes.Structure):
                 ("n_pairs", ctypes.c_int64), ("K", ctypes.c_int32),
                 ("filter", ctypes.c_int32), ("stride", ctypes.c_int32),
                 ("input_sorted", ctypes.c_int32), ("in_grid", ctypes.c_int64 * 4),
-                ("out_grid", ctypes.c_int64 * 4)]
+                ("out_grid", ctypes.c_int64 * 4), ("lattice", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 _lib = None
@@ -64,6 +67,7 @@ def lib() -> ctypes.CDLL:
     st = ctypes.c_int
     sig = {
         "scn_rulebook_build": (st, [P, i64, P, i32, i32, P, ctypes.POINTER(P)]),
+        "scn_rulebook_build_lattice": (st, [P, i64, P, i32, i32, i32, P, ctypes.POINTER(P)]),
         "scn_rulebook_get_info": (st, [P, ctypes.POINTER(_Info)]),
         "scn_rulebook_out_coords": (P, [P]),
         "scn_rulebook_in_rows": (P, [P]),
@@ -115,20 +119,25 @@ def _dev_tensor(t: torch.Tensor, dtype, shape, name: str) -> torch.Tensor:
 
 
 class Rulebook:
-    """Owner of a device rulebook built by ``scn_rulebook_build``.
+    """Owner of a device rulebook built by ``scn_rulebook_build_lattice``.
 
     ``coords`` is a device int32 [n, 4] tensor of (b, x, y, z) rows; ``grid``
-    is (B, mx, my, mz).  Attributes mirror ``scn_rulebook_info``.
+    is (B, mx, my, mz); ``lattice`` is "cubic" or "tetrahedral".  Attributes
+    mirror ``scn_rulebook_info``.
     """
 
-    def __init__(self, coords: torch.Tensor, grid: Sequence[int], filter: int, stride: int):
+    def __init__(self, coords: torch.Tensor, grid: Sequence[int], filter: int, stride: int,
+                 lattice: str = "cubic"):
         n = int(coords.shape[0]) if coords.dim() == 2 else -1
         _dev_tensor(coords, torch.int32, (n, 4), "coords")
+        if lattice not in LATTICES:
+            raise ValueError(f"lattice must be one of {sorted(LATTICES)}, got {lattice!r}")
         g = np.ascontiguousarray(np.asarray(grid, dtype=np.int64).reshape(4))
         h = ctypes.c_void_p()
-        _check(lib().scn_rulebook_build(_ptr(coords), n, g.ctypes.data_as(ctypes.c_void_p),
-                                        int(filter), int(stride), ctypes.c_void_p(_stream()),
-                                        ctypes.byref(h)), "scn_rulebook_build")
+        _check(lib().scn_rulebook_build_lattice(
+            _ptr(coords), n, g.ctypes.data_as(ctypes.c_void_p), int(filter), int(stride),
+            LATTICES[lattice], ctypes.c_void_p(_stream()), ctypes.byref(h)),
+            "scn_rulebook_build_lattice")
         self._h = h
         self.device = coords.device
         info = _Info()
@@ -136,6 +145,7 @@ class Rulebook:
         self.a_in, self.a_out, self.n_pairs = int(info.a_in), int(info.a_out), int(info.n_pairs)
         self.K, self.filter, self.stride = int(info.K), int(info.filter), int(info.stride)
         self.input_sorted = bool(info.input_sorted)
+        self.lattice = {v: k for k, v in LATTICES.items()}[int(info.lattice)]
         self.in_grid = tuple(int(v) for v in info.in_grid)
         self.out_grid = tuple(int(v) for v in info.out_grid)
         off = lib().scn_rulebook_offsets(self._h)
@@ -173,8 +183,9 @@ class Rulebook:
         return oc
 
 
-def build_rulebook(coords: torch.Tensor, grid: Sequence[int], filter: int, stride: int) -> Rulebook:
-    return Rulebook(coords, grid, filter, stride)
+def build_rulebook(coords: torch.Tensor, grid: Sequence[int], filter: int, stride: int,
+                   lattice: str = "cubic") -> Rulebook:
+    return Rulebook(coords, grid, filter, stride, lattice)
 
 
 def conv_fwd(rb: Rulebook, x: torch.Tensor, g_in: torch.Tensor, W: torch.Tensor,

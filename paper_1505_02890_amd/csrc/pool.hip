@@ -1,13 +1,17 @@
 // Sparse max-pooling (end of section 1.3: pooling works like the convolution,
 // over the same active-site rules and ground state) and its gradient, for
-// non-overlapping windows (filter == stride).  Max-pooling only moves data, so
-// the kernels are organised for coalesced HBM traffic: one thread per
-// (site, channel) with channels innermost, window rows from the rulebook's
-// per-output neighbour table, no atomics.
+// windows that tile the grid (filter == stride), leave gaps (filter < stride)
+// or overlap (filter > stride, the MP3/2 of the paper's networks), on the
+// cubic lattice (K = f^3 positions per window) or the tetrahedral one
+// (K = C(f+2, 3)).  Max-pooling only moves data, so the kernels are organised
+// for coalesced HBM traffic: threads over (site, channel) with channels
+// innermost, window rows from the rulebook's per-output neighbour table, no
+// atomics.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <initializer_list>
+#include <type_traits>
 
 #include "scn_internal.h"
 
@@ -73,31 +77,34 @@ __global__ void __launch_bounds__(256) maxpool_bwd_dx_kernel(const int32_t* __re
 // A block holds `per` sites with nc4 = C/4 threads each; argmax bytes of four
 // channels travel as one 32-bit word (byte e = channel 4*c4 + e).
 
-template <int F>
+template <int K>
 __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __restrict__ x,
                                                               const float4* __restrict__ g_in,
                                                               const int32_t* __restrict__ nbr,
                                                               int64_t a_out, int nc4, int per,
                                                               float4* __restrict__ y,
                                                               uint32_t* __restrict__ argmax) {
-  constexpr int K = F * F * F;
   const int ol = threadIdx.x / nc4, c4 = threadIdx.x - ol * nc4;
   const int64_t o = (int64_t)blockIdx.x * per + ol;
   if (ol >= per || o >= a_out) return;
   const float4 g = g_in[c4];
   const int32_t* nb = nbr + o * K;
   // first strict maximum in ascending k, per channel
-  // (planes of a 3-wide window one by one; smaller windows all at once)
-  constexpr int PL = F == 3 ? F * F : F * F * F, NPL = K / PL;
+  // (the 27 positions of a 3-wide cube window a plane of 9 at a time;
+  // smaller windows all at once)
+  constexpr int PL = K == 27 ? 9 : K, NPL = K / PL;
   float4 best = make_float4(0.f, 0.f, 0.f, 0.f);
   uint32_t b0 = 0, b1 = 0, b2 = 0, b3 = 0;
 #pragma unroll 1
   for (int kz = 0; kz < NPL; ++kz) {
+    // branch-free: an inactive position reads row 0 (there is one: the
+    // output is active) and takes g, so all window loads are in flight together
     float4 v[PL];
 #pragma unroll
     for (int i = 0; i < PL; ++i) {
       const int32_t r = nb[kz * PL + i];
-      v[i] = r >= 0 ? x[(int64_t)r * nc4 + c4] : g;
+      const float4 t = x[(int64_t)(r >= 0 ? r : 0) * nc4 + c4];
+      v[i] = r >= 0 ? t : g;
     }
 #pragma unroll
     for (int i = 0; i < PL; ++i) {
@@ -124,14 +131,13 @@ constexpr int PBV_ROWS = 256;  // outputs per block of the four-channel backward
 // zero_uncovered_kernel).  A winner at an inactive
 // position sends dy to the ground state: part[blk][c] sums those, over the
 // block's outputs in a fixed order (part may be null).
-template <int F>
+template <int K>
 __global__ void __launch_bounds__(256) maxpool_bwd_vec_kernel(const int32_t* __restrict__ nbr,
                                                               const uint32_t* __restrict__ argmax,
                                                               const float4* __restrict__ dy,
                                                               int64_t a_out, int nc4,
                                                               float4* __restrict__ dx,
                                                               float4* __restrict__ part) {
-  constexpr int K = F * F * F;
   __shared__ float4 red[256];
   const int rows = 256 / nc4;  // outputs in flight per block
   const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
@@ -335,6 +341,19 @@ __global__ void __launch_bounds__(256) maxpool_bwd_ground_finish(const float* __
 
 inline unsigned nblocks(int64_t n, int t) { return (unsigned)std::max<int64_t>(1, ceil_div(n, t)); }
 
+// calls fn(std::integral_constant<int, K>{}) for the window sizes of both
+// lattices: 1, 8, 27 (cube) and 4, 10 (tetrahedron)
+template <typename Fn>
+void with_window(int K, Fn fn) {
+  switch (K) {
+    case 1: fn(std::integral_constant<int, 1>{}); break;
+    case 4: fn(std::integral_constant<int, 4>{}); break;
+    case 8: fn(std::integral_constant<int, 8>{}); break;
+    case 10: fn(std::integral_constant<int, 10>{}); break;
+    default: fn(std::integral_constant<int, 27>{}); break;
+  }
+}
+
 // four-channel path: C % 4 == 0, C <= 1024, float rows 16-byte aligned, argmax
 // words 4-byte aligned
 inline bool pool_vec_ok(int C, std::initializer_list<const void*> rows, const void* argmax) {
@@ -373,15 +392,10 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
       const auto* g4 = reinterpret_cast<const float4*>(g_in);
       auto* y4 = reinterpret_cast<float4*>(y);
       auto* am4 = reinterpret_cast<uint32_t*>(argmax);
-      if (rb->f == 1)
-        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<1>, grid, dim3(256), 0, st, x4, g4, rb->nbr,
-                           rb->a_out, nc4, per, y4, am4);
-      else if (rb->f == 2)
-        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<2>, grid, dim3(256), 0, st, x4, g4, rb->nbr,
-                           rb->a_out, nc4, per, y4, am4);
-      else
-        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<3>, grid, dim3(256), 0, st, x4, g4, rb->nbr,
-                           rb->a_out, nc4, per, y4, am4);
+      with_window(rb->K, [&](auto k) {
+        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<decltype(k)::value>, grid, dim3(256), 0, st, x4,
+                           g4, rb->nbr, rb->a_out, nc4, per, y4, am4);
+      });
     } else {
       hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(nblocks(rb->a_out * C, 256)), dim3(256), 0, st,
                          x, g_in, rb->nbr, rb->a_out, C, rb->K, y, argmax);
@@ -467,15 +481,10 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
       const auto* dy4 = reinterpret_cast<const float4*>(dy);
       auto* dx4 = reinterpret_cast<float4*>(dx);
       auto* p4 = reinterpret_cast<float4*>(part);
-      if (rb->f == 1)
-        hipLaunchKernelGGL(maxpool_bwd_vec_kernel<1>, grid, dim3(256), 0, st, rb->nbr, am4, dy4,
-                           rb->a_out, C / 4, dx4, p4);
-      else if (rb->f == 2)
-        hipLaunchKernelGGL(maxpool_bwd_vec_kernel<2>, grid, dim3(256), 0, st, rb->nbr, am4, dy4,
-                           rb->a_out, C / 4, dx4, p4);
-      else
-        hipLaunchKernelGGL(maxpool_bwd_vec_kernel<3>, grid, dim3(256), 0, st, rb->nbr, am4, dy4,
-                           rb->a_out, C / 4, dx4, p4);
+      with_window(rb->K, [&](auto k) {
+        hipLaunchKernelGGL(maxpool_bwd_vec_kernel<decltype(k)::value>, grid, dim3(256), 0, st,
+                           rb->nbr, am4, dy4, rb->a_out, C / 4, dx4, p4);
+      });
       SCN_LAUNCH_CHECK();
     }
   } else {

@@ -12,6 +12,16 @@
 // numbering (ascending key) needs no sort, no hash probing and no atomics on
 // the output side, and every result is deterministic.
 //
+// Lattices (section 1.2).  The cubic lattice uses the grid [0, m)^3 and the
+// f^3 offsets of a cube.  The tetrahedral lattice is held in skewed integer
+// coordinates: its grid of size m is the sites x + y + z < m of a cube with
+// equal extents m, a filter of size f covers the C(f+2, 3) offsets
+// kx + ky + kz < f (numbered in the cube's scan order restricted to them),
+// and output o exists where its whole window lies in the grid, i.e. where
+// ox + oy + oz < (m - f) / s + 1.  Both lattices share every phase below; the
+// tetrahedral one masks the dilated rows to that output grid and visits only
+// its own offsets.
+//
 // Phases (one stream, two host synchronisations):
 //   1 mark inputs            bitmap OR per input; range / duplicate checks
 //   2 scan input words       rank of every input site
@@ -40,6 +50,17 @@ enum : uint32_t { F_RANGE = 1, F_DUP = 2, F_UNSORTED = 4 };
 struct GridDev {
   int32_t B, mx, my, mz;  // grid extents
   int32_t rw;             // 32-bit words per x-row
+  int32_t tet;            // 1: tetrahedral lattice, sites x + y + z < mx
+};
+
+// Window offsets of a filter of size F: the cube [0, F)^3, or on the
+// tetrahedral lattice its corner kx + ky + kz < F.  row_len(ky, kz) offsets
+// of x-row (ky, kz) are in the window (0 or fewer: none); offsets are counted
+// in scan order (x fastest).
+template <int F, bool TET>
+struct Win {
+  static constexpr int K = TET ? F * (F + 1) * (F + 2) / 6 : F * F * F;
+  static constexpr int row_len(int ky, int kz) { return TET ? F - ky - kz : F; }
 };
 
 __device__ inline uint64_t site_key(const GridDev& g, int64_t b, int64_t x, int64_t y,
@@ -88,7 +109,8 @@ __global__ void __launch_bounds__(256) mark_inputs_kernel(const int32_t* __restr
   if (i < n) {
     const int4 c = reinterpret_cast<const int4*>(coords)[i];
     const bool ok = c.x >= 0 && c.x < g.B && c.y >= 0 && c.y < g.mx && c.z >= 0 &&
-                    c.z < g.my && c.w >= 0 && c.w < g.mz;
+                    c.z < g.my && c.w >= 0 && c.w < g.mz &&
+                    (!g.tet || (int64_t)c.y + c.z + c.w < g.mx);
     if (!ok) {
       f |= F_RANGE;
     } else {
@@ -156,39 +178,50 @@ __device__ inline WordPos word_pos(int wo, const GridDev& g) {
 
 // ---- phase 4: output occupancy (dilation of the input bitmap) -------------
 // SM: 1 stride 1 (funnel shifts), 2 stride 2 (even-bit compression), 0 any.
-template <int F, int SM>
+// On the tetrahedral lattice the bits past the output grid (x + y + z >= mx)
+// are cleared and rows wholly past it are not read.
+template <int F, bool TET, int SM>
 __global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict__ inb, GridDev gi,
                                                      uint32_t* __restrict__ outb, GridDev go,
                                                      int nw_out, int s) {
+  using W = Win<F, TET>;
   const int wo = blockIdx.x * blockDim.x + threadIdx.x;
   if (wo >= nw_out) return;
   const WordPos wp = word_pos(wo, go);
   const int x0 = wp.wx * 32;
-  const int nvalid = min(32, go.mx - x0);
+  const int lim = TET ? go.mx - wp.y - wp.z : go.mx;  // x < lim on this row
+  const int nvalid = min(32, lim - x0);
+  if (nvalid <= 0) {
+    outb[wo] = 0u;
+    return;
+  }
   const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
   uint32_t v = 0;
 #pragma unroll
   for (int kz = 0; kz < F; ++kz)
 #pragma unroll
     for (int ky = 0; ky < F; ++ky) {
+      const int nx = W::row_len(ky, kz);
+      if (nx <= 0) continue;
       const int64_t base = row_base(gi, wp.b, (int64_t)s * wp.y + ky, (int64_t)s * wp.z + kz);
       if (SM == 1) {
 #pragma unroll
-        for (int kx = 0; kx < F; ++kx) v |= extract32(inb, base, gi.rw, (int64_t)x0 + kx);
+        for (int kx = 0; kx < F; ++kx)
+          if (kx < nx) v |= extract32(inb, base, gi.rw, (int64_t)x0 + kx);
       } else if (SM == 2) {
         const int64_t p = 2 * (int64_t)x0;  // multiple of 64
         const uint64_t lo = extract32(inb, base, gi.rw, p);
         const uint64_t hi = extract32(inb, base, gi.rw, p + 32);
         const uint64_t w64 = lo | (hi << 32);
         uint64_t t = w64;
-        if (F >= 2) t |= w64 >> 1;
-        if (F >= 3) {
-          const uint64_t nx = extract32(inb, base, gi.rw, p + 64) & 1u;
-          t |= (w64 >> 2) | (nx << 62);
+        if (nx >= 2) t |= w64 >> 1;
+        if (nx >= 3) {
+          const uint64_t nxt = extract32(inb, base, gi.rw, p + 64) & 1u;
+          t |= (w64 >> 2) | (nxt << 62);
         }
         v |= compress_even(t);
       } else {
-        constexpr uint32_t fm = (1u << F) - 1u;
+        const uint32_t fm = (1u << nx) - 1u;
         for (int j = 0; j < nvalid; ++j)
           if (extract32(inb, base, gi.rw, (int64_t)s * (x0 + j)) & fm) v |= 1u << j;
       }
@@ -197,14 +230,15 @@ __global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict_
 }
 
 // ---- phase 6: output coordinates and neighbour masks ----------------------
-template <int F, bool S1>
+template <int F, bool TET, bool S1>
 __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restrict__ inb, GridDev gi,
                                                         const uint32_t* __restrict__ outb,
                                                         const uint32_t* __restrict__ opref,
                                                         GridDev go, int nw_out, int s,
                                                         int32_t* __restrict__ out_coords,
                                                         uint32_t* __restrict__ masks) {
-  constexpr int K = F * F * F;
+  using W = Win<F, TET>;
+  constexpr int K = W::K;
   const int wo = blockIdx.x * blockDim.x + threadIdx.x;
   if (wo >= nw_out) return;
   uint32_t v = outb[wo];
@@ -213,19 +247,21 @@ __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restri
   const int x0 = wp.wx * 32;
   uint32_t rank = opref[wo];
   if (S1) {
-    // E[k] bit j: input site (x0 + j + kx, y + ky, z + kz) is active
+    // E[k] bit j: input site (x0 + j + kx, y + ky, z + kz) of offset k is active
     uint32_t E[K];
+    int k = 0;
 #pragma unroll
     for (int kz = 0; kz < F; ++kz)
 #pragma unroll
       for (int ky = 0; ky < F; ++ky) {
+        if (W::row_len(ky, kz) <= 0) continue;
         const int64_t base = row_base(gi, wp.b, wp.y + ky, wp.z + kz);
         const int64_t w = x0 >> 5;
         const uint32_t lo = w < gi.rw ? inb[base + w] : 0u;
         const uint32_t hi = w + 1 < gi.rw ? inb[base + w + 1] : 0u;
 #pragma unroll
         for (int kx = 0; kx < F; ++kx)
-          E[(kz * F + ky) * F + kx] = kx ? (lo >> kx) | (hi << (32 - kx)) : lo;
+          if (kx < W::row_len(ky, kz)) E[k++] = kx ? (lo >> kx) | (hi << (32 - kx)) : lo;
       }
     while (v) {
       const int j = __builtin_ctz(v);
@@ -243,14 +279,17 @@ __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restri
       v &= v - 1;
       const int64_t xi = (int64_t)s * (x0 + j);
       uint32_t m = 0;
+      int k = 0;
 #pragma unroll
       for (int kz = 0; kz < F; ++kz)
 #pragma unroll
         for (int ky = 0; ky < F; ++ky) {
+          if (W::row_len(ky, kz) <= 0) continue;
           const int64_t base = row_base(gi, wp.b, (int64_t)s * wp.y + ky, (int64_t)s * wp.z + kz);
           const uint32_t bits = extract32(inb, base, gi.rw, xi);
 #pragma unroll
-          for (int kx = 0; kx < F; ++kx) m |= ((bits >> kx) & 1u) << ((kz * F + ky) * F + kx);
+          for (int kx = 0; kx < F; ++kx)
+            if (kx < W::row_len(ky, kz)) m |= ((bits >> kx) & 1u) << k++;
         }
       reinterpret_cast<int4*>(out_coords)[rank] = make_int4(wp.b, x0 + j, wp.y, wp.z);
       masks[rank] = m;
@@ -288,24 +327,42 @@ __global__ void list_offsets_kernel(const uint64_t* __restrict__ pos, int64_t nt
 // ---- phase 9: emit the pair lists ------------------------------------------
 // One thread per output, one wave per tile.  All K rank lookups are issued
 // before any dependent load so they overlap.
-template <int F>
+template <int F, bool TET>
 __global__ void __launch_bounds__(256) emit_pairs_kernel(
     const uint32_t* __restrict__ masks, const int32_t* __restrict__ out_coords, int64_t a_out,
     int64_t nt, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
     GridDev gi, const int32_t* __restrict__ perm, const uint64_t* __restrict__ pos,
     int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows, int32_t* __restrict__ in_rank,
     int32_t* __restrict__ nbr, int32_t* __restrict__ inv, int inv_slots) {
-  constexpr int K = F * F * F;
+  using W = Win<F, TET>;
+  constexpr int K = W::K;
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t t = o >> 6;
   const bool live = o < a_out;
   const uint32_t m = live ? masks[o] : 0u;
   int4 c = make_int4(0, 0, 0, 0);
   if (live) c = reinterpret_cast<const int4*>(out_coords)[o];
+  // offset k -> (kx, ky, kz), unrolled to constants
+  int8_t ox[K], oy[K], oz[K];
+  {
+    int k = 0;
+#pragma unroll
+    for (int kz = 0; kz < F; ++kz)
+#pragma unroll
+      for (int ky = 0; ky < F; ++ky)
+#pragma unroll
+        for (int kx = 0; kx < F; ++kx)
+          if (kx < W::row_len(ky, kz)) {
+            ox[k] = kx;
+            oy[k] = ky;
+            oz[k] = kz;
+            ++k;
+          }
+  }
   uint32_t rank[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) {
-    const int kx = k % F, ky = (k / F) % F, kz = k / (F * F);
+    const int kx = ox[k], ky = oy[k], kz = oz[k];
     const int64_t xi = (int64_t)s * c.y + kx;
     const int64_t w = row_base(gi, c.x, (int64_t)s * c.z + ky, (int64_t)s * c.w + kz) + (xi >> 5);
     const bool bit = (m >> k) & 1u;
@@ -326,7 +383,7 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
       if (nbr) {
         // input -> its window(s): one slot, or (overlapping windows, f > s,
         // at most two per axis) the slot picked by which of the two it is
-        const int kx = k % F, ky = (k / F) % F, kz = k / (F * F);
+        const int kx = ox[k], ky = oy[k], kz = oz[k];
         const int slot = inv_slots == 1 ? 0 : (kx >= s) | ((ky >= s) << 1) | ((kz >= s) << 2);
         inv[(int64_t)row * inv_slots + slot] = (int32_t)(o * K + k);
       }
@@ -397,16 +454,58 @@ struct Temps {
   }
 };
 
+// Kernel variants by filter size and lattice.
+template <int F, bool TET>
+struct Kernels {
+  static constexpr int K = Win<F, TET>::K;
+  static void dilate(int sm, dim3 g, hipStream_t st, const uint32_t* inb, GridDev gi, uint32_t* outb,
+                     GridDev go, int nw_out, int s) {
+    if (sm == 1)
+      hipLaunchKernelGGL((dilate_kernel<F, TET, 1>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
+    else if (sm == 2)
+      hipLaunchKernelGGL((dilate_kernel<F, TET, 2>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
+    else
+      hipLaunchKernelGGL((dilate_kernel<F, TET, 0>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
+  }
+  template <typename... A>
+  static void out_sites(bool s1, dim3 g, hipStream_t st, A... a) {
+    if (s1)
+      hipLaunchKernelGGL((out_sites_kernel<F, TET, true>), g, dim3(256), 0, st, a...);
+    else
+      hipLaunchKernelGGL((out_sites_kernel<F, TET, false>), g, dim3(256), 0, st, a...);
+  }
+  template <typename... A>
+  static void tile_count(dim3 g, hipStream_t st, A... a) {
+    hipLaunchKernelGGL((tile_count_kernel<K>), g, dim3(256), 0, st, a...);
+  }
+  template <typename... A>
+  static void emit(dim3 g, hipStream_t st, A... a) {
+    hipLaunchKernelGGL((emit_pairs_kernel<F, TET>), g, dim3(256), 0, st, a...);
+  }
+};
+
+// calls fn(Kernels<F, TET>{}) for the runtime filter size and lattice
+template <typename Fn>
+void with_kernels(int f, int lattice, Fn fn) {
+  if (lattice == SCN_LATTICE_TETRAHEDRAL) {
+    if (f == 1) fn(Kernels<1, true>{}); else if (f == 2) fn(Kernels<2, true>{}); else fn(Kernels<3, true>{});
+  } else {
+    if (f == 1) fn(Kernels<1, false>{}); else if (f == 2) fn(Kernels<2, false>{}); else fn(Kernels<3, false>{});
+  }
+}
+
 scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f, int32_t s,
-                 hipStream_t st, scn_rulebook** out) {
+                 int32_t lattice, hipStream_t st, scn_rulebook** out) {
   if (!out) {
     set_error("scn_rulebook_build: out is NULL");
     return SCN_ERR_INVALID;
   }
   *out = nullptr;
   if (!grid || n < 0 || (n > 0 && !coords) || f < 1 || s < 1 ||
-      (reinterpret_cast<uintptr_t>(coords) & 15) != 0) {
-    set_error("scn_rulebook_build: invalid argument (n=%lld f=%d s=%d)", (long long)n, f, s);
+      (reinterpret_cast<uintptr_t>(coords) & 15) != 0 ||
+      (lattice != SCN_LATTICE_CUBIC && lattice != SCN_LATTICE_TETRAHEDRAL)) {
+    set_error("scn_rulebook_build: invalid argument (n=%lld f=%d s=%d lattice=%d)", (long long)n,
+              f, s, lattice);
     return SCN_ERR_INVALID;
   }
   for (int a = 0; a < 4; ++a)
@@ -414,6 +513,12 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
       set_error("scn_rulebook_build: grid extent %d is %lld", a, (long long)grid[a]);
       return SCN_ERR_INVALID;
     }
+  const bool tet = lattice == SCN_LATTICE_TETRAHEDRAL;
+  if (tet && (grid[2] != grid[1] || grid[3] != grid[1])) {
+    set_error("scn_rulebook_build: a tetrahedral grid has one size (got %lld, %lld, %lld)",
+              (long long)grid[1], (long long)grid[2], (long long)grid[3]);
+    return SCN_ERR_INVALID;
+  }
   if (f > 3) {
     set_error("scn_rulebook_build: filter %d > 3 is not supported", f);
     return SCN_ERR_UNSUPPORTED;
@@ -422,7 +527,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     set_error("scn_rulebook_build: %lld sites exceed INT32_MAX", (long long)n);
     return SCN_ERR_OVERFLOW;
   }
-  const int K = f * f * f;
+  const int K = tet ? f * (f + 1) * (f + 2) / 6 : f * f * f;
   int64_t go4[4] = {grid[0], 0, 0, 0};
   for (int a = 1; a < 4; ++a) go4[a] = grid[a] >= f ? (grid[a] - f) / s + 1 : 0;
   // bitmap words of each grid; bound them (2^26 words = 2^31 sites each)
@@ -437,9 +542,9 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   }
   const int64_t nw_in = (int64_t)nwi_d, nw_out = (int64_t)nwo_d;
   GridDev gi{(int32_t)grid[0], (int32_t)grid[1], (int32_t)grid[2], (int32_t)grid[3],
-             (int32_t)rw_in};
+             (int32_t)rw_in, tet ? 1 : 0};
   GridDev go{(int32_t)go4[0], (int32_t)std::max<int64_t>(go4[1], 0), (int32_t)go4[2],
-             (int32_t)go4[3], (int32_t)rw_out};
+             (int32_t)go4[3], (int32_t)rw_out, tet ? 1 : 0};
 
   Temps tmp(st);
   scn_status rc;
@@ -472,14 +577,10 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   if ((rc = exclusive_scan<uint32_t>(PopcountLoad{inb}, nw_in, ipref, ipref + nw_in, sc32, st)))
     return rc;
   {
-    auto dil = [&](auto fn) {
-      hipLaunchKernelGGL(fn, dim3(blocks_for(nw_out, 256)), dim3(256), 0, st, inb, gi, outb, go,
-                         (int)nw_out, s);
-    };
     const int sm = s == 1 ? 1 : (s == 2 ? 2 : 0);
-    if (f == 1) { if (sm == 1) dil(dilate_kernel<1, 1>); else if (sm == 2) dil(dilate_kernel<1, 2>); else dil(dilate_kernel<1, 0>); }
-    else if (f == 2) { if (sm == 1) dil(dilate_kernel<2, 1>); else if (sm == 2) dil(dilate_kernel<2, 2>); else dil(dilate_kernel<2, 0>); }
-    else { if (sm == 1) dil(dilate_kernel<3, 1>); else if (sm == 2) dil(dilate_kernel<3, 2>); else dil(dilate_kernel<3, 0>); }
+    with_kernels(f, lattice, [&](auto k) {
+      k.dilate(sm, dim3(blocks_for(nw_out, 256)), st, inb, gi, outb, go, (int)nw_out, s);
+    });
     SCN_LAUNCH_CHECK();
   }
   if ((rc = exclusive_scan<uint32_t>(PopcountLoad{outb}, nw_out, opref, opref + nw_out, sc32,
@@ -555,6 +656,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   rb->f = f;
   rb->s = s;
   rb->K = K;
+  rb->lattice = lattice;
   for (int a = 0; a < 4; ++a) {
     rb->gin[a] = grid[a];
     rb->gout[a] = go4[a];
@@ -579,23 +681,17 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     SCN_LAUNCH_CHECK();
   }
   if (a_out > 0) {
-    auto os = [&](auto fn) {
-      hipLaunchKernelGGL(fn, dim3(blocks_for(nw_out, 256)), dim3(256), 0, st, inb, gi, outb, opref,
-                         go, (int)nw_out, s, rb->out_coords, masks);
-    };
-    if (f == 1) { if (s == 1) os(out_sites_kernel<1, true>); else os(out_sites_kernel<1, false>); }
-    else if (f == 2) { if (s == 1) os(out_sites_kernel<2, true>); else os(out_sites_kernel<2, false>); }
-    else { if (s == 1) os(out_sites_kernel<3, true>); else os(out_sites_kernel<3, false>); }
+    with_kernels(f, lattice, [&](auto k) {
+      k.out_sites(s == 1, dim3(blocks_for(nw_out, 256)), st, (const uint32_t*)inb, gi,
+                  (const uint32_t*)outb, (const uint32_t*)opref, go, (int)nw_out, s,
+                  rb->out_coords, masks);
+    });
     SCN_LAUNCH_CHECK();
   }
-  {
-    auto tc = [&](auto fn) {
-      hipLaunchKernelGGL(fn, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st, masks, a_out, nt,
-                         cnt);
-    };
-    if (f == 1) tc(tile_count_kernel<1>); else if (f == 2) tc(tile_count_kernel<8>); else tc(tile_count_kernel<27>);
-    SCN_LAUNCH_CHECK();
-  }
+  with_kernels(f, lattice, [&](auto k) {
+    k.tile_count(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks, a_out, nt, cnt);
+  });
+  SCN_LAUNCH_CHECK();
   // positions: otile[k*nt + t] = off[k] + pairs of list k in tiles < t
   if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, ncnt, (uint64_t*)rb->otile,
                                      (uint64_t*)rb->otile + ncnt, sc64, st)))
@@ -610,13 +706,13 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     SCN_LAUNCH_CHECK();
   }
   if (a_out > 0) {
-    auto em = [&](auto fn) {
-      hipLaunchKernelGGL(fn, dim3(blocks_for(nt * TILE, 256)), dim3(256), 0, st, masks,
-                         rb->out_coords, a_out, nt, s, inb, ipref, gi, rb->perm,
-                         (const uint64_t*)rb->otile, rb->in_rows, rb->out_rows,
-                         sorted ? nullptr : rb->in_rank, rb->nbr, rb->inv, inv_slots);
-    };
-    if (f == 1) em(emit_pairs_kernel<1>); else if (f == 2) em(emit_pairs_kernel<2>); else em(emit_pairs_kernel<3>);
+    with_kernels(f, lattice, [&](auto k) {
+      k.emit(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks,
+             (const int32_t*)rb->out_coords, a_out, nt, s, (const uint32_t*)inb,
+             (const uint32_t*)ipref, gi, (const int32_t*)rb->perm, (const uint64_t*)rb->otile,
+             rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr, rb->inv,
+             inv_slots);
+    });
     SCN_LAUNCH_CHECK();
   }
   hipLaunchKernelGGL(in_tiles_kernel, dim3(blocks_for(K * nit + 1, 256)), dim3(256), 0, st,
@@ -644,7 +740,14 @@ scn_status scn_rulebook_build(const int32_t* coords, int64_t n, const int64_t* g
                               int32_t filter, int32_t stride, hipStream_t stream,
                               scn_rulebook** out) {
   scn::clear_error();
-  return scn::build(coords, n, grid, filter, stride, stream, out);
+  return scn::build(coords, n, grid, filter, stride, SCN_LATTICE_CUBIC, stream, out);
+}
+
+scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const int64_t* grid,
+                                      int32_t filter, int32_t stride, int32_t lattice,
+                                      hipStream_t stream, scn_rulebook** out) {
+  scn::clear_error();
+  return scn::build(coords, n, grid, filter, stride, lattice, stream, out);
 }
 
 scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info) {
@@ -659,6 +762,8 @@ scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info
   info->filter = rb->f;
   info->stride = rb->s;
   info->input_sorted = rb->input_sorted;
+  info->lattice = rb->lattice;
+  info->reserved = 0;
   for (int a = 0; a < 4; ++a) {
     info->in_grid[a] = rb->gin[a];
     info->out_grid[a] = rb->gout[a];

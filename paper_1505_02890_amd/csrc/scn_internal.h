@@ -15,7 +15,7 @@ namespace scn {
 // Rows of a rulebook tile: pair ranges are stored per (offset, tile of TILE
 // output rows) and per (offset, tile of TILE input ranks).
 constexpr int TILE = 64;
-constexpr int MAX_K = 27;  // f <= 3
+constexpr int MAX_K = 27;  // f <= 3 (the tetrahedral lattice needs at most 10)
 
 void set_error(const char* fmt, ...);
 void clear_error();
@@ -55,6 +55,7 @@ __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + 
 // Device layout of a rulebook.  All arrays are owned by the rulebook.
 struct scn_rulebook {
   int32_t f = 0, s = 0, K = 0;
+  int32_t lattice = SCN_LATTICE_CUBIC;
   int64_t gin[4] = {0, 0, 0, 0};   // B, mx, my, mz
   int64_t gout[4] = {0, 0, 0, 0};
   int64_t a_in = 0, a_out = 0, n_pairs = 0;

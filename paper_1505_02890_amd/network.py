@@ -11,6 +11,11 @@ All padding is valid, so the input grid is the size the network reduces to one
 site: working back from 1, a C2 adds 1 and an MP3/2 maps m to 2m + 1, which
 gives 62, 126 and 254 for 4, 5 and 6 levels.
 
+The same networks run on the tetrahedral lattice of section 1.2 (the rows
+marked with a triangle in the experiment's table): a C2 filter then covers 4
+sites, an MP3/2 region 10, and the grid of size m is the tetrahedron
+x + y + z < m in skewed coordinates; the sizes above are unchanged.
+
 Every step runs in the library's kernels (rulebook build, contraction,
 pooling); this module only sequences the calls and keeps the layer state.
 """
@@ -32,6 +37,11 @@ def input_size(levels: int) -> int:
         m = 2 * m + 1  # MP3/2: (m_in - 3) / 2 + 1 = m
         m += 1         # C2 before it
     return m
+
+
+def window_size(f: int, lattice: str = "cubic") -> int:
+    """Sites under a filter of size f: f^3, or C(f+2, 3) on the tetrahedral lattice."""
+    return f ** 3 if lattice == "cubic" else math.comb(f + 2, 3)
 
 
 @dataclass
@@ -59,12 +69,16 @@ def architecture(levels: int, classes: int = 50, width: int = 32, cin: int = 1) 
 
 
 class SparseNet:
-    """Random-initialised weights (He scaling) for `architecture(levels)`; the
-    input ground state is 0 (an empty site holds no signal)."""
+    """Random-initialised weights (He scaling) for `architecture(levels)` on
+    the cubic or tetrahedral lattice; the input ground state is 0 (an empty
+    site holds no signal)."""
 
     def __init__(self, levels: int, classes: int = 50, width: int = 32, seed: int = 0,
-                 device: str = "cuda"):
+                 device: str = "cuda", lattice: str = "cubic"):
+        if lattice not in ("cubic", "tetrahedral"):
+            raise ValueError(f"unknown lattice {lattice!r}")
         self.levels = levels
+        self.lattice = lattice
         self.layers = architecture(levels, classes, width)
         self.m = input_size(levels)
         g = torch.Generator().manual_seed(seed)
@@ -73,7 +87,7 @@ class SparseNet:
             if L.kind != "conv":
                 self.params.append(None)
                 continue
-            K = L.f ** 3
+            K = window_size(L.f, lattice)
             W = torch.randn(K, L.cin, L.cout, generator=g) * math.sqrt(2.0 / (K * L.cin))
             b = torch.randn(L.cout, generator=g) * 0.05
             self.params.append((W.to(device), b.to(device)))
@@ -86,7 +100,7 @@ class SparseNet:
         g = torch.zeros(x.shape[1], dtype=torch.float32, device=self.device)
         rec = []
         for L, p in zip(self.layers, self.params):
-            rb = scn.build_rulebook(coords, grid, L.f, L.s)
+            rb = scn.build_rulebook(coords, grid, L.f, L.s, lattice=self.lattice)
             if L.kind == "conv":
                 W, b = p
                 x, g = scn.conv_fwd(rb, x, g, W, b, relu=L.relu)

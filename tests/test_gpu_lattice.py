@@ -1,0 +1,273 @@
+"""GPU parity on the tetrahedral lattice (section 1.2): rulebooks,
+convolution and max-pooling built with ``scn_rulebook_build_lattice`` against
+the oracle on the same lattice, through the C ABI.
+
+Same bars as the cubic tests: rulebooks, pooling outputs, argmax and
+non-overlapping pooling gradients bit-exact; fp32 results within the
+tolerance rule of ``tests/helpers.py``.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from gen import stream_rng, tetra_random_sites, tetra_shell_sites  # noqa: E402
+
+from helpers import assert_close, dev, host  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+T = "tetrahedral"
+
+
+@pytest.fixture(scope="module")
+def scn():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1505_02890_amd as m
+    m.lib()  # raises if the HIP library is missing
+    return m
+
+
+def _pair(scn, coords, grid, f, s):
+    g = scn.build_rulebook(dev(coords, torch.int32), grid, f, s, lattice=T)
+    o = oracle.Rulebook(coords, grid, f, s, lattice=T)
+    return g, o
+
+
+def _check_rulebook(g, o):
+    oa = o.arrays()
+    assert g.lattice == T
+    assert (g.a_in, g.a_out, g.n_pairs, g.K) == (oa.a_in, oa.a_out, oa.n_pairs, oa.K)
+    assert tuple(g.out_grid) == tuple(oa.out_grid)
+    assert np.array_equal(g.offsets, oa.offsets)
+    oc, ir, orr = g.export()
+    assert np.array_equal(host(oc), oa.out_coords)
+    assert np.array_equal(host(ir), oa.in_rows)
+    assert np.array_equal(host(orr), oa.out_rows)
+
+
+RB_CASES = [
+    # (B, m, n, f, s, shuffle)
+    (1, 10, 80, 2, 1, True),
+    (2, 12, 300, 3, 1, True),
+    (3, 40, 900, 2, 1, False),     # x-rows of two words
+    (2, 70, 1500, 3, 1, True),     # x-rows of three words
+    (2, 33, 700, 2, 2, True),
+    (1, 65, 1200, 3, 2, True),     # MP3/2 windows
+    (2, 21, 400, 3, 3, True),
+    (1, 9, 165, 2, 1, True),       # every site active
+    (1, 11, 286, 3, 2, False),     # every site active, MP3/2
+    (2, 9, 100, 1, 1, True),
+    (1, 30, 200, 2, 3, True),      # stride above filter (gaps)
+    (4, 1, 4, 1, 1, True),         # one site per sample
+    (1, 2, 4, 3, 1, True),         # grid smaller than the filter: no outputs
+]
+
+
+@pytest.mark.parametrize("case", RB_CASES, ids=[str(i) for i in range(len(RB_CASES))])
+def test_rulebook_bit_exact(scn, case):
+    B, m, n, f, s, shuf = case
+    rng = stream_rng(61, RB_CASES.index(case))
+    coords = tetra_random_sites(rng, B, m, n, shuffle=shuf)
+    g, o = _pair(scn, coords, (B, m, m, m), f, s)
+    _check_rulebook(g, o)
+    assert g.K == math.comb(f + 2, 3)
+
+
+def test_rulebook_errors(scn):
+    ok = np.array([[0, 1, 1, 1]], np.int32)
+    with pytest.raises(scn.ScnError) as e:           # 2 + 2 + 1 >= 5
+        scn.build_rulebook(dev(np.array([[0, 1, 1, 1], [0, 2, 2, 1]], np.int32)),
+                           (1, 5, 5, 5), 2, 1, lattice=T)
+    assert e.value.status == "range"
+    with pytest.raises(scn.ScnError) as e:
+        scn.build_rulebook(dev(ok), (1, 5, 6, 5), 2, 1, lattice=T)
+    assert e.value.status == "invalid"
+    from paper_1505_02890_amd import _lib
+    import ctypes
+    h = ctypes.c_void_p()
+    g4 = np.array([1, 5, 5, 5], np.int64)
+    d = dev(ok)
+    rc = _lib.lib().scn_rulebook_build_lattice(
+        ctypes.c_void_p(d.data_ptr()), 1, g4.ctypes.data_as(ctypes.c_void_p), 2, 1, 2,
+        ctypes.c_void_p(torch.cuda.current_stream().cuda_stream), ctypes.byref(h))
+    assert rc == 1 and not h.value                    # unknown lattice: invalid
+    # the same site is fine on the cube
+    scn.build_rulebook(dev(np.array([[0, 2, 2, 1]], np.int32)), (1, 5, 5, 5), 2, 1)
+
+
+def test_rulebook_empty(scn):
+    g, o = _pair(scn, np.zeros((0, 4), np.int32), (2, 6, 6, 6), 2, 1)
+    assert g.a_out == 0 and g.n_pairs == 0 and g.K == 4
+    _check_rulebook(g, o)
+
+
+# --------------------------------------------------------------------------
+# convolution
+# --------------------------------------------------------------------------
+
+CONV_CASES = [
+    # (f, s, B, m, n, Cin, Cout, relu)
+    (2, 1, 2, 14, 300, 1, 16, False),
+    (2, 1, 1, 20, 600, 32, 32, True),
+    (3, 1, 2, 16, 500, 17, 3, True),
+    (3, 1, 1, 40, 1200, 64, 64, False),
+    (2, 2, 2, 17, 400, 32, 96, True),
+    (3, 2, 1, 19, 500, 3, 160, False),
+    (2, 1, 1, 70, 2500, 96, 128, True),
+    (1, 1, 1, 8, 60, 5, 7, False),
+]
+
+
+def _sq(a):
+    return None if a is None else np.asarray(a, np.float64) ** 2
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[str(i) for i in range(len(CONV_CASES))])
+def test_conv_fwd_bwd_parity(scn, case):
+    f, s, B, m, n, Cin, Cout, relu = case
+    seed = 620 + CONV_CASES.index(case)
+    rng = stream_rng(seed, 1)
+    coords = tetra_random_sites(rng, B, m, n)
+    K = math.comb(f + 2, 3)
+    x = rng.standard_normal((len(coords), Cin)).astype(np.float32)
+    g_in = (rng.standard_normal(Cin) * 0.5).astype(np.float32)
+    W = (rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin)).astype(np.float32)
+    bias = (rng.standard_normal(Cout) * 0.1).astype(np.float32)
+    g, o = _pair(scn, coords, (B, m, m, m), f, s)
+    _check_rulebook(g, o)
+    y_ref, go_ref = oracle.conv_fwd(o, x, g_in, W, bias, relu=relu)
+    pre_ref, gpre_ref = oracle.conv_fwd(o, x, g_in, W, bias, relu=False)
+    sig_y, sig_g = (np.sqrt(v) for v in oracle.conv_fwd(o, _sq(x), _sq(g_in), _sq(W), _sq(bias)))
+    yd, god = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias), relu=relu)
+    assert_close("y", host(yd), y_ref, sig_y)
+    assert_close("g_out", host(god), go_ref, sig_g)
+    rng = stream_rng(seed, 2)
+    dy = rng.uniform(-1, 1, size=(g.a_out, Cout)).astype(np.float32)
+    dg = rng.uniform(-1, 1, size=Cout).astype(np.float32)
+    if relu:
+        dy[np.abs(pre_ref) <= 1e-3 * (sig_y + 1e-30)] = 0.0
+        dg[np.abs(gpre_ref) <= 1e-3 * (sig_g + 1e-30)] = 0.0
+    ref = oracle.conv_bwd(o, x, g_in, W, bias, dy, dg, relu=relu)
+    dyb = dy * (pre_ref > 0) if relu else dy
+    dgb = dg * (gpre_ref > 0) if relu else dg
+    sig = {k: np.sqrt(v) for k, v in
+           oracle.conv_bwd(o, _sq(x), _sq(g_in), _sq(W), None, _sq(dyb), _sq(dgb)).items()}
+    out = scn.conv_bwd(g, dev(x), dev(g_in), dev(W), yd, god, dev(dy), dev(dg), relu=relu)
+    for k in ("dx", "dW", "dbias", "dg_in"):
+        assert_close(k, host(out[k]), ref[k], sig[k])
+
+
+def test_conv_rejects_cubic_weights(scn):
+    coords = tetra_random_sites(stream_rng(3, 3), 1, 10, 50)
+    g = scn.build_rulebook(dev(coords), (1, 10, 10, 10), 2, 1, lattice=T)
+    x = dev(np.ones((len(coords), 4), np.float32))
+    with pytest.raises(ValueError):
+        scn.conv_fwd(g, x, dev(np.zeros(4, np.float32)), dev(np.ones((8, 4, 4), np.float32)))
+
+
+# --------------------------------------------------------------------------
+# max-pooling
+# --------------------------------------------------------------------------
+
+POOL_CASES = [
+    # (f, s, B, m, n, C, zero_frac, g_scale)
+    (3, 2, 1, 21, 700, 16, 0.0, 0.5),      # MP3/2 (10-site regions)
+    (3, 2, 2, 15, 500, 5, 0.3, 0.0),       # one channel per thread, ties
+    (3, 2, 1, 11, 286, 64, 0.2, 0.1),      # every site active
+    (3, 2, 2, 33, 900, 12, 0.0, 1.5),      # ground state often wins
+    (2, 2, 2, 18, 500, 16, 0.0, 0.5),      # MP2/2 (4-site regions, gaps)
+    (2, 2, 1, 15, 400, 3, 0.5, 0.0),
+    (3, 3, 1, 20, 600, 8, 0.0, 2.0),
+]
+
+
+@pytest.mark.parametrize("case", POOL_CASES, ids=[str(i) for i in range(len(POOL_CASES))])
+def test_maxpool_parity(scn, case):
+    f, s, B, m, n, C, zf, gs = case
+    rng = stream_rng(640 + POOL_CASES.index(case), 0)
+    coords = tetra_random_sites(rng, B, m, n)
+    x = rng.standard_normal((len(coords), C)).astype(np.float32)
+    x[rng.random(x.shape) < zf] = 0.0
+    g_in = (np.abs(rng.standard_normal(C)) * gs).astype(np.float32)
+    g, o = _pair(scn, coords, (B, m, m, m), f, s)
+    _check_rulebook(g, o)
+    y_ref, go_ref, ak_ref, _ = oracle.maxpool_fwd(o, x, g_in)
+    yd, god, am = scn.maxpool_fwd(g, dev(x), dev(g_in))
+    assert np.array_equal(host(yd), y_ref.astype(np.float32))
+    assert np.array_equal(host(god), go_ref.astype(np.float32))
+    assert np.array_equal(host(am).astype(np.int32), ak_ref)
+    dy = rng.uniform(-1, 1, size=(g.a_out, C)).astype(np.float32)
+    dg = rng.uniform(-1, 1, size=C).astype(np.float32)
+    dx_ref, dgi_ref = oracle.maxpool_bwd(o, x, g_in, dy, dg)
+    dxd, dgid = scn.maxpool_bwd(g, am, dev(dy), dev(dg))
+    if f <= s:
+        assert np.array_equal(host(dxd), dx_ref.astype(np.float32))
+    else:
+        sig_dx = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), None)[0])
+        assert_close("dx", host(dxd), dx_ref, sig_dx)
+    sig = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), _sq(dg))[1])
+    assert_close("dg_in", host(dgid), dgi_ref, sig)
+
+
+# --------------------------------------------------------------------------
+# a full-size layer: shells of the object-recognition networks at m = 254
+# --------------------------------------------------------------------------
+
+def test_full_size_shells_rulebook_properties(scn):
+    """32 shell samples on the size-254 tetrahedral grid (the input of a
+    six-level network): every pair links an input to the output it lies
+    under through the offset of its list, the active outputs are exactly the
+    valid sites under some input, and a sample of outputs matches the oracle
+    run on that output's neighbourhood."""
+    B, m = 32, 254
+    rows = []
+    for b in range(B):
+        rng = stream_rng(6600, b)
+        semi = [0.5 * 80 * float(rng.uniform(0.6, 1.0)) for _ in range(3)]
+        s_ = tetra_shell_sites(rng, m, semi, (2, 4)[int(rng.integers(2))])
+        rows.append(np.concatenate([np.full((len(s_), 1), b, np.int64), s_], axis=1))
+    coords = np.ascontiguousarray(np.concatenate(rows).astype(np.int32))
+    for f, s in ((2, 1), (3, 2)):
+        g = scn.build_rulebook(dev(coords), (B, m, m, m), f, s, lattice=T)
+        oc, ir, orr = (host(t).astype(np.int64) for t in g.export())
+        offs = [(kx, ky, kz) for kz in range(f) for ky in range(f) for kx in range(f)
+                if kx + ky + kz < f]
+        assert g.K == len(offs)
+        q = (m - f) // s + 1
+        assert (oc[:, 1:].sum(1) < q).all()                      # valid output grid
+        ci = coords.astype(np.int64)
+        for k, (kx, ky, kz) in enumerate(offs):
+            lo, hi = g.offsets[k], g.offsets[k + 1]
+            a, o = ci[ir[lo:hi]], oc[orr[lo:hi]]
+            assert np.array_equal(a[:, 0], o[:, 0])
+            assert np.array_equal(a[:, 1:], s * o[:, 1:] + np.array([kx, ky, kz]))
+            assert (np.diff(orr[lo:hi]) > 0).all()
+        # every output has a pair, and a pair exists for every (input, valid
+        # window containing it): count windows per input independently
+        assert len(np.unique(orr)) == g.a_out
+        want = 0
+        for (kx, ky, kz) in offs:
+            d = ci[:, 1:] - np.array([kx, ky, kz])
+            okk = (d >= 0).all(1) & (d % s == 0).all(1) & ((d // s).sum(1) < q)
+            want += int(okk.sum())
+        assert g.n_pairs == want
+        # sampled outputs against the oracle on the sites around them
+        rng = stream_rng(6601, f)
+        for r in rng.choice(g.a_out, size=20, replace=False):
+            b, ox, oy, oz = oc[r]
+            near = ci[(ci[:, 0] == b) &
+                      (np.abs(ci[:, 1:] - s * np.array([ox, oy, oz])).max(1) <= f + 1)]
+            sub = oracle.Rulebook(np.ascontiguousarray(near.astype(np.int32)), (B, m, m, m), f, s,
+                                  lattice=T).arrays()
+            want_rows = {tuple(near[i]) for k in range(sub.K)
+                         for i, o_ in zip(sub.in_rows[sub.offsets[k]:sub.offsets[k + 1]],
+                                          sub.out_rows[sub.offsets[k]:sub.offsets[k + 1]])
+                         if tuple(sub.out_coords[o_]) == (b, ox, oy, oz)}
+            got_rows = {tuple(ci[i]) for i in ir[orr == r]}
+            assert got_rows == want_rows

@@ -14,7 +14,7 @@ import pytest
 sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
 import oracle  # noqa: E402
-from gen import shell_sites, stream_rng  # noqa: E402
+from gen import shell_sites, stream_rng, tetra_shell_sites  # noqa: E402
 from helpers import dev, host  # noqa: E402
 
 torch = pytest.importorskip("torch")
@@ -30,24 +30,30 @@ def scn():
     return m
 
 
-def _batch(batch, m, scale, seed):
+def _batch(batch, m, scale, seed, lattice="cubic"):
     rows = []
     for b in range(batch):
         rng = stream_rng(seed, b)
         semi = [0.5 * scale * float(rng.uniform(0.6, 1.0)) for _ in range(3)]
-        s = shell_sites(rng, m, semi, [m / 2.0] * 3, (2, 4)[int(rng.integers(2))])
+        power = (2, 4)[int(rng.integers(2))]
+        if lattice == "cubic":
+            s = shell_sites(rng, m, semi, [m / 2.0] * 3, power)
+        else:
+            s = tetra_shell_sites(rng, m, semi, power)
         rows.append(np.concatenate([np.full((len(s), 1), b, np.int64), s], axis=1))
     return np.ascontiguousarray(np.concatenate(rows).astype(np.int32))
 
 
-@pytest.mark.parametrize("levels,width,scale", [(1, 4, 3.0), (2, 4, 6.0), (3, 3, 12.0)])
-def test_network_matches_oracle_chain(scn, levels, width, scale):
+@pytest.mark.parametrize("lattice,levels,width,scale", [
+    ("cubic", 1, 4, 3.0), ("cubic", 2, 4, 6.0), ("cubic", 3, 3, 12.0),
+    ("tetrahedral", 1, 4, 1.5), ("tetrahedral", 2, 4, 4.0), ("tetrahedral", 3, 3, 9.0)])
+def test_network_matches_oracle_chain(scn, lattice, levels, width, scale):
     from paper_1505_02890_amd.network import SparseNet, input_size
 
     batch = 3
     m = input_size(levels)
-    coords = _batch(batch, m, scale, 4242 + levels)
-    net = SparseNet(levels, classes=5, width=width, seed=levels)
+    coords = _batch(batch, m, scale, 4242 + levels, lattice)
+    net = SparseNet(levels, classes=5, width=width, seed=levels, lattice=lattice)
     x = np.ones((len(coords), 1), np.float32)
     out, oc, rec = net.forward(dev(coords, torch.int32), dev(x), batch)
     assert [r[0] for r in rec] == [L.kind for L in net.layers]
@@ -55,7 +61,7 @@ def test_network_matches_oracle_chain(scn, levels, width, scale):
     c, grid, xr = coords, (batch, m, m, m), x.astype(np.float64)
     g = np.zeros(1)
     for L, p in zip(net.layers, net.params):
-        o = oracle.Rulebook(c, grid, L.f, L.s)
+        o = oracle.Rulebook(c, grid, L.f, L.s, lattice=lattice)
         if L.kind == "conv":
             W, b = (host(t).astype(np.float64) for t in p)
             xr, g = oracle.conv_fwd(o, xr, g, W, b, relu=L.relu)
