@@ -21,5 +21,7 @@ from .synth import (  # noqa: F401
     tetra_sites,
     tetra_random_sites,
     tetra_shell_sites,
+    triangle_sites,
+    tri_random_sites,
     stream_rng,
 )

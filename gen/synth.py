@@ -287,6 +287,29 @@ def tetra_random_sites(rng: np.random.Generator, batch: int, m: int, n: int,
     return np.concatenate([b[:, None], cell[i]], axis=1).astype(np.int32)
 
 
+def triangle_sites(m: int) -> np.ndarray:
+    """All sites x + y < m of a triangular grid of size m as int64[C(m+1, 2)][3]
+    (x, y, 0), y slowest."""
+    r = np.arange(max(int(m), 0))
+    y, x = np.meshgrid(r, r, indexing="ij")
+    keep = (x + y) < m
+    return np.stack([x[keep], y[keep], np.zeros(int(keep.sum()), np.int64)], axis=1).astype(np.int64)
+
+
+def tri_random_sites(rng: np.random.Generator, batch: int, m: int, n: int,
+                     shuffle: bool = True) -> np.ndarray:
+    """n distinct uniformly random sites of `batch` triangular grids of size m
+    as int32[n][4] rows (b, x, y, 0)."""
+    cell = triangle_sites(m)
+    vol = batch * len(cell)
+    n = min(int(n), vol)
+    flat = rng.choice(vol, size=n, replace=False)
+    if not shuffle:
+        flat = np.sort(flat)
+    b, i = flat // max(len(cell), 1), flat % max(len(cell), 1)
+    return np.concatenate([b[:, None], cell[i]], axis=1).astype(np.int32)
+
+
 def tetra_shell_sites(rng: np.random.Generator, m: int, semi: Sequence[float],
                       power: int = 2) -> np.ndarray:
     """The shell of `shell_sites` drawn on the tetrahedral grid of size m:

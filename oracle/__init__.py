@@ -24,9 +24,10 @@ from .build import LIB_PATH, build
 
 STATUS = {0: "ok", 1: "invalid", 2: "range", 3: "duplicate", 4: "overflow"}
 
-# section 1.2: the cubic lattice, and the tetrahedral lattice in skewed
-# coordinates (grid x + y + z < m, filter offsets kx + ky + kz < f)
-LATTICES = {"cubic": 0, "tetrahedral": 1}
+# section 1.2, Figure 2: the cubic and square lattices, and the tetrahedral
+# and triangular lattices in skewed coordinates (grid x + y (+ z) < m, filter
+# offsets kx + ky (+ kz) < f); the 2D lattices use grids with mz = 1
+LATTICES = {"cubic": 0, "tetrahedral": 1, "square": 2, "triangular": 3}
 
 _lib = None
 
@@ -87,7 +88,7 @@ class RulebookArrays:
 
 class Rulebook:
     """Owner of an oracle rulebook (H_in, H_out and the per-offset rule lists)
-    on the cubic or the tetrahedral lattice."""
+    on one of the lattices of Figure 2."""
 
     def __init__(self, coords: np.ndarray, grid: Sequence[int], f: int, s: int,
                  lattice: str = "cubic"):

@@ -19,6 +19,11 @@
 //    kx + ky + kz < f, numbered in the cubic scan order above restricted to
 //    those offsets, and output o is valid when its whole window lies in the
 //    grid, i.e. ox + oy + oz < floor((m - f) / s) + 1;
+//  * the 2D lattices of Figure 2 (i) and (ii) are the grids with mz = 1 and
+//    z = 0: the square lattice takes the f^2 offsets (kx, ky, 0), the
+//    triangular one (skewed coordinates, sites x + y < m, mx = my = m) the
+//    C(f+1, 2) offsets kx + ky < f, with the same numbering and validity
+//    rules as the 3D lattices;
 //  * site key = ((b*mz + z)*my + y)*mx + x; output rows are numbered in
 //    ascending key order starting at 0;
 //  * W is stored offset-major: W[k][ci][co] (row k*Cin + ci of the
@@ -49,7 +54,7 @@ uint64_t key_of(const Grid& g, int64_t b, int64_t x, int64_t y, int64_t z) {
 
 struct Rulebook {
   int f = 0, s = 0, K = 0;
-  int lattice = 0;  // 0 cubic, 1 tetrahedral
+  int lattice = 0;  // 0 cubic, 1 tetrahedral, 2 square, 3 triangular
   std::vector<int> offs;  // offset k -> (kz*f + ky)*f + kx of the cube scan
   Grid gin, gout;
   int64_t a_in = 0;
@@ -100,11 +105,16 @@ int orc_rb_build_lattice(const int32_t* coords, int64_t n, const int64_t* grid, 
                          int32_t s, int32_t lattice, void** out) {
   *out = nullptr;
   if (n < 0 || f < 1 || s < 1 || (n > 0 && coords == nullptr) || grid == nullptr) return INVALID;
-  if (lattice != 0 && lattice != 1) return INVALID;
+  if (lattice < 0 || lattice > 3) return INVALID;
+  const bool planar = lattice >= 2;                    // square, triangular
+  const bool simplex = lattice == 1 || lattice == 3;   // tetrahedral, triangular
   Grid g{grid[0], grid[1], grid[2], grid[3]};
   if (g.B < 1 || g.mx < 1 || g.my < 1 || g.mz < 1) return INVALID;
-  // a tetrahedral grid has one size m: the sites x + y + z < m
-  if (lattice == 1 && (g.my != g.mx || g.mz != g.mx)) return INVALID;
+  // a 2D grid has one z plane; a simplex grid has one size m: the sites
+  // with coordinate sum below m
+  if (planar && g.mz != 1) return INVALID;
+  if (simplex && (g.my != g.mx || (!planar && g.mz != g.mx))) return INVALID;
+  const int fz = planar ? 1 : f;  // filter extent along z
   const int64_t LIM = INT64_C(1) << 62;
   if (!mul_ok(g.B, g.mz, LIM) || !mul_ok(g.B * g.mz, g.my, LIM) ||
       !mul_ok(g.B * g.mz * g.my, g.mx, LIM))
@@ -115,20 +125,20 @@ int orc_rb_build_lattice(const int32_t* coords, int64_t n, const int64_t* grid, 
   rb->f = f;
   rb->s = s;
   rb->lattice = lattice;
-  for (int kz = 0; kz < f; ++kz)
+  for (int kz = 0; kz < fz; ++kz)
     for (int ky = 0; ky < f; ++ky)
       for (int kx = 0; kx < f; ++kx)
-        if (lattice == 0 || kx + ky + kz < f) rb->offs.push_back((kz * f + ky) * f + kx);
+        if (!simplex || kx + ky + kz < f) rb->offs.push_back((kz * f + ky) * f + kx);
   rb->K = static_cast<int>(rb->offs.size());
   rb->gin = g;
-  rb->gout = Grid{g.B, out_extent(g.mx, f, s), out_extent(g.my, f, s), out_extent(g.mz, f, s)};
+  rb->gout = Grid{g.B, out_extent(g.mx, f, s), out_extent(g.my, f, s), out_extent(g.mz, fz, s)};
   rb->a_in = n;
 
   for (int64_t r = 0; r < n; ++r) {
     const int32_t* c = coords + 4 * r;
     if (c[0] < 0 || c[0] >= g.B || c[1] < 0 || c[1] >= g.mx || c[2] < 0 || c[2] >= g.my ||
         c[3] < 0 || c[3] >= g.mz ||
-        (lattice == 1 && (int64_t)c[1] + c[2] + c[3] >= g.mx)) {
+        (simplex && (int64_t)c[1] + c[2] + c[3] >= g.mx)) {
       delete rb;
       return RANGE;
     }
@@ -152,8 +162,8 @@ int orc_rb_build_lattice(const int32_t* coords, int64_t n, const int64_t* grid, 
       bool ok = true;
       for (int a = 0; a < 3; ++a)
         ok = ok && d[a] >= 0 && d[a] % s == 0 && d[a] / s < m[a];
-      // tetrahedral: the output grid is the sites o with ox + oy + oz < m_out
-      if (lattice == 1) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;
+      // simplex lattices: the output grid is the sites with coordinate sum below m_out
+      if (simplex) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;
       if (ok) H_out.insert(key_of(go, c[0], d[0] / s, d[1] / s, d[2] / s));
     }
   }

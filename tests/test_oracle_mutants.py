@@ -53,20 +53,30 @@ MUTANTS = [
 
 # mistakes in the tetrahedral lattice (section 1.2), caught by its own pins
 LATTICE_MUTANTS = [
-    ("tetra_filter_one_too_big", "if (lattice == 0 || kx + ky + kz < f)",
-     "if (lattice == 0 || kx + ky + kz <= f)"),
-    ("tetra_output_bound_dropped", "if (lattice == 1) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;",
-     "if (lattice == 1) ok = ok;"),
-    ("tetra_output_bound_off_by_one", "if (lattice == 1) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;",
-     "if (lattice == 1) ok = ok && (d[0] + d[1] + d[2]) / s <= go.mx;"),
-    ("tetra_range_check_dropped", "(lattice == 1 && (int64_t)c[1] + c[2] + c[3] >= g.mx)",
-     "(lattice == 1 && false)"),
+    ("tetra_filter_one_too_big", "if (!simplex || kx + ky + kz < f)",
+     "if (!simplex || kx + ky + kz <= f)"),
+    ("tetra_output_bound_dropped", "if (simplex) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;",
+     "if (simplex) ok = ok;"),
+    ("tetra_output_bound_off_by_one", "if (simplex) ok = ok && (d[0] + d[1] + d[2]) / s < go.mx;",
+     "if (simplex) ok = ok && (d[0] + d[1] + d[2]) / s <= go.mx;"),
+    ("tetra_range_check_dropped", "(simplex && (int64_t)c[1] + c[2] + c[3] >= g.mx)",
+     "(simplex && false)"),
     ("tetra_offsets_reversed", "rb->K = static_cast<int>(rb->offs.size());",
      "std::reverse(rb->offs.begin(), rb->offs.end());\n  rb->K = static_cast<int>(rb->offs.size());"),
 ]
 
+# mistakes in the 2D lattices (Figure 2 (i), (ii)), caught by their pins
+PLANAR_MUTANTS = [
+    ("planar_filter_spans_z", "const int fz = planar ? 1 : f;", "const int fz = f;"),
+    ("planar_extra_planes_accepted", "if (planar && g.mz != 1) return INVALID;",
+     "if (planar && g.mz < 1) return INVALID;"),
+    ("triangle_is_square", "const bool simplex = lattice == 1 || lattice == 3;",
+     "const bool simplex = lattice == 1;"),
+]
+
 CASES = [m + ("test_oracle_pins.py",) for m in MUTANTS] + \
-        [m + ("test_oracle_lattice.py",) for m in LATTICE_MUTANTS]
+        [m + ("test_oracle_lattice.py",) for m in LATTICE_MUTANTS] + \
+        [m + ("test_oracle_lattice2d.py",) for m in PLANAR_MUTANTS]
 
 
 @pytest.mark.parametrize("name,old,new,pins", CASES, ids=[m[0] for m in CASES])
