@@ -17,8 +17,9 @@ workload.
     python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--no-cpu]
 
 With --network it instead times whole-network inference of the paper's
-object-recognition networks (nC2-MP3/2, scales 20/40/80, on the cubic and the
-tetrahedral lattice) and prints one JSON line per network.
+networks (the nC2-MP3/2 object-recognition networks at scales 20/40/80 on the
+cubic and the tetrahedral lattice; SquareNet and TriangLeNet on 32 x 32
+images) and prints one JSON line per network.
 """
 from __future__ import annotations
 
@@ -49,8 +50,8 @@ def parse():
                    help="input sites of the bounded CPU-oracle sample")
     p.add_argument("--network", action="store_true",
                    help="instead: whole-network inference throughput of the paper's "
-                        "object-recognition networks (scales 20/40/80, cubic and tetrahedral "
-                        "lattice), one JSON line each")
+                        "networks (3D object recognition on the cubic and tetrahedral "
+                        "lattices; 2D SquareNet / TriangLeNet), one JSON line each")
     p.add_argument("--batch", type=int, default=256,
                    help="samples per batch for --network (capped per network by the "
                         "rulebook's grid limit)")
@@ -128,63 +129,90 @@ def cpu_baseline(cfg, n_sites: int):
     }
 
 
-def network_bench(batch: int, reps: int, warmup: int) -> None:
-    """Inference throughput of nC2-MP3/2 networks (the object-recognition
-    experiment of section 2) on the cubic and the tetrahedral lattice: each
-    sample is one seeded shell (ellipsoid or rounded-box superquadric, random
-    rotation, semi-axes scale/2 * U(0.6, 1.0)) centred in the network's input
-    grid, features 1.0 at active sites, random He-scaled weights.  A batch is
-    timed end to end (every rulebook build, convolution and pooling, inputs
-    resident in HBM); median over `reps`."""
+def _time_net(net, cd, xd, batch_n, reps, warmup):
     import torch
 
-    from gen import shell_sites, stream_rng, tetra_shell_sites
-    from paper_1505_02890_amd.network import SparseNet, input_size, macs
+    for _ in range(warmup):
+        net.forward(cd, xd, batch_n)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        out, oc, rec = net.forward(cd, xd, batch_n)
+        torch.cuda.synchronize()
+        times.append(time.perf_counter() - t0)
+    return float(np.median(times)), out, rec
+
+
+def network_bench(batch: int, reps: int, warmup: int) -> None:
+    """Inference throughput of the paper's networks, each batch timed end to
+    end (every rulebook build, convolution and pooling, inputs resident in
+    HBM; median over `reps`), random He-scaled weights:
+      - the nC2-MP3/2 object-recognition networks of section 2 on the cubic
+        and the tetrahedral lattice: each sample one seeded shell (ellipsoid
+        or rounded-box superquadric, random rotation, semi-axes
+        scale/2 * U(0.6, 1.0)) centred in the input grid, features 1.0;
+      - SquareNet and TriangLeNet (the 2D comparison of section 2) on the
+        square and the triangular lattice: each sample a 32 x 32 three-channel
+        image (seeded N(0, 1) pixels) in the size-189 input grid, on the
+        triangular lattice as its affine image (a rhombus)."""
+    import torch
+
+    from gen import image_patch_sites, shell_sites, stream_rng, tetra_shell_sites
+    from paper_1505_02890_amd.network import PLANAR, SparseNet, input_size, macs
 
     # the paper's figures for these networks (GTX 780), context only
     paper = {"cubic": {20: (36, 1190), 40: (126, 794), 80: (406, 310)},
-             "tetrahedral": {20: (9, 1133), 40: (35, 675), 80: (143, 286)}}
-    for lattice, scale, levels in [(lat, sc, lv) for lat in ("cubic", "tetrahedral")
-                                   for sc, lv in ((20, 4), (40, 5), (80, 6))]:
-        m = input_size(levels)
+             "tetrahedral": {20: (9, 1133), 40: (35, 675), 80: (143, 286)},
+             "square": {32: (41, None)}, "triangular": {32: (30, None)}}
+    nets = [(lat, sc, lv) for lat in ("cubic", "tetrahedral")
+            for sc, lv in ((20, 4), (40, 5), (80, 6))]
+    nets += [("square", 32, 5), ("triangular", 32, 5)]
+    for lattice, scale, levels in nets:
+        planar = lattice in PLANAR
+        convs = 2 if planar else 1
+        m = input_size(levels, convs)
         # the rulebook's occupancy bitmap holds at most 2^26 words per grid
         # (the largest grid is the first convolution's output, m + 1 per axis)
-        words = (m + 1) * (m + 1) * ((m + 1 + 31) // 32)
+        words = (m + 1) * (1 if planar else m + 1) * ((m + 1 + 31) // 32)
         batch_n = min(batch, (1 << 26) // words)
         rows = []
         for b in range(batch_n):
             rng = stream_rng(150502890 + scale, b)
-            semi = [0.5 * scale * float(rng.uniform(0.6, 1.0)) for _ in range(3)]
-            power = (2, 4)[int(rng.integers(2))]
-            if lattice == "cubic":
-                sh = shell_sites(rng, m, semi, [m / 2.0] * 3, power)
+            if planar:
+                sh = image_patch_sites(lattice, m, scale, scale)
             else:
-                sh = tetra_shell_sites(rng, m, semi, power)
+                semi = [0.5 * scale * float(rng.uniform(0.6, 1.0)) for _ in range(3)]
+                power = (2, 4)[int(rng.integers(2))]
+                if lattice == "cubic":
+                    sh = shell_sites(rng, m, semi, [m / 2.0] * 3, power)
+                else:
+                    sh = tetra_shell_sites(rng, m, semi, power)
             rows.append(np.concatenate([np.full((len(sh), 1), b, np.int64), sh], axis=1))
         c = np.ascontiguousarray(np.concatenate(rows).astype(np.int32))
         cd = torch.from_numpy(c).cuda()
-        xd = torch.ones((len(c), 1), dtype=torch.float32, device="cuda")
-        net = SparseNet(levels, seed=scale, lattice=lattice)
-        for _ in range(warmup):
-            net.forward(cd, xd, batch_n)
-        torch.cuda.synchronize()
-        times = []
-        for _ in range(reps):
-            t0 = time.perf_counter()
-            out, oc, rec = net.forward(cd, xd, batch_n)
-            torch.cuda.synchronize()
-            times.append(time.perf_counter() - t0)
-        t = float(np.median(times))
+        if planar:
+            x = stream_rng(150502890 + scale, 1 << 20).standard_normal((len(c), 3))
+            xd = torch.from_numpy(x.astype(np.float32)).cuda()
+            net = SparseNet(levels, classes=10, seed=scale, lattice=lattice, convs=2, cin=3)
+            name, data = ("SquareNet" if lattice == "square" else "TriangLeNet"), \
+                "synthetic (seeded 32x32 three-channel images)"
+        else:
+            xd = torch.ones((len(c), 1), dtype=torch.float32, device="cuda")
+            net = SparseNet(levels, seed=scale, lattice=lattice)
+            name, data = f"nC2-MP3/2 {lattice} network", "synthetic (seeded shells)"
+        t, out, rec = _time_net(net, cd, xd, batch_n, reps, warmup)
+        ops, tps = paper[lattice][scale]
         print(json.dumps({
-            "metric": f"sparse CNN inference throughput (nC2-MP3/2 {lattice} network)",
+            "metric": f"sparse CNN inference throughput ({name})",
             "value": round(batch_n / t, 1), "unit": "tests/s", "higher_is_better": True,
-            "scale": scale, "levels": levels, "input_grid": m, "batch": batch_n,
-            "active_input_sites_per_sample": round(len(c) / batch_n, 1),
+            "lattice": lattice, "scale": scale, "levels": levels, "input_grid": m,
+            "batch": batch_n, "active_input_sites_per_sample": round(len(c) / batch_n, 1),
             "macs_per_sample_millions": round(macs(rec) / batch_n / 1e6, 2),
             "ms_per_batch": round(t * 1e3, 3), "final_sites": int(out.shape[0]),
-            "paper_gtx780": {"million_operations": paper[lattice][scale][0],
-                             "tests_per_s": paper[lattice][scale][1], "note": "context only"},
-            "dtype": "f32", "data": "synthetic (seeded shells)",
+            "paper_gtx780": {"million_operations": ops, "tests_per_s": tps,
+                             "note": "context only"},
+            "dtype": "f32", "data": data,
         }), flush=True)
 
 

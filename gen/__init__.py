@@ -22,6 +22,7 @@ from .synth import (  # noqa: F401
     tetra_random_sites,
     tetra_shell_sites,
     triangle_sites,
+    image_patch_sites,
     tri_random_sites,
     stream_rng,
 )

@@ -310,6 +310,22 @@ def tri_random_sites(rng: np.random.Generator, batch: int, m: int, n: int,
     return np.concatenate([b[:, None], cell[i]], axis=1).astype(np.int32)
 
 
+def image_patch_sites(lattice: str, m: int, h: int, w: int) -> np.ndarray:
+    """The sites of an h x w image placed in a 2D grid of size m as int64[h*w][3]
+    (x, y, 0), row-major: on the square lattice a centred h x w rectangle, on
+    the triangular lattice its affine image in skewed coordinates (a rhombus)
+    centred on the triangle's centroid."""
+    if lattice == "square":
+        x0, y0 = (m - w) // 2, (m - h) // 2
+    else:
+        x0, y0 = m // 3 - w // 2, m // 3 - h // 2
+    yy, xx = np.meshgrid(np.arange(h), np.arange(w), indexing="ij")
+    pts = np.stack([xx.ravel() + x0, yy.ravel() + y0, np.zeros(h * w, np.int64)], axis=1)
+    assert (pts[:, :2] >= 0).all() and (pts[:, :2] < m).all()
+    assert lattice == "square" or (pts[:, 0] + pts[:, 1] < m).all()
+    return pts.astype(np.int64)
+
+
 def tetra_shell_sites(rng: np.random.Generator, m: int, semi: Sequence[float],
                       power: int = 2) -> np.ndarray:
     """The shell of `shell_sites` drawn on the tetrahedral grid of size m:

@@ -66,9 +66,11 @@ typedef enum scn_status {
   SCN_ERR_NOMEM = 8        /* device allocation failed */
 } scn_status;
 
-/* lattices of scn_rulebook_build_lattice (section 1.2) */
+/* lattices of scn_rulebook_build_lattice (section 1.2, Figure 2) */
 #define SCN_LATTICE_CUBIC 0
 #define SCN_LATTICE_TETRAHEDRAL 1
+#define SCN_LATTICE_SQUARE 2
+#define SCN_LATTICE_TRIANGULAR 3
 
 /* flags of scn_conv_fwd / scn_conv_bwd */
 #define SCN_RELU 1u /* y = max(pre, 0) on active rows and on the ground state */
@@ -79,13 +81,13 @@ typedef struct scn_rulebook_info {
   int64_t a_in;        /* active input sites */
   int64_t a_out;       /* active output sites */
   int64_t n_pairs;     /* P = total (input row, output row) incidences */
-  int32_t K;           /* filter offsets: f^3, or C(f+2, 3) on the tetrahedral lattice */
+  int32_t K;           /* filter offsets: f^3, C(f+2, 3), f^2 or C(f+1, 2) by lattice */
   int32_t filter;      /* f */
   int32_t stride;      /* s */
   int32_t input_sorted;/* 1 if the caller's rows were already in ascending key order */
   int64_t in_grid[4];  /* B, mx, my, mz */
   int64_t out_grid[4]; /* B, floor((m-f)/s)+1 per axis */
-  int32_t lattice;     /* SCN_LATTICE_CUBIC or SCN_LATTICE_TETRAHEDRAL */
+  int32_t lattice;     /* SCN_LATTICE_* */
   int32_t reserved;    /* 0 */
 } scn_rulebook_info;
 
@@ -133,9 +135,17 @@ scn_status scn_rulebook_build(const int32_t* coords, int64_t n, const int64_t* g
  *  - output o exists where its whole window lies in the grid:
  *    ox + oy + oz < floor((m - f)/s) + 1, the output grid of the same size
  *    (out_grid holds the cube's extents, as for the cubic lattice).
+ * SCN_LATTICE_SQUARE and SCN_LATTICE_TRIANGULAR are the 2D lattices of
+ * Figure 2 (i) and (ii): grid (B, mx, my, 1), every site with z = 0.  The
+ * square filter covers the f^2 offsets (kx, ky, 0); the triangular lattice,
+ * held in skewed coordinates like the tetrahedral one, has the sites
+ * x + y < m (mx = my = m) and the C(f+1, 2) offsets kx + ky < f (3 for
+ * f = 2, 6 for f = 3), numbered in the square scan order restricted to them.
+ * out_grid[3] is 1.
  * Convolution and pooling on such a rulebook behave as on the cubic lattice
- * with these windows.  Another lattice value, or unequal tetrahedral extents,
- * is SCN_ERR_INVALID; all other arguments and errors as scn_rulebook_build.
+ * with these windows.  Another lattice value, unequal simplex extents or a
+ * 2D grid with mz != 1 is SCN_ERR_INVALID; all other arguments and errors
+ * as scn_rulebook_build.
  */
 scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const int64_t* grid,
                                       int32_t filter, int32_t stride, int32_t lattice,
@@ -215,8 +225,8 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
  * convolution).  rb must have stride >= 2; windows may overlap (filter >
  * stride: 3 over 2, the pooling the paper's networks use) or leave gaps.
  * For each active output o and channel c, y[o][c] is the maximum over the K
- * positions of the window (f^3, or C(f+2, 3) on the tetrahedral lattice: 10
- * for MP3/2), an active position holding x[row][c] and an inactive one
+ * positions of the window (the rulebook's K: f^3 on the cubic lattice, 10 for
+ * MP3/2 on the tetrahedral one), an active position holding x[row][c] and an inactive one
  * g_in[c]; ties keep the first position in ascending k.
  * argmax[o][c] receives that k.  g_out = g_in.
  *  x [a_in][C], g_in [C] -> y [a_out][C], g_out [C], argmax uint8 [a_out][C].

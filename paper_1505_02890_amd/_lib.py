@@ -19,8 +19,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("SCN_LIB") or os.path.join(HERE, "libscn.so")
 
 SCN_RELU = 1
-# section 1.2: the cubic lattice and the tetrahedral lattice (skewed coordinates)
-LATTICES = {"cubic": 0, "tetrahedral": 1}
+# section 1.2, Figure 2: the cubic and square lattices, and the tetrahedral and
+# triangular lattices in skewed coordinates (2D lattices: grids with mz = 1)
+LATTICES = {"cubic": 0, "tetrahedral": 1, "square": 2, "triangular": 3}
 STATUS = {0: "ok", 1: "invalid", 2: "range", 3: "duplicate", 4: "overflow",
           5: "unsupported", 6: "workspace", 7: "hip", 8: "nomem"}
 
@@ -122,8 +123,8 @@ class Rulebook:
     """Owner of a device rulebook built by ``scn_rulebook_build_lattice``.
 
     ``coords`` is a device int32 [n, 4] tensor of (b, x, y, z) rows; ``grid``
-    is (B, mx, my, mz); ``lattice`` is "cubic" or "tetrahedral".  Attributes
-    mirror ``scn_rulebook_info``.
+    is (B, mx, my, mz); ``lattice`` is "cubic", "tetrahedral", "square" or
+    "triangular".  Attributes mirror ``scn_rulebook_info``.
     """
 
     def __init__(self, coords: torch.Tensor, grid: Sequence[int], filter: int, stride: int,

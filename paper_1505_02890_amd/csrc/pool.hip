@@ -2,8 +2,8 @@
 // over the same active-site rules and ground state) and its gradient, for
 // windows that tile the grid (filter == stride), leave gaps (filter < stride)
 // or overlap (filter > stride, the MP3/2 of the paper's networks), on the
-// cubic lattice (K = f^3 positions per window) or the tetrahedral one
-// (K = C(f+2, 3)).  Max-pooling only moves data, so the kernels are organised
+// cubic lattice (K = f^3 positions per window), the tetrahedral one
+// (K = C(f+2, 3)) or the 2D square and triangular ones (K = f^2, C(f+1, 2)).  Max-pooling only moves data, so the kernels are organised
 // for coalesced HBM traffic: threads over (site, channel) with channels
 // innermost, window rows from the rulebook's per-output neighbour table, no
 // atomics.
@@ -341,14 +341,18 @@ __global__ void __launch_bounds__(256) maxpool_bwd_ground_finish(const float* __
 
 inline unsigned nblocks(int64_t n, int t) { return (unsigned)std::max<int64_t>(1, ceil_div(n, t)); }
 
-// calls fn(std::integral_constant<int, K>{}) for the window sizes of both
-// lattices: 1, 8, 27 (cube) and 4, 10 (tetrahedron)
+// calls fn(std::integral_constant<int, K>{}) for the window sizes of the
+// lattices: 1, 8, 27 (cube), 4, 10 (tetrahedron), 4, 9 (square), 3, 6
+// (triangle)
 template <typename Fn>
 void with_window(int K, Fn fn) {
   switch (K) {
     case 1: fn(std::integral_constant<int, 1>{}); break;
+    case 3: fn(std::integral_constant<int, 3>{}); break;
     case 4: fn(std::integral_constant<int, 4>{}); break;
+    case 6: fn(std::integral_constant<int, 6>{}); break;
     case 8: fn(std::integral_constant<int, 8>{}); break;
+    case 9: fn(std::integral_constant<int, 9>{}); break;
     case 10: fn(std::integral_constant<int, 10>{}); break;
     default: fn(std::integral_constant<int, 27>{}); break;
   }

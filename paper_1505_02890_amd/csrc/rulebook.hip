@@ -12,15 +12,18 @@
 // numbering (ascending key) needs no sort, no hash probing and no atomics on
 // the output side, and every result is deterministic.
 //
-// Lattices (section 1.2).  The cubic lattice uses the grid [0, m)^3 and the
-// f^3 offsets of a cube.  The tetrahedral lattice is held in skewed integer
-// coordinates: its grid of size m is the sites x + y + z < m of a cube with
-// equal extents m, a filter of size f covers the C(f+2, 3) offsets
-// kx + ky + kz < f (numbered in the cube's scan order restricted to them),
-// and output o exists where its whole window lies in the grid, i.e. where
-// ox + oy + oz < (m - f) / s + 1.  Both lattices share every phase below; the
-// tetrahedral one masks the dilated rows to that output grid and visits only
-// its own offsets.
+// Lattices (section 1.2, Figure 2).  The cubic lattice uses the grid
+// [0, m)^3 and the f^3 offsets of a cube.  The tetrahedral lattice is held in
+// skewed integer coordinates: its grid of size m is the sites x + y + z < m
+// of a cube with equal extents m, a filter of size f covers the C(f+2, 3)
+// offsets kx + ky + kz < f (numbered in the cube's scan order restricted to
+// them), and output o exists where its whole window lies in the grid, i.e.
+// where ox + oy + oz < (m - f) / s + 1.  The square and triangular lattices
+// are their 2D counterparts on grids with one z plane (mz = 1, z = 0): f^2
+// offsets (kx, ky, 0), or the C(f+1, 2) offsets kx + ky < f on the sites
+// x + y < m.  All lattices share every phase below; the simplex ones
+// (tetrahedral, triangular) mask the dilated rows to their output grid and
+// visit only their own offsets.
 //
 // Phases (one stream, two host synchronisations):
 //   1 mark inputs            bitmap OR per input; range / duplicate checks
@@ -50,17 +53,24 @@ enum : uint32_t { F_RANGE = 1, F_DUP = 2, F_UNSORTED = 4 };
 struct GridDev {
   int32_t B, mx, my, mz;  // grid extents
   int32_t rw;             // 32-bit words per x-row
-  int32_t tet;            // 1: tetrahedral lattice, sites x + y + z < mx
+  int32_t simplex;        // 1: sites with x + y + z < mx only (tetrahedral, triangular)
 };
 
-// Window offsets of a filter of size F: the cube [0, F)^3, or on the
-// tetrahedral lattice its corner kx + ky + kz < F.  row_len(ky, kz) offsets
-// of x-row (ky, kz) are in the window (0 or fewer: none); offsets are counted
-// in scan order (x fastest).
-template <int F, bool TET>
+// Window offsets of a filter of size F on lattice LAT: the cube [0, F)^3, its
+// corner kx + ky + kz < F (tetrahedral), the square [0, F)^2 x {0}, or its
+// corner kx + ky < F (triangular).  FZ is the window's extent along z;
+// row_len(ky, kz) offsets of x-row (ky, kz) are in the window (0 or fewer:
+// none); offsets are counted in scan order (x fastest).
+template <int F, int LAT>
 struct Win {
-  static constexpr int K = TET ? F * (F + 1) * (F + 2) / 6 : F * F * F;
-  static constexpr int row_len(int ky, int kz) { return TET ? F - ky - kz : F; }
+  static constexpr bool SIMPLEX = LAT == SCN_LATTICE_TETRAHEDRAL || LAT == SCN_LATTICE_TRIANGULAR;
+  static constexpr bool PLANAR = LAT == SCN_LATTICE_SQUARE || LAT == SCN_LATTICE_TRIANGULAR;
+  static constexpr int FZ = PLANAR ? 1 : F;
+  static constexpr int K = LAT == SCN_LATTICE_CUBIC         ? F * F * F
+                           : LAT == SCN_LATTICE_TETRAHEDRAL ? F * (F + 1) * (F + 2) / 6
+                           : LAT == SCN_LATTICE_SQUARE      ? F * F
+                                                            : F * (F + 1) / 2;
+  static constexpr int row_len(int ky, int kz) { return SIMPLEX ? F - ky - kz : F; }
 };
 
 __device__ inline uint64_t site_key(const GridDev& g, int64_t b, int64_t x, int64_t y,
@@ -110,7 +120,7 @@ __global__ void __launch_bounds__(256) mark_inputs_kernel(const int32_t* __restr
     const int4 c = reinterpret_cast<const int4*>(coords)[i];
     const bool ok = c.x >= 0 && c.x < g.B && c.y >= 0 && c.y < g.mx && c.z >= 0 &&
                     c.z < g.my && c.w >= 0 && c.w < g.mz &&
-                    (!g.tet || (int64_t)c.y + c.z + c.w < g.mx);
+                    (!g.simplex || (int64_t)c.y + c.z + c.w < g.mx);
     if (!ok) {
       f |= F_RANGE;
     } else {
@@ -178,18 +188,18 @@ __device__ inline WordPos word_pos(int wo, const GridDev& g) {
 
 // ---- phase 4: output occupancy (dilation of the input bitmap) -------------
 // SM: 1 stride 1 (funnel shifts), 2 stride 2 (even-bit compression), 0 any.
-// On the tetrahedral lattice the bits past the output grid (x + y + z >= mx)
+// On the simplex lattices the bits past the output grid (x + y + z >= mx)
 // are cleared and rows wholly past it are not read.
-template <int F, bool TET, int SM>
+template <int F, int LAT, int SM>
 __global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict__ inb, GridDev gi,
                                                      uint32_t* __restrict__ outb, GridDev go,
                                                      int nw_out, int s) {
-  using W = Win<F, TET>;
+  using W = Win<F, LAT>;
   const int wo = blockIdx.x * blockDim.x + threadIdx.x;
   if (wo >= nw_out) return;
   const WordPos wp = word_pos(wo, go);
   const int x0 = wp.wx * 32;
-  const int lim = TET ? go.mx - wp.y - wp.z : go.mx;  // x < lim on this row
+  const int lim = W::SIMPLEX ? go.mx - wp.y - wp.z : go.mx;  // x < lim on this row
   const int nvalid = min(32, lim - x0);
   if (nvalid <= 0) {
     outb[wo] = 0u;
@@ -198,7 +208,7 @@ __global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict_
   const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
   uint32_t v = 0;
 #pragma unroll
-  for (int kz = 0; kz < F; ++kz)
+  for (int kz = 0; kz < W::FZ; ++kz)
 #pragma unroll
     for (int ky = 0; ky < F; ++ky) {
       const int nx = W::row_len(ky, kz);
@@ -230,14 +240,14 @@ __global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict_
 }
 
 // ---- phase 6: output coordinates and neighbour masks ----------------------
-template <int F, bool TET, bool S1>
+template <int F, int LAT, bool S1>
 __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restrict__ inb, GridDev gi,
                                                         const uint32_t* __restrict__ outb,
                                                         const uint32_t* __restrict__ opref,
                                                         GridDev go, int nw_out, int s,
                                                         int32_t* __restrict__ out_coords,
                                                         uint32_t* __restrict__ masks) {
-  using W = Win<F, TET>;
+  using W = Win<F, LAT>;
   constexpr int K = W::K;
   const int wo = blockIdx.x * blockDim.x + threadIdx.x;
   if (wo >= nw_out) return;
@@ -251,7 +261,7 @@ __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restri
     uint32_t E[K];
     int k = 0;
 #pragma unroll
-    for (int kz = 0; kz < F; ++kz)
+    for (int kz = 0; kz < W::FZ; ++kz)
 #pragma unroll
       for (int ky = 0; ky < F; ++ky) {
         if (W::row_len(ky, kz) <= 0) continue;
@@ -281,7 +291,7 @@ __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restri
       uint32_t m = 0;
       int k = 0;
 #pragma unroll
-      for (int kz = 0; kz < F; ++kz)
+      for (int kz = 0; kz < W::FZ; ++kz)
 #pragma unroll
         for (int ky = 0; ky < F; ++ky) {
           if (W::row_len(ky, kz) <= 0) continue;
@@ -327,14 +337,14 @@ __global__ void list_offsets_kernel(const uint64_t* __restrict__ pos, int64_t nt
 // ---- phase 9: emit the pair lists ------------------------------------------
 // One thread per output, one wave per tile.  All K rank lookups are issued
 // before any dependent load so they overlap.
-template <int F, bool TET>
+template <int F, int LAT>
 __global__ void __launch_bounds__(256) emit_pairs_kernel(
     const uint32_t* __restrict__ masks, const int32_t* __restrict__ out_coords, int64_t a_out,
     int64_t nt, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
     GridDev gi, const int32_t* __restrict__ perm, const uint64_t* __restrict__ pos,
     int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows, int32_t* __restrict__ in_rank,
     int32_t* __restrict__ nbr, int32_t* __restrict__ inv, int inv_slots) {
-  using W = Win<F, TET>;
+  using W = Win<F, LAT>;
   constexpr int K = W::K;
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t t = o >> 6;
@@ -347,7 +357,7 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
   {
     int k = 0;
 #pragma unroll
-    for (int kz = 0; kz < F; ++kz)
+    for (int kz = 0; kz < W::FZ; ++kz)
 #pragma unroll
       for (int ky = 0; ky < F; ++ky)
 #pragma unroll
@@ -455,24 +465,24 @@ struct Temps {
 };
 
 // Kernel variants by filter size and lattice.
-template <int F, bool TET>
+template <int F, int LAT>
 struct Kernels {
-  static constexpr int K = Win<F, TET>::K;
+  static constexpr int K = Win<F, LAT>::K;
   static void dilate(int sm, dim3 g, hipStream_t st, const uint32_t* inb, GridDev gi, uint32_t* outb,
                      GridDev go, int nw_out, int s) {
     if (sm == 1)
-      hipLaunchKernelGGL((dilate_kernel<F, TET, 1>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
+      hipLaunchKernelGGL((dilate_kernel<F, LAT, 1>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
     else if (sm == 2)
-      hipLaunchKernelGGL((dilate_kernel<F, TET, 2>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
+      hipLaunchKernelGGL((dilate_kernel<F, LAT, 2>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
     else
-      hipLaunchKernelGGL((dilate_kernel<F, TET, 0>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
+      hipLaunchKernelGGL((dilate_kernel<F, LAT, 0>), g, dim3(256), 0, st, inb, gi, outb, go, nw_out, s);
   }
   template <typename... A>
   static void out_sites(bool s1, dim3 g, hipStream_t st, A... a) {
     if (s1)
-      hipLaunchKernelGGL((out_sites_kernel<F, TET, true>), g, dim3(256), 0, st, a...);
+      hipLaunchKernelGGL((out_sites_kernel<F, LAT, true>), g, dim3(256), 0, st, a...);
     else
-      hipLaunchKernelGGL((out_sites_kernel<F, TET, false>), g, dim3(256), 0, st, a...);
+      hipLaunchKernelGGL((out_sites_kernel<F, LAT, false>), g, dim3(256), 0, st, a...);
   }
   template <typename... A>
   static void tile_count(dim3 g, hipStream_t st, A... a) {
@@ -480,17 +490,25 @@ struct Kernels {
   }
   template <typename... A>
   static void emit(dim3 g, hipStream_t st, A... a) {
-    hipLaunchKernelGGL((emit_pairs_kernel<F, TET>), g, dim3(256), 0, st, a...);
+    hipLaunchKernelGGL((emit_pairs_kernel<F, LAT>), g, dim3(256), 0, st, a...);
   }
 };
 
-// calls fn(Kernels<F, TET>{}) for the runtime filter size and lattice
+// calls fn(Kernels<F, LAT>{}) for the runtime filter size and lattice
+template <int LAT, typename Fn>
+void with_filter(int f, Fn fn) {
+  if (f == 1) fn(Kernels<1, LAT>{});
+  else if (f == 2) fn(Kernels<2, LAT>{});
+  else fn(Kernels<3, LAT>{});
+}
+
 template <typename Fn>
 void with_kernels(int f, int lattice, Fn fn) {
-  if (lattice == SCN_LATTICE_TETRAHEDRAL) {
-    if (f == 1) fn(Kernels<1, true>{}); else if (f == 2) fn(Kernels<2, true>{}); else fn(Kernels<3, true>{});
-  } else {
-    if (f == 1) fn(Kernels<1, false>{}); else if (f == 2) fn(Kernels<2, false>{}); else fn(Kernels<3, false>{});
+  switch (lattice) {
+    case SCN_LATTICE_TETRAHEDRAL: with_filter<SCN_LATTICE_TETRAHEDRAL>(f, fn); break;
+    case SCN_LATTICE_SQUARE: with_filter<SCN_LATTICE_SQUARE>(f, fn); break;
+    case SCN_LATTICE_TRIANGULAR: with_filter<SCN_LATTICE_TRIANGULAR>(f, fn); break;
+    default: with_filter<SCN_LATTICE_CUBIC>(f, fn); break;
   }
 }
 
@@ -503,7 +521,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   *out = nullptr;
   if (!grid || n < 0 || (n > 0 && !coords) || f < 1 || s < 1 ||
       (reinterpret_cast<uintptr_t>(coords) & 15) != 0 ||
-      (lattice != SCN_LATTICE_CUBIC && lattice != SCN_LATTICE_TETRAHEDRAL)) {
+      lattice < SCN_LATTICE_CUBIC || lattice > SCN_LATTICE_TRIANGULAR) {
     set_error("scn_rulebook_build: invalid argument (n=%lld f=%d s=%d lattice=%d)", (long long)n,
               f, s, lattice);
     return SCN_ERR_INVALID;
@@ -513,9 +531,14 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
       set_error("scn_rulebook_build: grid extent %d is %lld", a, (long long)grid[a]);
       return SCN_ERR_INVALID;
     }
-  const bool tet = lattice == SCN_LATTICE_TETRAHEDRAL;
-  if (tet && (grid[2] != grid[1] || grid[3] != grid[1])) {
-    set_error("scn_rulebook_build: a tetrahedral grid has one size (got %lld, %lld, %lld)",
+  const bool planar = lattice == SCN_LATTICE_SQUARE || lattice == SCN_LATTICE_TRIANGULAR;
+  const bool simplex = lattice == SCN_LATTICE_TETRAHEDRAL || lattice == SCN_LATTICE_TRIANGULAR;
+  if (planar && grid[3] != 1) {
+    set_error("scn_rulebook_build: a 2D lattice needs mz = 1 (got %lld)", (long long)grid[3]);
+    return SCN_ERR_INVALID;
+  }
+  if (simplex && (grid[2] != grid[1] || (!planar && grid[3] != grid[1]))) {
+    set_error("scn_rulebook_build: a simplex grid has one size (got %lld, %lld, %lld)",
               (long long)grid[1], (long long)grid[2], (long long)grid[3]);
     return SCN_ERR_INVALID;
   }
@@ -527,9 +550,14 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     set_error("scn_rulebook_build: %lld sites exceed INT32_MAX", (long long)n);
     return SCN_ERR_OVERFLOW;
   }
-  const int K = tet ? f * (f + 1) * (f + 2) / 6 : f * f * f;
+  int K = 0;
+  with_kernels(f, lattice, [&](auto k) { K = decltype(k)::K; });
+  // the window's extent is f on every axis, except 1 along z on a 2D lattice
   int64_t go4[4] = {grid[0], 0, 0, 0};
-  for (int a = 1; a < 4; ++a) go4[a] = grid[a] >= f ? (grid[a] - f) / s + 1 : 0;
+  for (int a = 1; a < 4; ++a) {
+    const int fa = (a == 3 && planar) ? 1 : f;
+    go4[a] = grid[a] >= fa ? (grid[a] - fa) / s + 1 : 0;
+  }
   // bitmap words of each grid; bound them (2^26 words = 2^31 sites each)
   const int64_t rw_in = ceil_div(grid[1], 32), rw_out = ceil_div(std::max<int64_t>(go4[1], 1), 32);
   const double nwi_d = (double)grid[0] * grid[3] * grid[2] * rw_in;
@@ -542,9 +570,9 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   }
   const int64_t nw_in = (int64_t)nwi_d, nw_out = (int64_t)nwo_d;
   GridDev gi{(int32_t)grid[0], (int32_t)grid[1], (int32_t)grid[2], (int32_t)grid[3],
-             (int32_t)rw_in, tet ? 1 : 0};
+             (int32_t)rw_in, simplex ? 1 : 0};
   GridDev go{(int32_t)go4[0], (int32_t)std::max<int64_t>(go4[1], 0), (int32_t)go4[2],
-             (int32_t)go4[3], (int32_t)rw_out, tet ? 1 : 0};
+             (int32_t)go4[3], (int32_t)rw_out, simplex ? 1 : 0};
 
   Temps tmp(st);
   scn_status rc;

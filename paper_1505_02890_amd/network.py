@@ -16,6 +16,14 @@ marked with a triangle in the experiment's table): a C2 filter then covers 4
 sites, an MP3/2 region 10, and the grid of size m is the tetrahedron
 x + y + z < m in skewed coordinates; the sizes above are unchanged.
 
+The 2D networks of the square-versus-triangular comparison (section 2,
+SquareNet and TriangLeNet) have pairs of C2 layers between the poolings,
+
+    32C2 - 32C2 - MP3/2 - 64C2 - 64C2 - MP3/2 - ... - 192C2 - 192C2 - output,
+
+i.e. five levels of two convolutions each; they run on the square and the
+triangular lattice (grids with one z plane), with input size 189.
+
 Every step runs in the library's kernels (rulebook build, contraction,
 pooling); this module only sequences the calls and keeps the layer state.
 """
@@ -30,18 +38,23 @@ import torch
 from . import _lib as scn
 
 
-def input_size(levels: int) -> int:
-    """Grid size that `levels` x (C2, MP3/2) followed by one C2 reduce to 1."""
-    m = 2  # the last C2 maps 2 -> 1
+def input_size(levels: int, convs: int = 1) -> int:
+    """Grid size that `levels` x (convs x C2, MP3/2) followed by convs x C2
+    reduce to 1."""
+    m = 1 + convs  # each C2 adds one
     for _ in range(levels):
         m = 2 * m + 1  # MP3/2: (m_in - 3) / 2 + 1 = m
-        m += 1         # C2 before it
+        m += convs     # the C2 layers before it
     return m
 
 
+PLANAR = ("square", "triangular")
+
+
 def window_size(f: int, lattice: str = "cubic") -> int:
-    """Sites under a filter of size f: f^3, or C(f+2, 3) on the tetrahedral lattice."""
-    return f ** 3 if lattice == "cubic" else math.comb(f + 2, 3)
+    """Sites under a filter of size f on each lattice of Figure 2."""
+    return {"cubic": f ** 3, "tetrahedral": math.comb(f + 2, 3), "square": f * f,
+            "triangular": math.comb(f + 1, 2)}[lattice]
 
 
 @dataclass
@@ -54,33 +67,35 @@ class Layer:
     relu: bool = False
 
 
-def architecture(levels: int, classes: int = 50, width: int = 32, cin: int = 1) -> List[Layer]:
-    """nC2-MP3/2 per level (n = width, 2*width, ...), a last C2, then the 1x1x1
-    class layer."""
+def architecture(levels: int, classes: int = 50, width: int = 32, cin: int = 1,
+                 convs: int = 1) -> List[Layer]:
+    """convs x nC2 then MP3/2 per level (n = width, 2*width, ...), convs last
+    C2 layers, then the 1x1 class layer."""
     layers: List[Layer] = []
     c = cin
-    for i in range(levels):
-        layers.append(Layer("conv", 2, 1, c, width * (i + 1), True))
-        layers.append(Layer("pool", 3, 2))
-        c = width * (i + 1)
-    layers.append(Layer("conv", 2, 1, c, width * (levels + 1), True))
-    layers.append(Layer("conv", 1, 1, width * (levels + 1), classes, False))
+    for i in range(levels + 1):
+        for _ in range(convs):
+            layers.append(Layer("conv", 2, 1, c, width * (i + 1), True))
+            c = width * (i + 1)
+        if i < levels:
+            layers.append(Layer("pool", 3, 2))
+    layers.append(Layer("conv", 1, 1, c, classes, False))
     return layers
 
 
 class SparseNet:
-    """Random-initialised weights (He scaling) for `architecture(levels)` on
-    the cubic or tetrahedral lattice; the input ground state is 0 (an empty
-    site holds no signal)."""
+    """Random-initialised weights (He scaling) for `architecture(...)` on one
+    of the lattices of Figure 2; the input ground state is 0 (an empty site
+    holds no signal)."""
 
     def __init__(self, levels: int, classes: int = 50, width: int = 32, seed: int = 0,
-                 device: str = "cuda", lattice: str = "cubic"):
-        if lattice not in ("cubic", "tetrahedral"):
+                 device: str = "cuda", lattice: str = "cubic", convs: int = 1, cin: int = 1):
+        if lattice not in ("cubic", "tetrahedral") + PLANAR:
             raise ValueError(f"unknown lattice {lattice!r}")
         self.levels = levels
         self.lattice = lattice
-        self.layers = architecture(levels, classes, width)
-        self.m = input_size(levels)
+        self.layers = architecture(levels, classes, width, cin, convs)
+        self.m = input_size(levels, convs)
         g = torch.Generator().manual_seed(seed)
         self.params = []
         for L in self.layers:
@@ -94,9 +109,10 @@ class SparseNet:
         self.device = device
 
     def forward(self, coords: torch.Tensor, x: torch.Tensor, batch: int):
-        """coords int32 [n][4] (b, x, y, z) on the device, x [n][1].  Returns
-        (scores [a][classes], out_coords [a][4], per-layer records)."""
-        grid = (batch, self.m, self.m, self.m)
+        """coords int32 [n][4] (b, x, y, z) on the device (z = 0 on a 2D
+        lattice), x [n][cin].  Returns (scores [a][classes], out_coords [a][4],
+        per-layer records)."""
+        grid = (batch, self.m, self.m, 1 if self.lattice in PLANAR else self.m)
         g = torch.zeros(x.shape[1], dtype=torch.float32, device=self.device)
         rec = []
         for L, p in zip(self.layers, self.params):

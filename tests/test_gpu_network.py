@@ -14,7 +14,7 @@ import pytest
 sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
 import oracle  # noqa: E402
-from gen import shell_sites, stream_rng, tetra_shell_sites  # noqa: E402
+from gen import image_patch_sites, shell_sites, stream_rng, tetra_shell_sites  # noqa: E402
 from helpers import dev, host  # noqa: E402
 
 torch = pytest.importorskip("torch")
@@ -72,6 +72,40 @@ def test_network_matches_oracle_chain(scn, lattice, levels, width, scale):
     assert np.array_equal(host(oc), c)
     # one final site per sample whose shell survives the network
     assert len(c) == batch and np.array_equal(c[:, 0], np.arange(batch))
+    got = host(out).astype(np.float64)
+    scale_ref = np.sqrt(np.mean(xr ** 2)) + 1e-30
+    err = np.abs(got - xr)
+    assert np.all(err <= 1e-5 + 1e-4 * np.maximum(np.abs(xr), scale_ref)), err.max()
+
+
+@pytest.mark.parametrize("lattice,levels,patch", [("square", 1, 5), ("triangular", 1, 4),
+                                                  ("square", 2, 9), ("triangular", 2, 8)])
+def test_planar_network_matches_oracle_chain(scn, lattice, levels, patch):
+    """The 2D SquareNet / TriangLeNet shape (two C2 per level) on an image
+    patch with three channels, against the chain of oracle layers."""
+    from paper_1505_02890_amd.network import SparseNet, input_size
+
+    batch = 2
+    m = input_size(levels, convs=2)
+    cell = image_patch_sites(lattice, m, patch, patch)
+    coords = np.ascontiguousarray(np.concatenate(
+        [np.concatenate([np.full((len(cell), 1), b), cell], axis=1) for b in range(batch)]
+    ).astype(np.int32))
+    x = stream_rng(77, levels).standard_normal((len(coords), 3)).astype(np.float32)
+    net = SparseNet(levels, classes=4, width=4, seed=levels, lattice=lattice, convs=2, cin=3)
+    out, oc, rec = net.forward(dev(coords, torch.int32), dev(x), batch)
+    c, grid, xr = coords, (batch, m, m, 1), x.astype(np.float64)
+    g = np.zeros(3)
+    for L, p in zip(net.layers, net.params):
+        o = oracle.Rulebook(c, grid, L.f, L.s, lattice=lattice)
+        if L.kind == "conv":
+            W, b = (host(t).astype(np.float64) for t in p)
+            xr, g = oracle.conv_fwd(o, xr, g, W, b, relu=L.relu)
+        else:
+            xr, g, _, _ = oracle.maxpool_fwd(o, xr, g)
+        c, grid = o.arrays().out_coords, tuple(o.out_grid)
+    assert np.array_equal(host(oc), c)
+    assert len(c) == batch
     got = host(out).astype(np.float64)
     scale_ref = np.sqrt(np.mean(xr ** 2)) + 1e-30
     err = np.abs(got - xr)
