@@ -1,0 +1,102 @@
+"""GPU parity at the library's stated limits: the largest grid the occupancy
+bitmap accepts (B * my * mz * ceil(mx / 32) = 2^26 words), one word past it,
+and the widest layers (256 channels), against the oracle."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from gen import random_sites, stream_rng  # noqa: E402
+
+from helpers import assert_close, dev, host  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def scn():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1505_02890_amd as m
+    m.lib()  # raises if the HIP library is missing
+    return m
+
+
+def _check(g, o):
+    oa = o.arrays()
+    assert (g.a_in, g.a_out, g.n_pairs, g.K) == (oa.a_in, oa.a_out, oa.n_pairs, oa.K)
+    assert tuple(g.out_grid) == tuple(oa.out_grid)
+    assert np.array_equal(g.offsets, oa.offsets)
+    oc, ir, orr = g.export()
+    assert np.array_equal(host(oc), oa.out_coords)
+    assert np.array_equal(host(ir), oa.in_rows)
+    assert np.array_equal(host(orr), oa.out_rows)
+
+
+@pytest.mark.parametrize("grid,f,s", [((1, 2048, 2048, 512), 3, 1),   # exactly 2^26 words
+                                      ((2, 1024, 2048, 512), 2, 2),   # 2^26 words over two samples
+                                      ((1, 2048, 2048, 512), 3, 2)])
+def test_largest_bitmap_grid(scn, grid, f, s):
+    B, mx, my, mz = grid
+    assert B * my * mz * ((mx + 31) // 32) == 1 << 26
+    rng = stream_rng(81, f * 10 + s)
+    coords = random_sites(rng, B, (mx, my, mz), 4000)
+    # a few sites on the far corners of the grid
+    corners = np.array([[B - 1, mx - 1, my - 1, mz - 1], [0, 0, 0, 0], [B - 1, mx - 1, 0, mz - 1]],
+                       np.int32)
+    keep = ~(coords[:, None, :] == corners[None]).all(axis=2).any(axis=1)
+    coords = np.concatenate([coords[keep], corners]).astype(np.int32)
+    g = scn.build_rulebook(dev(coords), grid, f, s)
+    o = oracle.Rulebook(coords, grid, f, s)
+    _check(g, o)
+
+
+def test_one_word_past_the_bitmap_limit(scn):
+    coords = np.array([[0, 1, 1, 1]], np.int32)
+    with pytest.raises(scn.ScnError) as e:
+        scn.build_rulebook(dev(coords), (1, 2048, 2048, 513), 3, 1)
+    assert e.value.status == "unsupported"
+
+
+def _sq(a):
+    return None if a is None else np.asarray(a, np.float64) ** 2
+
+
+@pytest.mark.parametrize("f", [2, 3])
+def test_widest_layers(scn, f):
+    """256 input and 256 output channels (the largest the library takes)."""
+    Cin = Cout = 256
+    rng = stream_rng(82, f)
+    coords = random_sites(rng, 1, (20, 18, 16), 700)
+    K = f ** 3
+    x = rng.standard_normal((len(coords), Cin)).astype(np.float32)
+    g_in = (rng.standard_normal(Cin) * 0.5).astype(np.float32)
+    W = (rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin)).astype(np.float32)
+    bias = (rng.standard_normal(Cout) * 0.1).astype(np.float32)
+    grid = (1, 20, 18, 16)
+    g = scn.build_rulebook(dev(coords), grid, f, 1)
+    o = oracle.Rulebook(coords, grid, f, 1)
+    y_ref, go_ref = oracle.conv_fwd(o, x, g_in, W, bias)
+    sig_y, sig_g = (np.sqrt(v) for v in oracle.conv_fwd(o, _sq(x), _sq(g_in), _sq(W), _sq(bias)))
+    yd, god = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias))
+    assert_close("y", host(yd), y_ref, sig_y)
+    assert_close("g_out", host(god), go_ref, sig_g)
+    dy = stream_rng(83, f).uniform(-1, 1, size=(g.a_out, Cout)).astype(np.float32)
+    ref = oracle.conv_bwd(o, x, g_in, W, bias, dy, None)
+    sig = {k: np.sqrt(v) for k, v in
+           oracle.conv_bwd(o, _sq(x), _sq(g_in), _sq(W), None, _sq(dy), None).items()}
+    out = scn.conv_bwd(g, dev(x), dev(g_in), dev(W), None, None, dev(dy), None)
+    for k in ("dx", "dW", "dbias", "dg_in"):
+        assert_close(k, host(out[k]), ref[k], sig[k])
+
+
+def test_too_wide_layers_are_refused(scn):
+    coords = random_sites(stream_rng(84, 0), 1, (8, 8, 8), 50)
+    g = scn.build_rulebook(dev(coords), (1, 8, 8, 8), 2, 1)
+    x = dev(np.ones((50, 257), np.float32))
+    with pytest.raises(scn.ScnError) as e:
+        scn.conv_fwd(g, x, dev(np.zeros(257, np.float32)), dev(np.ones((8, 257, 4), np.float32)))
+    assert e.value.status == "unsupported"
