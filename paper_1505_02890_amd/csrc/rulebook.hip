@@ -147,12 +147,18 @@ __global__ void __launch_bounds__(256) mark_inputs_kernel(const int32_t* __restr
 struct PopcountLoad {
   const uint32_t* bm;
   __device__ uint32_t operator()(int64_t i) const { return (uint32_t)__popc(bm[i]); }
+  __device__ void chunk(int64_t i, uint32_t (&v)[SCAN_ITEMS]) const {
+    load16<uint32_t>(bm + i, v);
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j) v[j] = (uint32_t)__popc(v[j]);
+  }
 };
 
 template <typename T>
 struct PlainLoad {
   const T* v;
   __device__ T operator()(int64_t i) const { return v[i]; }
+  __device__ void chunk(int64_t i, T (&x)[SCAN_ITEMS]) const { load16<T>(v + i, x); }
 };
 
 // ---- phase 3: rank -> caller row ------------------------------------------

@@ -2,6 +2,11 @@
 // Deterministic: integer sums, fixed partition.  Used by the rulebook builder
 // to number active sites (popcounts of occupancy words) and to place pair
 // lists (per-tile pair counts).
+//
+// Each thread owns 16 consecutive elements.  Whole chunks move as 16-byte
+// vectors (four per thread for 32-bit elements, eight for 64-bit ones), so a
+// wave touches each cache line with as few instructions as the data needs;
+// only the last, partial chunk goes element by element.
 #pragma once
 
 #include "scn_internal.h"
@@ -36,15 +41,56 @@ __device__ inline T block_exclusive_scan(T v, T* total) {
   return before + inc - v;
 }
 
-// Load functor: T operator()(int64_t i) const, valid for i < n.
+// Load functor: T operator()(int64_t i) const, valid for i < n, and
+// void chunk(int64_t i, T (&v)[SCAN_ITEMS]) const for a whole chunk starting at
+// a multiple of SCAN_ITEMS with i + SCAN_ITEMS <= n.
+template <typename T, class Load>
+__device__ inline void load_items(const Load& ld, int64_t base, int64_t n, T (&v)[SCAN_ITEMS]) {
+  if (base + SCAN_ITEMS <= n) {
+    ld.chunk(base, v);
+  } else {
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j) v[j] = base + j < n ? ld(base + j) : T(0);
+  }
+}
+
+// 16 consecutive elements at p (16-byte aligned) as 16-byte vectors
+template <typename T>
+__device__ inline void load16(const T* p, T (&v)[SCAN_ITEMS]) {
+  constexpr int PER = 16 / sizeof(T);
+  const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+  for (int u = 0; u < SCAN_ITEMS / PER; ++u) {
+    const uint4 x = q[u];
+    const T* e = reinterpret_cast<const T*>(&x);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) v[u * PER + j] = e[j];
+  }
+}
+
+template <typename T>
+__device__ inline void store16(T* p, const T (&v)[SCAN_ITEMS]) {
+  constexpr int PER = 16 / sizeof(T);
+  uint4* q = reinterpret_cast<uint4*>(p);
+#pragma unroll
+  for (int u = 0; u < SCAN_ITEMS / PER; ++u) {
+    uint4 x;
+    T* e = reinterpret_cast<T*>(&x);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) e[j] = v[u * PER + j];
+    q[u] = x;
+  }
+}
+
 template <typename T, class Load>
 __global__ void __launch_bounds__(SCAN_THREADS) scan_reduce_kernel(Load ld, int64_t n,
                                                                    T* block_sums) {
   const int64_t base = (int64_t)blockIdx.x * SCAN_BLOCK + (int64_t)threadIdx.x * SCAN_ITEMS;
+  T v[SCAN_ITEMS];
+  load_items<T>(ld, base, n, v);
   T s = 0;
 #pragma unroll
-  for (int j = 0; j < SCAN_ITEMS; ++j)
-    if (base + j < n) s += ld(base + j);
+  for (int j = 0; j < SCAN_ITEMS; ++j) s += v[j];
   T tot;
   block_exclusive_scan<T>(s, &tot);
   if (threadIdx.x == 0) block_sums[blockIdx.x] = tot;
@@ -70,25 +116,32 @@ __global__ void __launch_bounds__(SCAN_THREADS) scan_down_kernel(Load ld, int64_
                                                                  const T* block_off, T* out) {
   const int64_t base = (int64_t)blockIdx.x * SCAN_BLOCK + (int64_t)threadIdx.x * SCAN_ITEMS;
   T v[SCAN_ITEMS];
+  load_items<T>(ld, base, n, v);
   T s = 0;
 #pragma unroll
-  for (int j = 0; j < SCAN_ITEMS; ++j) {
-    v[j] = base + j < n ? ld(base + j) : T(0);
-    s += v[j];
-  }
+  for (int j = 0; j < SCAN_ITEMS; ++j) s += v[j];
   T tot;
   T ex = block_exclusive_scan<T>(s, &tot) + block_off[blockIdx.x];
+  T o[SCAN_ITEMS];
 #pragma unroll
   for (int j = 0; j < SCAN_ITEMS; ++j) {
-    if (base + j < n) out[base + j] = ex;
+    o[j] = ex;
     ex += v[j];
+  }
+  if (base + SCAN_ITEMS <= n) {
+    store16<T>(out + base, o);
+  } else {
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j)
+      if (base + j < n) out[base + j] = o[j];
   }
 }
 
 inline int64_t scan_blocks(int64_t n) { return n > 0 ? ceil_div(n, SCAN_BLOCK) : 1; }
 
 // out[i] = sum_{j<i} ld(j) for i < n; *total = sum of all (device).  tmp holds
-// scan_blocks(n) elements of T.
+// scan_blocks(n) elements of T.  out (and the loader's array) must be 16-byte
+// aligned.
 template <typename T, class Load>
 scn_status exclusive_scan(Load ld, int64_t n, T* out, T* total, T* tmp, hipStream_t s) {
   const int64_t nb = scan_blocks(n);
