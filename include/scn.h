@@ -151,6 +151,23 @@ scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const in
                                       int32_t filter, int32_t stride, int32_t lattice,
                                       hipStream_t stream, scn_rulebook** out);
 
+/*
+ * The rulebook of the layer that follows prev (section 1.3: the active output
+ * sites of one layer are the active input sites of the next).  Its input
+ * sites are prev's active output sites, with their rows in prev's output
+ * order, on prev's output grid and lattice; filter and stride as in
+ * scn_rulebook_build.  The result equals scn_rulebook_build (or
+ * scn_rulebook_build_lattice) called with scn_rulebook_out_coords(prev),
+ * prev's a_out and out_grid, but reuses prev's output rank bitmap (every
+ * rulebook keeps it: 8 bytes per 32 sites of its output grid) instead of
+ * marking and ranking the sites again.  prev is only read, and may be freed
+ * once this call returns.  Errors: SCN_ERR_INVALID (NULL, or prev's output
+ * grid is empty), and as scn_rulebook_build.  The call synchronises stream
+ * twice.
+ */
+scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int32_t stride,
+                                   hipStream_t stream, scn_rulebook** out);
+
 /* Sizes and grids of a rulebook (host struct).  SCN_ERR_INVALID on null. */
 scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info);
 

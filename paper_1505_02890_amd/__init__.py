@@ -17,5 +17,6 @@ from ._lib import (  # noqa: F401
     lib,
     maxpool_bwd,
     maxpool_fwd,
+    next_rulebook,
     version,
 )

@@ -26,7 +26,8 @@ STATUS = {0: "ok", 1: "invalid", 2: "range", 3: "duplicate", 4: "overflow",
           5: "unsupported", 6: "workspace", 7: "hip", 8: "nomem"}
 
 EXPORTED = (
-    "scn_rulebook_build", "scn_rulebook_build_lattice", "scn_rulebook_get_info", "scn_rulebook_out_coords",
+    "scn_rulebook_build", "scn_rulebook_build_lattice", "scn_rulebook_build_next",
+    "scn_rulebook_get_info", "scn_rulebook_out_coords",
     "scn_rulebook_in_rows", "scn_rulebook_out_rows", "scn_rulebook_offsets",
     "scn_rulebook_export", "scn_rulebook_free", "scn_conv_fwd",
     "scn_conv_bwd_workspace_bytes", "scn_conv_bwd", "scn_maxpool_fwd",
@@ -69,6 +70,7 @@ def lib() -> ctypes.CDLL:
     sig = {
         "scn_rulebook_build": (st, [P, i64, P, i32, i32, P, ctypes.POINTER(P)]),
         "scn_rulebook_build_lattice": (st, [P, i64, P, i32, i32, i32, P, ctypes.POINTER(P)]),
+        "scn_rulebook_build_next": (st, [P, i32, i32, P, ctypes.POINTER(P)]),
         "scn_rulebook_get_info": (st, [P, ctypes.POINTER(_Info)]),
         "scn_rulebook_out_coords": (P, [P]),
         "scn_rulebook_in_rows": (P, [P]),
@@ -127,20 +129,28 @@ class Rulebook:
     "triangular".  Attributes mirror ``scn_rulebook_info``.
     """
 
-    def __init__(self, coords: torch.Tensor, grid: Sequence[int], filter: int, stride: int,
-                 lattice: str = "cubic"):
-        n = int(coords.shape[0]) if coords.dim() == 2 else -1
-        _dev_tensor(coords, torch.int32, (n, 4), "coords")
-        if lattice not in LATTICES:
-            raise ValueError(f"lattice must be one of {sorted(LATTICES)}, got {lattice!r}")
-        g = np.ascontiguousarray(np.asarray(grid, dtype=np.int64).reshape(4))
+    def __init__(self, coords: Optional[torch.Tensor], grid: Sequence[int], filter: int,
+                 stride: int, lattice: str = "cubic", prev: Optional["Rulebook"] = None):
         h = ctypes.c_void_p()
-        _check(lib().scn_rulebook_build_lattice(
-            _ptr(coords), n, g.ctypes.data_as(ctypes.c_void_p), int(filter), int(stride),
-            LATTICES[lattice], ctypes.c_void_p(_stream()), ctypes.byref(h)),
-            "scn_rulebook_build_lattice")
+        if prev is not None:
+            # the layer after prev: its sites are prev's active outputs
+            _check(lib().scn_rulebook_build_next(prev.handle, int(filter), int(stride),
+                                                 ctypes.c_void_p(_stream()), ctypes.byref(h)),
+                   "scn_rulebook_build_next")
+            device = prev.device
+        else:
+            n = int(coords.shape[0]) if coords.dim() == 2 else -1
+            _dev_tensor(coords, torch.int32, (n, 4), "coords")
+            if lattice not in LATTICES:
+                raise ValueError(f"lattice must be one of {sorted(LATTICES)}, got {lattice!r}")
+            g = np.ascontiguousarray(np.asarray(grid, dtype=np.int64).reshape(4))
+            _check(lib().scn_rulebook_build_lattice(
+                _ptr(coords), n, g.ctypes.data_as(ctypes.c_void_p), int(filter), int(stride),
+                LATTICES[lattice], ctypes.c_void_p(_stream()), ctypes.byref(h)),
+                "scn_rulebook_build_lattice")
+            device = coords.device
         self._h = h
-        self.device = coords.device
+        self.device = device
         info = _Info()
         _check(lib().scn_rulebook_get_info(self._h, ctypes.byref(info)), "scn_rulebook_get_info")
         self.a_in, self.a_out, self.n_pairs = int(info.a_in), int(info.a_out), int(info.n_pairs)
@@ -187,6 +197,12 @@ class Rulebook:
 def build_rulebook(coords: torch.Tensor, grid: Sequence[int], filter: int, stride: int,
                    lattice: str = "cubic") -> Rulebook:
     return Rulebook(coords, grid, filter, stride, lattice)
+
+
+def next_rulebook(prev: Rulebook, filter: int, stride: int) -> Rulebook:
+    """The rulebook of the layer after `prev` (its sites are prev's active
+    outputs, on prev's output grid and lattice)."""
+    return Rulebook(None, prev.out_grid, filter, stride, prev.lattice, prev=prev)
 
 
 def conv_fwd(rb: Rulebook, x: torch.Tensor, g_in: torch.Tensor, W: torch.Tensor,

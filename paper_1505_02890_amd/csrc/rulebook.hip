@@ -518,8 +518,13 @@ void with_kernels(int f, int lattice, Fn fn) {
   }
 }
 
+// Builds from the caller's sites, or (prev != null) from the active output
+// sites of prev: then coords/n/grid/lattice are prev's output layer, whose
+// rank bitmap (prev's H_out) serves as this build's H_in, so phases 1-3 are
+// skipped (the sites are valid, distinct and in key order by construction).
 scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f, int32_t s,
-                 int32_t lattice, hipStream_t st, scn_rulebook** out) {
+                 int32_t lattice, hipStream_t st, scn_rulebook** out,
+                 const scn_rulebook* prev = nullptr) {
   if (!out) {
     set_error("scn_rulebook_build: out is NULL");
     return SCN_ERR_INVALID;
@@ -582,14 +587,33 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
 
   Temps tmp(st);
   scn_status rc;
-  uint32_t *inb, *ipref, *outb, *opref, *flags;
+  uint32_t *inb, *ipref, *flags;
   uint32_t* sc32;  // scan block sums
   const int64_t nsb = std::max(scan_blocks(nw_in), scan_blocks(nw_out));
-  if ((rc = tmp.get(&inb, nw_in)) || (rc = tmp.get(&ipref, nw_in + 1)) ||
-      (rc = tmp.get(&outb, nw_out)) || (rc = tmp.get(&opref, nw_out + 1)) ||
-      (rc = tmp.get(&flags, 4)) || (rc = tmp.get(&sc32, nsb)))
+  // the output layer's rank bitmap (H_out) outlives the build: the rulebook
+  // keeps it for a following build_next
+  struct Hout {
+    uint32_t *bits = nullptr, *rank = nullptr;
+    hipStream_t s;
+    ~Hout() {
+      if (bits) dfree(bits, s);
+      if (rank) dfree(rank, s);
+    }
+  } hout;
+  hout.s = st;
+  if ((rc = dalloc((void**)&hout.bits, std::max<int64_t>(nw_out, 1) * 4, st)) ||
+      (rc = dalloc((void**)&hout.rank, (nw_out + 1) * 4, st)))
     return rc;
-  SCN_HIP(hipMemsetAsync(inb, 0, std::max<int64_t>(nw_in, 1) * 4, st));
+  uint32_t* const outb = hout.bits;
+  uint32_t* const opref = hout.rank;
+  if (prev) {
+    inb = prev->hout_bits;
+    ipref = prev->hout_rank;
+  } else {
+    if ((rc = tmp.get(&inb, nw_in)) || (rc = tmp.get(&ipref, nw_in + 1))) return rc;
+    SCN_HIP(hipMemsetAsync(inb, 0, std::max<int64_t>(nw_in, 1) * 4, st));
+  }
+  if ((rc = tmp.get(&flags, 4)) || (rc = tmp.get(&sc32, nsb))) return rc;
   SCN_HIP(hipMemsetAsync(flags, 0, 16, st));
 
   // host-pinned readback area
@@ -602,14 +626,16 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   if (!hb) SCN_HIP(hipHostMalloc((void**)&hb, sizeof(Readback), hipHostMallocDefault));
   std::memset(hb, 0, sizeof(Readback));
 
-  // phases 1-5
-  if (n > 0) {
-    hipLaunchKernelGGL(mark_inputs_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n,
-                       gi, inb, flags);
-    SCN_LAUNCH_CHECK();
+  // phases 1-5 (1-2 only for the caller's sites)
+  if (!prev) {
+    if (n > 0) {
+      hipLaunchKernelGGL(mark_inputs_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords,
+                         n, gi, inb, flags);
+      SCN_LAUNCH_CHECK();
+    }
+    if ((rc = exclusive_scan<uint32_t>(PopcountLoad{inb}, nw_in, ipref, ipref + nw_in, sc32, st)))
+      return rc;
   }
-  if ((rc = exclusive_scan<uint32_t>(PopcountLoad{inb}, nw_in, ipref, ipref + nw_in, sc32, st)))
-    return rc;
   {
     const int sm = s == 1 ? 1 : (s == 2 ? 2 : 0);
     with_kernels(f, lattice, [&](auto k) {
@@ -665,6 +691,8 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     ~Guard() {
       if (!keep && rb) {
         dfree(rb->block, s);
+        dfree(rb->hout_bits, s);
+        dfree(rb->hout_rank, s);
         delete rb;
       }
     }
@@ -691,6 +719,10 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   rb->s = s;
   rb->K = K;
   rb->lattice = lattice;
+  rb->hout_bits = hout.bits;
+  rb->hout_rank = hout.rank;
+  rb->hout_words = nw_out;
+  hout.bits = hout.rank = nullptr;  // owned by rb from here (freed with it)
   for (int a = 0; a < 4; ++a) {
     rb->gin[a] = grid[a];
     rb->gout[a] = go4[a];
@@ -784,6 +816,24 @@ scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const in
   return scn::build(coords, n, grid, filter, stride, lattice, stream, out);
 }
 
+scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int32_t stride,
+                                   hipStream_t stream, scn_rulebook** out) {
+  scn::clear_error();
+  if (!prev || !out) {
+    if (out) *out = nullptr;
+    scn::set_error("scn_rulebook_build_next: NULL argument");
+    return SCN_ERR_INVALID;
+  }
+  for (int a = 1; a < 4; ++a)
+    if (prev->gout[a] < 1) {
+      *out = nullptr;
+      scn::set_error("scn_rulebook_build_next: the previous layer's output grid is empty");
+      return SCN_ERR_INVALID;
+    }
+  return scn::build(prev->out_coords, prev->a_out, prev->gout, filter, stride, prev->lattice,
+                    stream, out, prev);
+}
+
 scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info) {
   if (!rb || !info) {
     scn::set_error("scn_rulebook_get_info: NULL argument");
@@ -831,6 +881,8 @@ scn_status scn_rulebook_export(const scn_rulebook* rb, int32_t* out_coords, int3
 void scn_rulebook_free(scn_rulebook* rb) {
   if (!rb) return;
   scn::dfree(rb->block, rb->stream);
+  scn::dfree(rb->hout_bits, rb->stream);
+  scn::dfree(rb->hout_rank, rb->stream);
   delete rb;
 }
 

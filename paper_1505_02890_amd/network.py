@@ -115,8 +115,12 @@ class SparseNet:
         grid = (batch, self.m, self.m, 1 if self.lattice in PLANAR else self.m)
         g = torch.zeros(x.shape[1], dtype=torch.float32, device=self.device)
         rec = []
+        rb = None
         for L, p in zip(self.layers, self.params):
-            rb = scn.build_rulebook(coords, grid, L.f, L.s, lattice=self.lattice)
+            # the first layer's sites are the input; each later layer's are the
+            # previous layer's active outputs (its rank bitmap is reused)
+            rb = (scn.build_rulebook(coords, grid, L.f, L.s, lattice=self.lattice) if rb is None
+                  else scn.next_rulebook(rb, L.f, L.s))
             if L.kind == "conv":
                 W, b = p
                 x, g = scn.conv_fwd(rb, x, g, W, b, relu=L.relu)
@@ -124,8 +128,7 @@ class SparseNet:
             else:
                 x, g, _ = scn.maxpool_fwd(rb, x, g)
                 rec.append(("pool", rb.a_in, rb.a_out, rb.n_pairs, x.shape[1], x.shape[1]))
-            coords, grid = rb.out_coords(), tuple(rb.out_grid)
-        return x, coords, rec
+        return x, rb.out_coords(), rec
 
 
 def macs(records) -> int:

@@ -1,0 +1,105 @@
+"""Chained rulebooks: scn_rulebook_build_next against a build from the
+previous layer's exported output sites and against the oracle, through the C
+ABI, on every lattice."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from gen import random_sites, stream_rng, tetra_random_sites, tri_random_sites  # noqa: E402
+
+from helpers import dev, host  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def scn():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1505_02890_amd as m
+    m.lib()  # raises if the HIP library is missing
+    return m
+
+
+def _arrays(g):
+    oc, ir, orr = g.export()
+    return host(oc), host(ir), host(orr)
+
+
+def _same(a, b):
+    assert (a.a_in, a.a_out, a.n_pairs, a.K, a.lattice) == (b.a_in, b.a_out, b.n_pairs, b.K, b.lattice)
+    assert tuple(a.out_grid) == tuple(b.out_grid) and a.input_sorted and b.input_sorted
+    assert np.array_equal(a.offsets, b.offsets)
+    for x, y in zip(_arrays(a), _arrays(b)):
+        assert np.array_equal(x, y)
+
+
+def _sites(lattice, rng, B, m, n):
+    if lattice == "cubic":
+        return random_sites(rng, B, (m, m, m), n), (B, m, m, m)
+    if lattice == "tetrahedral":
+        return tetra_random_sites(rng, B, m, n), (B, m, m, m)
+    if lattice == "square":
+        return random_sites(rng, B, (m, m, 1), n), (B, m, m, 1)
+    return tri_random_sites(rng, B, m, n), (B, m, m, 1)
+
+
+CHAINS = [
+    # (lattice, B, m, n, [(f, s), ...])
+    ("cubic", 2, 40, 3000, [(2, 1), (3, 2), (2, 1), (2, 2), (1, 1)]),
+    ("cubic", 1, 70, 5000, [(3, 1), (3, 3), (2, 1)]),
+    ("tetrahedral", 2, 40, 2500, [(2, 1), (3, 2), (2, 1), (3, 2)]),
+    ("square", 3, 90, 4000, [(2, 1), (2, 1), (3, 2), (2, 2)]),
+    ("triangular", 3, 90, 3000, [(2, 1), (3, 2), (2, 1), (3, 2)]),
+]
+
+
+@pytest.mark.parametrize("case", CHAINS, ids=[c[0] + str(i) for i, c in enumerate(CHAINS)])
+def test_chain_matches_rebuild_and_oracle(scn, case):
+    lattice, B, m, n, layers = case
+    coords, grid = _sites(lattice, stream_rng(91, CHAINS.index(case)), B, m, n)
+    f, s = layers[0]
+    g = scn.build_rulebook(dev(coords), grid, f, s, lattice=lattice)
+    o = oracle.Rulebook(coords, grid, f, s, lattice=lattice)
+    for f, s in layers[1:]:
+        nxt = scn.next_rulebook(g, f, s)
+        ref = scn.build_rulebook(g.out_coords(), g.out_grid, f, s, lattice=lattice)
+        _same(nxt, ref)
+        oa = o.arrays()
+        o = oracle.Rulebook(oa.out_coords, oa.out_grid, f, s, lattice=lattice)
+        ob = o.arrays()
+        oc, ir, orr = _arrays(nxt)
+        assert np.array_equal(oc, ob.out_coords) and np.array_equal(ir, ob.in_rows)
+        assert np.array_equal(orr, ob.out_rows) and np.array_equal(nxt.offsets, ob.offsets)
+        g = nxt
+
+
+def test_chain_from_empty_layer(scn):
+    g = scn.build_rulebook(dev(np.zeros((0, 4), np.int32)), (2, 9, 9, 9), 2, 1)
+    nxt = scn.next_rulebook(g, 3, 2)
+    assert nxt.a_in == 0 and nxt.a_out == 0 and nxt.n_pairs == 0
+    assert tuple(nxt.out_grid) == (2, 3, 3, 3)
+
+
+def test_chain_from_empty_grid_is_refused(scn):
+    coords = random_sites(stream_rng(92, 0), 1, (2, 9, 9), 20)
+    g = scn.build_rulebook(dev(coords), (1, 2, 9, 9), 3, 1)   # mx < f: output grid empty
+    assert g.out_grid[1] == 0
+    with pytest.raises(scn.ScnError) as e:
+        scn.next_rulebook(g, 2, 1)
+    assert e.value.status == "invalid"
+
+
+def test_chain_outlives_its_source(scn):
+    """The previous rulebook may be freed once the next one is built."""
+    coords, grid = _sites("cubic", stream_rng(93, 0), 1, 30, 1500)
+    g = scn.build_rulebook(dev(coords), grid, 2, 1)
+    ref = scn.build_rulebook(g.out_coords(), g.out_grid, 3, 2)
+    nxt = scn.next_rulebook(g, 3, 2)
+    g.close()
+    torch.cuda.synchronize()
+    _same(nxt, ref)
