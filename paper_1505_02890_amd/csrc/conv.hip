@@ -60,18 +60,32 @@ __device__ inline int64_t xcd_remap(int64_t b, int64_t n) {
 //                offset k contributes; subtracted per pair in the residual form)
 //   g_pre[co]  = B[co] + sum_k gw[k][co]
 // ---------------------------------------------------------------------------
+// One block per (k, 64 columns): thread (group g, column c) sums the input
+// channels ci = g (mod GW_GROUPS) in ascending order, then the group sums are
+// added in group order (fixed order, so the result is deterministic).
+constexpr int GW_GROUPS = 4;
 __global__ void __launch_bounds__(256) ground_w_kernel(const float* __restrict__ g_in,
                                                        const float* __restrict__ W, int K, int Cin,
                                                        int Cout, int ld, float* __restrict__ gw) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)K * ld) return;
-  const int k = (int)(i / ld), co = (int)(i - (int64_t)k * ld);
+  __shared__ float part[GW_GROUPS][64];
+  const int nb = ld / 64;  // column blocks (ld is a multiple of 64)
+  const int k = blockIdx.x / nb, c0 = (blockIdx.x - k * nb) * 64;
+  const int c = threadIdx.x & 63, grp = threadIdx.x >> 6;
+  const int co = c0 + c;
   float s = 0.f;
   if (co < Cout) {
     const float* wp = W + (int64_t)k * Cin * Cout + co;
-    for (int ci = 0; ci < Cin; ++ci) s = fmaf(g_in[ci], wp[(int64_t)ci * Cout], s);
+#pragma unroll 4
+    for (int ci = grp; ci < Cin; ci += GW_GROUPS) s = fmaf(g_in[ci], wp[(int64_t)ci * Cout], s);
   }
-  gw[i] = s;
+  part[grp][c] = s;
+  __syncthreads();
+  if (grp == 0) {
+    float t = part[0][c];
+#pragma unroll
+    for (int g = 1; g < GW_GROUPS; ++g) t += part[g][c];
+    gw[(int64_t)k * ld + co] = t;
+  }
 }
 
 __global__ void ground_pre_kernel(const float* __restrict__ gw, int ld,
@@ -1018,8 +1032,8 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
   hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)ceil_div((int64_t)rb->K * NcP * RkP, 256)),
                      dim3(256), 0, st, W, rb->K, Cin, Cout, 1, RkP, NcP, Wp);
   SCN_LAUNCH_CHECK();
-  hipLaunchKernelGGL(ground_w_kernel, dim3((unsigned)ceil_div((int64_t)rb->K * NcP, 256)),
-                     dim3(256), 0, st, g_in, W, rb->K, Cin, Cout, NcP, gw);
+  hipLaunchKernelGGL(ground_w_kernel, dim3((unsigned)(rb->K * (NcP / 64))), dim3(256), 0, st,
+                     g_in, W, rb->K, Cin, Cout, NcP, gw);
   SCN_LAUNCH_CHECK();
   hipLaunchKernelGGL(ground_pre_kernel, dim3((unsigned)ceil_div(Cout, 64)), dim3(64), 0, st, gw,
                      NcP, bias, rb->K, Cout, g_out);
