@@ -37,6 +37,10 @@
 //   8 scan of tile counts    list boundaries and per-tile pair ranges
 //   9 emit pairs             in_row / out_row (+ rank; pool maps)
 //  10 input-tile ranges      per (offset, tile of 64 input ranks)   [sync 2]
+//
+// The output layer's bitmap and its prefix (phases 4-5) stay with the
+// rulebook: they are H_out, and a build from this rulebook's output sites
+// (scn_rulebook_build_next) takes them as its H_in and skips phases 1-3.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
