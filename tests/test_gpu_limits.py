@@ -1,6 +1,7 @@
 """GPU parity at the library's stated limits: the largest grid the occupancy
 bitmap accepts (B * my * mz * ceil(mx / 32) = 2^26 words), one word past it,
-and the widest layers (256 channels), against the oracle."""
+the widest convolution layers (256 channels) and pooling at 1024+ channels,
+against the oracle."""
 from __future__ import annotations
 
 import numpy as np
@@ -100,3 +101,29 @@ def test_too_wide_layers_are_refused(scn):
     with pytest.raises(scn.ScnError) as e:
         scn.conv_fwd(g, x, dev(np.zeros(257, np.float32)), dev(np.ones((8, 257, 4), np.float32)))
     assert e.value.status == "unsupported"
+
+
+@pytest.mark.parametrize("C", [1024, 1028, 3])
+@pytest.mark.parametrize("f,s", [(2, 2), (3, 2)])
+def test_pooling_channel_extremes(scn, C, f, s):
+    """1024 channels (the widest four-channel path), 1028 (one channel per
+    thread) and 3, against the oracle."""
+    rng = stream_rng(85, C + f)
+    coords = random_sites(rng, 1, (12, 11, 10), 300)
+    x = rng.standard_normal((len(coords), C)).astype(np.float32)
+    g_in = (np.abs(rng.standard_normal(C)) * 0.5).astype(np.float32)
+    grid = (1, 12, 11, 10)
+    g = scn.build_rulebook(dev(coords), grid, f, s)
+    o = oracle.Rulebook(coords, grid, f, s)
+    y_ref, go_ref, ak_ref, _ = oracle.maxpool_fwd(o, x, g_in)
+    yd, god, am = scn.maxpool_fwd(g, dev(x), dev(g_in))
+    assert np.array_equal(host(yd), y_ref.astype(np.float32))
+    assert np.array_equal(host(am).astype(np.int32), ak_ref)
+    dy = rng.uniform(-1, 1, size=(g.a_out, C)).astype(np.float32)
+    dg = rng.uniform(-1, 1, size=C).astype(np.float32)
+    dx_ref, dgi_ref = oracle.maxpool_bwd(o, x, g_in, dy, dg)
+    dxd, dgid = scn.maxpool_bwd(g, am, dev(dy), dev(dg))
+    sig_dx = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), None)[0])
+    assert_close("dx", host(dxd), dx_ref, sig_dx)
+    sig = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), _sq(dg))[1])
+    assert_close("dg_in", host(dgid), dgi_ref, sig)
