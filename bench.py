@@ -320,6 +320,8 @@ def main():
             "fwd_ms": round(fms, 4), "bwd_ms": round(bms, 4),
             "fwd_alg_gbs": round(fwd_bytes / (fms / 1e3) / 1e9, 1),
             "bwd_alg_gbs": round(bwd_bytes / (bms / 1e3) / 1e9, 1),
+            "fwd_hbm_frac": round(fwd_bytes / (fms / 1e3) / 1e9 / HBM_PEAK_GBS, 3),
+            "bwd_hbm_frac": round(bwd_bytes / (bms / 1e3) / 1e9 / HBM_PEAK_GBS, 3),
         }
 
     pool22 = time_pool(2, 2)
@@ -357,6 +359,7 @@ def main():
             "bwd_dx_dw": round(2 * flop_pass / (med["bwd"] / 1e3) / 1e9, 1),
         },
         "rulebook_alg_gbs": round(rb_bytes / (med["rulebook"] / 1e3) / 1e9, 1),
+        "rulebook_hbm_frac": round(rb_bytes / (med["rulebook"] / 1e3) / 1e9 / HBM_PEAK_GBS, 3),
         "roofline": {
             "kernel": "gather_mfma_kernel (forward)",
             "bound": "mfma",
