@@ -274,6 +274,22 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
                            const float* dg_out, int32_t C, float* dx, float* dg_in, void* ws,
                            size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Device memory the library allocates for itself: rulebook storage and the
+ * temporaries of scn_rulebook_build* and scn_conv_fwd (workspaces of the
+ * backward passes are the caller's).  By default it comes from the device's
+ * stream-ordered pool (hipMallocAsync / hipFreeAsync).  Callers that manage
+ * device memory themselves (a framework's caching allocator) install
+ *   alloc(bytes, stream, ctx) -> 256-byte-aligned device pointer or NULL
+ *   free(ptr, stream, ctx)
+ * and the library calls them, ordered on the stream of the call that
+ * allocates or frees; a NULL from alloc is SCN_ERR_NOMEM.  NULL alloc or
+ * free restores the default.  Process-wide; it applies to calls that start
+ * after it returns.  A rulebook is freed with the allocator that built it.
+ */
+void scn_set_allocator(void* (*alloc)(size_t bytes, hipStream_t stream, void* ctx),
+                       void (*free)(void* ptr, hipStream_t stream, void* ctx), void* ctx);
+
 /* Message describing the last failing call on this thread ("" if none). */
 const char* scn_last_error(void);
 

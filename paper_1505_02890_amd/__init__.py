@@ -18,5 +18,6 @@ from ._lib import (  # noqa: F401
     maxpool_bwd,
     maxpool_fwd,
     next_rulebook,
+    set_allocator,
     version,
 )

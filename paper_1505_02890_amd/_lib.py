@@ -31,8 +31,12 @@ EXPORTED = (
     "scn_rulebook_in_rows", "scn_rulebook_out_rows", "scn_rulebook_offsets",
     "scn_rulebook_export", "scn_rulebook_free", "scn_conv_fwd",
     "scn_conv_bwd_workspace_bytes", "scn_conv_bwd", "scn_maxpool_fwd",
-    "scn_maxpool_bwd_workspace_bytes", "scn_maxpool_bwd", "scn_last_error", "scn_version",
+    "scn_maxpool_bwd_workspace_bytes", "scn_maxpool_bwd", "scn_set_allocator", "scn_last_error",
+    "scn_version",
 )
+
+_ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
+_FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p)
 
 
 class ScnError(RuntimeError):
@@ -84,6 +88,7 @@ def lib() -> ctypes.CDLL:
         "scn_maxpool_fwd": (st, [P, P, P, i32, P, P, P, P]),
         "scn_maxpool_bwd_workspace_bytes": (sz, [P, i32]),
         "scn_maxpool_bwd": (st, [P, P, P, P, i32, P, P, P, sz, P]),
+        "scn_set_allocator": (None, [_ALLOC_FN, _FREE_FN, P]),
         "scn_last_error": (ctypes.c_char_p, []),
         "scn_version": (ctypes.c_char_p, []),
     }
@@ -298,3 +303,41 @@ def maxpool_bwd(rb: Rulebook, argmax: torch.Tensor, dy: torch.Tensor,
 
 def version() -> str:
     return lib().scn_version().decode()
+
+
+# Every callback pair ever installed stays alive for the life of the process:
+# a rulebook built under a pair frees its memory through it, also after the
+# pair has been replaced.
+_hooks_kept = []
+
+
+def set_allocator(alloc=None, free=None) -> None:
+    """Route the library's own device allocations through alloc(bytes, stream)
+    -> pointer and free(pointer, stream) (``scn_set_allocator``).  ``"torch"``
+    installs PyTorch's caching allocator; no argument restores the library's
+    default pool."""
+    if alloc == "torch":
+        def alloc(nbytes, stream):
+            return torch.cuda.caching_allocator_alloc(int(nbytes), stream=int(stream))
+
+        def free(ptr, stream):
+            torch.cuda.caching_allocator_delete(int(ptr))
+    if alloc is None or free is None:
+        lib().scn_set_allocator(_ALLOC_FN(), _FREE_FN(), None)
+        return
+
+    def c_alloc(nbytes, stream, ctx):
+        try:
+            return int(alloc(nbytes, stream or 0)) or None
+        except Exception:  # the library reports SCN_ERR_NOMEM
+            return None
+
+    def c_free(ptr, stream, ctx):
+        try:
+            free(ptr, stream or 0)
+        except Exception:
+            pass
+
+    hooks = (_ALLOC_FN(c_alloc), _FREE_FN(c_free))
+    _hooks_kept.append(hooks)
+    lib().scn_set_allocator(hooks[0], hooks[1], None)

@@ -1,6 +1,7 @@
-// Error reporting, stream-ordered allocation and version string.
+// Error reporting, device allocation and version string.
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 
 #include "scn_internal.h"
 
@@ -34,9 +35,32 @@ static void keep_pool_memory() {
   done[dev] = true;
 }
 
-scn_status dalloc(void** p, size_t bytes, hipStream_t s) {
+static std::mutex g_alloc_mutex;
+static Allocator g_alloc;  // hooks set by scn_set_allocator (none: default pool)
+
+Allocator current_allocator() {
+  std::lock_guard<std::mutex> lock(g_alloc_mutex);
+  return g_alloc;
+}
+
+void set_allocator(const Allocator& a) {
+  std::lock_guard<std::mutex> lock(g_alloc_mutex);
+  g_alloc = a;
+}
+
+scn_status dalloc(void** p, size_t bytes, hipStream_t s, const Allocator& a) {
   *p = nullptr;
   if (bytes == 0) return SCN_OK;
+  if (a.alloc) {
+    *p = a.alloc(bytes, s, a.ctx);
+    if (!*p || (reinterpret_cast<uintptr_t>(*p) & 255) != 0) {
+      if (*p) a.free(*p, s, a.ctx);
+      *p = nullptr;
+      set_error("the caller's allocator gave no 256-byte-aligned block of %zu bytes", bytes);
+      return SCN_ERR_NOMEM;
+    }
+    return SCN_OK;
+  }
   keep_pool_memory();
   hipError_t e = hipMallocAsync(p, bytes, s);
   if (e != hipSuccess) {
@@ -48,12 +72,27 @@ scn_status dalloc(void** p, size_t bytes, hipStream_t s) {
   return SCN_OK;
 }
 
-void dfree(void* p, hipStream_t s) {
-  if (p) (void)hipFreeAsync(p, s);
+void dfree(void* p, hipStream_t s, const Allocator& a) {
+  if (!p) return;
+  if (a.alloc)
+    a.free(p, s, a.ctx);
+  else
+    (void)hipFreeAsync(p, s);
 }
 
 }  // namespace scn
 
 extern "C" const char* scn_last_error(void) { return scn::g_err; }
+
+extern "C" void scn_set_allocator(void* (*alloc)(size_t, hipStream_t, void*),
+                                  void (*free)(void*, hipStream_t, void*), void* ctx) {
+  scn::Allocator a;
+  if (alloc && free) {
+    a.alloc = alloc;
+    a.free = free;
+    a.ctx = ctx;
+  }
+  scn::set_allocator(a);
+}
 
 extern "C" const char* scn_version(void) { return "scn-mi355x 0.1 (gfx950)"; }

@@ -1020,14 +1020,16 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
   const int RkP = (int)ceil_div(Cin, 16) * 16, NcP = (int)ceil_div(Cout, 64) * 64;
   const size_t gw_bytes = ((size_t)rb->K * NcP * sizeof(float) + 255) & ~size_t(255);
   float* gw = nullptr;
+  const Allocator al = current_allocator();
   scn_status rc = dalloc(reinterpret_cast<void**>(&gw),
-                         gw_bytes + (size_t)rb->K * NcP * RkP * sizeof(float), st);
+                         gw_bytes + (size_t)rb->K * NcP * RkP * sizeof(float), st, al);
   if (rc) return rc;
   struct Free {
     float* p;
     hipStream_t s;
-    ~Free() { dfree(p, s); }
-  } free_gw{gw, st};
+    Allocator al;
+    ~Free() { dfree(p, s, al); }
+  } free_gw{gw, st, al};
   float* Wp = reinterpret_cast<float*>(reinterpret_cast<char*>(gw) + gw_bytes);
   hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)ceil_div((int64_t)rb->K * NcP * RkP, 256)),
                      dim3(256), 0, st, W, rb->K, Cin, Cout, 1, RkP, NcP, Wp);

@@ -457,20 +457,21 @@ inline unsigned blocks_for(int64_t n, int threads) {
 
 struct Temps {
   hipStream_t s;
+  Allocator al;
   void* p[12] = {nullptr};
   int n = 0;
-  explicit Temps(hipStream_t st) : s(st) {}
+  Temps(hipStream_t st, const Allocator& a) : s(st), al(a) {}
   template <typename T>
   scn_status get(T** out, size_t count) {
     void* q = nullptr;
-    scn_status st = dalloc(&q, std::max<size_t>(count, 1) * sizeof(T), s);
+    scn_status st = dalloc(&q, std::max<size_t>(count, 1) * sizeof(T), s, al);
     if (st != SCN_OK) return st;
     p[n++] = q;
     *out = static_cast<T*>(q);
     return SCN_OK;
   }
   ~Temps() {
-    for (int i = 0; i < n; ++i) dfree(p[i], s);
+    for (int i = 0; i < n; ++i) dfree(p[i], s, al);
   }
 };
 
@@ -589,7 +590,8 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   GridDev go{(int32_t)go4[0], (int32_t)std::max<int64_t>(go4[1], 0), (int32_t)go4[2],
              (int32_t)go4[3], (int32_t)rw_out, simplex ? 1 : 0};
 
-  Temps tmp(st);
+  const Allocator mem = current_allocator();  // every array of this build comes from it
+  Temps tmp(st, mem);
   scn_status rc;
   uint32_t *inb, *ipref, *flags;
   uint32_t* sc32;  // scan block sums
@@ -599,14 +601,16 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   struct Hout {
     uint32_t *bits = nullptr, *rank = nullptr;
     hipStream_t s;
+    Allocator al;
     ~Hout() {
-      if (bits) dfree(bits, s);
-      if (rank) dfree(rank, s);
+      if (bits) dfree(bits, s, al);
+      if (rank) dfree(rank, s, al);
     }
   } hout;
   hout.s = st;
-  if ((rc = dalloc((void**)&hout.bits, std::max<int64_t>(nw_out, 1) * 4, st)) ||
-      (rc = dalloc((void**)&hout.rank, (nw_out + 1) * 4, st)))
+  hout.al = mem;
+  if ((rc = dalloc((void**)&hout.bits, std::max<int64_t>(nw_out, 1) * 4, st, mem)) ||
+      (rc = dalloc((void**)&hout.rank, (nw_out + 1) * 4, st, mem)))
     return rc;
   uint32_t* const outb = hout.bits;
   uint32_t* const opref = hout.rank;
@@ -688,20 +692,21 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair + sz_perm) + sz_off + sz_ot +
                         sz_it + sz_nbr + sz_inv;
   scn_rulebook* rb = new scn_rulebook();
+  rb->alloc = mem;
   struct Guard {
     scn_rulebook* rb;
     hipStream_t s;
     bool keep = false;
     ~Guard() {
       if (!keep && rb) {
-        dfree(rb->block, s);
-        dfree(rb->hout_bits, s);
-        dfree(rb->hout_rank, s);
+        dfree(rb->block, s, rb->alloc);
+        dfree(rb->hout_bits, s, rb->alloc);
+        dfree(rb->hout_rank, s, rb->alloc);
         delete rb;
       }
     }
   } guard{rb, st};
-  if ((rc = dalloc(&rb->block, (size_t)total, st))) return rc;
+  if ((rc = dalloc(&rb->block, (size_t)total, st, mem))) return rc;
   char* cur = static_cast<char*>(rb->block);
   auto take = [&](int64_t bytes) {
     char* p = bytes ? cur : nullptr;
@@ -884,9 +889,9 @@ scn_status scn_rulebook_export(const scn_rulebook* rb, int32_t* out_coords, int3
 
 void scn_rulebook_free(scn_rulebook* rb) {
   if (!rb) return;
-  scn::dfree(rb->block, rb->stream);
-  scn::dfree(rb->hout_bits, rb->stream);
-  scn::dfree(rb->hout_rank, rb->stream);
+  scn::dfree(rb->block, rb->stream, rb->alloc);
+  scn::dfree(rb->hout_bits, rb->stream, rb->alloc);
+  scn::dfree(rb->hout_rank, rb->stream, rb->alloc);
   delete rb;
 }
 

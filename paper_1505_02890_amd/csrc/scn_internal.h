@@ -24,9 +24,17 @@ struct DeviceBuffer {
   void* p = nullptr;
 };
 
-// Stream-ordered allocation from the device's default memory pool.
-scn_status dalloc(void** p, size_t bytes, hipStream_t s);
-void dfree(void* p, hipStream_t s);
+// Device allocation: the caller's hooks (scn_set_allocator) or, by default,
+// stream-ordered allocation from the device's default memory pool.  A value
+// is a snapshot: memory goes back through the allocator that produced it.
+struct Allocator {
+  void* (*alloc)(size_t bytes, hipStream_t s, void* ctx) = nullptr;  // null: default pool
+  void (*free)(void* p, hipStream_t s, void* ctx) = nullptr;
+  void* ctx = nullptr;
+};
+Allocator current_allocator();
+scn_status dalloc(void** p, size_t bytes, hipStream_t s, const Allocator& a);
+void dfree(void* p, hipStream_t s, const Allocator& a);
 
 #define SCN_HIP(call)                                                                  \
   do {                                                                                 \
@@ -90,6 +98,7 @@ struct scn_rulebook {
   int inv_slots = 0;
 
   void* block = nullptr;  // single allocation holding all arrays above
+  scn::Allocator alloc;   // the allocator every array of the rulebook came from
 
   // The output layer's rank bitmap (H_out): occupancy words of the output grid
   // and their exclusive popcount prefix (hout_rank[hout_words] = a_out); the
