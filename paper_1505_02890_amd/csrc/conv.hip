@@ -954,10 +954,31 @@ __global__ void __launch_bounds__(256) dgin_kernel(const float* __restrict__ W,
   if (threadIdx.x == 0) dg_in[ci] = red[0];
 }
 
-inline int64_t dw_chunk(int64_t P) {
-  const int64_t want = ceil_div(std::max<int64_t>(P, 1), 2048);
-  return std::max<int64_t>(1024, ceil_div(want, 256) * 256);
+// Work-groups of the weight-gradient kernel that run at once on the current
+// device (per-CU occupancy times CUs), cached per device.
+int dw_slots() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev]) return cached[dev];
+  int per_cu = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &per_cu, reinterpret_cast<const void*>(dw_partial_kernel<true>), NT, 0) != hipSuccess ||
+      per_cu < 1)
+    per_cu = 1;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus < 1)
+    cus = 1;
+  (void)hipGetLastError();
+  cached[dev] = per_cu * cus;
+  return cached[dev];
 }
+
+// The (offset, chunk, column block) work items fill DW_ROUNDS whole rounds of
+// the concurrent work-groups: each offset's list is cut into at most
+// DW_ROUNDS * slots / (K * blocks) chunks, so the last round is nearly full
+// instead of holding a few stragglers that would take a round's time alone.
+constexpr int DW_ROUNDS = 4;
 
 struct BwdLayout {
   int64_t chp, maxc, nblk;
@@ -968,7 +989,10 @@ BwdLayout bwd_layout(const scn_rulebook* rb, int Cin, int Cout, uint32_t flags) 
   BwdLayout L{};
   int64_t pmax = 0;
   for (int k = 0; k < rb->K; ++k) pmax = std::max(pmax, rb->off_host[k + 1] - rb->off_host[k]);
-  L.chp = dw_chunk(rb->n_pairs);
+  const int64_t blocks = ceil_div(Cin, 64) * ceil_div(Cout, 64);
+  const int64_t target = std::max<int64_t>(1, DW_ROUNDS * (int64_t)dw_slots() / (rb->K * blocks));
+  const int64_t per = ceil_div(std::max<int64_t>(pmax, 1), target);
+  L.chp = std::max<int64_t>(DW_SC, ceil_div(per, DW_SC) * DW_SC);
   L.maxc = std::max<int64_t>(1, ceil_div(pmax, L.chp));
   L.nblk = std::max<int64_t>(1, ceil_div(rb->a_out, RB_ROWS));
   auto al = [](size_t b) { return (b + 255) & ~size_t(255); };
