@@ -8,11 +8,13 @@ per-offset pair lists) + forward + input gradient + weight/bias/ground-state
 gradients, with all inputs already resident in device memory.
 
 Printed (one JSON line): effective GFLOP/s counting active pairs only
-(3 contractions of 2*P*Cin*Cout flops per step), rulebook Msites/s, per-phase
-times, the roofline of the dominant kernel (the forward gather-MFMA
+(3 contractions of 2*P*Cin*Cout flops per step), rulebook Msites/s and its
+HBM fraction, per-phase times, the fraction of the fp32 MFMA peak of each
+contraction (the input and weight gradients also timed alone) and of the
+three together, the roofline of the dominant kernel (the forward gather-MFMA
 contraction, timed with HIP events on its stream), max-pooling phases on the
-convolution's output, and the CPU oracle timed on a bounded sample of the same
-workload.
+convolution's output, and the CPU oracle timed on a bounded sample of the
+same workload.
 
     python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--no-cpu]
 
@@ -290,9 +292,28 @@ def main():
     achieved = flop_pass / (fwd_ms / 1e3) / 1e12
     log(f"ms/step={ms_per_step:.3f} phases(ms)={ {k: round(v, 4) for k, v in med.items()} }")
 
+    # the two backward contractions timed on their own (outside the timed
+    # steps): input gradient alone, weight gradient alone; median of 10
+    r, y, g = step(None)
+
+    def time_need(need):
+        for _ in range(2):
+            scn.conv_bwd(r, x, g0, W, None, None, dy, None, need=need, ws=ws)
+        ts = []
+        for _ in range(10):
+            pe = [ev(), ev()]
+            pe[0].record(stream)
+            scn.conv_bwd(r, x, g0, W, None, None, dy, None, need=need, ws=ws)
+            pe[1].record(stream)
+            torch.cuda.synchronize()
+            ts.append(pe[0].elapsed_time(pe[1]))
+        return statistics.median(ts)
+
+    dx_ms, dw_ms = time_need(("dx",)), time_need(("dW",))
+    gemm_ms = fwd_ms + dx_ms + dw_ms
+
     # max-pooling on the convolution output: 2x2x2 stride 2 (windows partition
     # the inputs) and 3x3x3 stride 2 (overlapping windows), median of 5 runs
-    r, y, g = step(None)
     C = Cout
 
     def time_pool(f, s):
@@ -357,6 +378,16 @@ def main():
         "phase_gflops": {
             "fwd": round(flop_pass / (med["fwd"] / 1e3) / 1e9, 1),
             "bwd_dx_dw": round(2 * flop_pass / (med["bwd"] / 1e3) / 1e9, 1),
+            "dx_alone": round(flop_pass / (dx_ms / 1e3) / 1e9, 1),
+            "dw_alone": round(flop_pass / (dw_ms / 1e3) / 1e9, 1),
+        },
+        # fraction of the fp32 MFMA peak per contraction, and over the three
+        # together (the GEMM phase of the step)
+        "mfma_frac": {
+            "fwd": round(flop_pass / (fwd_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
+            "dx": round(flop_pass / (dx_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
+            "dw": round(flop_pass / (dw_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
+            "gemm_phase": round(3 * flop_pass / (gemm_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
         },
         "rulebook_alg_gbs": round(rb_bytes / (med["rulebook"] / 1e3) / 1e9, 1),
         "rulebook_hbm_frac": round(rb_bytes / (med["rulebook"] / 1e3) / 1e9 / HBM_PEAK_GBS, 3),
