@@ -310,7 +310,9 @@ def main():
         return statistics.median(ts)
 
     dx_ms, dw_ms = time_need(("dx",)), time_need(("dW",))
-    gemm_ms = fwd_ms + dx_ms + dw_ms
+    # the GEMM phase of a step: its forward and its backward call (one call
+    # computes dx, dW, dbias and dg_in; the column sums of dy are counted once)
+    gemm_ms = med["fwd"] + med["bwd"]
 
     # max-pooling on the convolution output: 2x2x2 stride 2 (windows partition
     # the inputs) and 3x3x3 stride 2 (overlapping windows), median of 5 runs
@@ -381,8 +383,8 @@ def main():
             "dx_alone": round(flop_pass / (dx_ms / 1e3) / 1e9, 1),
             "dw_alone": round(flop_pass / (dw_ms / 1e3) / 1e9, 1),
         },
-        # fraction of the fp32 MFMA peak per contraction, and over the three
-        # together (the GEMM phase of the step)
+        # fraction of the fp32 MFMA peak per contraction (the two backward
+        # ones timed alone), and over the step's forward and backward calls
         "mfma_frac": {
             "fwd": round(flop_pass / (fwd_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
             "dx": round(flop_pass / (dx_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
