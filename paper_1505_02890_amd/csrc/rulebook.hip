@@ -353,7 +353,7 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
     int64_t nt, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
     GridDev gi, const int32_t* __restrict__ perm, const uint64_t* __restrict__ pos,
     int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows, int32_t* __restrict__ in_rank,
-    int32_t* __restrict__ nbr, int32_t* __restrict__ inv, int inv_slots) {
+    int32_t* __restrict__ nbr) {
   using W = Win<F, LAT>;
   constexpr int K = W::K;
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -400,15 +400,68 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
       in_rows[p] = row;
       out_rows[p] = (int32_t)o;
       if (in_rank) in_rank[p] = (int32_t)rank[k];
-      if (nbr) {
-        // input -> its window(s): one slot, or (overlapping windows, f > s,
-        // at most two per axis) the slot picked by which of the two it is
-        const int kx = ox[k], ky = oy[k], kz = oz[k];
-        const int slot = inv_slots == 1 ? 0 : (kx >= s) | ((ky >= s) << 1) | ((kz >= s) << 2);
-        inv[(int64_t)row * inv_slots + slot] = (int32_t)(o * K + k);
-      }
     }
     if (nbr && live) nbr[o * K + k] = row;
+  }
+}
+
+// ---- phase 9b (pooling, stride >= 2): the windows of each input ----------
+// One thread per input row r (the caller's order).  Along each axis an input
+// at x lies in the window starting at s*floor(x/s) (offset x mod s < s) and,
+// when f > s, possibly in the one before it (offset x mod s + s); slot bit a
+// says which.  inv[r*slots + slot] = o*K + k for window o at offset k, or -1.
+// Every window that holds an active input inside the output grid is active,
+// so its row is its rank in the output bitmap.  The row of 4 or 32 bytes is
+// written at once instead of scattered from the pair emission.
+template <int F, int LAT>
+__device__ inline int window_index(int kx, int ky, int kz) {
+  using W = Win<F, LAT>;
+  int k = 0;
+  for (int z = 0; z < kz; ++z)
+    for (int y = 0; y < F; ++y) k += W::row_len(y, z);
+  for (int y = 0; y < ky; ++y) k += W::row_len(y, kz);
+  return k + kx;
+}
+
+template <int F, int LAT, int SLOTS>
+__global__ void __launch_bounds__(256) inv_windows_kernel(
+    const int32_t* __restrict__ coords, int64_t n, int s, GridDev go,
+    const uint32_t* __restrict__ outb, const uint32_t* __restrict__ opref,
+    int32_t* __restrict__ inv) {
+  using W = Win<F, LAT>;
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= n) return;
+  const int4 c = reinterpret_cast<const int4*>(coords)[r];
+  const int p[3] = {c.y, c.z, c.w};
+  const int m[3] = {go.mx, go.my, go.mz};
+  int v[SLOTS];
+#pragma unroll
+  for (int slot = 0; slot < SLOTS; ++slot) {
+    int o[3], k[3];
+    bool ok = true;
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      const int j = (slot >> a) & 1;
+      o[a] = p[a] / s - j;
+      k[a] = p[a] - s * o[a];
+      ok = ok && o[a] >= 0 && o[a] < m[a] && k[a] < F;
+    }
+    if (W::SIMPLEX) ok = ok && k[0] + k[1] + k[2] < F && o[0] + o[1] + o[2] < go.mx;
+    if (W::PLANAR) ok = ok && k[2] == 0;
+    v[slot] = -1;
+    if (ok) {
+      const int64_t w = row_base(go, c.x, o[1], o[2]) + (o[0] >> 5);
+      const uint32_t rank =
+          opref[w] + (uint32_t)__popc(outb[w] & ((1u << (o[0] & 31)) - 1u));
+      v[slot] = (int32_t)((int64_t)rank * W::K + window_index<F, LAT>(k[0], k[1], k[2]));
+    }
+  }
+  if (SLOTS == 8) {
+    int4* d = reinterpret_cast<int4*>(inv + r * 8);
+    d[0] = make_int4(v[0], v[1], v[2], v[3]);
+    d[1] = make_int4(v[4 % SLOTS], v[5 % SLOTS], v[6 % SLOTS], v[7 % SLOTS]);
+  } else {
+    inv[r] = v[0];
   }
 }
 
@@ -417,11 +470,6 @@ __global__ void pack_totals_kernel(uint32_t* __restrict__ flags, const uint32_t*
                                    const uint32_t* __restrict__ a_out) {
   flags[1] = *a_in;
   flags[2] = *a_out;
-}
-
-__global__ void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = v;
 }
 
 // ---- phase 10: pair ranges per tile of input ranks -------------------------
@@ -502,6 +550,13 @@ struct Kernels {
   template <typename... A>
   static void emit(dim3 g, hipStream_t st, A... a) {
     hipLaunchKernelGGL((emit_pairs_kernel<F, LAT>), g, dim3(256), 0, st, a...);
+  }
+  template <typename... A>
+  static void inv_windows(int slots, dim3 g, hipStream_t st, A... a) {
+    if (slots == 8)
+      hipLaunchKernelGGL((inv_windows_kernel<F, LAT, 8>), g, dim3(256), 0, st, a...);
+    else
+      hipLaunchKernelGGL((inv_windows_kernel<F, LAT, 1>), g, dim3(256), 0, st, a...);
   }
 };
 
@@ -774,19 +829,19 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   hipLaunchKernelGGL(list_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)rb->otile,
                      nt, K, rb->off_dev);
   SCN_LAUNCH_CHECK();
-  if (pool && n > 0) {
-    hipLaunchKernelGGL(fill_i32_kernel, dim3(blocks_for(n * inv_slots, 256)), dim3(256), 0, st,
-                       rb->inv, n * inv_slots,
-                       -1);
-    SCN_LAUNCH_CHECK();
-  }
   if (a_out > 0) {
     with_kernels(f, lattice, [&](auto k) {
       k.emit(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks,
              (const int32_t*)rb->out_coords, a_out, nt, s, (const uint32_t*)inb,
              (const uint32_t*)ipref, gi, (const int32_t*)rb->perm, (const uint64_t*)rb->otile,
-             rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr, rb->inv,
-             inv_slots);
+             rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr);
+    });
+    SCN_LAUNCH_CHECK();
+  }
+  if (pool && n > 0) {
+    with_kernels(f, lattice, [&](auto k) {
+      k.inv_windows(inv_slots, dim3(blocks_for(n, 256)), st, coords, n, s, go,
+                    (const uint32_t*)outb, (const uint32_t*)opref, rb->inv);
     });
     SCN_LAUNCH_CHECK();
   }
