@@ -547,6 +547,236 @@ scn_status launch_gather(GatherArgs a, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------
+// Dense-block forward (stride-1 rulebooks)
+// ---------------------------------------------------------------------------
+// The rulebook sorts the output rows by neighbour mask; cut into blocks of 32
+// (DENSE_ROWS) the rows of a block mostly share one mask.  One wave owns a
+// block and 64 output columns, with its 32 x 64 accumulators in registers:
+// for each offset k of the union of the block's masks it gathers the block's
+// 32 input rows (a row without offset k contributes zero) and multiplies them
+// by W_k, 64 input channels at a time.  Lane (n16, q) gathers block rows n16
+// and 16 + n16; a row's input at offset k is entry popcount(mask & (2^k - 1))
+// of its output-major neighbour list.  There is no scatter: the rows of a
+// block are distinct outputs, and the epilogue writes each once.  Rows hold
+// x - g_in, so y = g_pre + sum over active offsets of (x - g_in) W_k.  The
+// next (offset, channel chunk)'s rows are loaded while the current one is
+// multiplied.
+struct DenseArgs {
+  const float* x;          // [a_in][Cin]
+  const float* g_in;       // [Cin]
+  const float* Wp;         // packed like GatherArgs::Wp (fragment order, transposed W)
+  const float* add;        // [Cout] g_pre
+  const int32_t* nb;       // rulebook fnb
+  const uint32_t* nb_off;  // rulebook fnb_off
+  const int32_t* fperm;    // rulebook fperm
+  const uint32_t* fmask;   // rulebook fmask
+  float* y;                // [a_out][Cout]
+  int64_t a_out, nblk;
+  int K, Cin, Cout, NcP, relu, dvec_ok;
+};
+
+// One block row as the lane sees it: its mask and the start of its list.
+struct DRow {
+  uint32_t m, off;
+};
+
+// The rows of one (offset, 64-channel chunk) item: lane (n16, q) holds
+// channels 64ch + 16t + 4q .. +3 of block rows n16 and 16 + n16.
+template <int TC>
+struct DRows {
+  float4 v[2][TC];
+  int r0, r1;
+};
+
+__device__ inline int dense_src(const DenseArgs& a, const DRow& w, int k) {
+  // the list entry is read unconditionally (the list has a spare entry)
+  const int r = a.nb[w.off + __popc(w.m & ((1u << k) - 1u))];
+  return (w.m >> k) & 1u ? r : -1;
+}
+
+template <int NKT, bool VEC>
+__device__ inline DRows<(NKT < 4 ? NKT : 4)> dense_rows(const DenseArgs& a, const DRow& w0,
+                                                        const DRow& w1, int k, int ch, int q) {
+  constexpr int TC = NKT < 4 ? NKT : 4;
+  DRows<TC> R;
+  R.r0 = dense_src(a, w0, k);
+  R.r1 = dense_src(a, w1, k);
+  const float* p0 = a.x + (int64_t)(R.r0 >= 0 ? R.r0 : 0) * a.Cin;
+  const float* p1 = a.x + (int64_t)(R.r1 >= 0 ? R.r1 : 0) * a.Cin;
+#pragma unroll
+  for (int t = 0; t < TC; ++t) {
+    const int c = 64 * ch + 16 * t + 4 * q;
+    if (VEC) {
+      // channels past Cin read channel 0; their weights are zero
+      const int cc = c < a.Cin ? c : 0;
+      R.v[0][t] = *reinterpret_cast<const float4*>(p0 + cc);
+      R.v[1][t] = *reinterpret_cast<const float4*>(p1 + cc);
+    } else {
+      float e0[4], e1[4];
+#pragma unroll
+      for (int z = 0; z < 4; ++z) {
+        const int cz = c + z < a.Cin ? c + z : 0;
+        e0[z] = p0[cz];
+        e1[z] = p1[cz];
+      }
+      R.v[0][t] = make_float4(e0[0], e0[1], e0[2], e0[3]);
+      R.v[1][t] = make_float4(e1[0], e1[1], e1[2], e1[3]);
+    }
+  }
+  return R;
+}
+
+template <int NKT, bool VEC>
+__global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
+  constexpr int TC = NKT < 4 ? NKT : 4;        // 16-channel steps per chunk
+  constexpr int NCH = (NKT + 3) / 4;           // 64-channel chunks
+  const int lane = threadIdx.x & 63;
+  const int64_t b = (int64_t)blockIdx.x * (NT / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (b >= a.nblk) return;
+  const int cb = blockIdx.y;
+  const int n16 = lane & 15, q = lane >> 4;
+  const int ncb = a.NcP >> 6;
+  // the lane's two rows (past a_out: no offsets)
+  const int64_t pos0 = b * DENSE_ROWS + n16, pos1 = pos0 + 16;
+  const int o0 = pos0 < a.a_out ? a.fperm[pos0] : 0, o1 = pos1 < a.a_out ? a.fperm[pos1] : 0;
+  DRow w0, w1;
+  w0.m = pos0 < a.a_out ? a.fmask[pos0] : 0u;
+  w1.m = pos1 < a.a_out ? a.fmask[pos1] : 0u;
+  w0.off = a.nb_off[o0];
+  w1.off = a.nb_off[o1];
+  // union of the block's masks (lanes n16 cover all 32 rows)
+  uint32_t u = w0.m | w1.m;
+#pragma unroll
+  for (int d = 1; d < 16; d <<= 1) u |= (uint32_t)__shfl_xor((int)u, d, 16);
+  uint32_t U = (uint32_t)__builtin_amdgcn_readfirstlane((int)u);
+  v4f acc[2][4];
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[r][g] = v4f{0.f, 0.f, 0.f, 0.f};
+  if (U) {
+    int k = __builtin_ctz(U);
+    uint32_t rest = U & (U - 1);  // offsets after k
+    int ch = 0;
+    DRows<TC> cur = dense_rows<NKT, VEC>(a, w0, w1, k, 0, q);
+    while (true) {
+      // the next item: the next chunk of k, else chunk 0 of the next offset
+      // (past the last item: the current one again, in bounds and unused)
+      const bool last_chunk = ch == NCH - 1;
+      const bool done = last_chunk && !rest;
+      const int kn = last_chunk ? (rest ? __builtin_ctz(rest) : k) : k;
+      const int chn = last_chunk ? (rest ? 0 : ch) : ch + 1;
+      DRows<TC> nxt = dense_rows<NKT, VEC>(a, w0, w1, kn, chn, q);
+      const float* wp = a.Wp + (((int64_t)k * ncb + cb) * 4) * (NKT * 256) + lane * 4;
+#pragma unroll
+      for (int t = 0; t < TC; ++t) {
+        const int tg = 4 * ch + t;  // global 16-channel step
+        if (NCH > 1 && tg >= NKT) break;
+        float4 A[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          A[g] = *reinterpret_cast<const float4*>(wp + (int64_t)g * (NKT * 256) + tg * 256);
+        const int c = 16 * tg + 4 * q;
+        float4 gq;
+        if (VEC) {
+          gq = *reinterpret_cast<const float4*>(a.g_in + (c < a.Cin ? c : 0));
+        } else {
+          gq = make_float4(a.g_in[c < a.Cin ? c : 0], a.g_in[c + 1 < a.Cin ? c + 1 : 0],
+                           a.g_in[c + 2 < a.Cin ? c + 2 : 0], a.g_in[c + 3 < a.Cin ? c + 3 : 0]);
+        }
+        const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 d0 = cur.v[0][t], d1 = cur.v[1][t];
+        d0.x -= gq.x; d0.y -= gq.y; d0.z -= gq.z; d0.w -= gq.w;
+        d1.x -= gq.x; d1.y -= gq.y; d1.z -= gq.z; d1.w -= gq.w;
+        const float4 B0 = cur.r0 >= 0 ? d0 : z, B1 = cur.r1 >= 0 ? d1 : z;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          acc[0][g] = mfma4(A[g].x, B0.x, acc[0][g]);
+          acc[1][g] = mfma4(A[g].x, B1.x, acc[1][g]);
+          acc[0][g] = mfma4(A[g].y, B0.y, acc[0][g]);
+          acc[1][g] = mfma4(A[g].y, B1.y, acc[1][g]);
+          acc[0][g] = mfma4(A[g].z, B0.z, acc[0][g]);
+          acc[1][g] = mfma4(A[g].z, B1.z, acc[1][g]);
+          acc[0][g] = mfma4(A[g].w, B0.w, acc[0][g]);
+          acc[1][g] = mfma4(A[g].w, B1.w, acc[1][g]);
+        }
+      }
+      if (done) break;
+      if (last_chunk) rest &= rest - 1;
+      k = kn;
+      ch = chn;
+      cur = nxt;
+    }
+  }
+  // epilogue: rows n16 and 16 + n16 of the block, columns 64cb + 16g + 4q .. +3
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int64_t pos = r ? pos1 : pos0;
+    if (pos >= a.a_out) continue;
+    float* dp = a.y + (int64_t)(r ? o1 : o0) * a.Cout;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int col = 64 * cb + 16 * g + 4 * q;
+      if (col >= a.Cout) continue;
+      float e[4] = {acc[r][g][0], acc[r][g][1], acc[r][g][2], acc[r][g][3]};
+#pragma unroll
+      for (int u2 = 0; u2 < 4; ++u2) {
+        if (col + u2 < a.Cout) e[u2] += a.add[col + u2];
+        if (a.relu) e[u2] = e[u2] > 0.f ? e[u2] : 0.f;
+      }
+      if (a.dvec_ok && col + 3 < a.Cout) {
+        *reinterpret_cast<float4*>(dp + col) = make_float4(e[0], e[1], e[2], e[3]);
+      } else {
+#pragma unroll
+        for (int u2 = 0; u2 < 4; ++u2)
+          if (col + u2 < a.Cout) dp[col + u2] = e[u2];
+      }
+    }
+  }
+}
+
+typedef void (*DenseFn)(DenseArgs);
+
+template <int NKT>
+DenseFn pick_dense(bool vec) {
+  return vec ? dense_fwd_kernel<NKT, true> : dense_fwd_kernel<NKT, false>;
+}
+
+DenseFn dense_fn(int nkt, bool vec) {
+  switch (nkt) {
+    case 1: return pick_dense<1>(vec);
+    case 2: return pick_dense<2>(vec);
+    case 3: return pick_dense<3>(vec);
+    case 4: return pick_dense<4>(vec);
+    case 5: return pick_dense<5>(vec);
+    case 6: return pick_dense<6>(vec);
+    case 7: return pick_dense<7>(vec);
+    case 8: return pick_dense<8>(vec);
+    case 9: return pick_dense<9>(vec);
+    case 10: return pick_dense<10>(vec);
+    case 11: return pick_dense<11>(vec);
+    case 12: return pick_dense<12>(vec);
+    case 13: return pick_dense<13>(vec);
+    case 14: return pick_dense<14>(vec);
+    case 15: return pick_dense<15>(vec);
+    default: return pick_dense<16>(vec);
+  }
+}
+
+scn_status launch_dense(DenseArgs a, hipStream_t st) {
+  if (a.a_out <= 0 || a.nblk <= 0) return SCN_OK;
+  const bool vec = ((a.Cin & 3) == 0) && ((reinterpret_cast<uintptr_t>(a.x) & 15) == 0) &&
+                   ((reinterpret_cast<uintptr_t>(a.g_in) & 15) == 0);
+  a.dvec_ok = ((a.Cout & 3) == 0) && ((reinterpret_cast<uintptr_t>(a.y) & 15) == 0);
+  const int nkt = (int)ceil_div(a.Cin, 16);
+  const int64_t nwg = ceil_div(a.nblk, NT / 64);
+  hipLaunchKernelGGL(dense_fn(nkt, vec), dim3((unsigned)nwg, (unsigned)(a.NcP / 64)), dim3(NT), 0,
+                     st, a);
+  SCN_LAUNCH_CHECK();
+  return SCN_OK;
+}
+
+// ---------------------------------------------------------------------------
 // Backward helpers
 // ---------------------------------------------------------------------------
 constexpr int RB_ROWS = 1024;  // rows per column-sum block
@@ -1064,6 +1294,33 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
   hipLaunchKernelGGL(ground_pre_kernel, dim3((unsigned)ceil_div(Cout, 64)), dim3(64), 0, st, gw,
                      NcP, bias, rb->K, Cout, g_out);
   SCN_LAUNCH_CHECK();
+  if (rb->fnb) {
+    DenseArgs d{};
+    d.x = x;
+    d.g_in = g_in;
+    d.Wp = Wp;
+    d.add = g_out;  // holds g_pre until the ReLU below
+    d.nb = rb->fnb;
+    d.nb_off = rb->fnb_off;
+    d.fperm = rb->fperm;
+    d.fmask = rb->fmask;
+    d.y = y;
+    d.a_out = rb->a_out;
+    d.nblk = rb->n_fblocks;
+    d.K = rb->K;
+    d.Cin = Cin;
+    d.Cout = Cout;
+    d.NcP = NcP;
+    d.relu = relu;
+    rc = launch_dense(d, st);
+    if (rc) return rc;
+    if (relu) {
+      hipLaunchKernelGGL(relu_vec_kernel, dim3((unsigned)ceil_div(Cout, 256)), dim3(256), 0, st,
+                         g_out, Cout);
+      SCN_LAUNCH_CHECK();
+    }
+    return SCN_OK;
+  }
   GatherArgs a{};
   a.src = x;
   a.gidx = rb->in_rows;

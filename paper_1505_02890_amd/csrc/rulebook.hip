@@ -42,6 +42,7 @@
 // rulebook: they are H_out, and a build from this rulebook's output sites
 // (scn_rulebook_build_next) takes them as its H_in and skips phases 1-3.
 #include <hip/hip_runtime.h>
+#include <hipcub/device/device_radix_sort.hpp>
 
 #include <algorithm>
 #include <cstring>
@@ -353,7 +354,7 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
     int64_t nt, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
     GridDev gi, const int32_t* __restrict__ perm, const uint64_t* __restrict__ pos,
     int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows, int32_t* __restrict__ in_rank,
-    int32_t* __restrict__ nbr) {
+    int32_t* __restrict__ nbr, const uint32_t* __restrict__ fnb_off, int32_t* __restrict__ fnb) {
   using W = Win<F, LAT>;
   constexpr int K = W::K;
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -389,6 +390,8 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
     const uint32_t pw = bit ? ipref[w] : 0u, bw = bit ? inb[w] : 0u;
     rank[k] = pw + (uint32_t)__popc(bw & ((1u << (xi & 31)) - 1u));
   }
+  // output-major neighbour list of the dense forward view
+  int32_t* nb = fnb && live ? fnb + fnb_off[o] : nullptr;
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     const bool bit = (m >> k) & 1u;
@@ -400,6 +403,7 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
       in_rows[p] = row;
       out_rows[p] = (int32_t)o;
       if (in_rank) in_rank[p] = (int32_t)rank[k];
+      if (nb) *nb++ = row;
     }
     if (nbr && live) nbr[o * K + k] = row;
   }
@@ -465,6 +469,12 @@ __global__ void __launch_bounds__(256) inv_windows_kernel(
   }
 }
 
+// ---- phase 9c (stride 1): row numbers for the mask sort -------------------
+__global__ void iota_kernel(int32_t* __restrict__ v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) v[i] = (int32_t)i;
+}
+
 // flags[1] = number of active inputs, flags[2] = number of active outputs
 __global__ void pack_totals_kernel(uint32_t* __restrict__ flags, const uint32_t* __restrict__ a_in,
                                    const uint32_t* __restrict__ a_out) {
@@ -506,7 +516,7 @@ inline unsigned blocks_for(int64_t n, int threads) {
 struct Temps {
   hipStream_t s;
   Allocator al;
-  void* p[12] = {nullptr};
+  void* p[16] = {nullptr};
   int n = 0;
   Temps(hipStream_t st, const Allocator& a) : s(st), al(a) {}
   template <typename T>
@@ -744,8 +754,14 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
                 sz_off = al((K + 1) * 8), sz_ot = al((K * nt + 1) * 8),
                 sz_it = al((K * nit + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
                 sz_inv = pool ? al(n * 4 * inv_slots) : 0;
+  // dense forward table for stride-1 rulebooks (see scn_rulebook)
+  const bool dense = s == 1 && a_out > 0;
+  const int64_t nfb = dense ? ceil_div(a_out, DENSE_ROWS) : 0;
+  const int64_t sz_fnb = al((pmax + 1) * 4), sz_fnboff = al((a_out + 1) * 4),
+                sz_fperm = al(a_out * 4), sz_fmask = al(a_out * 4);
   const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair + sz_perm) + sz_off + sz_ot +
-                        sz_it + sz_nbr + sz_inv;
+                        sz_it + sz_nbr + sz_inv +
+                        (dense ? sz_fnb + sz_fnboff + sz_fperm + sz_fmask : 0);
   scn_rulebook* rb = new scn_rulebook();
   rb->alloc = mem;
   struct Guard {
@@ -779,6 +795,11 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   rb->nbr = pool ? (int32_t*)take(sz_nbr) : nullptr;
   rb->inv = pool ? (int32_t*)take(sz_inv) : nullptr;
   rb->inv_slots = inv_slots;
+  rb->n_fblocks = nfb;
+  rb->fnb = dense ? (int32_t*)take(sz_fnb) : nullptr;
+  rb->fnb_off = dense ? (uint32_t*)take(sz_fnboff) : nullptr;
+  rb->fperm = dense ? (int32_t*)take(sz_fperm) : nullptr;
+  rb->fmask = dense ? (uint32_t*)take(sz_fmask) : nullptr;
   rb->f = f;
   rb->s = s;
   rb->K = K;
@@ -829,14 +850,36 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   hipLaunchKernelGGL(list_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)rb->otile,
                      nt, K, rb->off_dev);
   SCN_LAUNCH_CHECK();
+  if (dense) {
+    // start of each output's neighbour list: exclusive sum of mask popcounts
+    uint32_t* sc_nb = nullptr;
+    if ((rc = tmp.get(&sc_nb, scan_blocks(a_out))) ||
+        (rc = exclusive_scan<uint32_t>(PopcountLoad{masks}, a_out, rb->fnb_off,
+                                       rb->fnb_off + a_out, sc_nb, st)))
+      return rc;
+  }
   if (a_out > 0) {
     with_kernels(f, lattice, [&](auto k) {
       k.emit(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks,
              (const int32_t*)rb->out_coords, a_out, nt, s, (const uint32_t*)inb,
              (const uint32_t*)ipref, gi, (const int32_t*)rb->perm, (const uint64_t*)rb->otile,
-             rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr);
+             rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr,
+             (const uint32_t*)rb->fnb_off, rb->fnb);
     });
     SCN_LAUNCH_CHECK();
+  }
+  if (dense) {
+    // the output rows sorted by neighbour mask (a stable radix sort)
+    int32_t* iota = nullptr;
+    char* sort_tmp = nullptr;
+    size_t sort_bytes = 0;
+    SCN_HIP(hipcub::DeviceRadixSort::SortPairs(nullptr, sort_bytes, masks, rb->fmask, iota,
+                                               rb->fperm, (int)a_out, 0, K, st));
+    if ((rc = tmp.get(&iota, a_out)) || (rc = tmp.get(&sort_tmp, sort_bytes))) return rc;
+    hipLaunchKernelGGL(iota_kernel, dim3(blocks_for(a_out, 256)), dim3(256), 0, st, iota, a_out);
+    SCN_LAUNCH_CHECK();
+    SCN_HIP(hipcub::DeviceRadixSort::SortPairs(sort_tmp, sort_bytes, masks, rb->fmask, iota,
+                                               rb->fperm, (int)a_out, 0, K, st));
   }
   if (pool && n > 0) {
     with_kernels(f, lattice, [&](auto k) {

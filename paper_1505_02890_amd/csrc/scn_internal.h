@@ -16,6 +16,7 @@ namespace scn {
 // output rows) and per (offset, tile of TILE input ranks).
 constexpr int TILE = 64;
 constexpr int MAX_K = 27;  // f <= 3 (the tetrahedral lattice needs at most 10)
+constexpr int DENSE_ROWS = 32;  // output rows per block of the dense forward table
 
 void set_error(const char* fmt, ...);
 void clear_error();
@@ -96,6 +97,20 @@ struct scn_rulebook {
   int32_t* nbr = nullptr;
   int32_t* inv = nullptr;
   int inv_slots = 0;
+
+  // Dense forward view (stride-1 rulebooks with outputs).  fnb holds, for
+  // each output row o in key order, the caller rows of its active inputs in
+  // ascending offset order, starting at fnb_off[o] (fnb_off[a_out] = P; fnb
+  // has one spare entry).  fperm lists the output rows sorted by neighbour
+  // mask (bit k: the input at offset k is active), a stable sort, so rows with
+  // equal masks stay in key order; fmask[pos] is the mask of row fperm[pos].
+  // The forward cuts the sorted order into blocks of DENSE_ROWS rows, whose
+  // masks mostly agree.
+  int64_t n_fblocks = 0;
+  int32_t* fnb = nullptr;
+  uint32_t* fnb_off = nullptr;
+  int32_t* fperm = nullptr;
+  uint32_t* fmask = nullptr;
 
   void* block = nullptr;  // single allocation holding all arrays above
   scn::Allocator alloc;   // the allocator every array of the rulebook came from
