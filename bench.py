@@ -11,8 +11,9 @@ Printed (one JSON line): effective GFLOP/s counting active pairs only
 (3 contractions of 2*P*Cin*Cout flops per step), rulebook Msites/s and its
 HBM fraction, per-phase times, the fraction of the fp32 MFMA peak of each
 contraction (the input and weight gradients also timed alone) and of the
-three together, the roofline of the dominant kernel (the forward gather-MFMA
-contraction, timed with HIP events on its stream), max-pooling phases on the
+step's forward and backward together, the roofline of the dominant kernel
+(the forward dense-block contraction, timed with HIP events on its stream),
+max-pooling phases on the
 convolution's output, and the CPU oracle timed on a bounded sample of the
 same workload.
 
@@ -70,7 +71,7 @@ def measured_traffic():
     same counter's reading for a device copy of known size), or None when the
     kernel source has changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "gather_fwd_1M_traffic.txt")
+    path = os.path.join(ROOT, "profiles", "dense_fwd_1M_traffic.txt")
     src = os.path.join(ROOT, "paper_1505_02890_amd", "csrc", "conv.hip")
     if not os.path.exists(path):
         return None
@@ -287,7 +288,8 @@ def main():
     flop_pass = 2.0 * P * Cin * Cout
     value = 3 * flop_pass / (ms_per_step / 1e3) / 1e9
 
-    # dominant kernel: the forward contraction (gather -> MFMA -> LDS scatter)
+    # dominant kernel: the forward contraction (dense blocks of mask-sorted
+    # output rows: gather -> MFMA -> one store per row)
     fwd_ms = med["fwd"]
     achieved = flop_pass / (fwd_ms / 1e3) / 1e12
     log(f"ms/step={ms_per_step:.3f} phases(ms)={ {k: round(v, 4) for k, v in med.items()} }")
@@ -394,7 +396,7 @@ def main():
         "rulebook_alg_gbs": round(rb_bytes / (med["rulebook"] / 1e3) / 1e9, 1),
         "rulebook_hbm_frac": round(rb_bytes / (med["rulebook"] / 1e3) / 1e9 / HBM_PEAK_GBS, 3),
         "roofline": {
-            "kernel": "gather_mfma_kernel (forward)",
+            "kernel": "dense_fwd_kernel (forward)",
             "bound": "mfma",
             "achieved": round(achieved, 3),
             "peak": MFMA_FP32_PEAK_TFLOPS,
