@@ -290,6 +290,22 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
 void scn_set_allocator(void* (*alloc)(size_t bytes, hipStream_t stream, void* ctx),
                        void (*free)(void* ptr, hipStream_t stream, void* ctx), void* ctx);
 
+/*
+ * Which stride-1 rulebooks carry the dense forward view, used by
+ * scn_conv_fwd instead of the per-offset pair lists: the output rows sorted
+ * by their neighbour masks (the set of active offsets) so that blocks of 32
+ * rows share one offset set, and each output's input rows in offset order.
+ * Building the view costs a radix sort and one more list per rulebook; it
+ * pays back when the layer is large and has many offsets.  A stride-1
+ * rulebook built after this call carries the view when it has at least
+ * min_rows output rows and at least min_offsets offsets (K).  Defaults:
+ * min_rows = 1048576, min_offsets = 9 (set with negative arguments).
+ * Process-wide.  Results agree with the pair-list forward to rounding (each
+ * output sums its active offsets in ascending order either way).
+ * Errors: none (always SCN_OK).
+ */
+scn_status scn_set_dense_forward(int64_t min_rows, int32_t min_offsets);
+
 /* Message describing the last failing call on this thread ("" if none). */
 const char* scn_last_error(void);
 

@@ -19,5 +19,6 @@ from ._lib import (  # noqa: F401
     maxpool_fwd,
     next_rulebook,
     set_allocator,
+    set_dense_forward,
     version,
 )

@@ -31,8 +31,8 @@ EXPORTED = (
     "scn_rulebook_in_rows", "scn_rulebook_out_rows", "scn_rulebook_offsets",
     "scn_rulebook_export", "scn_rulebook_free", "scn_conv_fwd",
     "scn_conv_bwd_workspace_bytes", "scn_conv_bwd", "scn_maxpool_fwd",
-    "scn_maxpool_bwd_workspace_bytes", "scn_maxpool_bwd", "scn_set_allocator", "scn_last_error",
-    "scn_version",
+    "scn_maxpool_bwd_workspace_bytes", "scn_maxpool_bwd", "scn_set_allocator",
+    "scn_set_dense_forward", "scn_last_error", "scn_version",
 )
 
 _ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
@@ -89,6 +89,7 @@ def lib() -> ctypes.CDLL:
         "scn_maxpool_bwd_workspace_bytes": (sz, [P, i32]),
         "scn_maxpool_bwd": (st, [P, P, P, P, i32, P, P, P, sz, P]),
         "scn_set_allocator": (None, [_ALLOC_FN, _FREE_FN, P]),
+        "scn_set_dense_forward": (st, [i64, i32]),
         "scn_last_error": (ctypes.c_char_p, []),
         "scn_version": (ctypes.c_char_p, []),
     }
@@ -309,6 +310,13 @@ def version() -> str:
 # a rulebook built under a pair frees its memory through it, also after the
 # pair has been replaced.
 _hooks_kept = []
+
+
+def set_dense_forward(min_rows: int = -1, min_offsets: int = -1) -> None:
+    """Stride-1 rulebooks built from now on carry the dense forward view when
+    they have at least ``min_rows`` outputs and ``min_offsets`` offsets
+    (``scn_set_dense_forward``; negative values restore the defaults)."""
+    _check(lib().scn_set_dense_forward(int(min_rows), int(min_offsets)), "scn_set_dense_forward")
 
 
 def set_allocator(alloc=None, free=None) -> None:

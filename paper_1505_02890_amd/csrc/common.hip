@@ -1,6 +1,7 @@
 // Error reporting, device allocation and version string.
 #include <cstdarg>
 #include <cstdio>
+#include <atomic>
 #include <mutex>
 
 #include "scn_internal.h"
@@ -48,6 +49,14 @@ void set_allocator(const Allocator& a) {
   g_alloc = a;
 }
 
+static std::atomic<int64_t> g_dense_rows{DENSE_MIN_ROWS};
+static std::atomic<int32_t> g_dense_k{DENSE_MIN_K};
+
+bool dense_forward_for(int64_t a_out, int K) {
+  return a_out > 0 && a_out >= g_dense_rows.load(std::memory_order_relaxed) &&
+         K >= g_dense_k.load(std::memory_order_relaxed);
+}
+
 scn_status dalloc(void** p, size_t bytes, hipStream_t s, const Allocator& a) {
   *p = nullptr;
   if (bytes == 0) return SCN_OK;
@@ -93,6 +102,14 @@ extern "C" void scn_set_allocator(void* (*alloc)(size_t, hipStream_t, void*),
     a.ctx = ctx;
   }
   scn::set_allocator(a);
+}
+
+extern "C" scn_status scn_set_dense_forward(int64_t min_rows, int32_t min_offsets) {
+  scn::g_dense_rows.store(min_rows < 0 ? scn::DENSE_MIN_ROWS : min_rows,
+                          std::memory_order_relaxed);
+  scn::g_dense_k.store(min_offsets < 0 ? scn::DENSE_MIN_K : min_offsets,
+                       std::memory_order_relaxed);
+  return SCN_OK;
 }
 
 extern "C" const char* scn_version(void) { return "scn-mi355x 0.1 (gfx950)"; }

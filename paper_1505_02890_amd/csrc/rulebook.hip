@@ -755,7 +755,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
                 sz_it = al((K * nit + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
                 sz_inv = pool ? al(n * 4 * inv_slots) : 0;
   // dense forward table for stride-1 rulebooks (see scn_rulebook)
-  const bool dense = s == 1 && a_out > 0;
+  const bool dense = s == 1 && dense_forward_for(a_out, K);
   const int64_t nfb = dense ? ceil_div(a_out, DENSE_ROWS) : 0;
   const int64_t sz_fnb = al((pmax + 1) * 4), sz_fnboff = al((a_out + 1) * 4),
                 sz_fperm = al(a_out * 4), sz_fmask = al(a_out * 4);

@@ -16,7 +16,13 @@ namespace scn {
 // output rows) and per (offset, tile of TILE input ranks).
 constexpr int TILE = 64;
 constexpr int MAX_K = 27;  // f <= 3 (the tetrahedral lattice needs at most 10)
-constexpr int DENSE_ROWS = 32;  // output rows per block of the dense forward table
+constexpr int DENSE_ROWS = 32;  // output rows per block of the dense forward view
+// Default policy for the dense forward view (scn_set_dense_forward): stride-1
+// rulebooks with at least this many output rows and offsets.  Below them the
+// view's sort and extra launches cost more than the forward saves (measured
+// on the paper's networks, whose 2x2x2 layers never gain).
+constexpr int64_t DENSE_MIN_ROWS = int64_t(1) << 20;
+constexpr int DENSE_MIN_K = 9;
 
 void set_error(const char* fmt, ...);
 void clear_error();
@@ -34,6 +40,9 @@ struct Allocator {
   void* ctx = nullptr;
 };
 Allocator current_allocator();
+// whether a stride-1 rulebook with a_out outputs and K offsets gets the dense
+// forward view (scn_set_dense_forward)
+bool dense_forward_for(int64_t a_out, int K);
 scn_status dalloc(void** p, size_t bytes, hipStream_t s, const Allocator& a);
 void dfree(void* p, hipStream_t s, const Allocator& a);
 

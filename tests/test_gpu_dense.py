@@ -1,0 +1,139 @@
+"""GPU parity of the dense-block forward (stride-1 rulebooks that carry the
+mask-sorted view, scn_set_dense_forward) against the oracle, on every
+lattice and across channel counts: one to sixteen 16-channel steps, one to
+four 64-channel chunks, several 64-column blocks, ragged last blocks, ReLU
+on and off, sorted and shuffled inputs.  The same layers with the view
+switched off (the per-offset pair-list forward) agree to rounding; repeated
+calls are bitwise identical."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from gen import random_sites, stream_rng, tetra_random_sites, tri_random_sites  # noqa: E402
+
+from helpers import assert_close, dev, host  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def scn():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1505_02890_amd as m
+    m.lib()  # raises if the HIP library is missing
+    m.set_dense_forward(0, 1)  # every stride-1 rulebook with outputs
+    yield m
+    m.set_dense_forward()
+
+
+def _K(lattice, f):
+    return {"cubic": f ** 3, "tetrahedral": math.comb(f + 2, 3), "square": f * f,
+            "triangular": math.comb(f + 1, 2)}[lattice]
+
+
+def _sites(lattice, rng, B, m, n, shuffle=True):
+    if lattice == "cubic":
+        return random_sites(rng, B, (m, m, m), n, shuffle=shuffle), (B, m, m, m)
+    if lattice == "tetrahedral":
+        return tetra_random_sites(rng, B, m, n, shuffle=shuffle), (B, m, m, m)
+    if lattice == "square":
+        return random_sites(rng, B, (m, m, 1), n, shuffle=shuffle), (B, m, m, 1)
+    return tri_random_sites(rng, B, m, n, shuffle=shuffle), (B, m, m, 1)
+
+
+def _sq(a):
+    return None if a is None else np.asarray(a, np.float64) ** 2
+
+
+CASES = [
+    # (lattice, f, B, m, n, Cin, Cout, relu, shuffle)
+    ("cubic", 3, 2, 24, 3000, 64, 64, False, True),      # the benchmark's shape, small
+    ("cubic", 3, 1, 30, 2500, 1, 16, True, True),        # one channel (non-vector loads)
+    ("cubic", 2, 2, 20, 1800, 3, 32, True, False),       # sorted input
+    ("cubic", 3, 1, 22, 1500, 17, 5, False, True),       # ragged channels and columns
+    ("cubic", 2, 1, 18, 1200, 96, 96, True, True),       # two chunks, two column blocks
+    ("cubic", 3, 1, 16, 700, 256, 72, False, True),      # four chunks
+    ("cubic", 2, 1, 14, 2744, 32, 32, False, True),      # every site active
+    ("tetrahedral", 3, 2, 30, 2000, 48, 40, True, True),
+    ("tetrahedral", 2, 1, 26, 1500, 64, 64, False, False),
+    ("square", 3, 3, 60, 2500, 32, 64, True, True),
+    ("triangular", 3, 3, 70, 2400, 64, 32, False, True),
+    ("triangular", 2, 1, 9, 45, 8, 8, False, True),       # one block, grid filled
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"{c[0]}{i}" for i, c in enumerate(CASES)])
+def test_dense_forward_parity(scn, case):
+    lattice, f, B, m, n, Cin, Cout, relu, shuffle = case
+    rng = stream_rng(170, CASES.index(case))
+    coords, grid = _sites(lattice, rng, B, m, n, shuffle)
+    K = _K(lattice, f)
+    x = rng.standard_normal((len(coords), Cin)).astype(np.float32)
+    g_in = (rng.standard_normal(Cin) * 0.5).astype(np.float32)
+    W = (rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin)).astype(np.float32)
+    bias = (rng.standard_normal(Cout) * 0.1).astype(np.float32)
+    g = scn.build_rulebook(dev(coords), grid, f, 1, lattice=lattice)
+    o = oracle.Rulebook(coords, grid, f, 1, lattice=lattice)
+    assert g.a_out == o.arrays().a_out
+    y_ref, go_ref = oracle.conv_fwd(o, x, g_in, W, bias, relu=relu)
+    sig_y, sig_g = (np.sqrt(v) for v in oracle.conv_fwd(o, _sq(x), _sq(g_in), _sq(W), _sq(bias)))
+    yd, god = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias), relu=relu)
+    assert_close("y", host(yd), y_ref, sig_y)
+    assert_close("g_out", host(god), go_ref, sig_g)
+    # repeated calls: bitwise identical
+    yd2, _ = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias), relu=relu)
+    assert torch.equal(yd, yd2)
+
+
+@pytest.mark.parametrize("lattice,f", [("cubic", 3), ("cubic", 2), ("tetrahedral", 3),
+                                       ("triangular", 3)])
+def test_dense_matches_pair_lists(scn, lattice, f):
+    """The view changes neither the rulebook nor (beyond rounding) the forward."""
+    rng = stream_rng(171, _K(lattice, f))
+    coords, grid = _sites(lattice, rng, 2, 28, 2500)
+    Cin, Cout = 32, 48
+    K = _K(lattice, f)
+    x = dev(rng.standard_normal((len(coords), Cin)).astype(np.float32))
+    g_in = dev((rng.standard_normal(Cin) * 0.5).astype(np.float32))
+    W = dev((rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin)).astype(np.float32))
+    bias = dev((rng.standard_normal(Cout) * 0.1).astype(np.float32))
+    gd = scn.build_rulebook(dev(coords), grid, f, 1, lattice=lattice)
+    scn.set_dense_forward(1 << 62, 1)  # no view
+    try:
+        gp = scn.build_rulebook(dev(coords), grid, f, 1, lattice=lattice)
+    finally:
+        scn.set_dense_forward(0, 1)
+    for a, b in zip(gd.export(), gp.export()):
+        assert torch.equal(a, b)
+    yd, god = scn.conv_fwd(gd, x, g_in, W, bias, relu=True)
+    yp, gop = scn.conv_fwd(gp, x, g_in, W, bias, relu=True)
+    assert torch.equal(god, gop)
+    sig = torch.sqrt(scn.conv_fwd(gp, x * x, g_in * g_in, W * W, bias * bias)[0].double())
+    assert_close("y dense vs pair lists", host(yd), host(yp).astype(np.float64), host(sig))
+
+
+def test_dense_empty_and_strided(scn):
+    """No outputs: nothing to launch.  Strided rulebooks never carry the view
+    and still match the oracle."""
+    g = scn.build_rulebook(dev(np.zeros((0, 4), np.int32)), (1, 8, 8, 8), 3, 1)
+    y, go = scn.conv_fwd(g, dev(np.zeros((0, 4), np.float32)), dev(np.zeros(4, np.float32)),
+                         dev(np.ones((27, 4, 8), np.float32)), None)
+    assert y.shape == (0, 8)
+    rng = stream_rng(172, 0)
+    coords, grid = _sites("cubic", rng, 1, 25, 1500)
+    x = rng.standard_normal((len(coords), 16)).astype(np.float32)
+    g_in = (rng.standard_normal(16) * 0.5).astype(np.float32)
+    W = (rng.standard_normal((8, 16, 24)) / 8).astype(np.float32)
+    g = scn.build_rulebook(dev(coords), grid, 2, 2)
+    o = oracle.Rulebook(coords, grid, 2, 2)
+    y_ref, _ = oracle.conv_fwd(o, x, g_in, W, None)
+    sig = np.sqrt(oracle.conv_fwd(o, _sq(x), _sq(g_in), _sq(W), None)[0])
+    yd, _ = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), None)
+    assert_close("y strided", host(yd), y_ref, sig)
