@@ -1134,31 +1134,51 @@ __global__ void __launch_bounds__(NT) dw_partial_kernel(DwArgs a) {
   }
 }
 
-// dW[k][ci][co] = sum_c part + g_in[ci] * u0[co];  T[k][co] = sum_c partT
-__global__ void dw_reduce_kernel(const float* __restrict__ part, const float* __restrict__ partT,
-                                 const int64_t* __restrict__ off, int K, int Cin, int Cout,
-                                 int64_t chp, int64_t maxc, const float* __restrict__ g_in,
-                                 const float* __restrict__ u0, float* __restrict__ dW,
-                                 float* __restrict__ T) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// dW[k][ci][co] = sum_c part + g_in[ci] * u0[co];  T[k][co] = sum_c partT.
+// A block covers RED_E consecutive elements; thread group g (of RED_G) sums
+// the chunks c = g (mod RED_G) in ascending order, and the group sums are
+// added in group order (a fixed order, so the result is deterministic).
+constexpr int RED_E = 32, RED_G = 8;
+__global__ void __launch_bounds__(RED_E * RED_G) dw_reduce_kernel(
+    const float* __restrict__ part, const float* __restrict__ partT,
+    const int64_t* __restrict__ off, int K, int Cin, int Cout, int64_t chp, int64_t maxc,
+    const float* __restrict__ g_in, const float* __restrict__ u0, float* __restrict__ dW,
+    float* __restrict__ T) {
+  __shared__ float red[2][RED_G][RED_E];
+  const int le = threadIdx.x % RED_E, g = threadIdx.x / RED_E;
+  const int64_t i = (int64_t)blockIdx.x * RED_E + le;
   const int64_t per = (int64_t)Cin * Cout;
+  float s = 0.f, t = 0.f;
   if (i < (int64_t)K * per) {
     const int k = (int)(i / per);
     const int64_t e = i - k * per;
-    const int ci = (int)(e / Cout), co = (int)(e - (int64_t)ci * Cout);
     const int64_t nch = ceil_div(off[k + 1] - off[k], chp);
     const float* p = part + (int64_t)k * maxc * per + e;
-    float s = 0.f;
-    for (int64_t c = 0; c < nch; ++c) s += p[c * per];
-    if (dW) dW[i] = s + g_in[ci] * u0[co];
+#pragma unroll 4
+    for (int64_t c = g; c < nch; c += RED_G) s += p[c * per];
   }
   if (i < (int64_t)K * Cout) {
     const int k = (int)(i / Cout), co = (int)(i % Cout);
     const int64_t nch = ceil_div(off[k + 1] - off[k], chp);
-    float s = 0.f;
-    for (int64_t c = 0; c < nch; ++c) s += partT[((int64_t)k * maxc + c) * Cout + co];
-    T[i] = s;
+    for (int64_t c = g; c < nch; c += RED_G) t += partT[((int64_t)k * maxc + c) * Cout + co];
   }
+  red[0][g][le] = s;
+  red[1][g][le] = t;
+  __syncthreads();
+  if (g != 0) return;
+  s = red[0][0][le];
+  t = red[1][0][le];
+#pragma unroll
+  for (int h = 1; h < RED_G; ++h) {
+    s += red[0][h][le];
+    t += red[1][h][le];
+  }
+  if (i < (int64_t)K * per && dW) {
+    const int64_t e = i % per;
+    const int ci = (int)(e / Cout), co = (int)(e - (int64_t)ci * Cout);
+    dW[i] = s + g_in[ci] * u0[co];
+  }
+  if (i < (int64_t)K * Cout) T[i] = t;
 }
 
 // dg_in[ci] = sum_k sum_co W[k][ci][co] * (u0[co] - T[k][co]); one block per ci,
@@ -1466,7 +1486,8 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
       SCN_LAUNCH_CHECK();
     }
     const int64_t nred = std::max<int64_t>((int64_t)K * Cin * Cout, (int64_t)K * Cout);
-    hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)ceil_div(nred, 256)), dim3(256), 0, st,
+    hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)ceil_div(nred, RED_E)),
+                       dim3(RED_E * RED_G), 0, st,
                        part, partT, rb->off_dev, K, Cin, Cout, L.chp, L.maxc, g_in, u0, dW, T);
     SCN_LAUNCH_CHECK();
     if (dg_in) {
