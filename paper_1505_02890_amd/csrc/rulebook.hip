@@ -513,20 +513,49 @@ inline unsigned blocks_for(int64_t n, int threads) {
   return (unsigned)std::max<int64_t>(1, ceil_div(n, threads));
 }
 
+// Build temporaries.  reserve(bytes) takes one block from the allocator and
+// get() carves 256-byte-aligned pieces from it, so a build phase costs one
+// allocation and one free (each is a host call of tens of microseconds); a
+// request that does not fit gets a block of its own.
 struct Temps {
   hipStream_t s;
   Allocator al;
   void* p[16] = {nullptr};
   int n = 0;
+  char* cur = nullptr;
+  size_t left = 0;
   Temps(hipStream_t st, const Allocator& a) : s(st), al(a) {}
+  static size_t round(size_t b) { return (std::max<size_t>(b, 1) + 255) & ~size_t(255); }
+  scn_status take(void** q, size_t bytes) {
+    if (n >= 16) {
+      set_error("scn_rulebook_build: too many temporary blocks");
+      return SCN_ERR_NOMEM;
+    }
+    scn_status st = dalloc(q, bytes, s, al);
+    if (st == SCN_OK) p[n++] = *q;
+    return st;
+  }
+  scn_status reserve(size_t bytes) {
+    void* q = nullptr;
+    scn_status st = take(&q, bytes);
+    if (st != SCN_OK) return st;
+    cur = static_cast<char*>(q);
+    left = bytes;
+    return SCN_OK;
+  }
   template <typename T>
   scn_status get(T** out, size_t count) {
+    const size_t b = round(count * sizeof(T));
+    if (b <= left) {
+      *out = reinterpret_cast<T*>(cur);
+      cur += b;
+      left -= b;
+      return SCN_OK;
+    }
     void* q = nullptr;
-    scn_status st = dalloc(&q, std::max<size_t>(count, 1) * sizeof(T), s, al);
-    if (st != SCN_OK) return st;
-    p[n++] = q;
+    scn_status st = take(&q, b);
     *out = static_cast<T*>(q);
-    return SCN_OK;
+    return st;
   }
   ~Temps() {
     for (int i = 0; i < n; ++i) dfree(p[i], s, al);
@@ -669,16 +698,20 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     Allocator al;
     ~Hout() {
       if (bits) dfree(bits, s, al);
-      if (rank) dfree(rank, s, al);
     }
   } hout;
   hout.s = st;
   hout.al = mem;
-  if ((rc = dalloc((void**)&hout.bits, std::max<int64_t>(nw_out, 1) * 4, st, mem)) ||
-      (rc = dalloc((void**)&hout.rank, (nw_out + 1) * 4, st, mem)))
+  // bits and their prefix in one block (freed through its start, bits)
+  const size_t hbits_bytes = Temps::round((size_t)std::max<int64_t>(nw_out, 1) * 4);
+  if ((rc = dalloc((void**)&hout.bits, hbits_bytes + Temps::round((nw_out + 1) * 4), st, mem)))
     return rc;
+  hout.rank = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(hout.bits) + hbits_bytes);
   uint32_t* const outb = hout.bits;
   uint32_t* const opref = hout.rank;
+  if ((rc = tmp.reserve((prev ? 0 : Temps::round(nw_in * 4) + Temps::round((nw_in + 1) * 4)) +
+                         Temps::round(16) + Temps::round(nsb * 4))))
+    return rc;
   if (prev) {
     inb = prev->hout_bits;
     ipref = prev->hout_rank;
@@ -771,8 +804,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     ~Guard() {
       if (!keep && rb) {
         dfree(rb->block, s, rb->alloc);
-        dfree(rb->hout_bits, s, rb->alloc);
-        dfree(rb->hout_rank, s, rb->alloc);
+        dfree(rb->hout_bits, s, rb->alloc);  // also holds hout_rank
         delete rb;
       }
     }
@@ -822,6 +854,18 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   uint32_t* masks;
   uint64_t *cnt, *sc64;
   const int64_t ncnt = K * nt;
+  // the mask sort's scratch size (a query; no device work)
+  size_t sort_bytes = 0;
+  if (dense)
+    SCN_HIP(hipcub::DeviceRadixSort::SortPairs(nullptr, sort_bytes, (uint32_t*)nullptr,
+                                               (uint32_t*)nullptr, (int32_t*)nullptr,
+                                               (int32_t*)nullptr, (int)a_out, 0, K, st));
+  if ((rc = tmp.reserve(Temps::round(a_out * 4) + Temps::round(ncnt * 8) +
+                        Temps::round(scan_blocks(ncnt) * 8) +
+                        (dense ? Temps::round(scan_blocks(a_out) * 4) +
+                                     Temps::round(a_out * 4) + Temps::round(sort_bytes)
+                               : 0))))
+    return rc;
   if ((rc = tmp.get(&masks, a_out)) || (rc = tmp.get(&cnt, ncnt)) ||
       (rc = tmp.get(&sc64, scan_blocks(ncnt))))
     return rc;
@@ -872,9 +916,6 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     // the output rows sorted by neighbour mask (a stable radix sort)
     int32_t* iota = nullptr;
     char* sort_tmp = nullptr;
-    size_t sort_bytes = 0;
-    SCN_HIP(hipcub::DeviceRadixSort::SortPairs(nullptr, sort_bytes, masks, rb->fmask, iota,
-                                               rb->fperm, (int)a_out, 0, K, st));
     if ((rc = tmp.get(&iota, a_out)) || (rc = tmp.get(&sort_tmp, sort_bytes))) return rc;
     hipLaunchKernelGGL(iota_kernel, dim3(blocks_for(a_out, 256)), dim3(256), 0, st, iota, a_out);
     SCN_LAUNCH_CHECK();
@@ -988,8 +1029,7 @@ scn_status scn_rulebook_export(const scn_rulebook* rb, int32_t* out_coords, int3
 void scn_rulebook_free(scn_rulebook* rb) {
   if (!rb) return;
   scn::dfree(rb->block, rb->stream, rb->alloc);
-  scn::dfree(rb->hout_bits, rb->stream, rb->alloc);
-  scn::dfree(rb->hout_rank, rb->stream, rb->alloc);
+  scn::dfree(rb->hout_bits, rb->stream, rb->alloc);  // also holds hout_rank
   delete rb;
 }
 

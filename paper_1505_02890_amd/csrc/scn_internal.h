@@ -126,7 +126,8 @@ struct scn_rulebook {
 
   // The output layer's rank bitmap (H_out): occupancy words of the output grid
   // and their exclusive popcount prefix (hout_rank[hout_words] = a_out); the
-  // H_in of a rulebook built from this one's output sites.
+  // H_in of a rulebook built from this one's output sites.  One allocation,
+  // starting at hout_bits.
   uint32_t* hout_bits = nullptr;
   uint32_t* hout_rank = nullptr;
   int64_t hout_words = 0;
