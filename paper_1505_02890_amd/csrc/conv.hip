@@ -88,14 +88,16 @@ __global__ void __launch_bounds__(256) ground_w_kernel(const float* __restrict__
   }
 }
 
+// g_pre (kept for the contraction's epilogue) and g_out = act(g_pre)
 __global__ void ground_pre_kernel(const float* __restrict__ gw, int ld,
-                                  const float* __restrict__ bias, int K, int Cout,
-                                  float* __restrict__ g_pre) {
+                                  const float* __restrict__ bias, int K, int Cout, int relu,
+                                  float* __restrict__ g_pre, float* __restrict__ g_out) {
   const int co = blockIdx.x * blockDim.x + threadIdx.x;
   if (co >= Cout) return;
   float s = bias ? bias[co] : 0.f;
   for (int k = 0; k < K; ++k) s += gw[(int64_t)k * ld + co];
   g_pre[co] = s;
+  g_out[co] = relu && !(s > 0.f) ? 0.f : s;
 }
 
 __global__ void zero_kernel(float* __restrict__ p, int64_t n) {
@@ -131,11 +133,6 @@ __global__ void __launch_bounds__(256) pack_w_kernel(const float* __restrict__ W
     v = W[(k * Cin + ci) * Cout + co];
   }
   Wp[i] = v;
-}
-
-__global__ void relu_vec_kernel(float* __restrict__ v, int n) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) v[i] = v[i] > 0.f ? v[i] : 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -1290,9 +1287,9 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
     return SCN_ERR_UNSUPPORTED;
   }
   const int relu = (flags & SCN_RELU) ? 1 : 0;
-  // scratch: gw [K][NcP] and the packed weights [K][NcP][RkP]
+  // scratch: gw [K][NcP], g_pre [NcP] and the packed weights [K][NcP][RkP]
   const int RkP = (int)ceil_div(Cin, 16) * 16, NcP = (int)ceil_div(Cout, 64) * 64;
-  const size_t gw_bytes = ((size_t)rb->K * NcP * sizeof(float) + 255) & ~size_t(255);
+  const size_t gw_bytes = ((size_t)(rb->K + 1) * NcP * sizeof(float) + 255) & ~size_t(255);
   float* gw = nullptr;
   const Allocator al = current_allocator();
   scn_status rc = dalloc(reinterpret_cast<void**>(&gw),
@@ -1304,6 +1301,7 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
     Allocator al;
     ~Free() { dfree(p, s, al); }
   } free_gw{gw, st, al};
+  float* const gpre = gw + (size_t)rb->K * NcP;
   float* Wp = reinterpret_cast<float*>(reinterpret_cast<char*>(gw) + gw_bytes);
   hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)ceil_div((int64_t)rb->K * NcP * RkP, 256)),
                      dim3(256), 0, st, W, rb->K, Cin, Cout, 1, RkP, NcP, Wp);
@@ -1312,14 +1310,14 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
                      g_in, W, rb->K, Cin, Cout, NcP, gw);
   SCN_LAUNCH_CHECK();
   hipLaunchKernelGGL(ground_pre_kernel, dim3((unsigned)ceil_div(Cout, 64)), dim3(64), 0, st, gw,
-                     NcP, bias, rb->K, Cout, g_out);
+                     NcP, bias, rb->K, Cout, relu, gpre, g_out);
   SCN_LAUNCH_CHECK();
   if (rb->fnb) {
     DenseArgs d{};
     d.x = x;
     d.g_in = g_in;
     d.Wp = Wp;
-    d.add = g_out;  // holds g_pre until the ReLU below
+    d.add = gpre;
     d.nb = rb->fnb;
     d.nb_off = rb->fnb_off;
     d.fperm = rb->fperm;
@@ -1332,14 +1330,7 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
     d.Cout = Cout;
     d.NcP = NcP;
     d.relu = relu;
-    rc = launch_dense(d, st);
-    if (rc) return rc;
-    if (relu) {
-      hipLaunchKernelGGL(relu_vec_kernel, dim3((unsigned)ceil_div(Cout, 256)), dim3(256), 0, st,
-                         g_out, Cout);
-      SCN_LAUNCH_CHECK();
-    }
-    return SCN_OK;
+    return launch_dense(d, st);
   }
   GatherArgs a{};
   a.src = x;
@@ -1352,20 +1343,13 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
   a.NcP = NcP;
   a.Rk = Cin;
   a.Nc = Cout;
-  a.add = g_out;  // holds g_pre until the ReLU below
+  a.add = gpre;
   a.relu = relu;
   a.dst = y;
   a.wmap = nullptr;
   a.nrows = rb->a_out;
   a.K = rb->K;
-  rc = launch_gather(a, st);
-  if (rc) return rc;
-  if (relu) {
-    hipLaunchKernelGGL(relu_vec_kernel, dim3((unsigned)ceil_div(Cout, 256)), dim3(256), 0, st,
-                       g_out, Cout);
-    SCN_LAUNCH_CHECK();
-  }
-  return SCN_OK;
+  return launch_gather(a, st);
 }
 
 size_t scn_conv_bwd_workspace_bytes(const scn_rulebook* rb, int32_t Cin, int32_t Cout,

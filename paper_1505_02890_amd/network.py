@@ -115,12 +115,16 @@ class SparseNet:
         grid = (batch, self.m, self.m, 1 if self.lattice in PLANAR else self.m)
         g = torch.zeros(x.shape[1], dtype=torch.float32, device=self.device)
         rec = []
-        rb = None
-        for L, p in zip(self.layers, self.params):
-            # the first layer's sites are the input; each later layer's are the
-            # previous layer's active outputs (its rank bitmap is reused)
-            rb = (scn.build_rulebook(coords, grid, L.f, L.s, lattice=self.lattice) if rb is None
-                  else scn.next_rulebook(rb, L.f, L.s))
+        # Rulebooks depend only on the active sites, not on the features: build
+        # the whole chain first (each build synchronises), then issue every
+        # convolution and pooling back to back with no synchronisation between.
+        # The first layer's sites are the input; each later layer's are the
+        # previous layer's active outputs (its rank bitmap is reused).
+        rbs = []
+        for L in self.layers:
+            rbs.append(scn.build_rulebook(coords, grid, L.f, L.s, lattice=self.lattice)
+                       if not rbs else scn.next_rulebook(rbs[-1], L.f, L.s))
+        for L, p, rb in zip(self.layers, self.params, rbs):
             if L.kind == "conv":
                 W, b = p
                 x, g = scn.conv_fwd(rb, x, g, W, b, relu=L.relu)
