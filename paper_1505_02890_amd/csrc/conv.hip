@@ -623,17 +623,51 @@ __device__ inline DRows<(NKT < 4 ? NKT : 4)> dense_rows(const DenseArgs& a, cons
   return R;
 }
 
+// rows of an item whose input rows are already known
+template <int NKT, bool VEC>
+__device__ inline DRows<(NKT < 4 ? NKT : 4)> dense_rows_i(const DenseArgs& a, int r0, int r1,
+                                                          int ch, int q) {
+  constexpr int TC = NKT < 4 ? NKT : 4;
+  DRows<TC> R;
+  R.r0 = r0;
+  R.r1 = r1;
+  const float* p0 = a.x + (int64_t)(r0 >= 0 ? r0 : 0) * a.Cin;
+  const float* p1 = a.x + (int64_t)(r1 >= 0 ? r1 : 0) * a.Cin;
+#pragma unroll
+  for (int t = 0; t < TC; ++t) {
+    const int c = 64 * ch + 16 * t + 4 * q;
+    if (VEC) {
+      const int cc = c < a.Cin ? c : 0;
+      R.v[0][t] = *reinterpret_cast<const float4*>(p0 + cc);
+      R.v[1][t] = *reinterpret_cast<const float4*>(p1 + cc);
+    } else {
+      float e0[4], e1[4];
+#pragma unroll
+      for (int z = 0; z < 4; ++z) {
+        const int cz = c + z < a.Cin ? c + z : 0;
+        e0[z] = p0[cz];
+        e1[z] = p1[cz];
+      }
+      R.v[0][t] = make_float4(e0[0], e0[1], e0[2], e0[3]);
+      R.v[1][t] = make_float4(e1[0], e1[1], e1[2], e1[3]);
+    }
+  }
+  return R;
+}
+
 template <int NKT, bool VEC>
 __global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
   constexpr int TC = NKT < 4 ? NKT : 4;        // 16-channel steps per chunk
   constexpr int NCH = (NKT + 3) / 4;           // 64-channel chunks
+  __shared__ float gsh[16 * NKT];  // g_in, zero past Cin (those weights are zero)
+  for (int c = threadIdx.x; c < 16 * NKT; c += NT) gsh[c] = c < a.Cin ? a.g_in[c] : 0.f;
+  __syncthreads();
   const int lane = threadIdx.x & 63;
   const int64_t b = (int64_t)blockIdx.x * (NT / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (b >= a.nblk) return;
   const int cb = blockIdx.y;
   const int n16 = lane & 15, q = lane >> 4;
   const int ncb = a.NcP >> 6;
-  // the lane's two rows (past a_out: no offsets)
   const int64_t pos0 = b * DENSE_ROWS + n16, pos1 = pos0 + 16;
   const int o0 = pos0 < a.a_out ? a.fperm[pos0] : 0, o1 = pos1 < a.a_out ? a.fperm[pos1] : 0;
   DRow w0, w1;
@@ -641,46 +675,62 @@ __global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
   w1.m = pos1 < a.a_out ? a.fmask[pos1] : 0u;
   w0.off = a.nb_off[o0];
   w1.off = a.nb_off[o1];
-  // union of the block's masks (lanes n16 cover all 32 rows)
   uint32_t u = w0.m | w1.m;
 #pragma unroll
   for (int d = 1; d < 16; d <<= 1) u |= (uint32_t)__shfl_xor((int)u, d, 16);
-  uint32_t U = (uint32_t)__builtin_amdgcn_readfirstlane((int)u);
+  const uint32_t U = (uint32_t)__builtin_amdgcn_readfirstlane((int)u);
   v4f acc[2][4];
 #pragma unroll
   for (int r = 0; r < 2; ++r)
 #pragma unroll
     for (int g = 0; g < 4; ++g) acc[r][g] = v4f{0.f, 0.f, 0.f, 0.f};
   if (U) {
-    int k = __builtin_ctz(U);
-    uint32_t rest = U & (U - 1);  // offsets after k
-    int ch = 0;
-    DRows<TC> cur = dense_rows<NKT, VEC>(a, w0, w1, k, 0, q);
-    while (true) {
-      // the next item: the next chunk of k, else chunk 0 of the next offset
-      // (past the last item: the current one again, in bounds and unused)
-      const bool last_chunk = ch == NCH - 1;
-      const bool done = last_chunk && !rest;
-      const int kn = last_chunk ? (rest ? __builtin_ctz(rest) : k) : k;
-      const int chn = last_chunk ? (rest ? 0 : ch) : ch + 1;
-      DRows<TC> nxt = dense_rows<NKT, VEC>(a, w0, w1, kn, chn, q);
-      const float* wp = a.Wp + (((int64_t)k * ncb + cb) * 4) * (NKT * 256) + lane * 4;
-#pragma unroll
-      for (int t = 0; t < TC; ++t) {
-        const int tg = 4 * ch + t;  // global 16-channel step
-        if (NCH > 1 && tg >= NKT) break;
-        float4 A[4];
+    // item = (offset k, channel chunk ch), in order; `rest` holds the offsets
+    // after k; past the last item an item stays where it is (its loads are in
+    // bounds and unused)
+    struct Item {
+      int k, ch;
+      uint32_t rest;
+    };
+    auto advance = [&](Item& t) {
+      if (t.ch + 1 < NCH) {
+        ++t.ch;
+      } else if (t.rest) {
+        t.k = __builtin_ctz(t.rest);
+        t.rest &= t.rest - 1;
+        t.ch = 0;
+      }
+    };
+    Item c{__builtin_ctz(U), 0, U & (U - 1)};
+    Item n = c;
+    advance(n);
+    Item nn = n;
+    advance(nn);
+    const int nit = __builtin_popcount(U) * NCH;
+    int n0 = dense_src(a, w0, n.k), n1 = dense_src(a, w1, n.k);
+    DRows<TC> cur = dense_rows_i<NKT, VEC>(a, dense_src(a, w0, c.k), dense_src(a, w1, c.k), 0, q);
+    DRows<TC> nxt;
+    int nn0 = 0, nn1 = 0;
+    for (int it = 0; it < nit; ++it) {
+      const int ch = c.ch;
+      const float* wp = a.Wp + (((int64_t)c.k * ncb + cb) * 4) * (NKT * 256) + lane * 4;
+      auto wload = [&](int t, float4 (&A)[4]) {
+        const int tg = 4 * ch + t < NKT ? 4 * ch + t : NKT - 1;  // past NKT: never used
 #pragma unroll
         for (int g = 0; g < 4; ++g)
           A[g] = *reinterpret_cast<const float4*>(wp + (int64_t)g * (NKT * 256) + tg * 256);
-        const int c = 16 * tg + 4 * q;
-        float4 gq;
-        if (VEC) {
-          gq = *reinterpret_cast<const float4*>(a.g_in + (c < a.Cin ? c : 0));
-        } else {
-          gq = make_float4(a.g_in[c < a.Cin ? c : 0], a.g_in[c + 1 < a.Cin ? c + 1 : 0],
-                           a.g_in[c + 2 < a.Cin ? c + 2 : 0], a.g_in[c + 3 < a.Cin ? c + 3 : 0]);
-        }
+      };
+      // the next item's rows and the indices after it: issued after this
+      // item's last weight load, so the waits for the weights leave them in
+      // flight
+      auto prefetch = [&]() {
+        nxt = dense_rows_i<NKT, VEC>(a, n0, n1, n.ch, q);
+        nn0 = dense_src(a, w0, nn.k);
+        nn1 = dense_src(a, w1, nn.k);
+      };
+      auto mult = [&](int t, const float4 (&A)[4]) {
+        const int tg = 4 * ch + t;
+        const float4 gq = *reinterpret_cast<const float4*>(&gsh[16 * tg + 4 * q]);
         const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
         float4 d0 = cur.v[0][t], d1 = cur.v[1][t];
         d0.x -= gq.x; d0.y -= gq.y; d0.z -= gq.z; d0.w -= gq.w;
@@ -697,11 +747,30 @@ __global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
           acc[0][g] = mfma4(A[g].w, B0.w, acc[0][g]);
           acc[1][g] = mfma4(A[g].w, B1.w, acc[1][g]);
         }
+      };
+      // weights two 16-channel steps ahead of their products (two register
+      // sets, alternating)
+      float4 A0[4], A1[4];
+      wload(0, A0);
+      if (TC > 1) wload(1, A1);
+      if (TC <= 2) prefetch();
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < TC; ++t) {
+        if (NCH > 1 && 4 * ch + t >= NKT) break;
+        // step t's products, then step t + 2's weights into the set just read
+        if (t & 1) mult(t, A1); else mult(t, A0);
+        if (t + 2 < TC) {
+          if (t & 1) wload(t + 2, A1); else wload(t + 2, A0);
+          if (t + 2 == TC - 1) prefetch();
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
-      if (done) break;
-      if (last_chunk) rest &= rest - 1;
-      k = kn;
-      ch = chn;
+      c = n;
+      n = nn;
+      advance(nn);
+      n0 = nn0;
+      n1 = nn1;
       cur = nxt;
     }
   }
