@@ -34,8 +34,13 @@
  *  - All pointers named x, y, W, g_*, d*, coords, argmax are DEVICE pointers
  *    owned by the caller and never retained.  Host pointers are marked "host".
  *  - Calls are asynchronous on the given HIP stream unless stated otherwise;
- *    only scn_rulebook_build synchronises (twice: to read back the number of
- *    output sites, then the per-offset list boundaries).
+ *    only the rulebook builds wait for the device (twice: to read back the
+ *    number of output sites, then the per-offset list boundaries).  A build
+ *    returns once its host-side sizes are known; its last kernels may still
+ *    be running on its stream.  Every entry point that takes a rulebook and
+ *    a different stream orders that stream after them (hipStreamWaitEvent);
+ *    raw array pointers of a rulebook (scn_rulebook_out_coords and the like)
+ *    are valid in the build stream's order.
  *  - No call allocates the caller's outputs.  Status codes are returned; no
  *    exception crosses the ABI.  scn_last_error() gives a message for the last
  *    failing call on the calling thread.
@@ -106,7 +111,9 @@ typedef struct scn_rulebook_info {
  *  n       number of active input sites (>= 0; 0 gives an empty rulebook).
  *  grid    host int64[4] = (B, mx, my, mz), all >= 1.
  *  filter  f in {1, 2, 3};  stride s >= 1 (s <= f not required).
- *  stream  HIP stream for all device work; the call synchronises it twice.
+ *  stream  HIP stream for all device work; the call waits for it twice (the
+ *          second time only for the list boundaries, with the build's last
+ *          kernels queued behind them).
  *  out     receives a library-owned rulebook, freed by scn_rulebook_free.
  *
  * Output ordering is canonical: output rows ascend by key, and each
@@ -162,8 +169,8 @@ scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const in
  * rulebook keeps it: 8 bytes per 32 sites of its output grid) instead of
  * marking and ranking the sites again.  prev is only read, and may be freed
  * once this call returns.  Errors: SCN_ERR_INVALID (NULL, or prev's output
- * grid is empty), and as scn_rulebook_build.  The call synchronises stream
- * twice.
+ * grid is empty), and as scn_rulebook_build.  It waits for stream as
+ * scn_rulebook_build does, and orders stream after prev's build.
  */
 scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int32_t stride,
                                    hipStream_t stream, scn_rulebook** out);

@@ -1346,6 +1346,7 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
                         const float* W, const float* bias, int32_t Cin, int32_t Cout,
                         uint32_t flags, float* y, float* g_out, hipStream_t st) {
   clear_error();
+  if (scn_status rc0 = after_build(rb, st)) return rc0;
   if (!rb || !g_in || !W || !g_out || Cin < 1 || Cout < 1 || (rb->a_in > 0 && !x) ||
       (rb->a_out > 0 && !y)) {
     set_error("scn_conv_fwd: invalid argument");
@@ -1433,6 +1434,7 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
                         float* dx, float* dg_in, float* dW, float* dbias, void* ws,
                         size_t ws_bytes, hipStream_t st) {
   clear_error();
+  if (scn_status rc0 = after_build(rb, st)) return rc0;
   const int relu = (flags & SCN_RELU) ? 1 : 0;
   if (!rb || !g_in || !W || Cin < 1 || Cout < 1 || (rb->a_out > 0 && !dy) ||
       (rb->a_in > 0 && !x) || (relu && rb->a_out > 0 && !y) || (relu && dg_out && !g_out)) {

@@ -379,6 +379,7 @@ extern "C" {
 scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* g_in, int32_t C,
                            float* y, float* g_out, uint8_t* argmax, hipStream_t st) {
   clear_error();
+  if (scn_status rc0 = after_build(rb, st)) return rc0;
   if (!rb || !g_in || !g_out || C < 1 || (rb->a_in > 0 && !x) ||
       (rb->a_out > 0 && (!y || !argmax))) {
     set_error("scn_maxpool_fwd: invalid argument");
@@ -423,6 +424,7 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
                            const float* dg_out, int32_t C, float* dx, float* dg_in, void* ws,
                            size_t ws_bytes, hipStream_t st) {
   clear_error();
+  if (scn_status rc0 = after_build(rb, st)) return rc0;
   if (!rb || C < 1 || (rb->a_out > 0 && (!argmax || !dy)) || (rb->a_in > 0 && !dx)) {
     set_error("scn_maxpool_bwd: invalid argument");
     return SCN_ERR_INVALID;

@@ -803,8 +803,9 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     bool keep = false;
     ~Guard() {
       if (!keep && rb) {
-        dfree(rb->block, s, rb->alloc);
+        dfree(rb->block, s, rb->alloc);  // stream-ordered: after any queued kernel
         dfree(rb->hout_bits, s, rb->alloc);  // also holds hout_rank
+        if (rb->done) (void)hipEventDestroy(rb->done);
         delete rb;
       }
     }
@@ -894,6 +895,20 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   hipLaunchKernelGGL(list_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)rb->otile,
                      nt, K, rb->off_dev);
   SCN_LAUNCH_CHECK();
+  // From here the host needs only the list boundaries: copy them now, queue
+  // the rest of the build behind the copy, and wait for the copy alone, so
+  // the GPU keeps working while the caller goes on.  One event per host
+  // thread and device marks the copy.
+  SCN_HIP(hipMemcpyAsync(hb->off, rb->off_dev, (K + 1) * 8, hipMemcpyDeviceToHost, st));
+  static thread_local hipEvent_t copied[64] = {};
+  int dev = 0;
+  SCN_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) {
+    set_error("scn_rulebook_build: device %d out of range", dev);
+    return SCN_ERR_HIP;
+  }
+  if (!copied[dev]) SCN_HIP(hipEventCreateWithFlags(&copied[dev], hipEventDisableTiming));
+  SCN_HIP(hipEventRecord(copied[dev], st));
   if (dense) {
     // start of each output's neighbour list: exclusive sum of mask popcounts
     uint32_t* sc_nb = nullptr;
@@ -932,8 +947,9 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   hipLaunchKernelGGL(in_tiles_kernel, dim3(blocks_for(K * nit + 1, 256)), dim3(256), 0, st,
                      rb->in_rank, rb->off_dev, K, nit, rb->itile);
   SCN_LAUNCH_CHECK();
-  SCN_HIP(hipMemcpyAsync(hb->off, rb->off_dev, (K + 1) * 8, hipMemcpyDeviceToHost, st));
-  SCN_HIP(hipStreamSynchronize(st));
+  SCN_HIP(hipEventCreateWithFlags(&rb->done, hipEventDisableTiming));
+  SCN_HIP(hipEventRecord(rb->done, st));
+  SCN_HIP(hipEventSynchronize(copied[dev]));
   rb->n_pairs = hb->off[K];
   if (rb->n_pairs > INT32_MAX || rb->n_pairs > pmax) {
     set_error("scn_rulebook_build: %lld pairs exceed the supported count", (long long)rb->n_pairs);
@@ -978,6 +994,10 @@ scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int
       scn::set_error("scn_rulebook_build_next: the previous layer's output grid is empty");
       return SCN_ERR_INVALID;
     }
+  if (scn_status rc = scn::after_build(prev, stream)) {
+    *out = nullptr;
+    return rc;
+  }
   return scn::build(prev->out_coords, prev->a_out, prev->gout, filter, stride, prev->lattice,
                     stream, out, prev);
 }
@@ -1015,6 +1035,7 @@ scn_status scn_rulebook_export(const scn_rulebook* rb, int32_t* out_coords, int3
     scn::set_error("scn_rulebook_export: rb is NULL");
     return SCN_ERR_INVALID;
   }
+  if (scn_status rc = scn::after_build(rb, stream)) return rc;
   if (out_coords && rb->a_out > 0)
     SCN_HIP(hipMemcpyAsync(out_coords, rb->out_coords, rb->a_out * 16, hipMemcpyDeviceToDevice,
                            stream));
@@ -1030,6 +1051,7 @@ void scn_rulebook_free(scn_rulebook* rb) {
   if (!rb) return;
   scn::dfree(rb->block, rb->stream, rb->alloc);
   scn::dfree(rb->hout_bits, rb->stream, rb->alloc);  // also holds hout_rank
+  if (rb->done) (void)hipEventDestroy(rb->done);
   delete rb;
 }
 

@@ -121,6 +121,11 @@ struct scn_rulebook {
   int32_t* fperm = nullptr;
   uint32_t* fmask = nullptr;
 
+  // Recorded on `stream` after the build's last kernel.  The build returns
+  // once the host fields are known, with its last kernels possibly still
+  // running; entry points called on another stream wait for this event.
+  hipEvent_t done = nullptr;
+
   void* block = nullptr;  // single allocation holding all arrays above
   scn::Allocator alloc;   // the allocator every array of the rulebook came from
 
@@ -132,3 +137,16 @@ struct scn_rulebook {
   uint32_t* hout_rank = nullptr;
   int64_t hout_words = 0;
 };
+
+namespace scn {
+// Orders work on stream st after the rulebook's build (a no-op on the build's
+// own stream, where the order already holds).
+inline scn_status after_build(const scn_rulebook* rb, hipStream_t st) {
+  if (rb && rb->done && st != rb->stream && hipStreamWaitEvent(st, rb->done, 0) != hipSuccess) {
+    set_error("HIP error ordering after the rulebook's build: %s",
+              hipGetErrorString(hipGetLastError()));
+    return SCN_ERR_HIP;
+  }
+  return SCN_OK;
+}
+}  // namespace scn

@@ -103,3 +103,32 @@ def test_chain_outlives_its_source(scn):
     g.close()
     torch.cuda.synchronize()
     _same(nxt, ref)
+
+
+def test_use_on_another_stream_right_after_the_build(scn):
+    """The build returns before its last kernels finish (emission, the mask
+    sort); a call on another stream is ordered after them by the library."""
+    rng = stream_rng(94, 0)
+    coords, grid = _sites("cubic", rng, 1, 40, 6000)
+    Cin, Cout = 16, 24
+    x = dev(rng.standard_normal((len(coords), Cin)).astype(np.float32))
+    g_in = dev(np.zeros(Cin, np.float32))
+    W = dev((rng.standard_normal((27, Cin, Cout)) / 20).astype(np.float32))
+    cd = dev(coords)
+    torch.cuda.synchronize()
+    scn.set_dense_forward(0, 1)
+    try:
+        g = scn.build_rulebook(cd, grid, 3, 1)
+    finally:
+        scn.set_dense_forward()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        y, _ = scn.conv_fwd(g, x, g_in, W, None)
+        oc, ir, orr = g.export()
+    side.synchronize()
+    o = oracle.Rulebook(coords, grid, 3, 1)
+    oa = o.arrays()
+    assert np.array_equal(host(oc), oa.out_coords) and np.array_equal(host(ir), oa.in_rows)
+    assert np.array_equal(host(orr), oa.out_rows)
+    y_ref, _ = oracle.conv_fwd(o, host(x), host(g_in), host(W), None)
+    assert np.allclose(host(y), y_ref, rtol=1e-4, atol=1e-4)
