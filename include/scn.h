@@ -175,6 +175,25 @@ scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const in
 scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int32_t stride,
                                    hipStream_t stream, scn_rulebook** out);
 
+/*
+ * The rulebooks of a chain of layers in one call: layer 0 is built from the
+ * caller's sites as by scn_rulebook_build_lattice (coords, n, grid, lattice),
+ * and layer i > 0 from the active output sites of layer i - 1, as by
+ * scn_rulebook_build_next, with filters[i] and strides[i] (host int32
+ * [n_layers], 1 <= n_layers <= 64).  out is a host array of n_layers
+ * handles, each freed by scn_rulebook_free.  Every layer's first phase is
+ * queued before the call's first wait and every layer's second phase before
+ * its second, so the whole chain waits for the device twice (a network of L
+ * layers built one by one waits 2L times).  The rulebooks equal those of
+ * the layer-by-layer builds.  Errors: as scn_rulebook_build_lattice for any
+ * layer, and SCN_ERR_INVALID for a bad n_layers or a layer whose input grid
+ * would be empty; on an error every out[i] is NULL.
+ */
+scn_status scn_rulebook_build_chain(const int32_t* coords, int64_t n, const int64_t* grid,
+                                   int32_t lattice, int32_t n_layers, const int32_t* filters,
+                                   const int32_t* strides, hipStream_t stream,
+                                   scn_rulebook** out);
+
 /* Sizes and grids of a rulebook (host struct).  SCN_ERR_INVALID on null. */
 scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info);
 

@@ -10,6 +10,7 @@ from ._lib import (  # noqa: F401
     SCN_RELU,
     Rulebook,
     ScnError,
+    build_chain,
     build_rulebook,
     conv_bwd,
     conv_bwd_workspace,

@@ -27,6 +27,7 @@ STATUS = {0: "ok", 1: "invalid", 2: "range", 3: "duplicate", 4: "overflow",
 
 EXPORTED = (
     "scn_rulebook_build", "scn_rulebook_build_lattice", "scn_rulebook_build_next",
+    "scn_rulebook_build_chain",
     "scn_rulebook_get_info", "scn_rulebook_out_coords",
     "scn_rulebook_in_rows", "scn_rulebook_out_rows", "scn_rulebook_offsets",
     "scn_rulebook_export", "scn_rulebook_free", "scn_conv_fwd",
@@ -75,6 +76,7 @@ def lib() -> ctypes.CDLL:
         "scn_rulebook_build": (st, [P, i64, P, i32, i32, P, ctypes.POINTER(P)]),
         "scn_rulebook_build_lattice": (st, [P, i64, P, i32, i32, i32, P, ctypes.POINTER(P)]),
         "scn_rulebook_build_next": (st, [P, i32, i32, P, ctypes.POINTER(P)]),
+        "scn_rulebook_build_chain": (st, [P, i64, P, i32, i32, P, P, P, ctypes.POINTER(P)]),
         "scn_rulebook_get_info": (st, [P, ctypes.POINTER(_Info)]),
         "scn_rulebook_out_coords": (P, [P]),
         "scn_rulebook_in_rows": (P, [P]),
@@ -155,6 +157,15 @@ class Rulebook:
                 LATTICES[lattice], ctypes.c_void_p(_stream()), ctypes.byref(h)),
                 "scn_rulebook_build_lattice")
             device = coords.device
+        self._adopt(h, device)
+
+    @classmethod
+    def _from_handle(cls, h: ctypes.c_void_p, device) -> "Rulebook":
+        rb = cls.__new__(cls)
+        rb._adopt(h, device)
+        return rb
+
+    def _adopt(self, h: ctypes.c_void_p, device) -> None:
         self._h = h
         self.device = device
         info = _Info()
@@ -310,6 +321,27 @@ def version() -> str:
 # a rulebook built under a pair frees its memory through it, also after the
 # pair has been replaced.
 _hooks_kept = []
+
+
+def build_chain(coords: torch.Tensor, grid, layers, lattice: str = "cubic") -> list:
+    """Rulebooks of a chain of layers (``scn_rulebook_build_chain``): layer 0
+    from ``coords`` on ``grid``, each later layer from the previous layer's
+    active outputs; ``layers`` is a sequence of (filter, stride).  The chain
+    waits for the device twice in all."""
+    n = int(coords.shape[0]) if coords.dim() == 2 else -1
+    _dev_tensor(coords, torch.int32, (n, 4), "coords")
+    if lattice not in LATTICES:
+        raise ValueError(f"lattice must be one of {sorted(LATTICES)}, got {lattice!r}")
+    nl = len(layers)
+    g = np.ascontiguousarray(np.asarray(grid, dtype=np.int64).reshape(4))
+    fs = np.ascontiguousarray([int(f) for f, _ in layers], dtype=np.int32)
+    ss = np.ascontiguousarray([int(s) for _, s in layers], dtype=np.int32)
+    hs = (ctypes.c_void_p * max(nl, 1))()
+    _check(lib().scn_rulebook_build_chain(
+        _ptr(coords), n, g.ctypes.data_as(ctypes.c_void_p), LATTICES[lattice], nl,
+        fs.ctypes.data_as(ctypes.c_void_p), ss.ctypes.data_as(ctypes.c_void_p),
+        ctypes.c_void_p(_stream()), hs), "scn_rulebook_build_chain")
+    return [Rulebook._from_handle(ctypes.c_void_p(hs[i]), coords.device) for i in range(nl)]
 
 
 def set_dense_forward(min_rows: int = -1, min_offsets: int = -1) -> None:

@@ -46,6 +46,8 @@
 
 #include <algorithm>
 #include <cstring>
+#include <memory>
+#include <vector>
 
 #include "scan.h"
 #include "scn_internal.h"
@@ -518,12 +520,13 @@ inline unsigned blocks_for(int64_t n, int threads) {
 // allocation and one free (each is a host call of tens of microseconds); a
 // request that does not fit gets a block of its own.
 struct Temps {
-  hipStream_t s;
+  hipStream_t s = nullptr;
   Allocator al;
   void* p[16] = {nullptr};
   int n = 0;
   char* cur = nullptr;
   size_t left = 0;
+  Temps() = default;
   Temps(hipStream_t st, const Allocator& a) : s(st), al(a) {}
   static size_t round(size_t b) { return (std::max<size_t>(b, 1) + 255) & ~size_t(255); }
   scn_status take(void** q, size_t bytes) {
@@ -617,10 +620,409 @@ void with_kernels(int f, int lattice, Fn fn) {
   }
 }
 
+// Host-pinned read-back area of one layer: flags and totals after phase 1,
+// the list boundaries after phase 2.
+struct Readback {
+  uint32_t flags, a_in, a_out, pad;
+  int64_t off[MAX_K + 1];
+};
+constexpr int MAX_CHAIN = 64;  // layers of one scn_rulebook_build_chain call
+
+// One pinned array of read-back slots per host thread, kept for the life of
+// the process.
+scn_status readback_slots(Readback** out) {
+  static thread_local Readback* hb = nullptr;
+  if (!hb) SCN_HIP(hipHostMalloc((void**)&hb, MAX_CHAIN * sizeof(Readback), hipHostMallocDefault));
+  *out = hb;
+  return SCN_OK;
+}
+
+// The event recorded after a build's list-boundary copy (one per host thread
+// and device).
+scn_status copy_event(hipEvent_t* out) {
+  static thread_local hipEvent_t ev[64] = {};
+  int dev = 0;
+  SCN_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) {
+    set_error("scn_rulebook_build: device %d out of range", dev);
+    return SCN_ERR_HIP;
+  }
+  if (!ev[dev]) SCN_HIP(hipEventCreateWithFlags(&ev[dev], hipEventDisableTiming));
+  *out = ev[dev];
+  return SCN_OK;
+}
+
+// The build of one layer, in steps:
+//   check()   host only: arguments, output grid, bitmap sizes;
+//   phase1()  device: mark the caller's sites (first layer only), rank them,
+//             dilate, rank the outputs; queues the copy of the flags and
+//             totals to the layer's read-back slot;
+//   sized()   after the host has waited for that copy: errors, a_out, the
+//             rulebook's storage;
+//   phase2()  device: output sites and masks, per-tile counts, list
+//             boundaries (copied out, then `copied` is recorded), emission,
+//             the mask sort, pooling windows, input tiles;
+//   finish()  after the host has waited for the boundary copy: pair count.
+// A layer built from the previous layer's outputs (`chained`) uses that
+// layer's output rank bitmap (its H_out) as its H_in and skips marking (its
+// sites are valid, distinct and in key order by construction).
+struct LayerBuild {
+  // inputs
+  const int32_t* coords = nullptr;
+  int64_t n = 0;
+  int64_t grid[4] = {0, 0, 0, 0};
+  int32_t f = 0, s = 0, lattice = 0;
+  hipStream_t st = nullptr;
+  bool chained = false;
+  const uint32_t* prev_bits = nullptr;
+  const uint32_t* prev_rank = nullptr;
+  Readback* hb = nullptr;
+  // derived
+  bool planar = false, simplex = false;
+  int K = 0;
+  int64_t go4[4] = {0, 0, 0, 0};
+  int64_t nw_in = 0, nw_out = 0, nsb = 0;
+  GridDev gi{}, go{};
+  Allocator mem;
+  Temps tmp;
+  // the output layer's rank bitmap (H_out) outlives the build: the rulebook
+  // keeps it for a following chained build
+  struct Hout {
+    uint32_t *bits = nullptr, *rank = nullptr;
+    hipStream_t s = nullptr;
+    Allocator al;
+    ~Hout() {
+      if (bits) dfree(bits, s, al);
+    }
+  } hout;
+  uint32_t *inb = nullptr, *ipref = nullptr, *flags = nullptr, *sc32 = nullptr;
+  // after phase 1
+  int64_t a_out = 0, nt = 0, nit = 0, pmax = 0, nfb = 0;
+  bool sorted = true, pool = false, dense = false;
+  int inv_slots = 0;
+  scn_rulebook* rb = nullptr;
+  bool keep = false;
+  uint32_t* masks = nullptr;
+  uint64_t *cnt = nullptr, *sc64 = nullptr;
+  int64_t ncnt = 0;
+  size_t sort_bytes = 0;
+
+  ~LayerBuild() {
+    if (!keep && rb) {
+      dfree(rb->block, st, rb->alloc);      // stream-ordered: after any queued kernel
+      dfree(rb->hout_bits, st, rb->alloc);  // also holds hout_rank
+      if (rb->done) (void)hipEventDestroy(rb->done);
+      delete rb;
+    }
+  }
+
+  scn_status check() {
+    if (n < 0 || (n > 0 && !coords) || f < 1 || s < 1 ||
+        (reinterpret_cast<uintptr_t>(coords) & 15) != 0 || lattice < SCN_LATTICE_CUBIC ||
+        lattice > SCN_LATTICE_TRIANGULAR) {
+      set_error("scn_rulebook_build: invalid argument (n=%lld f=%d s=%d lattice=%d)",
+                (long long)n, f, s, lattice);
+      return SCN_ERR_INVALID;
+    }
+    for (int a = 0; a < 4; ++a)
+      if (grid[a] < 1 || grid[a] > INT32_MAX) {
+        set_error("scn_rulebook_build: grid extent %d is %lld", a, (long long)grid[a]);
+        return SCN_ERR_INVALID;
+      }
+    planar = lattice == SCN_LATTICE_SQUARE || lattice == SCN_LATTICE_TRIANGULAR;
+    simplex = lattice == SCN_LATTICE_TETRAHEDRAL || lattice == SCN_LATTICE_TRIANGULAR;
+    if (planar && grid[3] != 1) {
+      set_error("scn_rulebook_build: a 2D lattice needs mz = 1 (got %lld)", (long long)grid[3]);
+      return SCN_ERR_INVALID;
+    }
+    if (simplex && (grid[2] != grid[1] || (!planar && grid[3] != grid[1]))) {
+      set_error("scn_rulebook_build: a simplex grid has one size (got %lld, %lld, %lld)",
+                (long long)grid[1], (long long)grid[2], (long long)grid[3]);
+      return SCN_ERR_INVALID;
+    }
+    if (f > 3) {
+      set_error("scn_rulebook_build: filter %d > 3 is not supported", f);
+      return SCN_ERR_UNSUPPORTED;
+    }
+    if (n > INT32_MAX) {
+      set_error("scn_rulebook_build: %lld sites exceed INT32_MAX", (long long)n);
+      return SCN_ERR_OVERFLOW;
+    }
+    with_kernels(f, lattice, [&](auto k) { K = decltype(k)::K; });
+    // the window's extent is f on every axis, except 1 along z on a 2D lattice
+    go4[0] = grid[0];
+    for (int a = 1; a < 4; ++a) {
+      const int fa = (a == 3 && planar) ? 1 : f;
+      go4[a] = grid[a] >= fa ? (grid[a] - fa) / s + 1 : 0;
+    }
+    // bitmap words of each grid; bound them (2^26 words = 2^31 sites each)
+    const int64_t rw_in = ceil_div(grid[1], 32),
+                  rw_out = ceil_div(std::max<int64_t>(go4[1], 1), 32);
+    const double nwi_d = (double)grid[0] * grid[3] * grid[2] * rw_in;
+    const double nwo_d = (double)go4[0] * go4[3] * go4[2] * rw_out;
+    const double LIMW = (double)(int64_t(1) << 26);
+    if (nwi_d > LIMW || nwo_d > LIMW) {
+      set_error("scn_rulebook_build: grid too large for the occupancy bitmap (%.3g / %.3g words)",
+                nwi_d, nwo_d);
+      return SCN_ERR_UNSUPPORTED;
+    }
+    nw_in = (int64_t)nwi_d;
+    nw_out = (int64_t)nwo_d;
+    gi = GridDev{(int32_t)grid[0], (int32_t)grid[1], (int32_t)grid[2], (int32_t)grid[3],
+                 (int32_t)rw_in, simplex ? 1 : 0};
+    go = GridDev{(int32_t)go4[0], (int32_t)std::max<int64_t>(go4[1], 0), (int32_t)go4[2],
+                 (int32_t)go4[3], (int32_t)rw_out, simplex ? 1 : 0};
+    return SCN_OK;
+  }
+
+  scn_status phase1() {
+    mem = current_allocator();  // every array of this build comes from it
+    tmp.s = st;
+    tmp.al = mem;
+    hout.s = st;
+    hout.al = mem;
+    scn_status rc;
+    nsb = std::max(scan_blocks(nw_in), scan_blocks(nw_out));
+    // bits and their prefix in one block (freed through its start, bits)
+    const size_t hbits_bytes = Temps::round((size_t)std::max<int64_t>(nw_out, 1) * 4);
+    if ((rc = dalloc((void**)&hout.bits, hbits_bytes + Temps::round((nw_out + 1) * 4), st, mem)))
+      return rc;
+    hout.rank = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(hout.bits) + hbits_bytes);
+    if ((rc = tmp.reserve((chained ? 0 : Temps::round(nw_in * 4) + Temps::round((nw_in + 1) * 4)) +
+                          Temps::round(16) + Temps::round(nsb * 4))))
+      return rc;
+    if (chained) {
+      inb = const_cast<uint32_t*>(prev_bits);
+      ipref = const_cast<uint32_t*>(prev_rank);
+    } else {
+      if ((rc = tmp.get(&inb, nw_in)) || (rc = tmp.get(&ipref, nw_in + 1))) return rc;
+      SCN_HIP(hipMemsetAsync(inb, 0, std::max<int64_t>(nw_in, 1) * 4, st));
+    }
+    if ((rc = tmp.get(&flags, 4)) || (rc = tmp.get(&sc32, nsb))) return rc;
+    SCN_HIP(hipMemsetAsync(flags, 0, 16, st));
+    std::memset(hb, 0, sizeof(Readback));
+    // phases 1-5 (1-2 only for the caller's sites)
+    if (!chained) {
+      if (n > 0) {
+        hipLaunchKernelGGL(mark_inputs_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords,
+                           n, gi, inb, flags);
+        SCN_LAUNCH_CHECK();
+      }
+      if ((rc = exclusive_scan<uint32_t>(PopcountLoad{inb}, nw_in, ipref, ipref + nw_in, sc32,
+                                         st)))
+        return rc;
+    }
+    {
+      const int sm = s == 1 ? 1 : (s == 2 ? 2 : 0);
+      with_kernels(f, lattice, [&](auto k) {
+        k.dilate(sm, dim3(blocks_for(nw_out, 256)), st, inb, gi, hout.bits, go, (int)nw_out, s);
+      });
+      SCN_LAUNCH_CHECK();
+    }
+    if ((rc = exclusive_scan<uint32_t>(PopcountLoad{hout.bits}, nw_out, hout.rank,
+                                       hout.rank + nw_out, sc32, st)))
+      return rc;
+    // flags and both totals in one read-back
+    hipLaunchKernelGGL(pack_totals_kernel, dim3(1), dim3(1), 0, st, flags, ipref + nw_in,
+                       hout.rank + nw_out);
+    SCN_LAUNCH_CHECK();
+    SCN_HIP(hipMemcpyAsync(&hb->flags, flags, 12, hipMemcpyDeviceToHost, st));
+    return SCN_OK;
+  }
+
+  scn_status sized() {
+    scn_status rc;
+    if (hb->flags & F_RANGE) {
+      set_error("scn_rulebook_build: a site lies outside the grid (%lld,%lld,%lld,%lld)",
+                (long long)grid[0], (long long)grid[1], (long long)grid[2], (long long)grid[3]);
+      return SCN_ERR_RANGE;
+    }
+    if ((hb->flags & F_DUP) || (int64_t)hb->a_in != n) {
+      set_error("scn_rulebook_build: duplicate site in the input list");
+      return SCN_ERR_DUPLICATE;
+    }
+    a_out = hb->a_out;
+    sorted = !(hb->flags & F_UNSORTED);
+    // pooling tables (window rows per output, windows per input) for stride >= 2
+    pool = s >= 2;
+    inv_slots = pool ? (f > s ? 8 : 1) : 0;
+    nt = std::max<int64_t>(1, ceil_div(a_out, TILE));
+    nit = std::max<int64_t>(1, ceil_div(n, TILE));
+    pmax = std::min<int64_t>(n, a_out) * K;
+    if (pool && a_out * K > INT32_MAX) {
+      set_error("scn_rulebook_build: %lld pooling windows exceed the supported count",
+                (long long)a_out);
+      return SCN_ERR_OVERFLOW;
+    }
+    // persistent rulebook storage in one block
+    auto al = [](int64_t bytes) { return (bytes + 255) & ~int64_t(255); };
+    const int64_t sz_oc = al(a_out * 16), sz_pair = al(pmax * 4), sz_perm = al(n * 4),
+                  sz_off = al((K + 1) * 8), sz_ot = al((K * nt + 1) * 8),
+                  sz_it = al((K * nit + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
+                  sz_inv = pool ? al(n * 4 * inv_slots) : 0;
+    // dense forward view for large stride-1 rulebooks (see scn_rulebook)
+    dense = s == 1 && dense_forward_for(a_out, K);
+    nfb = dense ? ceil_div(a_out, DENSE_ROWS) : 0;
+    const int64_t sz_fnb = al((pmax + 1) * 4), sz_fnboff = al((a_out + 1) * 4),
+                  sz_fperm = al(a_out * 4), sz_fmask = al(a_out * 4);
+    const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair + sz_perm) + sz_off +
+                          sz_ot + sz_it + sz_nbr + sz_inv +
+                          (dense ? sz_fnb + sz_fnboff + sz_fperm + sz_fmask : 0);
+    rb = new scn_rulebook();
+    rb->alloc = mem;
+    rb->stream = st;
+    if ((rc = dalloc(&rb->block, (size_t)total, st, mem))) return rc;
+    char* cur = static_cast<char*>(rb->block);
+    auto take = [&](int64_t bytes) {
+      char* p = bytes ? cur : nullptr;
+      cur += bytes;
+      return p;
+    };
+    rb->out_coords = (int32_t*)take(sz_oc);
+    rb->in_rows = (int32_t*)take(sz_pair);
+    rb->out_rows = (int32_t*)take(sz_pair);
+    rb->in_rank = sorted ? rb->in_rows : (int32_t*)take(sz_pair);
+    rb->perm = sorted ? nullptr : (int32_t*)take(sz_perm);  // identity when sorted
+    rb->off_dev = (int64_t*)take(sz_off);
+    rb->otile = (int64_t*)take(sz_ot);
+    rb->itile = (int64_t*)take(sz_it);
+    rb->nbr = pool ? (int32_t*)take(sz_nbr) : nullptr;
+    rb->inv = pool ? (int32_t*)take(sz_inv) : nullptr;
+    rb->inv_slots = inv_slots;
+    rb->n_fblocks = nfb;
+    rb->fnb = dense ? (int32_t*)take(sz_fnb) : nullptr;
+    rb->fnb_off = dense ? (uint32_t*)take(sz_fnboff) : nullptr;
+    rb->fperm = dense ? (int32_t*)take(sz_fperm) : nullptr;
+    rb->fmask = dense ? (uint32_t*)take(sz_fmask) : nullptr;
+    rb->f = f;
+    rb->s = s;
+    rb->K = K;
+    rb->lattice = lattice;
+    rb->hout_bits = hout.bits;
+    rb->hout_rank = hout.rank;
+    rb->hout_words = nw_out;
+    hout.bits = hout.rank = nullptr;  // owned by rb from here (freed with it)
+    for (int a = 0; a < 4; ++a) {
+      rb->gin[a] = grid[a];
+      rb->gout[a] = go4[a];
+    }
+    rb->a_in = n;
+    rb->a_out = a_out;
+    rb->input_sorted = sorted ? 1 : 0;
+    rb->n_otiles = nt;
+    rb->n_itiles = nit;
+
+    ncnt = K * nt;
+    // the mask sort's scratch size (a query; no device work)
+    if (dense)
+      SCN_HIP(hipcub::DeviceRadixSort::SortPairs(nullptr, sort_bytes, (uint32_t*)nullptr,
+                                                 (uint32_t*)nullptr, (int32_t*)nullptr,
+                                                 (int32_t*)nullptr, (int)a_out, 0, K, st));
+    if ((rc = tmp.reserve(Temps::round(a_out * 4) + Temps::round(ncnt * 8) +
+                          Temps::round(scan_blocks(ncnt) * 8) +
+                          (dense ? Temps::round(scan_blocks(a_out) * 4) +
+                                       Temps::round(a_out * 4) + Temps::round(sort_bytes)
+                                 : 0))))
+      return rc;
+    if ((rc = tmp.get(&masks, a_out)) || (rc = tmp.get(&cnt, ncnt)) ||
+        (rc = tmp.get(&sc64, scan_blocks(ncnt))))
+      return rc;
+    return SCN_OK;
+  }
+
+  scn_status phase2(hipEvent_t copied) {
+    scn_status rc;
+    const uint32_t* outb = rb->hout_bits;
+    const uint32_t* opref = rb->hout_rank;
+    if (n > 0 && !sorted) {
+      hipLaunchKernelGGL(perm_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n, gi,
+                         inb, ipref, rb->perm);
+      SCN_LAUNCH_CHECK();
+    }
+    if (a_out > 0) {
+      with_kernels(f, lattice, [&](auto k) {
+        k.out_sites(s == 1, dim3(blocks_for(nw_out, 256)), st, (const uint32_t*)inb, gi, outb,
+                    opref, go, (int)nw_out, s, rb->out_coords, masks);
+      });
+      SCN_LAUNCH_CHECK();
+    }
+    with_kernels(f, lattice, [&](auto k) {
+      k.tile_count(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks, a_out, nt, cnt);
+    });
+    SCN_LAUNCH_CHECK();
+    // positions: otile[k*nt + t] = off[k] + pairs of list k in tiles < t
+    if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, ncnt, (uint64_t*)rb->otile,
+                                       (uint64_t*)rb->otile + ncnt, sc64, st)))
+      return rc;
+    hipLaunchKernelGGL(list_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)rb->otile,
+                       nt, K, rb->off_dev);
+    SCN_LAUNCH_CHECK();
+    // From here the host needs only the list boundaries: copy them now and
+    // queue the rest of the build behind the copy, so the GPU keeps working
+    // while the caller waits for the copy alone.
+    SCN_HIP(hipMemcpyAsync(hb->off, rb->off_dev, (K + 1) * 8, hipMemcpyDeviceToHost, st));
+    SCN_HIP(hipEventRecord(copied, st));
+    if (dense) {
+      // start of each output's neighbour list: exclusive sum of mask popcounts
+      uint32_t* sc_nb = nullptr;
+      if ((rc = tmp.get(&sc_nb, scan_blocks(a_out))) ||
+          (rc = exclusive_scan<uint32_t>(PopcountLoad{masks}, a_out, rb->fnb_off,
+                                         rb->fnb_off + a_out, sc_nb, st)))
+        return rc;
+    }
+    if (a_out > 0) {
+      with_kernels(f, lattice, [&](auto k) {
+        k.emit(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks,
+               (const int32_t*)rb->out_coords, a_out, nt, s, (const uint32_t*)inb,
+               (const uint32_t*)ipref, gi, (const int32_t*)rb->perm, (const uint64_t*)rb->otile,
+               rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr,
+               (const uint32_t*)rb->fnb_off, rb->fnb);
+      });
+      SCN_LAUNCH_CHECK();
+    }
+    if (dense) {
+      // the output rows sorted by neighbour mask (a stable radix sort)
+      int32_t* iota = nullptr;
+      char* sort_tmp = nullptr;
+      if ((rc = tmp.get(&iota, a_out)) || (rc = tmp.get(&sort_tmp, sort_bytes))) return rc;
+      hipLaunchKernelGGL(iota_kernel, dim3(blocks_for(a_out, 256)), dim3(256), 0, st, iota,
+                         a_out);
+      SCN_LAUNCH_CHECK();
+      SCN_HIP(hipcub::DeviceRadixSort::SortPairs(sort_tmp, sort_bytes, masks, rb->fmask, iota,
+                                                 rb->fperm, (int)a_out, 0, K, st));
+    }
+    if (pool && n > 0) {
+      with_kernels(f, lattice, [&](auto k) {
+        k.inv_windows(inv_slots, dim3(blocks_for(n, 256)), st, coords, n, s, go, outb, opref,
+                      rb->inv);
+      });
+      SCN_LAUNCH_CHECK();
+    }
+    hipLaunchKernelGGL(in_tiles_kernel, dim3(blocks_for(K * nit + 1, 256)), dim3(256), 0, st,
+                       rb->in_rank, rb->off_dev, K, nit, rb->itile);
+    SCN_LAUNCH_CHECK();
+    SCN_HIP(hipEventCreateWithFlags(&rb->done, hipEventDisableTiming));
+    SCN_HIP(hipEventRecord(rb->done, st));
+    return SCN_OK;
+  }
+
+  scn_status finish(scn_rulebook** out) {
+    rb->n_pairs = hb->off[K];
+    if (rb->n_pairs > INT32_MAX || rb->n_pairs > pmax) {
+      set_error("scn_rulebook_build: %lld pairs exceed the supported count",
+                (long long)rb->n_pairs);
+      return SCN_ERR_OVERFLOW;
+    }
+    for (int k = 0; k <= K; ++k) rb->off_host[k] = hb->off[k];
+    keep = true;
+    *out = rb;
+    return SCN_OK;
+  }
+};
+
 // Builds from the caller's sites, or (prev != null) from the active output
 // sites of prev: then coords/n/grid/lattice are prev's output layer, whose
-// rank bitmap (prev's H_out) serves as this build's H_in, so phases 1-3 are
-// skipped (the sites are valid, distinct and in key order by construction).
+// rank bitmap (prev's H_out) serves as this build's H_in.
 scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f, int32_t s,
                  int32_t lattice, hipStream_t st, scn_rulebook** out,
                  const scn_rulebook* prev = nullptr) {
@@ -629,335 +1031,97 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     return SCN_ERR_INVALID;
   }
   *out = nullptr;
-  if (!grid || n < 0 || (n > 0 && !coords) || f < 1 || s < 1 ||
-      (reinterpret_cast<uintptr_t>(coords) & 15) != 0 ||
-      lattice < SCN_LATTICE_CUBIC || lattice > SCN_LATTICE_TRIANGULAR) {
-    set_error("scn_rulebook_build: invalid argument (n=%lld f=%d s=%d lattice=%d)", (long long)n,
-              f, s, lattice);
+  if (!grid) {
+    set_error("scn_rulebook_build: grid is NULL");
     return SCN_ERR_INVALID;
   }
-  for (int a = 0; a < 4; ++a)
-    if (grid[a] < 1 || grid[a] > INT32_MAX) {
-      set_error("scn_rulebook_build: grid extent %d is %lld", a, (long long)grid[a]);
-      return SCN_ERR_INVALID;
-    }
-  const bool planar = lattice == SCN_LATTICE_SQUARE || lattice == SCN_LATTICE_TRIANGULAR;
-  const bool simplex = lattice == SCN_LATTICE_TETRAHEDRAL || lattice == SCN_LATTICE_TRIANGULAR;
-  if (planar && grid[3] != 1) {
-    set_error("scn_rulebook_build: a 2D lattice needs mz = 1 (got %lld)", (long long)grid[3]);
-    return SCN_ERR_INVALID;
-  }
-  if (simplex && (grid[2] != grid[1] || (!planar && grid[3] != grid[1]))) {
-    set_error("scn_rulebook_build: a simplex grid has one size (got %lld, %lld, %lld)",
-              (long long)grid[1], (long long)grid[2], (long long)grid[3]);
-    return SCN_ERR_INVALID;
-  }
-  if (f > 3) {
-    set_error("scn_rulebook_build: filter %d > 3 is not supported", f);
-    return SCN_ERR_UNSUPPORTED;
-  }
-  if (n > INT32_MAX) {
-    set_error("scn_rulebook_build: %lld sites exceed INT32_MAX", (long long)n);
-    return SCN_ERR_OVERFLOW;
-  }
-  int K = 0;
-  with_kernels(f, lattice, [&](auto k) { K = decltype(k)::K; });
-  // the window's extent is f on every axis, except 1 along z on a 2D lattice
-  int64_t go4[4] = {grid[0], 0, 0, 0};
-  for (int a = 1; a < 4; ++a) {
-    const int fa = (a == 3 && planar) ? 1 : f;
-    go4[a] = grid[a] >= fa ? (grid[a] - fa) / s + 1 : 0;
-  }
-  // bitmap words of each grid; bound them (2^26 words = 2^31 sites each)
-  const int64_t rw_in = ceil_div(grid[1], 32), rw_out = ceil_div(std::max<int64_t>(go4[1], 1), 32);
-  const double nwi_d = (double)grid[0] * grid[3] * grid[2] * rw_in;
-  const double nwo_d = (double)go4[0] * go4[3] * go4[2] * rw_out;
-  const double LIMW = (double)(int64_t(1) << 26);
-  if (nwi_d > LIMW || nwo_d > LIMW) {
-    set_error("scn_rulebook_build: grid too large for the occupancy bitmap (%.3g / %.3g words)",
-              nwi_d, nwo_d);
-    return SCN_ERR_UNSUPPORTED;
-  }
-  const int64_t nw_in = (int64_t)nwi_d, nw_out = (int64_t)nwo_d;
-  GridDev gi{(int32_t)grid[0], (int32_t)grid[1], (int32_t)grid[2], (int32_t)grid[3],
-             (int32_t)rw_in, simplex ? 1 : 0};
-  GridDev go{(int32_t)go4[0], (int32_t)std::max<int64_t>(go4[1], 0), (int32_t)go4[2],
-             (int32_t)go4[3], (int32_t)rw_out, simplex ? 1 : 0};
-
-  const Allocator mem = current_allocator();  // every array of this build comes from it
-  Temps tmp(st, mem);
-  scn_status rc;
-  uint32_t *inb, *ipref, *flags;
-  uint32_t* sc32;  // scan block sums
-  const int64_t nsb = std::max(scan_blocks(nw_in), scan_blocks(nw_out));
-  // the output layer's rank bitmap (H_out) outlives the build: the rulebook
-  // keeps it for a following build_next
-  struct Hout {
-    uint32_t *bits = nullptr, *rank = nullptr;
-    hipStream_t s;
-    Allocator al;
-    ~Hout() {
-      if (bits) dfree(bits, s, al);
-    }
-  } hout;
-  hout.s = st;
-  hout.al = mem;
-  // bits and their prefix in one block (freed through its start, bits)
-  const size_t hbits_bytes = Temps::round((size_t)std::max<int64_t>(nw_out, 1) * 4);
-  if ((rc = dalloc((void**)&hout.bits, hbits_bytes + Temps::round((nw_out + 1) * 4), st, mem)))
-    return rc;
-  hout.rank = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(hout.bits) + hbits_bytes);
-  uint32_t* const outb = hout.bits;
-  uint32_t* const opref = hout.rank;
-  if ((rc = tmp.reserve((prev ? 0 : Temps::round(nw_in * 4) + Temps::round((nw_in + 1) * 4)) +
-                         Temps::round(16) + Temps::round(nsb * 4))))
-    return rc;
+  LayerBuild L;
+  L.coords = coords;
+  L.n = n;
+  for (int a = 0; a < 4; ++a) L.grid[a] = grid[a];
+  L.f = f;
+  L.s = s;
+  L.lattice = lattice;
+  L.st = st;
   if (prev) {
-    inb = prev->hout_bits;
-    ipref = prev->hout_rank;
-  } else {
-    if ((rc = tmp.get(&inb, nw_in)) || (rc = tmp.get(&ipref, nw_in + 1))) return rc;
-    SCN_HIP(hipMemsetAsync(inb, 0, std::max<int64_t>(nw_in, 1) * 4, st));
+    L.chained = true;
+    L.prev_bits = prev->hout_bits;
+    L.prev_rank = prev->hout_rank;
   }
-  if ((rc = tmp.get(&flags, 4)) || (rc = tmp.get(&sc32, nsb))) return rc;
-  SCN_HIP(hipMemsetAsync(flags, 0, 16, st));
-
-  // host-pinned readback area
-  struct Readback {
-    uint32_t flags, a_in, a_out, pad;
-    int64_t off[MAX_K + 1];
-  };
-  // one pinned readback area per host thread, kept for the life of the process
-  static thread_local Readback* hb = nullptr;
-  if (!hb) SCN_HIP(hipHostMalloc((void**)&hb, sizeof(Readback), hipHostMallocDefault));
-  std::memset(hb, 0, sizeof(Readback));
-
-  // phases 1-5 (1-2 only for the caller's sites)
-  if (!prev) {
-    if (n > 0) {
-      hipLaunchKernelGGL(mark_inputs_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords,
-                         n, gi, inb, flags);
-      SCN_LAUNCH_CHECK();
-    }
-    if ((rc = exclusive_scan<uint32_t>(PopcountLoad{inb}, nw_in, ipref, ipref + nw_in, sc32, st)))
-      return rc;
-  }
-  {
-    const int sm = s == 1 ? 1 : (s == 2 ? 2 : 0);
-    with_kernels(f, lattice, [&](auto k) {
-      k.dilate(sm, dim3(blocks_for(nw_out, 256)), st, inb, gi, outb, go, (int)nw_out, s);
-    });
-    SCN_LAUNCH_CHECK();
-  }
-  if ((rc = exclusive_scan<uint32_t>(PopcountLoad{outb}, nw_out, opref, opref + nw_out, sc32,
-                                     st)))
+  scn_status rc;
+  hipEvent_t copied = nullptr;
+  if ((rc = readback_slots(&L.hb)) || (rc = copy_event(&copied)) || (rc = L.check()) ||
+      (rc = L.phase1()))
     return rc;
-  // flags and both totals in one read-back
-  hipLaunchKernelGGL(pack_totals_kernel, dim3(1), dim3(1), 0, st, flags, ipref + nw_in,
-                     opref + nw_out);
-  SCN_LAUNCH_CHECK();
-  SCN_HIP(hipMemcpyAsync(&hb->flags, flags, 12, hipMemcpyDeviceToHost, st));
   SCN_HIP(hipStreamSynchronize(st));
-  if (hb->flags & F_RANGE) {
-    set_error("scn_rulebook_build: a site lies outside the grid (%lld,%lld,%lld,%lld)",
-              (long long)grid[0], (long long)grid[1], (long long)grid[2], (long long)grid[3]);
-    return SCN_ERR_RANGE;
-  }
-  if ((hb->flags & F_DUP) || (int64_t)hb->a_in != n) {
-    set_error("scn_rulebook_build: duplicate site in the input list");
-    return SCN_ERR_DUPLICATE;
-  }
-  const int64_t a_out = hb->a_out;
-  const bool sorted = !(hb->flags & F_UNSORTED);
-  // pooling tables (window rows per output, windows per input) for stride >= 2
-  const bool pool = s >= 2;
-  const int inv_slots = pool ? (f > s ? 8 : 1) : 0;
-  const int64_t nt = std::max<int64_t>(1, ceil_div(a_out, TILE));
-  const int64_t nit = std::max<int64_t>(1, ceil_div(n, TILE));
-  const int64_t pmax = std::min<int64_t>(n, a_out) * K;
-  if (pool && a_out * K > INT32_MAX) {
-    set_error("scn_rulebook_build: %lld pooling windows exceed the supported count",
-              (long long)a_out);
-    return SCN_ERR_OVERFLOW;
-  }
+  if ((rc = L.sized()) || (rc = L.phase2(copied))) return rc;
+  SCN_HIP(hipEventSynchronize(copied));
+  return L.finish(out);
+}
 
-  // persistent rulebook storage in one block
-  auto al = [](int64_t bytes) { return (bytes + 255) & ~int64_t(255); };
-  const int64_t sz_oc = al(a_out * 16), sz_pair = al(pmax * 4), sz_perm = al(n * 4),
-                sz_off = al((K + 1) * 8), sz_ot = al((K * nt + 1) * 8),
-                sz_it = al((K * nit + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
-                sz_inv = pool ? al(n * 4 * inv_slots) : 0;
-  // dense forward table for stride-1 rulebooks (see scn_rulebook)
-  const bool dense = s == 1 && dense_forward_for(a_out, K);
-  const int64_t nfb = dense ? ceil_div(a_out, DENSE_ROWS) : 0;
-  const int64_t sz_fnb = al((pmax + 1) * 4), sz_fnboff = al((a_out + 1) * 4),
-                sz_fperm = al(a_out * 4), sz_fmask = al(a_out * 4);
-  const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair + sz_perm) + sz_off + sz_ot +
-                        sz_it + sz_nbr + sz_inv +
-                        (dense ? sz_fnb + sz_fnboff + sz_fperm + sz_fmask : 0);
-  scn_rulebook* rb = new scn_rulebook();
-  rb->alloc = mem;
-  struct Guard {
-    scn_rulebook* rb;
-    hipStream_t s;
-    bool keep = false;
-    ~Guard() {
-      if (!keep && rb) {
-        dfree(rb->block, s, rb->alloc);  // stream-ordered: after any queued kernel
-        dfree(rb->hout_bits, s, rb->alloc);  // also holds hout_rank
-        if (rb->done) (void)hipEventDestroy(rb->done);
-        delete rb;
+// Layers 0 .. nl-1: layer 0 from the caller's sites, layer i from the active
+// outputs of layer i-1.  Phase 1 of every layer is queued before the host's
+// first wait, and phase 2 of every layer before its second, so the chain
+// waits twice in all.  On an error no rulebook is returned.
+scn_status build_chain(const int32_t* coords, int64_t n, const int64_t* grid, int32_t lattice,
+                       int32_t nl, const int32_t* filters, const int32_t* strides,
+                       hipStream_t st, scn_rulebook** out) {
+  if (!out || !grid || !filters || !strides || nl < 1 || nl > MAX_CHAIN) {
+    set_error("scn_rulebook_build_chain: invalid argument (%d layers, at most %d)", nl,
+              MAX_CHAIN);
+    return SCN_ERR_INVALID;
+  }
+  for (int i = 0; i < nl; ++i) out[i] = nullptr;
+  std::vector<std::unique_ptr<LayerBuild>> Ls;
+  Readback* hb = nullptr;
+  hipEvent_t copied = nullptr;
+  scn_status rc;
+  if ((rc = readback_slots(&hb)) || (rc = copy_event(&copied))) return rc;
+  for (int i = 0; i < nl; ++i) {
+    Ls.emplace_back(new LayerBuild());
+    LayerBuild& L = *Ls.back();
+    L.f = filters[i];
+    L.s = strides[i];
+    L.lattice = lattice;
+    L.st = st;
+    L.hb = hb + i;
+    if (i == 0) {
+      L.coords = coords;
+      L.n = n;
+      for (int a = 0; a < 4; ++a) L.grid[a] = grid[a];
+    } else {
+      const LayerBuild& P = *Ls[i - 1];
+      for (int a = 0; a < 4; ++a) {
+        if (a > 0 && P.go4[a] < 1) {
+          set_error("scn_rulebook_build_chain: layer %d's output grid is empty", i - 1);
+          return SCN_ERR_INVALID;
+        }
+        L.grid[a] = P.go4[a];
       }
+      L.chained = true;
+      L.prev_bits = P.hout.bits;
+      L.prev_rank = P.hout.rank;
     }
-  } guard{rb, st};
-  if ((rc = dalloc(&rb->block, (size_t)total, st, mem))) return rc;
-  char* cur = static_cast<char*>(rb->block);
-  auto take = [&](int64_t bytes) {
-    char* p = bytes ? cur : nullptr;
-    cur += bytes;
-    return p;
-  };
-  rb->out_coords = (int32_t*)take(sz_oc);
-  rb->in_rows = (int32_t*)take(sz_pair);
-  rb->out_rows = (int32_t*)take(sz_pair);
-  rb->in_rank = sorted ? rb->in_rows : (int32_t*)take(sz_pair);
-  rb->perm = sorted ? nullptr : (int32_t*)take(sz_perm);  // identity when sorted
-  rb->off_dev = (int64_t*)take(sz_off);
-  rb->otile = (int64_t*)take(sz_ot);
-  rb->itile = (int64_t*)take(sz_it);
-  rb->nbr = pool ? (int32_t*)take(sz_nbr) : nullptr;
-  rb->inv = pool ? (int32_t*)take(sz_inv) : nullptr;
-  rb->inv_slots = inv_slots;
-  rb->n_fblocks = nfb;
-  rb->fnb = dense ? (int32_t*)take(sz_fnb) : nullptr;
-  rb->fnb_off = dense ? (uint32_t*)take(sz_fnboff) : nullptr;
-  rb->fperm = dense ? (int32_t*)take(sz_fperm) : nullptr;
-  rb->fmask = dense ? (uint32_t*)take(sz_fmask) : nullptr;
-  rb->f = f;
-  rb->s = s;
-  rb->K = K;
-  rb->lattice = lattice;
-  rb->hout_bits = hout.bits;
-  rb->hout_rank = hout.rank;
-  rb->hout_words = nw_out;
-  hout.bits = hout.rank = nullptr;  // owned by rb from here (freed with it)
-  for (int a = 0; a < 4; ++a) {
-    rb->gin[a] = grid[a];
-    rb->gout[a] = go4[a];
+    if ((rc = L.check()) || (rc = L.phase1())) return rc;
   }
-  rb->a_in = n;
-  rb->a_out = a_out;
-  rb->input_sorted = sorted ? 1 : 0;
-  rb->stream = st;
-  rb->n_otiles = nt;
-  rb->n_itiles = nit;
-
-  uint32_t* masks;
-  uint64_t *cnt, *sc64;
-  const int64_t ncnt = K * nt;
-  // the mask sort's scratch size (a query; no device work)
-  size_t sort_bytes = 0;
-  if (dense)
-    SCN_HIP(hipcub::DeviceRadixSort::SortPairs(nullptr, sort_bytes, (uint32_t*)nullptr,
-                                               (uint32_t*)nullptr, (int32_t*)nullptr,
-                                               (int32_t*)nullptr, (int)a_out, 0, K, st));
-  if ((rc = tmp.reserve(Temps::round(a_out * 4) + Temps::round(ncnt * 8) +
-                        Temps::round(scan_blocks(ncnt) * 8) +
-                        (dense ? Temps::round(scan_blocks(a_out) * 4) +
-                                     Temps::round(a_out * 4) + Temps::round(sort_bytes)
-                               : 0))))
-    return rc;
-  if ((rc = tmp.get(&masks, a_out)) || (rc = tmp.get(&cnt, ncnt)) ||
-      (rc = tmp.get(&sc64, scan_blocks(ncnt))))
-    return rc;
-
-  if (n > 0 && !sorted) {
-    hipLaunchKernelGGL(perm_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n, gi,
-                       inb, ipref, rb->perm);
-    SCN_LAUNCH_CHECK();
+  SCN_HIP(hipStreamSynchronize(st));
+  for (int i = 0; i < nl; ++i) {
+    LayerBuild& L = *Ls[i];
+    if (i > 0) {
+      // this layer's sites: the previous layer's outputs
+      L.n = Ls[i - 1]->a_out;
+      L.coords = Ls[i - 1]->rb->out_coords;
+    }
+    if ((rc = L.sized()) || (rc = L.phase2(copied))) return rc;
   }
-  if (a_out > 0) {
-    with_kernels(f, lattice, [&](auto k) {
-      k.out_sites(s == 1, dim3(blocks_for(nw_out, 256)), st, (const uint32_t*)inb, gi,
-                  (const uint32_t*)outb, (const uint32_t*)opref, go, (int)nw_out, s,
-                  rb->out_coords, masks);
-    });
-    SCN_LAUNCH_CHECK();
-  }
-  with_kernels(f, lattice, [&](auto k) {
-    k.tile_count(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks, a_out, nt, cnt);
-  });
-  SCN_LAUNCH_CHECK();
-  // positions: otile[k*nt + t] = off[k] + pairs of list k in tiles < t
-  if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, ncnt, (uint64_t*)rb->otile,
-                                     (uint64_t*)rb->otile + ncnt, sc64, st)))
-    return rc;
-  hipLaunchKernelGGL(list_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)rb->otile,
-                     nt, K, rb->off_dev);
-  SCN_LAUNCH_CHECK();
-  // From here the host needs only the list boundaries: copy them now, queue
-  // the rest of the build behind the copy, and wait for the copy alone, so
-  // the GPU keeps working while the caller goes on.  One event per host
-  // thread and device marks the copy.
-  SCN_HIP(hipMemcpyAsync(hb->off, rb->off_dev, (K + 1) * 8, hipMemcpyDeviceToHost, st));
-  static thread_local hipEvent_t copied[64] = {};
-  int dev = 0;
-  SCN_HIP(hipGetDevice(&dev));
-  if (dev < 0 || dev >= 64) {
-    set_error("scn_rulebook_build: device %d out of range", dev);
-    return SCN_ERR_HIP;
-  }
-  if (!copied[dev]) SCN_HIP(hipEventCreateWithFlags(&copied[dev], hipEventDisableTiming));
-  SCN_HIP(hipEventRecord(copied[dev], st));
-  if (dense) {
-    // start of each output's neighbour list: exclusive sum of mask popcounts
-    uint32_t* sc_nb = nullptr;
-    if ((rc = tmp.get(&sc_nb, scan_blocks(a_out))) ||
-        (rc = exclusive_scan<uint32_t>(PopcountLoad{masks}, a_out, rb->fnb_off,
-                                       rb->fnb_off + a_out, sc_nb, st)))
+  SCN_HIP(hipEventSynchronize(copied));  // the last layer's copy, so every layer's
+  std::vector<scn_rulebook*> res(nl, nullptr);
+  for (int i = 0; i < nl; ++i)
+    if ((rc = Ls[i]->finish(&res[i]))) {
+      for (int j = 0; j < i; ++j) Ls[j]->keep = false;  // freed with their builders
       return rc;
-  }
-  if (a_out > 0) {
-    with_kernels(f, lattice, [&](auto k) {
-      k.emit(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks,
-             (const int32_t*)rb->out_coords, a_out, nt, s, (const uint32_t*)inb,
-             (const uint32_t*)ipref, gi, (const int32_t*)rb->perm, (const uint64_t*)rb->otile,
-             rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr,
-             (const uint32_t*)rb->fnb_off, rb->fnb);
-    });
-    SCN_LAUNCH_CHECK();
-  }
-  if (dense) {
-    // the output rows sorted by neighbour mask (a stable radix sort)
-    int32_t* iota = nullptr;
-    char* sort_tmp = nullptr;
-    if ((rc = tmp.get(&iota, a_out)) || (rc = tmp.get(&sort_tmp, sort_bytes))) return rc;
-    hipLaunchKernelGGL(iota_kernel, dim3(blocks_for(a_out, 256)), dim3(256), 0, st, iota, a_out);
-    SCN_LAUNCH_CHECK();
-    SCN_HIP(hipcub::DeviceRadixSort::SortPairs(sort_tmp, sort_bytes, masks, rb->fmask, iota,
-                                               rb->fperm, (int)a_out, 0, K, st));
-  }
-  if (pool && n > 0) {
-    with_kernels(f, lattice, [&](auto k) {
-      k.inv_windows(inv_slots, dim3(blocks_for(n, 256)), st, coords, n, s, go,
-                    (const uint32_t*)outb, (const uint32_t*)opref, rb->inv);
-    });
-    SCN_LAUNCH_CHECK();
-  }
-  hipLaunchKernelGGL(in_tiles_kernel, dim3(blocks_for(K * nit + 1, 256)), dim3(256), 0, st,
-                     rb->in_rank, rb->off_dev, K, nit, rb->itile);
-  SCN_LAUNCH_CHECK();
-  SCN_HIP(hipEventCreateWithFlags(&rb->done, hipEventDisableTiming));
-  SCN_HIP(hipEventRecord(rb->done, st));
-  SCN_HIP(hipEventSynchronize(copied[dev]));
-  rb->n_pairs = hb->off[K];
-  if (rb->n_pairs > INT32_MAX || rb->n_pairs > pmax) {
-    set_error("scn_rulebook_build: %lld pairs exceed the supported count", (long long)rb->n_pairs);
-    return SCN_ERR_OVERFLOW;
-  }
-  for (int k = 0; k <= K; ++k) rb->off_host[k] = hb->off[k];
-  guard.keep = true;
-  *out = rb;
+    }
+  for (int i = 0; i < nl; ++i) out[i] = res[i];
   return SCN_OK;
 }
 
@@ -978,6 +1142,14 @@ scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const in
                                       hipStream_t stream, scn_rulebook** out) {
   scn::clear_error();
   return scn::build(coords, n, grid, filter, stride, lattice, stream, out);
+}
+
+scn_status scn_rulebook_build_chain(const int32_t* coords, int64_t n, const int64_t* grid,
+                                   int32_t lattice, int32_t n_layers, const int32_t* filters,
+                                   const int32_t* strides, hipStream_t stream,
+                                   scn_rulebook** out) {
+  scn::clear_error();
+  return scn::build_chain(coords, n, grid, lattice, n_layers, filters, strides, stream, out);
 }
 
 scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int32_t stride,

@@ -116,14 +116,12 @@ class SparseNet:
         g = torch.zeros(x.shape[1], dtype=torch.float32, device=self.device)
         rec = []
         # Rulebooks depend only on the active sites, not on the features: build
-        # the whole chain first (each build synchronises), then issue every
-        # convolution and pooling back to back with no synchronisation between.
-        # The first layer's sites are the input; each later layer's are the
-        # previous layer's active outputs (its rank bitmap is reused).
-        rbs = []
-        for L in self.layers:
-            rbs.append(scn.build_rulebook(coords, grid, L.f, L.s, lattice=self.lattice)
-                       if not rbs else scn.next_rulebook(rbs[-1], L.f, L.s))
+        # the whole chain first, in one call that waits for the device twice,
+        # then issue every convolution and pooling back to back.  The first
+        # layer's sites are the input; each later layer's are the previous
+        # layer's active outputs (its rank bitmap is reused).
+        rbs = scn.build_chain(coords, grid, [(L.f, L.s) for L in self.layers],
+                              lattice=self.lattice)
         for L, p, rb in zip(self.layers, self.params, rbs):
             if L.kind == "conv":
                 W, b = p

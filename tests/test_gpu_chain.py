@@ -30,9 +30,10 @@ def _arrays(g):
     return host(oc), host(ir), host(orr)
 
 
-def _same(a, b):
+def _same(a, b, sorted_inputs=True):
     assert (a.a_in, a.a_out, a.n_pairs, a.K, a.lattice) == (b.a_in, b.a_out, b.n_pairs, b.K, b.lattice)
-    assert tuple(a.out_grid) == tuple(b.out_grid) and a.input_sorted and b.input_sorted
+    assert tuple(a.out_grid) == tuple(b.out_grid) and a.input_sorted == b.input_sorted
+    assert a.input_sorted or not sorted_inputs
     assert np.array_equal(a.offsets, b.offsets)
     for x, y in zip(_arrays(a), _arrays(b)):
         assert np.array_equal(x, y)
@@ -132,3 +133,33 @@ def test_use_on_another_stream_right_after_the_build(scn):
     assert np.array_equal(host(orr), oa.out_rows)
     y_ref, _ = oracle.conv_fwd(o, host(x), host(g_in), host(W), None)
     assert np.allclose(host(y), y_ref, rtol=1e-4, atol=1e-4)
+
+
+@pytest.mark.parametrize("case", CHAINS, ids=[c[0] + str(i) for i, c in enumerate(CHAINS)])
+def test_chain_build_matches_layer_by_layer(scn, case):
+    """scn_rulebook_build_chain (two waits for the whole chain) gives the
+    rulebooks of the layer-by-layer builds."""
+    lattice, B, m, n, layers = case
+    coords, grid = _sites(lattice, stream_rng(91, CHAINS.index(case)), B, m, n)
+    chain = scn.build_chain(dev(coords), grid, layers, lattice=lattice)
+    assert len(chain) == len(layers)
+    g = None
+    for (f, s), c in zip(layers, chain):
+        first = g is None
+        g = (scn.build_rulebook(dev(coords), grid, f, s, lattice=lattice) if first
+             else scn.next_rulebook(g, f, s))
+        _same(c, g, sorted_inputs=not first)   # layer 0 takes the caller's order
+
+
+def test_chain_build_errors(scn):
+    coords = random_sites(stream_rng(92, 1), 1, (2, 9, 9), 20)
+    with pytest.raises(scn.ScnError) as e:   # layer 0's output grid is empty (mx < f)
+        scn.build_chain(dev(coords), (1, 2, 9, 9), [(3, 1), (2, 1)])
+    assert e.value.status == "invalid"
+    with pytest.raises(scn.ScnError) as e:
+        scn.build_chain(dev(coords), (1, 2, 9, 9), [])
+    assert e.value.status == "invalid"
+    bad = np.array([[0, 1, 1, 1], [0, 1, 1, 1]], np.int32)   # duplicate site in layer 0
+    with pytest.raises(scn.ScnError) as e:
+        scn.build_chain(dev(bad), (1, 9, 9, 9), [(2, 1), (2, 2)])
+    assert e.value.status == "duplicate"
