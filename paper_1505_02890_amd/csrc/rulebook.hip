@@ -1050,7 +1050,8 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   }
   scn_status rc;
   hipEvent_t copied = nullptr;
-  if ((rc = readback_slots(&L.hb)) || (rc = copy_event(&copied)) || (rc = L.check()) ||
+  // arguments first: no device call before they are known to be valid
+  if ((rc = L.check()) || (rc = readback_slots(&L.hb)) || (rc = copy_event(&copied)) ||
       (rc = L.phase1()))
     return rc;
   SCN_HIP(hipStreamSynchronize(st));
@@ -1076,7 +1077,6 @@ scn_status build_chain(const int32_t* coords, int64_t n, const int64_t* grid, in
   Readback* hb = nullptr;
   hipEvent_t copied = nullptr;
   scn_status rc;
-  if ((rc = readback_slots(&hb)) || (rc = copy_event(&copied))) return rc;
   for (int i = 0; i < nl; ++i) {
     Ls.emplace_back(new LayerBuild());
     LayerBuild& L = *Ls.back();
@@ -1084,7 +1084,6 @@ scn_status build_chain(const int32_t* coords, int64_t n, const int64_t* grid, in
     L.s = strides[i];
     L.lattice = lattice;
     L.st = st;
-    L.hb = hb + i;
     if (i == 0) {
       L.coords = coords;
       L.n = n;
@@ -1102,7 +1101,11 @@ scn_status build_chain(const int32_t* coords, int64_t n, const int64_t* grid, in
       L.prev_bits = P.hout.bits;
       L.prev_rank = P.hout.rank;
     }
-    if ((rc = L.check()) || (rc = L.phase1())) return rc;
+    if ((rc = L.check())) return rc;
+    // arguments first: no device call before layer 0's are known to be valid
+    if (i == 0 && ((rc = readback_slots(&hb)) || (rc = copy_event(&copied)))) return rc;
+    L.hb = hb + i;
+    if ((rc = L.phase1())) return rc;
   }
   SCN_HIP(hipStreamSynchronize(st));
   for (int i = 0; i < nl; ++i) {

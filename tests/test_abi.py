@@ -54,6 +54,15 @@ def test_host_side_argument_errors(libscn):
     assert b"filter" in libscn.scn_last_error()
     bad = (ctypes.c_int64 * 4)(1, 0, 4, 4)
     assert libscn.scn_rulebook_build(None, 0, bad, 2, 1, None, ctypes.byref(out)) == 1
+    outs = (ctypes.c_void_p * 2)(123, 456)
+    fs = (ctypes.c_int32 * 2)(2, 2)
+    ss = (ctypes.c_int32 * 2)(1, 2)
+    assert libscn.scn_rulebook_build_chain(None, 5, grid, 0, 2, fs, ss, None, outs) == 1
+    assert outs[0] is None and outs[1] is None
+    assert libscn.scn_rulebook_build_chain(None, 0, grid, 0, 0, fs, ss, None, outs) == 1
+    assert libscn.scn_rulebook_build_chain(None, 0, grid, 0, 65, fs, ss, None, outs) == 1
+    big = (ctypes.c_int32 * 2)(4, 2)
+    assert libscn.scn_rulebook_build_chain(None, 0, grid, 0, 2, big, ss, None, outs) == 5
     assert libscn.scn_conv_fwd(None, None, None, None, None, 1, 1, 0, None, None, None) == 1
     assert libscn.scn_maxpool_fwd(None, None, None, 1, None, None, None, None) == 1
     assert libscn.scn_conv_bwd_workspace_bytes(None, 4, 4, 0) == 0
