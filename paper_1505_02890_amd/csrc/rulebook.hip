@@ -365,35 +365,51 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
   const uint32_t m = live ? masks[o] : 0u;
   int4 c = make_int4(0, 0, 0, 0);
   if (live) c = reinterpret_cast<const int4*>(out_coords)[o];
-  // offset k -> (kx, ky, kz), unrolled to constants
-  int8_t ox[K], oy[K], oz[K];
+  // Rank lookups one window row (ky, kz) at a time: its inputs sit at bits
+  // sh .. sh + len - 1 counted from word w of the input bitmap, so the row
+  // needs w's prefix and bits and, when it runs past bit 31, the next word's
+  // bits (that word's prefix is w's plus popcount(w)).  Words are read only
+  // for rows with an active input, so every read word holds a site.
+  uint32_t rank[K];
   {
+    const int64_t x0 = (int64_t)s * c.y;
+    const int sh = (int)(x0 & 31);
     int k = 0;
 #pragma unroll
     for (int kz = 0; kz < W::FZ; ++kz)
 #pragma unroll
-      for (int ky = 0; ky < F; ++ky)
+      for (int ky = 0; ky < F; ++ky) {
+        const int len = W::row_len(ky, kz);
+        if (len <= 0) continue;
+        const uint32_t rbits = (m >> k) & ((1u << len) - 1u);
+        const uint32_t high = sh + len > 32 ? rbits >> (32 - sh) : 0u;
+        const int64_t w =
+            row_base(gi, c.x, (int64_t)s * c.z + ky, (int64_t)s * c.w + kz) + (x0 >> 5);
+        uint32_t p0 = 0u, b0 = 0u, b1 = 0u;
+        if (rbits) {
+          p0 = ipref[w];
+          b0 = inb[w];
+        }
+        if (high) b1 = inb[w + 1];
 #pragma unroll
         for (int kx = 0; kx < F; ++kx)
-          if (kx < W::row_len(ky, kz)) {
-            ox[k] = kx;
-            oy[k] = ky;
-            oz[k] = kz;
-            ++k;
+          if (kx < len) {
+            const int xb = sh + kx;
+            rank[k + kx] = xb < 32 ? p0 + (uint32_t)__popc(b0 & ((1u << xb) - 1u))
+                                   : p0 + (uint32_t)__popc(b0) +
+                                         (uint32_t)__popc(b1 & ((1u << (xb - 32)) - 1u));
           }
-  }
-  uint32_t rank[K];
-#pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const int kx = ox[k], ky = oy[k], kz = oz[k];
-    const int64_t xi = (int64_t)s * c.y + kx;
-    const int64_t w = row_base(gi, c.x, (int64_t)s * c.z + ky, (int64_t)s * c.w + kz) + (xi >> 5);
-    const bool bit = (m >> k) & 1u;
-    const uint32_t pw = bit ? ipref[w] : 0u, bw = bit ? inb[w] : 0u;
-    rank[k] = pw + (uint32_t)__popc(bw & ((1u << (xi & 31)) - 1u));
+        k += len;
+      }
   }
   // output-major neighbour list of the dense forward view
   int32_t* nb = fnb && live ? fnb + fnb_off[o] : nullptr;
+  // Window table (rulebooks with stride >= 2): a lane's K entries are K words
+  // apart, so the wave stages its 64 rows in LDS (dynamic, 64*K words per
+  // wave) and writes them out as one contiguous run.  Stored straight from
+  // the lanes, every store instruction touched 64 cache lines.
+  extern __shared__ int4 emit_lds[];
+  int32_t* stage = reinterpret_cast<int32_t*>(emit_lds) + (threadIdx.x >> 6) * (64 * K);
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     const bool bit = (m >> k) & 1u;
@@ -407,7 +423,20 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
       if (in_rank) in_rank[p] = (int32_t)rank[k];
       if (nb) *nb++ = row;
     }
-    if (nbr && live) nbr[o * K + k] = row;
+    if (nbr) stage[(threadIdx.x & 63) * K + k] = row;
+  }
+  if (nbr) {
+    __syncthreads();
+    const int64_t o0 = o & ~(int64_t)63;  // the wave's first output
+    if (o0 < a_out) {
+      // 64-output runs start 256-byte aligned in nbr
+      const int64_t n = ((o0 + 64 < a_out ? o0 + 64 : a_out) - o0) * K, n4 = n >> 2;
+      const int lane = threadIdx.x & 63;
+      const int4* src = reinterpret_cast<const int4*>(stage);
+      int4* dst = reinterpret_cast<int4*>(nbr + o0 * K);
+      for (int64_t i = lane; i < n4; i += 64) dst[i] = src[i];
+      for (int64_t i = 4 * n4 + lane; i < n; i += 64) nbr[o0 * K + i] = stage[i];
+    }
   }
 }
 
@@ -590,8 +619,8 @@ struct Kernels {
     hipLaunchKernelGGL((tile_count_kernel<K>), g, dim3(256), 0, st, a...);
   }
   template <typename... A>
-  static void emit(dim3 g, hipStream_t st, A... a) {
-    hipLaunchKernelGGL((emit_pairs_kernel<F, LAT>), g, dim3(256), 0, st, a...);
+  static void emit(dim3 g, size_t lds, hipStream_t st, A... a) {
+    hipLaunchKernelGGL((emit_pairs_kernel<F, LAT>), g, dim3(256), lds, st, a...);
   }
   template <typename... A>
   static void inv_windows(int slots, dim3 g, hipStream_t st, A... a) {
@@ -972,8 +1001,10 @@ struct LayerBuild {
     }
     if (a_out > 0) {
       with_kernels(f, lattice, [&](auto k) {
-        k.emit(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks,
-               (const int32_t*)rb->out_coords, a_out, nt, s, (const uint32_t*)inb,
+        // LDS stages the window table: 64*K words per wave of 256-thread blocks
+        k.emit(dim3(blocks_for(nt * TILE, 256)), rb->nbr ? (size_t)256 * K * 4 : 0, st,
+               (const uint32_t*)masks, (const int32_t*)rb->out_coords, a_out, nt, s,
+               (const uint32_t*)inb,
                (const uint32_t*)ipref, gi, (const int32_t*)rb->perm, (const uint64_t*)rb->otile,
                rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr,
                (const uint32_t*)rb->fnb_off, rb->fnb);
