@@ -1,4 +1,5 @@
-// Device-wide exclusive prefix sum (reduce, scan of block totals, downsweep).
+// Device-wide exclusive prefix sum (reduce, scan of block totals, downsweep;
+// one work-group for short inputs).
 // Deterministic: integer sums, fixed partition.  Used by the rulebook builder
 // to number active sites (popcounts of occupancy words) and to place pair
 // lists (per-tile pair counts).
@@ -137,14 +138,56 @@ __global__ void __launch_bounds__(SCAN_THREADS) scan_down_kernel(Load ld, int64_
   }
 }
 
+// The whole scan in one work-group, chunk by chunk with a running carry: for
+// inputs of a few chunks one launch costs less than the three above.
+template <typename T, class Load>
+__global__ void __launch_bounds__(SCAN_THREADS) scan_single_kernel(Load ld, int64_t n, T* out,
+                                                                   T* total) {
+  T carry = 0;
+  for (int64_t c = 0; c < n; c += SCAN_BLOCK) {
+    const int64_t base = c + (int64_t)threadIdx.x * SCAN_ITEMS;
+    T v[SCAN_ITEMS];
+    load_items<T>(ld, base, n, v);
+    T s = 0;
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j) s += v[j];
+    T tot;
+    T ex = block_exclusive_scan<T>(s, &tot) + carry;
+    T o[SCAN_ITEMS];
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j) {
+      o[j] = ex;
+      ex += v[j];
+    }
+    if (base + SCAN_ITEMS <= n) {
+      store16<T>(out + base, o);
+    } else {
+#pragma unroll
+      for (int j = 0; j < SCAN_ITEMS; ++j)
+        if (base + j < n) out[base + j] = o[j];
+    }
+    carry += tot;
+  }
+  if (threadIdx.x == 0) *total = carry;
+}
+
+// inputs of at most this many chunks take scan_single_kernel
+constexpr int64_t SCAN_SINGLE_MAX_BLOCKS = 4;
+
 inline int64_t scan_blocks(int64_t n) { return n > 0 ? ceil_div(n, SCAN_BLOCK) : 1; }
 
 // out[i] = sum_{j<i} ld(j) for i < n; *total = sum of all (device).  tmp holds
-// scan_blocks(n) elements of T.  out (and the loader's array) must be 16-byte
-// aligned.
+// scan_blocks(n) elements of T (unused for inputs of a few chunks).  out (and
+// the loader's array) must be 16-byte aligned.
 template <typename T, class Load>
 scn_status exclusive_scan(Load ld, int64_t n, T* out, T* total, T* tmp, hipStream_t s) {
   const int64_t nb = scan_blocks(n);
+  if (nb <= SCAN_SINGLE_MAX_BLOCKS) {
+    hipLaunchKernelGGL((scan_single_kernel<T, Load>), dim3(1), dim3(SCAN_THREADS), 0, s, ld, n,
+                       out, total);
+    SCN_LAUNCH_CHECK();
+    return SCN_OK;
+  }
   if (n > 0) {
     hipLaunchKernelGGL((scan_reduce_kernel<T, Load>), dim3((unsigned)nb), dim3(SCAN_THREADS), 0,
                        s, ld, n, tmp);
