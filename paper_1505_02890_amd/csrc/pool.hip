@@ -184,29 +184,34 @@ __global__ void __launch_bounds__(256) maxpool_bwd_vec_kernel(const int32_t* __r
 // Overlapping windows (filter > stride): an input lies in up to 8 windows.
 // dx[r][c] = sum over its windows (slot order 0..7, a fixed order) of
 // dy[o][c] where the input won channel c of window o.  win[r*8 + j] = o*K + k
-// or -1.
+// or -1.  The window size K is a compile-time constant, so the slot
+// decodes are multiplications, and an empty slot loads nothing (its lanes
+// are masked off); every slot load is still issued before the first use.
+template <int K>
 __global__ void __launch_bounds__(256) maxpool_bwd_overlap_vec_kernel(
     const int32_t* __restrict__ win, const uint32_t* __restrict__ argmax,
-    const float4* __restrict__ dy, int64_t a_in, int nc4, int per, int K,
-    float4* __restrict__ dx) {
+    const float4* __restrict__ dy, int64_t a_in, int nc4, int per, float4* __restrict__ dx) {
   const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
   const int64_t r = (int64_t)blockIdx.x * per + rl;
   if (rl >= per || r >= a_in) return;
   const int4 w0 = reinterpret_cast<const int4*>(win)[2 * r];
   const int4 w1 = reinterpret_cast<const int4*>(win)[2 * r + 1];
   const int32_t t[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-  // branch-free: an empty slot reads window 0 with an offset no argmax holds,
-  // so all slot loads are in flight together
   uint32_t am[8];
   float4 d[8];
   uint32_t kk[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const int32_t o = t[j] >= 0 ? t[j] / K : 0;
-    kk[j] = t[j] >= 0 ? (uint32_t)(t[j] - o * K) : 255u;
+    const bool ok = t[j] >= 0;
+    const uint32_t o = ok ? (uint32_t)t[j] / K : 0u;
+    kk[j] = ok ? (uint32_t)t[j] - o * K : 255u;  // 255: no argmax byte holds it
     const int64_t jj = (int64_t)o * nc4 + c4;
-    am[j] = argmax[jj];
-    d[j] = dy[jj];
+    am[j] = 0u;
+    d[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (ok) {
+      am[j] = argmax[jj];
+      d[j] = dy[jj];
+    }
   }
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
@@ -448,10 +453,13 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
     if (rb->a_in > 0) {
       if (vec) {
         const int nc4 = C / 4, per = 256 / nc4;
-        hipLaunchKernelGGL(maxpool_bwd_overlap_vec_kernel, dim3(nblocks(rb->a_in, per)), dim3(256),
-                           0, st, rb->inv, reinterpret_cast<const uint32_t*>(argmax),
-                           reinterpret_cast<const float4*>(dy), rb->a_in, nc4, per, rb->K,
-                           reinterpret_cast<float4*>(dx));
+        with_window(rb->K, [&](auto k) {
+          hipLaunchKernelGGL(maxpool_bwd_overlap_vec_kernel<decltype(k)::value>,
+                             dim3(nblocks(rb->a_in, per)), dim3(256), 0, st, rb->inv,
+                             reinterpret_cast<const uint32_t*>(argmax),
+                             reinterpret_cast<const float4*>(dy), rb->a_in, nc4, per,
+                             reinterpret_cast<float4*>(dx));
+        });
       } else {
         hipLaunchKernelGGL(maxpool_bwd_overlap_kernel, dim3(nblocks(rb->a_in * C, 256)), dim3(256),
                            0, st, rb->inv, argmax, dy, rb->a_in, C, rb->K, dx);
