@@ -279,6 +279,8 @@ POOL_CASES = [
     (3, 2, 1, (7, 7, 7), 343, 64, 0.2, 0.1),     # MP3/2, every site active
     (3, 2, 2, (30, 9, 8), 900, 12, 0.0, 1.5),    # MP3/2, ground state often wins
     (2, 3, 1, (14, 13, 11), 500, 8, 0.0, 0.5),   # gaps between windows
+    (1, 2, 2, (15, 12, 11), 700, 8, 0.0, 0.5),   # one-site windows (K = 1)
+    (3, 2, 1, (40, 33, 30), 6000, 4, 0.1, 0.3),  # MP3/2 over many output waves, ragged last
 ]
 
 
