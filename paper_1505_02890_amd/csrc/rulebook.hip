@@ -42,7 +42,7 @@
 // rulebook: they are H_out, and a build from this rulebook's output sites
 // (scn_rulebook_build_next) takes them as its H_in and skips phases 1-3.
 #include <hip/hip_runtime.h>
-#include <hipcub/device/device_radix_sort.hpp>
+#include <rocprim/device/device_radix_sort.hpp>
 
 #include <algorithm>
 #include <cstring>
@@ -54,6 +54,22 @@
 
 namespace scn {
 namespace {
+
+// The dense forward's mask sort: a stable onesweep radix sort of (mask, row)
+// pairs over the K mask bits, 9 bits per pass (3 passes for the 27-offset
+// cube; 8-bit digits take 4 passes of the same length each).
+using MaskSortCfg = rocprim::radix_sort_config<
+    rocprim::default_config, rocprim::default_config,
+    rocprim::radix_sort_onesweep_config<rocprim::kernel_config<512, 16>,
+                                        rocprim::kernel_config<512, 16>, 9,
+                                        rocprim::block_radix_rank_algorithm::match>>;
+
+inline hipError_t mask_sort(void* tmp, size_t& bytes, const uint32_t* keys_in, uint32_t* keys_out,
+                            const int32_t* rows_in, int32_t* rows_out, int64_t n, int bits,
+                            hipStream_t st) {
+  return rocprim::radix_sort_pairs<MaskSortCfg>(tmp, bytes, keys_in, keys_out, rows_in, rows_out,
+                                                (size_t)n, 0u, (unsigned)bits, st);
+}
 
 enum : uint32_t { F_RANGE = 1, F_DUP = 2, F_UNSORTED = 4 };
 
@@ -944,9 +960,7 @@ struct LayerBuild {
     ncnt = K * nt;
     // the mask sort's scratch size (a query; no device work)
     if (dense)
-      SCN_HIP(hipcub::DeviceRadixSort::SortPairs(nullptr, sort_bytes, (uint32_t*)nullptr,
-                                                 (uint32_t*)nullptr, (int32_t*)nullptr,
-                                                 (int32_t*)nullptr, (int)a_out, 0, K, st));
+      SCN_HIP(mask_sort(nullptr, sort_bytes, nullptr, nullptr, nullptr, nullptr, a_out, K, st));
     if ((rc = tmp.reserve(Temps::round(a_out * 4) + Temps::round(ncnt * 8) +
                           Temps::round(scan_blocks(ncnt) * 8) +
                           (dense ? Temps::round(scan_blocks(a_out) * 4) +
@@ -1019,8 +1033,7 @@ struct LayerBuild {
       hipLaunchKernelGGL(iota_kernel, dim3(blocks_for(a_out, 256)), dim3(256), 0, st, iota,
                          a_out);
       SCN_LAUNCH_CHECK();
-      SCN_HIP(hipcub::DeviceRadixSort::SortPairs(sort_tmp, sort_bytes, masks, rb->fmask, iota,
-                                                 rb->fperm, (int)a_out, 0, K, st));
+      SCN_HIP(mask_sort(sort_tmp, sort_bytes, masks, rb->fmask, iota, rb->fperm, a_out, K, st));
     }
     if (pool && n > 0) {
       with_kernels(f, lattice, [&](auto k) {
