@@ -93,7 +93,8 @@ typedef struct scn_rulebook_info {
   int64_t in_grid[4];  /* B, mx, my, mz */
   int64_t out_grid[4]; /* B, floor((m-f)/s)+1 per axis */
   int32_t lattice;     /* SCN_LATTICE_* */
-  int32_t reserved;    /* 0 */
+  int32_t dense_view;  /* 1 if the rulebook carries the dense forward view
+                          (scn_set_dense_forward), else 0 */
 } scn_rulebook_info;
 
 /*
@@ -107,7 +108,9 @@ typedef struct scn_rulebook_info {
  * when windows overlap).
  *
  *  coords  device int32[n][4] rows (b, x, y, z); row i is row i of the
- *          layer's feature matrix.  Not retained.
+ *          layer's feature matrix.  Not retained, but read by kernels the
+ *          call queues on `stream` (some after it returns): keep it valid in
+ *          stream order (free it on `stream`, or after synchronising it).
  *  n       number of active input sites (>= 0; 0 gives an empty rulebook).
  *  grid    host int64[4] = (B, mx, my, mz), all >= 1.
  *  filter  f in {1, 2, 3};  stride s >= 1 (s <= f not required).
@@ -167,8 +170,10 @@ scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const in
  * scn_rulebook_build_lattice) called with scn_rulebook_out_coords(prev),
  * prev's a_out and out_grid, but reuses prev's output rank bitmap (every
  * rulebook keeps it: 8 bytes per 32 sites of its output grid) instead of
- * marking and ranking the sites again.  prev is only read, and may be freed
- * once this call returns.  Errors: SCN_ERR_INVALID (NULL, or prev's output
+ * marking and ranking the sites again.  prev is only read, by kernels queued
+ * on `stream` (some after the call returns).  If `stream` is not the stream
+ * prev was built on, that stream is made to wait for them, so prev may be
+ * freed (scn_rulebook_free, ordered on prev's stream) once this call returns.  Errors: SCN_ERR_INVALID (NULL, or prev's output
  * grid is empty), and as scn_rulebook_build.  It waits for stream as
  * scn_rulebook_build does, and orders stream after prev's build.
  */

@@ -53,7 +53,7 @@ class _Info(ctypes.Structure):
                 ("filter", ctypes.c_int32), ("stride", ctypes.c_int32),
                 ("input_sorted", ctypes.c_int32), ("in_grid", ctypes.c_int64 * 4),
                 ("out_grid", ctypes.c_int64 * 4), ("lattice", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("dense_view", ctypes.c_int32)]
 
 
 _lib = None
@@ -173,6 +173,7 @@ class Rulebook:
         self.a_in, self.a_out, self.n_pairs = int(info.a_in), int(info.a_out), int(info.n_pairs)
         self.K, self.filter, self.stride = int(info.K), int(info.filter), int(info.stride)
         self.input_sorted = bool(info.input_sorted)
+        self.dense_view = bool(info.dense_view)
         self.lattice = {v: k for k, v in LATTICES.items()}[int(info.lattice)]
         self.in_grid = tuple(int(v) for v in info.in_grid)
         self.out_grid = tuple(int(v) for v in info.out_grid)

@@ -757,7 +757,12 @@ __global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int t = 0; t < TC; ++t) {
-        if (NCH > 1 && 4 * ch + t >= NKT) break;
+        if (NCH > 1 && 4 * ch + t >= NKT) {
+          // a last chunk shorter than the step that issues the prefetch
+          // (t = TC - 3) issues it here, so the next item's rows are loaded
+          if (t <= TC - 3) prefetch();
+          break;
+        }
         // step t's products, then step t + 2's weights into the set just read
         if (t & 1) mult(t, A1); else mult(t, A0);
         if (t + 2 < TC) {

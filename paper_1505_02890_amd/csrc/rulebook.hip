@@ -1100,6 +1100,10 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     return rc;
   SCN_HIP(hipStreamSynchronize(st));
   if ((rc = L.sized()) || (rc = L.phase2(copied))) return rc;
+  // The build's last kernels read prev's output bitmap and sites after the
+  // call returns.  prev is freed on its own stream, so that stream waits
+  // for them: a free of prev after this call is then ordered after them.
+  if (prev && prev->stream != st) SCN_HIP(hipStreamWaitEvent(prev->stream, L.rb->done, 0));
   SCN_HIP(hipEventSynchronize(copied));
   return L.finish(out);
 }
@@ -1234,7 +1238,7 @@ scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info
   info->stride = rb->s;
   info->input_sorted = rb->input_sorted;
   info->lattice = rb->lattice;
-  info->reserved = 0;
+  info->dense_view = rb->fnb ? 1 : 0;
   for (int a = 0; a < 4; ++a) {
     info->in_grid[a] = rb->gin[a];
     info->out_grid[a] = rb->gout[a];

@@ -106,6 +106,27 @@ def test_chain_outlives_its_source(scn):
     _same(nxt, ref)
 
 
+def test_chain_on_another_stream_outlives_its_source(scn):
+    """The next rulebook built on another stream than its source's, then the
+    source freed at once (its free is ordered on its own stream): the next
+    build's last kernels, which read the source's output bitmap and sites,
+    still run before that free, so the result equals a fresh build."""
+    coords, grid = _sites("cubic", stream_rng(93, 1), 2, 40, 6000)
+    g = scn.build_rulebook(dev(coords), grid, 2, 1)
+    ref = scn.build_rulebook(g.out_coords(), g.out_grid, 3, 2)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        nxt = scn.next_rulebook(g, 3, 2)
+        g.close()
+    # a build on the source's stream right after the free may take the freed
+    # memory from the pool and overwrite it
+    other = scn.build_rulebook(dev(coords), grid, 3, 1)
+    torch.cuda.synchronize()
+    _same(nxt, ref)
+    assert other.a_in == len(coords)
+
+
 def test_use_on_another_stream_right_after_the_build(scn):
     """The build returns before its last kernels finish (emission, the mask
     sort); a call on another stream is ordered after them by the library."""

@@ -3,19 +3,25 @@
 * Small stacks run through the oracle layer by layer: every layer of the GPU
   sees the same fp32 input as the oracle (the oracle's previous output rounded
   to fp32) and is compared in isolation, forward and backward.
-* Large layers are compared inside an interior sub-box: the oracle runs on
-  the active sites inside a cube; an output whose whole window lies inside
-  the cube sees exactly the same inputs as in the full problem, and so does an
-  input whose every output lies inside.  The GPU runs the full-size layer in
-  the same launch configuration as the benchmark and is compared at those
-  sites; the weight gradient is compared with an output gradient that is zero
-  outside the interior outputs, on both sides.
-* Full-size rulebooks are checked against their definition, recomputed with
-  numpy: the output set is the set of valid window origins of the active
-  inputs, and pair (r, o) of offset k exists iff site s*o + k is active.
+* Large layers run at full size, in the launch configuration the benchmark
+  times, and are compared inside an interior sub-box: the oracle runs on the
+  active sites inside a cube; an output whose whole window lies inside the
+  cube sees exactly the same inputs as in the full problem, and so does an
+  input whose every output lies inside.  The weight gradient is compared with
+  an output gradient that is zero outside the interior outputs, on both sides.
+* Every layer of the two deep stacks (the surfaces, five conv + pool levels;
+  the deep step, a 3x3x3 conv and six conv + pool levels) runs this way on
+  its own full-size input: the active sites the definition gives for the
+  layers below it, with seeded features.
+* Full-size rulebooks are checked against their definition, computed here
+  with numpy on a dense occupancy grid: output o is active iff some site
+  s*o + k of its window is active, and pair (r, o) of offset k exists iff
+  site s*o + k is active with row r.
 
-Tolerances follow tests/helpers.py; rulebooks, pooling values, argmax and
-pooling input gradients are compared bit-exactly.
+Tolerances follow tests/helpers.py: rulebooks, pooling values, argmax and
+(disjoint-window) pooling input gradients bit-exact; per-site results under
+the plain 1e-4 / 1e-5 rule; reductions over pairs relative to the rss of
+their terms.
 """
 from __future__ import annotations
 
@@ -27,7 +33,8 @@ torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 from gen import make_config, make_dy, stream_rng  # noqa: E402
 
-from helpers import assert_close, dev, host, keys_of  # noqa: E402
+from helpers import (assert_exact, assert_reduction, assert_site, definition_rulebook,  # noqa: E402
+                     dev, host, keys_of, kink_flips, sq)
 
 pytestmark = pytest.mark.gpu
 
@@ -41,67 +48,28 @@ def scn():
     return m
 
 
-def _sq(a):
-    return None if a is None else np.asarray(a, np.float64) ** 2
-
-
 def _f32(a):
-    return np.asarray(a, np.float64).astype(np.float32)
+    a = np.asarray(a)
+    return a if a.dtype == np.float32 else a.astype(np.float32)
+
+
+def step(msg):
+    print(f"[configs] {msg}", flush=True)
 
 
 # --------------------------------------------------------------------------
-# rulebook against its definition (numpy)
+# rulebook against its definition (helpers.definition_rulebook)
 # --------------------------------------------------------------------------
 
-def definition_rulebook(coords, grid, f, s):
-    """(out_coords sorted by key, offsets, in_rows, out_rows) from the
-    definition, vectorised with numpy."""
-    c = np.asarray(coords, np.int64)
-    B, mx, my, mz = (int(v) for v in grid)
-    ox, oy, oz = ((m - f) // s + 1 if m >= f else 0 for m in (mx, my, mz))
-    okey = lambda b, x, y, z: ((b * oz + z) * oy + y) * ox + x  # noqa: E731
-    ikeys = keys_of(c, grid)
-    order = np.argsort(ikeys, kind="stable")
-    sk = ikeys[order]
-    offs = [(kx, ky, kz) for kz in range(f) for ky in range(f) for kx in range(f)]
-    cand = []
-    for kx, ky, kz in offs:
-        d = c[:, 1:4] - np.array([kx, ky, kz])
-        ok = np.all((d >= 0) & (d % s == 0), axis=1)
-        o = d[ok] // s
-        ok2 = (o[:, 0] < ox) & (o[:, 1] < oy) & (o[:, 2] < oz)
-        o, b = o[ok2], c[ok][ok2, 0]
-        cand.append(okey(b, o[:, 0], o[:, 1], o[:, 2]))
-    ok_keys = np.unique(np.concatenate(cand)) if cand else np.zeros(0, np.int64)
-    x = ok_keys % ox if ox else ok_keys
-    y = (ok_keys // ox) % oy if ox else ok_keys
-    z = (ok_keys // (ox * oy)) % oz if ox else ok_keys
-    b = ok_keys // (ox * oy * oz) if ox else ok_keys
-    out_coords = np.stack([b, x, y, z], axis=1).astype(np.int32)
-    in_rows, out_rows, offsets = [], [], [0]
-    for kx, ky, kz in offs:
-        q = ((b * mz + (s * z + kz)) * my + (s * y + ky)) * mx + (s * x + kx)
-        pos = np.searchsorted(sk, q)
-        posc = np.minimum(pos, len(sk) - 1) if len(sk) else pos
-        hit = (pos < len(sk)) & (sk[posc] == q) if len(sk) else np.zeros(len(q), bool)
-        rows = np.nonzero(hit)[0]
-        in_rows.append(order[posc[hit]].astype(np.int32))
-        out_rows.append(rows.astype(np.int32))
-        offsets.append(offsets[-1] + len(rows))
-    return (out_coords, np.array(offsets, np.int64), np.concatenate(in_rows),
-            np.concatenate(out_rows))
-
-
-def check_rulebook_definition(g, coords, grid, f, s):
-    """Asserts the GPU rulebook equals the definition; returns the
-    definition's output sites (the next layer's input, independent of the GPU)."""
-    oc, off, ir, orr = definition_rulebook(coords, grid, f, s)
-    assert g.a_out == len(oc) and np.array_equal(g.offsets, off)
+def check_rulebook_definition(g, defn):
+    """The GPU rulebook equals the definition, bit for bit."""
+    oc, off, ir, orr = defn
+    assert g.a_out == len(oc)
+    assert_exact("offsets", np.asarray(g.offsets), off)
     goc, gir, gorr = g.export()
-    assert np.array_equal(host(goc), oc)
-    assert np.array_equal(host(gir), ir)
-    assert np.array_equal(host(gorr), orr)
-    return oc
+    assert_exact("out_coords", host(goc), oc)
+    assert_exact("in_rows", host(gir), ir)
+    assert_exact("out_rows", host(gorr), orr)
 
 
 # --------------------------------------------------------------------------
@@ -110,7 +78,7 @@ def check_rulebook_definition(g, coords, grid, f, s):
 
 def subbox(coords, n_target, seed):
     """Sites of one sample inside a cube around a random active site, grown
-    until it holds about n_target sites.  Returns (mask, lo, hi)."""
+    until it holds about n_target sites.  Returns (mask, b, lo, hi)."""
     rng = stream_rng(seed, 7)
     c = np.asarray(coords, np.int64)
     centre = c[int(rng.integers(len(c)))]
@@ -138,56 +106,64 @@ def find_rows(sorted_coords, grid_out, query_coords):
 
 
 def conv_layer_interior(scn, coords, grid, x, g_in, W, bias, f, s, relu, seed, n_sub=6000,
-                        check_def=True):
-    """Full-size GPU layer vs oracle on an interior sub-box: y, dx, dW, dbias, dg_in."""
+                        defn=None):
+    """Full-size GPU layer vs oracle on an interior sub-box: y, g_out, dx (per
+    site), dW, dbias, dg_in (reductions).  Returns the definition's output
+    sites and grid (or the GPU's, when defn is None and the rulebook was
+    checked elsewhere)."""
     x = _f32(x)
     g_in = _f32(g_in)
     K, Cin, Cout = W.shape
-    gd = dev(np.ascontiguousarray(coords, np.int32))
-    g = scn.build_rulebook(gd, grid, f, s)
-    def_oc = check_rulebook_definition(g, coords, grid, f, s) if check_def else None
-    goc = host(g.out_coords())
-    yd, god = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias), relu=relu)
-    # sub-box
+    g = scn.build_rulebook(dev(np.ascontiguousarray(coords, np.int32)), grid, f, s)
+    if defn is not None:
+        check_rulebook_definition(g, defn)
+        out_sites = defn[0]
+    else:
+        out_sites = host(g.out_coords())
+    xd = dev(x)
+    yd, god = scn.conv_fwd(g, xd, dev(g_in), dev(W), dev(bias), relu=relu)
     m, b, lo, hi = subbox(coords, n_sub, seed)
     sub = np.ascontiguousarray(np.asarray(coords)[m], np.int32)
     o = oracle.Rulebook(sub, grid, f, s)
-    oa = o.arrays()
-    oc = oa.out_coords.astype(np.int64)
+    oc = o.arrays().out_coords.astype(np.int64)
     # interior outputs: window s*o + [0, f) inside the cube
     io = (oc[:, 0] == b) & np.all((s * oc[:, 1:4] >= lo) & (s * oc[:, 1:4] + f - 1 <= hi), axis=1)
     assert io.sum() > 0
     y_ref, go_ref = oracle.conv_fwd(o, x[m], g_in, W, bias, relu=relu)
-    pre_ref, gpre_ref = oracle.conv_fwd(o, x[m], g_in, W, bias, relu=False)
-    sig_y, sig_g = (np.sqrt(v) for v in oracle.conv_fwd(o, _sq(x[m]), _sq(g_in), _sq(W), _sq(bias)))
-    gr = find_rows(goc, g.out_grid, oc[io])
-    assert_close("y", host(yd)[gr], y_ref[io], sig_y[io])
-    assert_close("g_out", host(god), go_ref, sig_g)
-    # backward: interior outputs carry the gradient (zero where the oracle's
-    # pre-activation is within rounding of the ReLU kink), others zero
-    dy_o = make_dy(seed, len(oc), Cout)
-    keep = io.copy()[:, None] & np.ones((1, Cout), bool)
+    gr = find_rows(out_sites, g.out_grid, oc[io])
+    y_gpu = host(yd)[gr]
+    assert_site("y", y_gpu, y_ref[io])
+    assert_site("g_out", host(god), go_ref)
+    pre_ref = oracle.conv_fwd(o, x[m], g_in, W, bias, relu=False)[0] if relu else y_ref
     if relu:
-        keep &= ~(np.abs(pre_ref) <= 1e-3 * (sig_y + 1e-30))
-    dy_o = np.where(keep, dy_o, 0.0).astype(np.float32)
-    dy_full = np.zeros((g.a_out, Cout), np.float32)
-    dy_full[gr] = dy_o[io]
+        assert kink_flips(y_gpu, pre_ref[io]) <= 1e-4 * y_gpu.size + 1
+    # backward: interior outputs carry the gradient, the others zero; the
+    # ReLU mask of the interior rows is the oracle's forward on both sides
+    dy_o = make_dy(seed, len(oc), Cout)
+    dy_o[~io] = 0.0
+    gr_t = torch.from_numpy(gr).cuda()
+    dy_full = torch.zeros((g.a_out, Cout), dtype=torch.float32, device="cuda")
+    dy_full[gr_t] = dev(dy_o[io])
     dg = np.zeros(Cout, np.float32)
+    if relu:
+        yd[gr_t] = dev(_f32(y_ref[io]))
+        god = dev(_f32(go_ref))
     ref = oracle.conv_bwd(o, x[m], g_in, W, bias, dy_o, dg, relu=relu)
     dyb = dy_o * (pre_ref > 0) if relu else dy_o
     sig = {k: np.sqrt(v) for k, v in
-           oracle.conv_bwd(o, _sq(x[m]), _sq(g_in), _sq(W), None, _sq(dyb), None).items()}
-    out = scn.conv_bwd(g, dev(x), dev(g_in), dev(W), yd, god, dev(dy_full), dev(dg), relu=relu)
+           oracle.conv_bwd(o, sq(x[m]), sq(g_in), sq(W), None, sq(dyb), None).items()}
+    out = scn.conv_bwd(g, xd, dev(g_in), dev(W), yd, god, dy_full, dev(dg), relu=relu)
     for k in ("dW", "dbias", "dg_in"):
-        assert_close(k, host(out[k]), ref[k], sig[k])
+        assert_reduction(k, host(out[k]), ref[k], sig[k])
     # dx at inputs whose outputs all lie inside: coordinates in [lo+f-1, hi-f+1]
     ii = inside(sub, b, lo + f - 1, hi - f + 1)
     rows_full = np.nonzero(m)[0][ii]
-    assert_close("dx", host(out["dx"])[rows_full], ref["dx"][ii], sig["dx"][ii])
-    return def_oc, g.out_grid
+    assert_site("dx", host(out["dx"])[rows_full], ref["dx"][ii])
+    del yd, dy_full, out
+    return out_sites, g.out_grid
 
 
-def pool_layer_interior(scn, coords, grid, x, g_in, f, seed, n_sub=6000, s=None):
+def pool_layer_interior(scn, coords, grid, x, g_in, f, seed, n_sub=6000, s=None, defn=None):
     """Max-pool (filter f, stride s, default s = f) at full size; outputs whose
     window lies in an interior sub-box are compared with the oracle run on the
     sub-box alone."""
@@ -195,8 +171,11 @@ def pool_layer_interior(scn, coords, grid, x, g_in, f, seed, n_sub=6000, s=None)
     x = _f32(x)
     g_in = _f32(g_in)
     g = scn.build_rulebook(dev(np.ascontiguousarray(coords, np.int32)), grid, f, s)
-    def_oc = check_rulebook_definition(g, coords, grid, f, s)
-    goc = host(g.out_coords())
+    if defn is not None:
+        check_rulebook_definition(g, defn)
+        out_sites = defn[0]
+    else:
+        out_sites = host(g.out_coords())
     yd, god, am = scn.maxpool_fwd(g, dev(x), dev(g_in))
     m, b, lo, hi = subbox(coords, n_sub, seed)
     sub = np.ascontiguousarray(np.asarray(coords)[m], np.int32)
@@ -204,26 +183,98 @@ def pool_layer_interior(scn, coords, grid, x, g_in, f, seed, n_sub=6000, s=None)
     oc = o.arrays().out_coords.astype(np.int64)
     io = (oc[:, 0] == b) & np.all((s * oc[:, 1:4] >= lo) & (s * oc[:, 1:4] + f - 1 <= hi), axis=1)
     y_ref, _, ak_ref, _ = oracle.maxpool_fwd(o, x[m], g_in)
-    gr = find_rows(goc, g.out_grid, oc[io])
-    assert np.array_equal(host(yd)[gr], y_ref[io].astype(np.float32))
-    assert np.array_equal(host(am)[gr].astype(np.int32), ak_ref[io])
-    dy_o = np.zeros((len(oc), x.shape[1]), np.float32)
-    dy_o[io] = make_dy(seed, int(io.sum()), x.shape[1])
-    dy_full = np.zeros((g.a_out, x.shape[1]), np.float32)
-    dy_full[gr] = dy_o[io]
+    gr = find_rows(out_sites, g.out_grid, oc[io])
+    assert_exact("pool y", host(yd)[gr], y_ref[io].astype(np.float32))
+    assert_exact("argmax", host(am)[gr].astype(np.int32), ak_ref[io])
+    assert_exact("pool g_out", host(god), g_in)
+    C = x.shape[1]
+    dy_o = np.zeros((len(oc), C), np.float32)
+    dy_o[io] = make_dy(seed, int(io.sum()), C)
+    dy_full = torch.zeros((g.a_out, C), dtype=torch.float32, device="cuda")
+    dy_full[torch.from_numpy(gr).cuda()] = dev(dy_o[io])
     dx_ref, dg_ref = oracle.maxpool_bwd(o, x[m], g_in, dy_o, None)
-    dxd, dgd = scn.maxpool_bwd(g, am, dev(dy_full))
+    dxd, dgd = scn.maxpool_bwd(g, am, dy_full)
     # every input of the cube: each of its windows is interior (same argmax on
     # both sides) or carries a zero output gradient on both sides
     rows = np.nonzero(m)[0]
     if f <= s:
-        assert np.array_equal(host(dxd)[rows], dx_ref.astype(np.float32))
+        assert_exact("pool dx", host(dxd)[rows], dx_ref.astype(np.float32))
     else:
-        sig_dx = np.sqrt(oracle.maxpool_bwd(o, x[m], g_in, _sq(dy_o), None)[0])
-        assert_close("pool dx", host(dxd)[rows], dx_ref, sig_dx)
-    sig = np.sqrt(oracle.maxpool_bwd(o, x[m], g_in, _sq(dy_o), None)[1])
-    assert_close("pool dg_in", host(dgd), dg_ref, sig)
-    return def_oc, g.out_grid
+        assert_site("pool dx", host(dxd)[rows], dx_ref)
+    sig = np.sqrt(oracle.maxpool_bwd(o, x[m], g_in, sq(dy_o), None)[1])
+    assert_reduction("pool dg_in", host(dgd), dg_ref, sig)
+    del yd, am, dy_full, dxd
+    return out_sites, g.out_grid
+
+
+# --------------------------------------------------------------------------
+# per-layer inputs of the deep stacks
+# --------------------------------------------------------------------------
+
+class StackChain:
+    """The input sites of every layer of a workload's stack, from the
+    definition (each layer's active outputs are the next layer's inputs), and
+    each layer's definition rulebook; computed on first use."""
+
+    def __init__(self, cfg):
+        self.cfg = cfg
+        self.sites = {0: (cfg.coords, tuple(cfg.grid))}
+        self.defs = {}
+
+    def defn(self, li):
+        if li not in self.defs:
+            coords, grid = self.inputs(li)
+            L = self.cfg.layers[li]
+            step(f"definition of layer {li} ({L.kind} f={L.f} s={L.s}) on {len(coords)} sites")
+            self.defs[li] = definition_rulebook(coords, grid, L.f, L.s)
+        return self.defs[li]
+
+    def inputs(self, li):
+        if li not in self.sites:
+            prev_coords, prev_grid = self.inputs(li - 1)
+            L = self.cfg.layers[li - 1]
+            oc = self.defn(li - 1)[0]
+            og = (prev_grid[0],) + tuple((m - L.f) // L.s + 1 for m in prev_grid[1:])
+            self.sites[li] = (oc, og)
+        return self.sites[li]
+
+
+def layer_features(cfg, li, n, C):
+    """Seeded input features of layer li of a stack: the workload's own input
+    for layer 0, else ReLU-like values (about half exact zeros) and a
+    non-negative ground state, as a ReLU layer below would give."""
+    if li == 0:
+        return cfg.features, cfg.g0
+    rng = stream_rng(cfg.seed, 100 + li)
+    x = rng.standard_normal((n, C), dtype=np.float32)
+    np.maximum(x, 0.0, out=x)
+    g = np.abs(rng.standard_normal(C)).astype(np.float32) * 0.3
+    g[rng.random(C) < 0.3] = 0.0
+    return x, g
+
+
+def run_stack_layer(scn, cfg, chain, li, n_sub):
+    L = cfg.layers[li]
+    coords, grid = chain.inputs(li)
+    defn = chain.defn(li)
+    C = L.cin if L.kind == "conv" else cfg.layers[li - 1].cout
+    x, g_in = layer_features(cfg, li, len(coords), C)
+    step(f"layer {li}: {L.kind} f={L.f} s={L.s} C={C}->{L.cout or C} on {len(coords)} sites")
+    if L.kind == "conv":
+        conv_layer_interior(scn, coords, grid, x, g_in, cfg.weights[li], cfg.biases[li], L.f,
+                            L.s, L.relu, seed=cfg.seed + 1000 + li, n_sub=n_sub, defn=defn)
+    else:
+        pool_layer_interior(scn, coords, grid, x, g_in, L.f, seed=cfg.seed + 1000 + li,
+                            n_sub=n_sub, s=L.s, defn=defn)
+    torch.cuda.empty_cache()
+
+
+def _sub_for(L, base):
+    """Sub-box size that keeps the oracle's work per layer to seconds."""
+    if L.kind != "conv":
+        return base
+    macs = L.f ** 3 * L.cin * max(L.cout, 1)
+    return int(max(800, min(base, 3e8 / max(macs, 1) / 3)))
 
 
 # --------------------------------------------------------------------------
@@ -238,27 +289,29 @@ def test_trefoil_forward_chain(scn):
     o = oracle.Rulebook(cfg.coords, cfg.grid, conv.f, conv.s)
     oa = o.arrays()
     oc, ir, orr = g.export()
-    assert np.array_equal(host(oc), oa.out_coords) and np.array_equal(host(ir), oa.in_rows)
-    assert np.array_equal(host(orr), oa.out_rows) and g.a_out > g.a_in  # growth (Figure 1)
+    assert_exact("out_coords", host(oc), oa.out_coords)
+    assert_exact("in_rows", host(ir), oa.in_rows)
+    assert_exact("out_rows", host(orr), oa.out_rows)
+    assert g.a_out > g.a_in  # growth (Figure 1)
     y, g1 = scn.conv_fwd(g, dev(cfg.features), dev(cfg.g0), dev(cfg.weights[0]),
                          dev(cfg.biases[0]))
     y_ref, g1_ref = oracle.conv_fwd(o, cfg.features, cfg.g0, cfg.weights[0], cfg.biases[0])
-    sig = np.sqrt(oracle.conv_fwd(o, _sq(cfg.features), _sq(cfg.g0), _sq(cfg.weights[0]),
-                                  _sq(cfg.biases[0]))[0])
-    assert_close("y", host(y), y_ref, sig)
+    assert_site("y", host(y), y_ref)
+    assert_site("g_out", host(g1), g1_ref)
     x2, g2 = _f32(y_ref), _f32(g1_ref)
     pg = scn.build_rulebook(dev(oa.out_coords), oa.out_grid, pool.f, pool.s)
     po = oracle.Rulebook(oa.out_coords, oa.out_grid, pool.f, pool.s)
     yp, gp, am = scn.maxpool_fwd(pg, dev(x2), dev(g2))
     yp_ref, gp_ref, ak_ref, _ = oracle.maxpool_fwd(po, x2, g2)
     assert pg.a_out < pg.a_in  # shrinkage (Figure 1)
-    assert np.array_equal(host(yp), yp_ref.astype(np.float32))
-    assert np.array_equal(host(am).astype(np.int32), ak_ref)
+    assert_exact("pool y", host(yp), yp_ref.astype(np.float32))
+    assert_exact("argmax", host(am).astype(np.int32), ak_ref)
 
 
 def test_curve_batch_stack_layerwise(scn):
     """16 closed walks in 64^3; 4 x [2x2x2 conv + ReLU, 2x2x2/2 max-pool],
-    channels 32/64/96/128; every layer forward and backward in isolation."""
+    channels 32/64/96/128; every layer forward and backward in isolation,
+    the backward chained through the oracle's gradients."""
     cfg = make_config(1)
     coords, grid = cfg.coords, cfg.grid
     x, g = _f32(cfg.features), _f32(cfg.g0)
@@ -269,22 +322,23 @@ def test_curve_batch_stack_layerwise(scn):
         oa = o.arrays()
         gr = scn.build_rulebook(dev(np.ascontiguousarray(coords)), grid, L.f, L.s)
         goc, gir, gorr = gr.export()
-        assert np.array_equal(host(goc), oa.out_coords) and np.array_equal(host(gir), oa.in_rows)
-        assert np.array_equal(host(gorr), oa.out_rows)
+        assert_exact(f"layer {li} out_coords", host(goc), oa.out_coords)
+        assert_exact(f"layer {li} in_rows", host(gir), oa.in_rows)
+        assert_exact(f"layer {li} out_rows", host(gorr), oa.out_rows)
         if L.kind == "conv":
             W, b = cfg.weights[li], cfg.biases[li]
             y_ref, go_ref = oracle.conv_fwd(o, x, g, W, b, relu=L.relu)
-            pre_ref, _ = oracle.conv_fwd(o, x, g, W, b, relu=False)
-            sig = np.sqrt(oracle.conv_fwd(o, _sq(x), _sq(g), _sq(W), _sq(b))[0])
+            pre_ref, gpre_ref = oracle.conv_fwd(o, x, g, W, b, relu=False)
             yd, god = scn.conv_fwd(gr, dev(x), dev(g), dev(W), dev(b), relu=L.relu)
-            assert_close(f"layer {li} y", host(yd), y_ref, sig)
-            assert_close(f"layer {li} g", host(god), go_ref)
-            saved.append(dict(o=o, g=gr, x=x, gin=g, pre=pre_ref, sig=sig, W=W, b=b, L=L))
+            assert_site(f"layer {li} y", host(yd), y_ref)
+            assert_site(f"layer {li} g", host(god), go_ref)
+            saved.append(dict(o=o, g=gr, x=x, gin=g, y=y_ref, go=go_ref, pre=pre_ref,
+                              gpre=gpre_ref, W=W, b=b, L=L))
         else:
             y_ref, go_ref, ak_ref, _ = oracle.maxpool_fwd(o, x, g)
             yd, god, am = scn.maxpool_fwd(gr, dev(x), dev(g))
-            assert np.array_equal(host(yd), y_ref.astype(np.float32)), f"layer {li}"
-            assert np.array_equal(host(am).astype(np.int32), ak_ref), f"layer {li}"
+            assert_exact(f"layer {li} pool y", host(yd), y_ref.astype(np.float32))
+            assert_exact(f"layer {li} argmax", host(am).astype(np.int32), ak_ref)
             saved.append(dict(o=o, g=gr, x=x, gin=g, am=am, L=L))
         coords, grid = oa.out_coords, oa.out_grid
         x, g = _f32(y_ref), _f32(go_ref)
@@ -297,44 +351,50 @@ def test_curve_batch_stack_layerwise(scn):
         if L.kind == "pool":
             dx_ref, dgi_ref = oracle.maxpool_bwd(o, S["x"], S["gin"], dy, dg)
             dxd, dgid = scn.maxpool_bwd(gr, S["am"], dev(dy), dev(dg))
-            assert np.array_equal(host(dxd), dx_ref.astype(np.float32)), f"layer {li}"
-            sg = np.sqrt(oracle.maxpool_bwd(o, S["x"], S["gin"], _sq(dy), _sq(dg))[1])
-            assert_close(f"layer {li} dg_in", host(dgid), dgi_ref, sg)
+            assert_exact(f"layer {li} pool dx", host(dxd), dx_ref.astype(np.float32))
+            sg = np.sqrt(oracle.maxpool_bwd(o, S["x"], S["gin"], sq(dy), sq(dg))[1])
+            assert_reduction(f"layer {li} dg_in", host(dgid), dgi_ref, sg)
         else:
-            # output gradient vanishes where the pre-activation is within rounding of 0
-            dy = np.where(np.abs(S["pre"]) <= 1e-3 * (S["sig"] + 1e-30), 0.0, dy).astype(np.float32)
-            _, go_ref = oracle.conv_fwd(o, S["x"], S["gin"], S["W"], S["b"], relu=True)
-            yd, god = scn.conv_fwd(gr, dev(S["x"]), dev(S["gin"]), dev(S["W"]), dev(S["b"]),
-                                   relu=True)
+            # the ReLU mask comes from the oracle's forward on both sides
             ref = oracle.conv_bwd(o, S["x"], S["gin"], S["W"], S["b"], dy, dg, relu=True)
             dyb = dy * (S["pre"] > 0)
-            _, gpre = oracle.conv_fwd(o, S["x"], S["gin"], S["W"], S["b"], relu=False)
-            dgb = dg * (gpre > 0)
+            dgb = dg * (S["gpre"] > 0)
             sig = {k: np.sqrt(v) for k, v in oracle.conv_bwd(
-                o, _sq(S["x"]), _sq(S["gin"]), _sq(S["W"]), None, _sq(dyb), _sq(dgb)).items()}
-            out = scn.conv_bwd(gr, dev(S["x"]), dev(S["gin"]), dev(S["W"]), yd, god, dev(dy),
-                               dev(dg), relu=True)
-            for k in ("dx", "dW", "dbias", "dg_in"):
-                assert_close(f"layer {li} {k}", host(out[k]), ref[k], sig[k])
+                o, sq(S["x"]), sq(S["gin"]), sq(S["W"]), None, sq(dyb), sq(dgb)).items()}
+            out = scn.conv_bwd(gr, dev(S["x"]), dev(S["gin"]), dev(S["W"]), dev(_f32(S["y"])),
+                               dev(_f32(S["go"])), dev(dy), dev(dg), relu=True)
+            assert_site(f"layer {li} dx", host(out["dx"]), ref["dx"])
+            for k in ("dW", "dbias", "dg_in"):
+                assert_reduction(f"layer {li} {k}", host(out[k]), ref[k], sig[k])
             dx_ref, dgi_ref = ref["dx"], ref["dg_in"]
         dy, dg = _f32(dx_ref), _f32(dgi_ref)
 
 
-def test_surfaces_first_levels_interior(scn):
-    """32 voxelised shells in 128^3: first 2x2x2 conv (1->32, ReLU) and first
-    max-pool at full size, compared inside interior sub-boxes."""
+@pytest.fixture(scope="module")
+def surfaces():
     cfg = make_config(2)
-    L0 = cfg.layers[0]
-    oc, og = conv_layer_interior(scn, cfg.coords, cfg.grid, cfg.features, cfg.g0,
-                                 cfg.weights[0], cfg.biases[0], L0.f, L0.s, L0.relu,
-                                 seed=cfg.seed)
-    # pool the first level's active set (from the definition) with seeded features
-    xp = stream_rng(cfg.seed, 9).standard_normal((len(oc), L0.cout)).astype(np.float32)
-    xp[xp < 0] = 0.0  # ReLU-like zeros: many ties with the zero ground state
-    pool_layer_interior(scn, oc, og, xp, np.zeros(L0.cout, np.float32), 2, seed=cfg.seed + 1)
-    # the paper's overlapping 3x3x3 stride-2 pooling on the same level
-    pool_layer_interior(scn, oc, og, xp, np.zeros(L0.cout, np.float32), 3, seed=cfg.seed + 2,
-                        s=2)
+    return cfg, StackChain(cfg)
+
+
+@pytest.mark.parametrize("li", list(range(10)))
+def test_surfaces_layer(scn, surfaces, li):
+    """32 voxelised shells in 128^3, 5 x [2x2x2 conv + ReLU, 2x2x2/2
+    max-pool], channels 32..160: layer li at full size on the definition's
+    sites, forward and backward, against the oracle in a sub-box; the
+    rulebook against its definition."""
+    cfg, chain = surfaces
+    run_stack_layer(scn, cfg, chain, li, _sub_for(cfg.layers[li], 6000))
+
+
+def test_surfaces_overlapping_pool(scn, surfaces):
+    """The paper's overlapping 3x3x3 stride-2 pooling on the first level's
+    active set (ReLU-like features, many ties with the zero ground state)."""
+    cfg, chain = surfaces
+    oc, og = chain.inputs(1)
+    xp = stream_rng(cfg.seed, 9).standard_normal((len(oc), 32)).astype(np.float32)
+    xp[xp < 0] = 0.0
+    pool_layer_interior(scn, oc, og, xp, np.zeros(32, np.float32), 3, seed=cfg.seed + 2, s=2,
+                        defn=definition_rulebook(oc, og, 3, 2))
 
 
 def test_microbenchmark_interior(scn):
@@ -342,25 +402,43 @@ def test_microbenchmark_interior(scn):
     rulebook against its definition; y, dx, dW, dbias, dg_in in sub-boxes."""
     cfg = make_config(3)
     L = cfg.layers[0]
+    defn = definition_rulebook(cfg.coords, cfg.grid, L.f, L.s)
     for i in range(2):
         conv_layer_interior(scn, cfg.coords, cfg.grid, cfg.features, cfg.g0, cfg.weights[0],
                             cfg.biases[0], L.f, L.s, L.relu, seed=cfg.seed + 10 * i,
-                            n_sub=3000, check_def=(i == 0))
+                            n_sub=3000, defn=defn if i == 0 else None)
 
 
-def test_deep_step_first_levels_interior(scn):
-    """8 samples of curve bundles and shells in 256^3 (2-4M sites): the 3x3x3
-    conv (1->64, ReLU), the next 2x2x2 conv (64->96, ReLU) and max-pool."""
+def test_default_dense_view_wide_input(scn):
+    """The 1M-site geometry with 80 input channels (a last 64-channel chunk of
+    one 16-channel step) under the default dense-view policy, which picks the
+    mask-sorted forward for this 3x3x3 layer of 4.4M outputs."""
+    cfg = make_config(3)
+    rng = stream_rng(cfg.seed, 300)
+    Cin, Cout = 80, 48
+    x = rng.standard_normal((len(cfg.coords), Cin), dtype=np.float32)
+    g_in = (rng.standard_normal(Cin) * 0.3).astype(np.float32)
+    W = (rng.standard_normal((27, Cin, Cout)) / np.sqrt(27 * Cin)).astype(np.float32)
+    bias = (rng.standard_normal(Cout) * 0.1).astype(np.float32)
+    g = scn.build_rulebook(dev(cfg.coords), cfg.grid, 3, 1)
+    assert g.dense_view
+    del g
+    conv_layer_interior(scn, cfg.coords, cfg.grid, x, g_in, W, bias, 3, 1, True,
+                        seed=cfg.seed + 30, n_sub=2500)
+
+
+@pytest.fixture(scope="module")
+def deep():
     cfg = make_config(4)
-    L0, L1 = cfg.layers[0], cfg.layers[1]
     assert 2_000_000 <= len(cfg.coords) <= 4_000_000
-    oc, og = conv_layer_interior(scn, cfg.coords, cfg.grid, cfg.features, cfg.g0,
-                                 cfg.weights[0], cfg.biases[0], L0.f, L0.s, L0.relu,
-                                 seed=cfg.seed, n_sub=4000)
-    x1 = stream_rng(cfg.seed, 11).standard_normal((len(oc), L0.cout)).astype(np.float32)
-    oc1, og1 = conv_layer_interior(scn, oc, og, x1, np.zeros(L0.cout, np.float32),
-                                   cfg.weights[1], cfg.biases[1], L1.f, L1.s, L1.relu,
-                                   seed=cfg.seed + 1, n_sub=3000)
-    xp = stream_rng(cfg.seed, 12).standard_normal((len(oc1), L1.cout)).astype(np.float32)
-    pool_layer_interior(scn, oc1, og1, xp, np.full(L1.cout, 0.25, np.float32), 2,
-                        seed=cfg.seed + 2)
+    return cfg, StackChain(cfg)
+
+
+@pytest.mark.parametrize("li", list(range(13)))
+def test_deep_step_layer(scn, deep, li):
+    """8 samples of curve bundles and shells in 256^3 (2-4M sites): the
+    3x3x3 conv (1->64, ReLU) and 6 x [2x2x2 conv + ReLU, 2x2x2/2 max-pool],
+    channels 96..256: layer li at full size on the definition's sites,
+    forward and backward, against the oracle in a sub-box."""
+    cfg, chain = deep
+    run_stack_layer(scn, cfg, chain, li, _sub_for(cfg.layers[li], 4000))

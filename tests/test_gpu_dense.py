@@ -1,10 +1,11 @@
 """GPU parity of the dense-block forward (stride-1 rulebooks that carry the
 mask-sorted view, scn_set_dense_forward) against the oracle, on every
 lattice and across channel counts: one to sixteen 16-channel steps, one to
-four 64-channel chunks, several 64-column blocks, ragged last blocks, ReLU
-on and off, sorted and shuffled inputs.  The same layers with the view
-switched off (the per-offset pair-list forward) agree to rounding; repeated
-calls are bitwise identical."""
+four 64-channel chunks (including last chunks of a single 16-channel step:
+Cin = 80, 136, 200), several 64-column blocks, ragged last blocks, ReLU on and
+off, sorted and shuffled inputs.  The same layers with the view switched off
+(the per-offset pair-list forward) also match the oracle and give the same
+rulebook; repeated calls are bitwise identical."""
 from __future__ import annotations
 
 import math
@@ -17,7 +18,7 @@ torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 from gen import random_sites, stream_rng, tetra_random_sites, tri_random_sites  # noqa: E402
 
-from helpers import assert_close, dev, host  # noqa: E402
+from helpers import assert_site, dev, host  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -48,10 +49,6 @@ def _sites(lattice, rng, B, m, n, shuffle=True):
     return tri_random_sites(rng, B, m, n, shuffle=shuffle), (B, m, m, 1)
 
 
-def _sq(a):
-    return None if a is None else np.asarray(a, np.float64) ** 2
-
-
 CASES = [
     # (lattice, f, B, m, n, Cin, Cout, relu, shuffle)
     ("cubic", 3, 2, 24, 3000, 64, 64, False, True),      # the benchmark's shape, small
@@ -66,6 +63,11 @@ CASES = [
     ("square", 3, 3, 60, 2500, 32, 64, True, True),
     ("triangular", 3, 3, 70, 2400, 64, 32, False, True),
     ("triangular", 2, 1, 9, 45, 8, 8, False, True),       # one block, grid filled
+    # last 64-channel chunk of one 16-channel step (Cin % 64 in 65..80)
+    ("cubic", 3, 1, 18, 1200, 80, 40, True, True),
+    ("cubic", 2, 1, 16, 1000, 136, 64, False, True),
+    ("cubic", 3, 1, 14, 600, 200, 48, True, True),
+    ("tetrahedral", 3, 1, 24, 1500, 80, 72, False, True),
 ]
 
 
@@ -82,11 +84,11 @@ def test_dense_forward_parity(scn, case):
     g = scn.build_rulebook(dev(coords), grid, f, 1, lattice=lattice)
     o = oracle.Rulebook(coords, grid, f, 1, lattice=lattice)
     assert g.a_out == o.arrays().a_out
+    assert g.dense_view
     y_ref, go_ref = oracle.conv_fwd(o, x, g_in, W, bias, relu=relu)
-    sig_y, sig_g = (np.sqrt(v) for v in oracle.conv_fwd(o, _sq(x), _sq(g_in), _sq(W), _sq(bias)))
     yd, god = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias), relu=relu)
-    assert_close("y", host(yd), y_ref, sig_y)
-    assert_close("g_out", host(god), go_ref, sig_g)
+    assert_site("y", host(yd), y_ref)
+    assert_site("g_out", host(god), go_ref)
     # repeated calls: bitwise identical
     yd2, _ = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias), relu=relu)
     assert torch.equal(yd, yd2)
@@ -95,28 +97,31 @@ def test_dense_forward_parity(scn, case):
 @pytest.mark.parametrize("lattice,f", [("cubic", 3), ("cubic", 2), ("tetrahedral", 3),
                                        ("triangular", 3)])
 def test_dense_matches_pair_lists(scn, lattice, f):
-    """The view changes neither the rulebook nor (beyond rounding) the forward."""
+    """The view leaves the rulebook unchanged, and the forward with and
+    without it both match the oracle."""
     rng = stream_rng(171, _K(lattice, f))
     coords, grid = _sites(lattice, rng, 2, 28, 2500)
     Cin, Cout = 32, 48
     K = _K(lattice, f)
-    x = dev(rng.standard_normal((len(coords), Cin)).astype(np.float32))
-    g_in = dev((rng.standard_normal(Cin) * 0.5).astype(np.float32))
-    W = dev((rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin)).astype(np.float32))
-    bias = dev((rng.standard_normal(Cout) * 0.1).astype(np.float32))
+    x = rng.standard_normal((len(coords), Cin)).astype(np.float32)
+    g_in = (rng.standard_normal(Cin) * 0.5).astype(np.float32)
+    W = (rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin)).astype(np.float32)
+    bias = (rng.standard_normal(Cout) * 0.1).astype(np.float32)
     gd = scn.build_rulebook(dev(coords), grid, f, 1, lattice=lattice)
     scn.set_dense_forward(1 << 62, 1)  # no view
     try:
         gp = scn.build_rulebook(dev(coords), grid, f, 1, lattice=lattice)
     finally:
         scn.set_dense_forward(0, 1)
+    assert gd.dense_view and not gp.dense_view
     for a, b in zip(gd.export(), gp.export()):
         assert torch.equal(a, b)
-    yd, god = scn.conv_fwd(gd, x, g_in, W, bias, relu=True)
-    yp, gop = scn.conv_fwd(gp, x, g_in, W, bias, relu=True)
-    assert torch.equal(god, gop)
-    sig = torch.sqrt(scn.conv_fwd(gp, x * x, g_in * g_in, W * W, bias * bias)[0].double())
-    assert_close("y dense vs pair lists", host(yd), host(yp).astype(np.float64), host(sig))
+    o = oracle.Rulebook(coords, grid, f, 1, lattice=lattice)
+    y_ref, go_ref = oracle.conv_fwd(o, x, g_in, W, bias, relu=True)
+    for name, g in (("dense view", gd), ("pair lists", gp)):
+        yd, god = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias), relu=True)
+        assert_site(f"y ({name})", host(yd), y_ref)
+        assert_site(f"g_out ({name})", host(god), go_ref)
 
 
 def test_dense_empty_and_strided(scn):
@@ -133,7 +138,7 @@ def test_dense_empty_and_strided(scn):
     W = (rng.standard_normal((8, 16, 24)) / 8).astype(np.float32)
     g = scn.build_rulebook(dev(coords), grid, 2, 2)
     o = oracle.Rulebook(coords, grid, 2, 2)
+    assert not g.dense_view
     y_ref, _ = oracle.conv_fwd(o, x, g_in, W, None)
-    sig = np.sqrt(oracle.conv_fwd(o, _sq(x), _sq(g_in), _sq(W), None)[0])
     yd, _ = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), None)
-    assert_close("y strided", host(yd), y_ref, sig)
+    assert_site("y strided", host(yd), y_ref)

@@ -18,7 +18,7 @@ torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 from gen import stream_rng, tetra_random_sites, tetra_shell_sites  # noqa: E402
 
-from helpers import assert_close, dev, host  # noqa: E402
+from helpers import conv_parity, dev, host, pool_parity  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 T = "tetrahedral"
@@ -124,10 +124,6 @@ CONV_CASES = [
 ]
 
 
-def _sq(a):
-    return None if a is None else np.asarray(a, np.float64) ** 2
-
-
 @pytest.mark.parametrize("case", CONV_CASES, ids=[str(i) for i in range(len(CONV_CASES))])
 def test_conv_fwd_bwd_parity(scn, case):
     f, s, B, m, n, Cin, Cout, relu = case
@@ -141,26 +137,7 @@ def test_conv_fwd_bwd_parity(scn, case):
     bias = (rng.standard_normal(Cout) * 0.1).astype(np.float32)
     g, o = _pair(scn, coords, (B, m, m, m), f, s)
     _check_rulebook(g, o)
-    y_ref, go_ref = oracle.conv_fwd(o, x, g_in, W, bias, relu=relu)
-    pre_ref, gpre_ref = oracle.conv_fwd(o, x, g_in, W, bias, relu=False)
-    sig_y, sig_g = (np.sqrt(v) for v in oracle.conv_fwd(o, _sq(x), _sq(g_in), _sq(W), _sq(bias)))
-    yd, god = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias), relu=relu)
-    assert_close("y", host(yd), y_ref, sig_y)
-    assert_close("g_out", host(god), go_ref, sig_g)
-    rng = stream_rng(seed, 2)
-    dy = rng.uniform(-1, 1, size=(g.a_out, Cout)).astype(np.float32)
-    dg = rng.uniform(-1, 1, size=Cout).astype(np.float32)
-    if relu:
-        dy[np.abs(pre_ref) <= 1e-3 * (sig_y + 1e-30)] = 0.0
-        dg[np.abs(gpre_ref) <= 1e-3 * (sig_g + 1e-30)] = 0.0
-    ref = oracle.conv_bwd(o, x, g_in, W, bias, dy, dg, relu=relu)
-    dyb = dy * (pre_ref > 0) if relu else dy
-    dgb = dg * (gpre_ref > 0) if relu else dg
-    sig = {k: np.sqrt(v) for k, v in
-           oracle.conv_bwd(o, _sq(x), _sq(g_in), _sq(W), None, _sq(dyb), _sq(dgb)).items()}
-    out = scn.conv_bwd(g, dev(x), dev(g_in), dev(W), yd, god, dev(dy), dev(dg), relu=relu)
-    for k in ("dx", "dW", "dbias", "dg_in"):
-        assert_close(k, host(out[k]), ref[k], sig[k])
+    conv_parity(scn, g, o, x, g_in, W, bias, relu, seed)
 
 
 def test_conv_rejects_cubic_weights(scn):
@@ -197,22 +174,7 @@ def test_maxpool_parity(scn, case):
     g_in = (np.abs(rng.standard_normal(C)) * gs).astype(np.float32)
     g, o = _pair(scn, coords, (B, m, m, m), f, s)
     _check_rulebook(g, o)
-    y_ref, go_ref, ak_ref, _ = oracle.maxpool_fwd(o, x, g_in)
-    yd, god, am = scn.maxpool_fwd(g, dev(x), dev(g_in))
-    assert np.array_equal(host(yd), y_ref.astype(np.float32))
-    assert np.array_equal(host(god), go_ref.astype(np.float32))
-    assert np.array_equal(host(am).astype(np.int32), ak_ref)
-    dy = rng.uniform(-1, 1, size=(g.a_out, C)).astype(np.float32)
-    dg = rng.uniform(-1, 1, size=C).astype(np.float32)
-    dx_ref, dgi_ref = oracle.maxpool_bwd(o, x, g_in, dy, dg)
-    dxd, dgid = scn.maxpool_bwd(g, am, dev(dy), dev(dg))
-    if f <= s:
-        assert np.array_equal(host(dxd), dx_ref.astype(np.float32))
-    else:
-        sig_dx = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), None)[0])
-        assert_close("dx", host(dxd), dx_ref, sig_dx)
-    sig = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), _sq(dg))[1])
-    assert_close("dg_in", host(dgid), dgi_ref, sig)
+    pool_parity(scn, g, o, x, g_in, rng, f > s)
 
 
 # --------------------------------------------------------------------------

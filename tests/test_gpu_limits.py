@@ -12,7 +12,7 @@ torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 from gen import random_sites, stream_rng  # noqa: E402
 
-from helpers import assert_close, dev, host  # noqa: E402
+from helpers import conv_parity, dev, host, pool_parity  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -62,10 +62,6 @@ def test_one_word_past_the_bitmap_limit(scn):
     assert e.value.status == "unsupported"
 
 
-def _sq(a):
-    return None if a is None else np.asarray(a, np.float64) ** 2
-
-
 @pytest.mark.parametrize("f", [2, 3])
 def test_widest_layers(scn, f):
     """256 input and 256 output channels (the largest the library takes)."""
@@ -80,18 +76,7 @@ def test_widest_layers(scn, f):
     grid = (1, 20, 18, 16)
     g = scn.build_rulebook(dev(coords), grid, f, 1)
     o = oracle.Rulebook(coords, grid, f, 1)
-    y_ref, go_ref = oracle.conv_fwd(o, x, g_in, W, bias)
-    sig_y, sig_g = (np.sqrt(v) for v in oracle.conv_fwd(o, _sq(x), _sq(g_in), _sq(W), _sq(bias)))
-    yd, god = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), dev(bias))
-    assert_close("y", host(yd), y_ref, sig_y)
-    assert_close("g_out", host(god), go_ref, sig_g)
-    dy = stream_rng(83, f).uniform(-1, 1, size=(g.a_out, Cout)).astype(np.float32)
-    ref = oracle.conv_bwd(o, x, g_in, W, bias, dy, None)
-    sig = {k: np.sqrt(v) for k, v in
-           oracle.conv_bwd(o, _sq(x), _sq(g_in), _sq(W), None, _sq(dy), None).items()}
-    out = scn.conv_bwd(g, dev(x), dev(g_in), dev(W), None, None, dev(dy), None)
-    for k in ("dx", "dW", "dbias", "dg_in"):
-        assert_close(k, host(out[k]), ref[k], sig[k])
+    conv_parity(scn, g, o, x, g_in, W, bias, False, 83 + f)
 
 
 def test_too_wide_layers_are_refused(scn):
@@ -115,15 +100,4 @@ def test_pooling_channel_extremes(scn, C, f, s):
     grid = (1, 12, 11, 10)
     g = scn.build_rulebook(dev(coords), grid, f, s)
     o = oracle.Rulebook(coords, grid, f, s)
-    y_ref, go_ref, ak_ref, _ = oracle.maxpool_fwd(o, x, g_in)
-    yd, god, am = scn.maxpool_fwd(g, dev(x), dev(g_in))
-    assert np.array_equal(host(yd), y_ref.astype(np.float32))
-    assert np.array_equal(host(am).astype(np.int32), ak_ref)
-    dy = rng.uniform(-1, 1, size=(g.a_out, C)).astype(np.float32)
-    dg = rng.uniform(-1, 1, size=C).astype(np.float32)
-    dx_ref, dgi_ref = oracle.maxpool_bwd(o, x, g_in, dy, dg)
-    dxd, dgid = scn.maxpool_bwd(g, am, dev(dy), dev(dg))
-    sig_dx = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), None)[0])
-    assert_close("dx", host(dxd), dx_ref, sig_dx)
-    sig = np.sqrt(oracle.maxpool_bwd(o, x, g_in, _sq(dy), _sq(dg))[1])
-    assert_close("dg_in", host(dgid), dgi_ref, sig)
+    pool_parity(scn, g, o, x, g_in, rng, f > s)

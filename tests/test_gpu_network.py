@@ -15,7 +15,7 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
 import oracle  # noqa: E402
 from gen import image_patch_sites, shell_sites, stream_rng, tetra_shell_sites  # noqa: E402
-from helpers import dev, host  # noqa: E402
+from helpers import assert_exact, assert_site, dev, host  # noqa: E402
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -69,13 +69,12 @@ def test_network_matches_oracle_chain(scn, lattice, levels, width, scale):
             xr, g, _, _ = oracle.maxpool_fwd(o, xr, g)
         c, grid = o.arrays().out_coords, tuple(o.out_grid)
 
-    assert np.array_equal(host(oc), c)
+    assert_exact("final sites", host(oc), c)
     # one final site per sample whose shell survives the network
     assert len(c) == batch and np.array_equal(c[:, 0], np.arange(batch))
-    got = host(out).astype(np.float64)
-    scale_ref = np.sqrt(np.mean(xr ** 2)) + 1e-30
-    err = np.abs(got - xr)
-    assert np.all(err <= 1e-5 + 1e-4 * np.maximum(np.abs(xr), scale_ref)), err.max()
+    # every class score, elementwise (the chain carries fp32 rounding through
+    # all layers on the library's side)
+    assert_site("scores", host(out), xr)
 
 
 @pytest.mark.parametrize("lattice,levels,patch", [("square", 1, 5), ("triangular", 1, 4),
@@ -104,9 +103,6 @@ def test_planar_network_matches_oracle_chain(scn, lattice, levels, patch):
         else:
             xr, g, _, _ = oracle.maxpool_fwd(o, xr, g)
         c, grid = o.arrays().out_coords, tuple(o.out_grid)
-    assert np.array_equal(host(oc), c)
+    assert_exact("final sites", host(oc), c)
     assert len(c) == batch
-    got = host(out).astype(np.float64)
-    scale_ref = np.sqrt(np.mean(xr ** 2)) + 1e-30
-    err = np.abs(got - xr)
-    assert np.all(err <= 1e-5 + 1e-4 * np.maximum(np.abs(xr), scale_ref)), err.max()
+    assert_site("scores", host(out), xr)
