@@ -241,6 +241,29 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
                         const float* W, const float* bias, int32_t Cin, int32_t Cout,
                         uint32_t flags, float* y, float* g_out, hipStream_t stream);
 
+/*
+ * scn_conv_fwd for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation and result, bit for bit, with the
+ * forward's scratch (the ground-state terms and the packed weights) in a
+ * static device array of scn_conv_fwd_noalloc_max_bytes() bytes (8 MiB) that
+ * the library holds on each GPU it runs on until the process ends.  The call
+ * allocates nothing; the caller still passes every input and output.
+ * Scratch needed: 4*((K+1)*NcP rounded up to 64 floats + K*NcP*RkP) bytes
+ * with NcP = 64*ceil(Cout/64) and RkP = 16*ceil(Cin/16); every 3x3x3 layer
+ * with Cin, Cout <= 256 fits.  Larger shapes return SCN_ERR_WORKSPACE before
+ * any device work.  All calls on one GPU share its array: calls that overlap
+ * on a GPU (on different streams, or from several threads without stream
+ * order between them) race and give undefined results; calls ordered on one
+ * stream do not.  Errors: as scn_conv_fwd, and SCN_ERR_WORKSPACE.
+ */
+scn_status scn_conv_fwd_noalloc(const scn_rulebook* rb, const float* x, const float* g_in,
+                                const float* W, const float* bias, int32_t Cin, int32_t Cout,
+                                uint32_t flags, float* y, float* g_out, hipStream_t stream);
+
+/* Size in bytes of the static scratch array of scn_conv_fwd_noalloc. */
+size_t scn_conv_fwd_noalloc_max_bytes(void);
+
 /* Bytes of device workspace scn_conv_bwd needs for this rulebook and shape. */
 size_t scn_conv_bwd_workspace_bytes(const scn_rulebook* rb, int32_t Cin, int32_t Cout,
                                     uint32_t flags);

@@ -33,7 +33,8 @@ EXPORTED = (
     "scn_rulebook_export", "scn_rulebook_free", "scn_conv_fwd",
     "scn_conv_bwd_workspace_bytes", "scn_conv_bwd", "scn_maxpool_fwd",
     "scn_maxpool_bwd_workspace_bytes", "scn_maxpool_bwd", "scn_set_allocator",
-    "scn_set_dense_forward", "scn_last_error", "scn_version",
+    "scn_set_dense_forward", "scn_last_error", "scn_version", "scn_conv_fwd_noalloc",
+    "scn_conv_fwd_noalloc_max_bytes",
 )
 
 _ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
@@ -85,6 +86,8 @@ def lib() -> ctypes.CDLL:
         "scn_rulebook_export": (st, [P, P, P, P, P]),
         "scn_rulebook_free": (None, [P]),
         "scn_conv_fwd": (st, [P, P, P, P, P, i32, i32, u32, P, P, P]),
+        "scn_conv_fwd_noalloc": (st, [P, P, P, P, P, i32, i32, u32, P, P, P]),
+        "scn_conv_fwd_noalloc_max_bytes": (sz, []),
         "scn_conv_bwd_workspace_bytes": (sz, [P, i32, i32, u32]),
         "scn_conv_bwd": (st, [P, P, P, P, P, P, P, P, i32, i32, u32, P, P, P, P, P, sz, P]),
         "scn_maxpool_fwd": (st, [P, P, P, i32, P, P, P, P]),
@@ -224,8 +227,12 @@ def next_rulebook(prev: Rulebook, filter: int, stride: int) -> Rulebook:
 
 
 def conv_fwd(rb: Rulebook, x: torch.Tensor, g_in: torch.Tensor, W: torch.Tensor,
-             bias: Optional[torch.Tensor] = None, relu: bool = False):
-    """Returns (y [a_out, Cout], g_out [Cout])."""
+             bias: Optional[torch.Tensor] = None, relu: bool = False,
+             y: Optional[torch.Tensor] = None, g_out: Optional[torch.Tensor] = None,
+             noalloc: bool = False):
+    """Returns (y [a_out, Cout], g_out [Cout]); y and g_out are allocated here
+    unless given.  noalloc=True calls scn_conv_fwd_noalloc (the library then
+    allocates nothing)."""
     K, Cin, Cout = (int(v) for v in W.shape)
     if K != rb.K:
         raise ValueError(f"W has {K} offsets, rulebook has {rb.K}")
@@ -234,11 +241,16 @@ def conv_fwd(rb: Rulebook, x: torch.Tensor, g_in: torch.Tensor, W: torch.Tensor,
     _dev_tensor(g_in, torch.float32, (Cin,), "g_in")
     if bias is not None:
         _dev_tensor(bias, torch.float32, (Cout,), "bias")
-    y = torch.empty((rb.a_out, Cout), dtype=torch.float32, device=x.device)
-    g_out = torch.empty(Cout, dtype=torch.float32, device=x.device)
-    _check(lib().scn_conv_fwd(rb.handle, _ptr(x), _ptr(g_in), _ptr(W), _ptr(bias), Cin, Cout,
-                              SCN_RELU if relu else 0, _ptr(y), _ptr(g_out),
-                              ctypes.c_void_p(_stream())), "scn_conv_fwd")
+    if y is None:
+        y = torch.empty((rb.a_out, Cout), dtype=torch.float32, device=x.device)
+    _dev_tensor(y, torch.float32, (rb.a_out, Cout), "y")
+    if g_out is None:
+        g_out = torch.empty(Cout, dtype=torch.float32, device=x.device)
+    _dev_tensor(g_out, torch.float32, (Cout,), "g_out")
+    name = "scn_conv_fwd_noalloc" if noalloc else "scn_conv_fwd"
+    _check(getattr(lib(), name)(rb.handle, _ptr(x), _ptr(g_in), _ptr(W), _ptr(bias), Cin, Cout,
+                                SCN_RELU if relu else 0, _ptr(y), _ptr(g_out),
+                                ctypes.c_void_p(_stream())), name)
     return y, g_out
 
 

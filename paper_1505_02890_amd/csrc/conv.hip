@@ -31,6 +31,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "scn_internal.h"
 
@@ -1345,39 +1346,47 @@ BwdLayout bwd_layout(const scn_rulebook* rb, int Cin, int Cout, uint32_t flags) 
 
 using namespace scn;
 
-extern "C" {
+// The forward's scratch: gw [K][NcP] and g_pre [NcP] (256-byte aligned),
+// then the packed weights [K][NcP][RkP].  Every element is written by the
+// forward's first kernels before any is read.
+struct FwdScratch {
+  int RkP, NcP;
+  size_t gw_bytes, total;
+};
 
-scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_in,
-                        const float* W, const float* bias, int32_t Cin, int32_t Cout,
-                        uint32_t flags, float* y, float* g_out, hipStream_t st) {
-  clear_error();
-  if (scn_status rc0 = after_build(rb, st)) return rc0;
+static FwdScratch fwd_scratch(const scn_rulebook* rb, int Cin, int Cout) {
+  FwdScratch f;
+  f.RkP = (int)ceil_div(Cin, 16) * 16;
+  f.NcP = (int)ceil_div(Cout, 64) * 64;
+  f.gw_bytes = ((size_t)(rb->K + 1) * f.NcP * sizeof(float) + 255) & ~size_t(255);
+  f.total = f.gw_bytes + (size_t)rb->K * f.NcP * f.RkP * sizeof(float);
+  return f;
+}
+
+static scn_status fwd_check(const char* who, const scn_rulebook* rb, const float* x,
+                            const float* g_in, const float* W, int32_t Cin, int32_t Cout,
+                            float* y, float* g_out) {
   if (!rb || !g_in || !W || !g_out || Cin < 1 || Cout < 1 || (rb->a_in > 0 && !x) ||
       (rb->a_out > 0 && !y)) {
-    set_error("scn_conv_fwd: invalid argument");
+    set_error("%s: invalid argument", who);
     return SCN_ERR_INVALID;
   }
   if (Cin > 256) {
-    set_error("scn_conv_fwd: Cin %d > 256 is not supported", Cin);
+    set_error("%s: Cin %d > 256 is not supported", who, Cin);
     return SCN_ERR_UNSUPPORTED;
   }
+  return SCN_OK;
+}
+
+// Steps 2-3 with the ground state, on a scratch block laid out as FwdScratch.
+static scn_status fwd_run(const scn_rulebook* rb, const float* x, const float* g_in,
+                          const float* W, const float* bias, int32_t Cin, int32_t Cout,
+                          uint32_t flags, float* y, float* g_out, hipStream_t st,
+                          const FwdScratch& fs, float* gw) {
   const int relu = (flags & SCN_RELU) ? 1 : 0;
-  // scratch: gw [K][NcP], g_pre [NcP] and the packed weights [K][NcP][RkP]
-  const int RkP = (int)ceil_div(Cin, 16) * 16, NcP = (int)ceil_div(Cout, 64) * 64;
-  const size_t gw_bytes = ((size_t)(rb->K + 1) * NcP * sizeof(float) + 255) & ~size_t(255);
-  float* gw = nullptr;
-  const Allocator al = current_allocator();
-  scn_status rc = dalloc(reinterpret_cast<void**>(&gw),
-                         gw_bytes + (size_t)rb->K * NcP * RkP * sizeof(float), st, al);
-  if (rc) return rc;
-  struct Free {
-    float* p;
-    hipStream_t s;
-    Allocator al;
-    ~Free() { dfree(p, s, al); }
-  } free_gw{gw, st, al};
+  const int RkP = fs.RkP, NcP = fs.NcP;
   float* const gpre = gw + (size_t)rb->K * NcP;
-  float* Wp = reinterpret_cast<float*>(reinterpret_cast<char*>(gw) + gw_bytes);
+  float* Wp = reinterpret_cast<float*>(reinterpret_cast<char*>(gw) + fs.gw_bytes);
   hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)ceil_div((int64_t)rb->K * NcP * RkP, 256)),
                      dim3(256), 0, st, W, rb->K, Cin, Cout, 1, RkP, NcP, Wp);
   SCN_LAUNCH_CHECK();
@@ -1425,6 +1434,82 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
   a.nrows = rb->a_out;
   a.K = rb->K;
   return launch_gather(a, st);
+}
+
+// Scratch of scn_conv_fwd_noalloc: one array per GPU the library runs on,
+// held until the process ends.  In host code its name is not a device
+// address; the address each device gives it (hipGetSymbolAddress, once per
+// device) is what kernels and copies get.
+constexpr size_t NOALLOC_SCRATCH_BYTES = size_t(8) << 20;
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+static std::mutex g_scratch_mutex;
+static void* g_scratch_ptr[64] = {};
+
+static scn_status noalloc_scratch(void** out) {
+  int dev = 0;
+  SCN_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) {
+    set_error("scn_conv_fwd_noalloc: device %d out of range", dev);
+    return SCN_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    SCN_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) {
+      set_error("scn_conv_fwd_noalloc: no device address for the scratch array");
+      return SCN_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SCN_OK;
+}
+
+extern "C" {
+
+scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_in,
+                        const float* W, const float* bias, int32_t Cin, int32_t Cout,
+                        uint32_t flags, float* y, float* g_out, hipStream_t st) {
+  clear_error();
+  if (scn_status rc0 = after_build(rb, st)) return rc0;
+  if (scn_status rc0 = fwd_check("scn_conv_fwd", rb, x, g_in, W, Cin, Cout, y, g_out))
+    return rc0;
+  const FwdScratch fs = fwd_scratch(rb, Cin, Cout);
+  float* gw = nullptr;
+  const Allocator al = current_allocator();
+  scn_status rc = dalloc(reinterpret_cast<void**>(&gw), fs.total, st, al);
+  if (rc) return rc;
+  struct Free {
+    float* p;
+    hipStream_t s;
+    Allocator al;
+    ~Free() { dfree(p, s, al); }
+  } free_gw{gw, st, al};
+  return fwd_run(rb, x, g_in, W, bias, Cin, Cout, flags, y, g_out, st, fs, gw);
+}
+
+size_t scn_conv_fwd_noalloc_max_bytes(void) { return NOALLOC_SCRATCH_BYTES; }
+
+scn_status scn_conv_fwd_noalloc(const scn_rulebook* rb, const float* x, const float* g_in,
+                                const float* W, const float* bias, int32_t Cin, int32_t Cout,
+                                uint32_t flags, float* y, float* g_out, hipStream_t st) {
+  clear_error();
+  if (scn_status rc0 = after_build(rb, st)) return rc0;
+  if (scn_status rc0 = fwd_check("scn_conv_fwd_noalloc", rb, x, g_in, W, Cin, Cout, y, g_out))
+    return rc0;
+  const FwdScratch fs = fwd_scratch(rb, Cin, Cout);
+  if (fs.total > NOALLOC_SCRATCH_BYTES) {
+    set_error("scn_conv_fwd_noalloc: K=%d Cin=%d Cout=%d needs %zu bytes of scratch, more than "
+              "the %zu the library holds",
+              rb->K, Cin, Cout, fs.total, NOALLOC_SCRATCH_BYTES);
+    return SCN_ERR_WORKSPACE;
+  }
+  void* base = nullptr;
+  if (scn_status rc0 = noalloc_scratch(&base)) return rc0;
+  return fwd_run(rb, x, g_in, W, bias, Cin, Cout, flags, y, g_out, st, fs,
+                 static_cast<float*>(base));
 }
 
 size_t scn_conv_bwd_workspace_bytes(const scn_rulebook* rb, int32_t Cin, int32_t Cout,
