@@ -9,15 +9,16 @@ gradients, with all inputs already resident in device memory.
 
 Printed (one JSON line): effective GFLOP/s counting active pairs only
 (3 contractions of 2*P*Cin*Cout flops per step), rulebook Msites/s and its
-HBM fraction, per-phase times, the fraction of the fp32 MFMA peak of each
-contraction (the input and weight gradients also timed alone) and of the
-step's forward and backward together, the roofline of the dominant kernel
-(the forward dense-block contraction, timed with HIP events on its stream),
-max-pooling phases on the
-convolution's output, and the CPU oracle timed on a bounded sample of the
-same workload.
+HBM fraction, per-phase times, each contraction kernel's own duration
+(HIP events the library records around it on its stream, scn_set_kernel_timer)
+and its fraction of the fp32 MFMA peak, the roofline of the dominant kernel
+(the forward dense-block contraction), measured ceilings (a streaming copy,
+a register-only MFMA loop), max-pooling phases on the convolution's output,
+whole-step timings of the other four workloads (the trefoil forward; the
+curve, surface and deep stacks forward + backward), and the CPU oracle timed
+on bounded samples of the same workload on one core and on all cores.
 
-    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--no-cpu]
+    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--no-cpu] [--no-configs]
 
 With --network it instead times whole-network inference of the paper's
 networks (the nC2-MP3/2 object-recognition networks at scales 20/40/80 on the
@@ -50,7 +51,11 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-sites", type=int, default=60000,
-                   help="input sites of the bounded CPU-oracle sample")
+                   help="input sites of the bounded one-core CPU-oracle sample")
+    p.add_argument("--cpu-sites-each", type=int, default=25000,
+                   help="input sites per process of the all-core CPU-oracle sample")
+    p.add_argument("--no-configs", action="store_true",
+                   help="skip the whole-step timings of the other four workloads")
     p.add_argument("--network", action="store_true",
                    help="instead: whole-network inference throughput of the paper's "
                         "networks (3D object recognition on the cubic and tetrahedral "
@@ -87,49 +92,118 @@ def measured_traffic():
     return float(kv["traffic_bytes"])
 
 
-def cpu_baseline(cfg, n_sites: int):
-    """The oracle (single-threaded, fp64, naive loops) on the sites of the
-    workload inside a sub-box holding about n_sites sites: rulebook + forward
-    + backward, reported in the same unit as the GPU value."""
-    import oracle
-    from gen import make_dy
-
-    c = cfg.coords
-    m = cfg.grid[1]
-    # grow a centred cube until it holds enough sites
-    centre = np.median(c[:, 1:4], axis=0)
+def _centred_sample(c, m, n_sites, centre):
+    """Sites in the smallest cube around `centre` that holds >= n_sites."""
     lo_h, hi_h = 1, m
     while lo_h < hi_h:
         h = (lo_h + hi_h) // 2
-        sel = np.all(np.abs(c[:, 1:4] - centre) <= h, axis=1)
-        if sel.sum() >= n_sites:
+        if np.all(np.abs(c[:, 1:4] - centre) <= h, axis=1).sum() >= n_sites:
             hi_h = h
         else:
             lo_h = h + 1
-    sel = np.all(np.abs(c[:, 1:4] - centre) <= lo_h, axis=1)
-    coords = c[sel]
-    x = cfg.features[sel]
-    W = cfg.weights[0]
-    L = cfg.layers[0]
+    return np.all(np.abs(c[:, 1:4] - centre) <= lo_h, axis=1), lo_h
+
+
+def _oracle_step(coords, grid, x, g0, W, bias, f, s, dy_seed):
+    """The oracle (fp64, naive loops) on one sample: rulebook, forward,
+    backward.  Returns (flops, rulebook s, forward s, backward s, a_out, P)."""
+    import oracle
+    from gen import make_dy
+
     t0 = time.perf_counter()
-    rb = oracle.Rulebook(coords, cfg.grid, L.f, L.s)
+    rb = oracle.Rulebook(coords, grid, f, s)
     t1 = time.perf_counter()
-    y, g = oracle.conv_fwd(rb, x, cfg.g0, W, cfg.biases[0])
+    oracle.conv_fwd(rb, x, g0, W, bias)
     t2 = time.perf_counter()
-    dy = make_dy(cfg.seed + 1000, rb.a_out, L.cout)
-    oracle.conv_bwd(rb, x, cfg.g0, W, cfg.biases[0], dy, None)
+    dy = make_dy(dy_seed, rb.a_out, W.shape[2])
+    oracle.conv_bwd(rb, x, g0, W, bias, dy, None)
     t3 = time.perf_counter()
-    flops = 3 * 2.0 * rb.n_pairs * L.cin * L.cout
-    return {
-        "value": round(flops / (t3 - t0) / 1e9, 4),
-        "unit": "GFLOP/s",
-        "cores": 1,
+    flops = 3 * 2.0 * rb.n_pairs * W.shape[1] * W.shape[2]
+    return flops, t1 - t0, t2 - t1, t3 - t2, rb.a_out, rb.n_pairs
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, n_sites: int, n_sites_each: int):
+    """The oracle, as it stands, on the host: (1) one thread on the sites of
+    the workload inside a centred cube of about n_sites sites; (2) every
+    available core (one process each, at most 16) on disjoint cubes of about
+    n_sites_each sites around different centres, timed together.  Each runs
+    rulebook + forward + backward; the value is in the GPU's unit."""
+    import multiprocessing
+    from concurrent.futures import ProcessPoolExecutor
+
+    c = cfg.coords
+    m = cfg.grid[1]
+    L = cfg.layers[0]
+    args = (cfg.g0, cfg.weights[0], cfg.biases[0], L.f, L.s)
+    sel, h = _centred_sample(c, m, n_sites, np.median(c[:, 1:4], axis=0))
+    fl, trb, tf, tb, a_out, P = _oracle_step(c[sel], cfg.grid, cfg.features[sel], *args[:3],
+                                             L.f, L.s, cfg.seed + 1000)
+    single = {
+        "value": round(fl / (trb + tf + tb) / 1e9, 4), "unit": "GFLOP/s", "cores": 1,
         "kind": "oracle",
-        "sample": (f"{len(coords)} of the {len(c)} input sites (those in a centred "
-                   f"cube of half-width {lo_h}), a_out={rb.a_out}, pairs={rb.n_pairs}; "
-                   f"rulebook {t1 - t0:.2f}s, forward {t2 - t1:.2f}s, backward {t3 - t2:.2f}s"),
-        "rulebook_msites_per_s": round(len(coords) / (t1 - t0) / 1e6, 4),
+        "sample": (f"{int(sel.sum())} of the {len(c)} input sites (a centred cube of half-width "
+                   f"{h}), a_out={a_out}, pairs={P}; rulebook {trb:.2f}s, forward {tf:.2f}s, "
+                   f"backward {tb:.2f}s"),
+        "rulebook_msites_per_s": round(int(sel.sum()) / trb / 1e6, 4),
     }
+    # all cores: disjoint cubes around well-separated active sites
+    try:
+        ncpu = len(os.sched_getaffinity(0))
+    except AttributeError:
+        ncpu = os.cpu_count() or 1
+    workers = max(1, min(16, ncpu))
+    rng = np.random.default_rng(cfg.seed + 77)
+    jobs, taken = [], np.zeros(len(c), bool)
+    for i in rng.permutation(len(c)):
+        if len(jobs) == workers:
+            break
+        if taken[i]:
+            continue
+        s_i, _ = _centred_sample(c, m, n_sites_each, c[i, 1:4])
+        if np.any(s_i & taken):
+            continue
+        taken |= s_i
+        jobs.append((np.ascontiguousarray(c[s_i]), tuple(cfg.grid),
+                     np.ascontiguousarray(cfg.features[s_i])) + args + (cfg.seed + 2000 + i,))
+    ctx = multiprocessing.get_context("spawn")
+    with ProcessPoolExecutor(max_workers=len(jobs), mp_context=ctx) as ex:
+        # the workers' start-up (interpreter, numpy, oracle library) stays
+        # outside the timed region
+        list(ex.map(_warm, range(len(jobs))))
+        t0 = time.perf_counter()
+        res = list(ex.map(_oracle_job, jobs))
+        wall = time.perf_counter() - t0
+    tot = sum(r[0] for r in res)
+    sites = sum(len(j[0]) for j in jobs)
+    allcore = {
+        "value": round(tot / wall / 1e9, 4), "unit": "GFLOP/s", "cores": len(jobs),
+        "kind": "oracle",
+        "sample": (f"{len(jobs)} disjoint cubes of about {n_sites_each} input sites each "
+                   f"({sites} sites, {sum(r[5] for r in res)} pairs), one process per core, "
+                   f"wall {wall:.2f}s"),
+        "host_cpus": ncpu, "cpu_model": _cpu_model(),
+    }
+    return single, allcore
+
+
+def _warm(_):
+    import oracle  # noqa: F401
+    return 0
+
+
+def _oracle_job(job):
+    coords, grid, x, g0, W, bias, f, s, seed = job
+    return _oracle_step(coords, grid, x, g0, W, bias, f, s, seed)
 
 
 def _time_net(net, cd, xd, batch_n, reps, warmup):
@@ -219,6 +293,172 @@ def network_bench(batch: int, reps: int, warmup: int) -> None:
         }), flush=True)
 
 
+class KernelTimer:
+    """Pairs of HIP events the library records around its contraction
+    kernels (scn_set_kernel_timer): forward, input gradient, weight
+    gradient, one set per timed step."""
+
+    def __init__(self, scn, stream, n):
+        import torch
+
+        self.scn, self.stream = scn, stream
+        self.sets = []
+        for _ in range(n):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+            for e in ev:
+                e.record(stream)  # creates the HIP event
+            self.sets.append(ev)
+        torch.cuda.synchronize()
+        self.i = 0
+
+    def arm(self):
+        import ctypes
+
+        ev = self.sets[self.i]
+        self.i += 1
+        arr = (ctypes.c_void_p * 6)(*[e.cuda_event for e in ev])
+        self.scn.lib().scn_set_kernel_timer(arr)
+
+    def disarm(self):
+        self.scn.lib().scn_set_kernel_timer(None)
+
+    def ms(self, which):
+        j = {"fwd": 0, "dx": 2, "dw": 4}[which]
+        return [ev[j].elapsed_time(ev[j + 1]) for ev in self.sets[:self.i]]
+
+
+def ceilings(scn, dev):
+    """Measured ceilings: a 1 GiB streaming copy (HBM) and a register-only
+    loop of fp32 MFMA products (matrix cores), median of 10 each."""
+    import ctypes
+
+    import torch
+
+    stream = torch.cuda.current_stream()
+    nbytes = 1 << 30
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    L = scn.lib()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+
+    def timed(fn, reps=10):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return statistics.median(ts)
+
+    def copy():
+        assert L.scn_ceiling_copy(ctypes.c_void_p(a.data_ptr()), ctypes.c_void_p(b.data_ptr()),
+                                  nbytes, sp) == 0
+
+    copy_ms = timed(copy)
+    assert torch.equal(a[:1024], b[:1024])
+    out = torch.empty(4 * 2048, dtype=torch.float32, device=dev)
+    flops = ctypes.c_double()
+
+    def mfma():
+        assert L.scn_ceiling_mfma_f32(ctypes.c_void_p(out.data_ptr()), 2048, 4096,
+                                      ctypes.byref(flops), sp) == 0
+
+    mfma_ms = timed(mfma)
+    copy_gbs = 2.0 * nbytes / (copy_ms / 1e3) / 1e9
+    mfma_tf = flops.value / (mfma_ms / 1e3) / 1e12
+    return {
+        "hbm_copy": {"bytes_moved": 2 * nbytes, "ms": round(copy_ms, 4),
+                     "gbs": round(copy_gbs, 1), "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4)},
+        "mfma_f32_loop": {"flops": flops.value, "ms": round(mfma_ms, 4),
+                          "tflops": round(mfma_tf, 2),
+                          "frac_of_peak": round(mfma_tf / MFMA_FP32_PEAK_TFLOPS, 4)},
+    }
+
+
+CONFIG_WORKLOADS = {
+    0: "one knotted closed lattice walk (400 steps) in 32^3; C2 1->16 -> MP2/2; forward",
+    1: "16 closed lattice walks in 64^3; 4 x [C2 + ReLU -> MP2/2], ch 32/64/96/128; fwd + bwd",
+    2: "32 voxelised superquadric shells in 128^3; 5 x [C2 + ReLU -> MP2/2], ch 32..160; "
+       "fwd + bwd",
+    4: "8 samples of curve bundles + shells in 256^3; C3 1->64 + ReLU, 6 x [C2 + ReLU -> "
+       "MP2/2], ch 96..256; fwd + bwd",
+}
+
+
+def config_bench(scn, index, reps, warmup):
+    """Whole step of workload `index` (chain of rulebooks, forward and, for
+    the trained stacks, backward from U[-1, 1] output gradients), inputs in
+    HBM; median of `reps` steps."""
+    import torch
+
+    from gen import make_config, make_dy
+    from paper_1505_02890_amd.stack import StackStep, conv_flops
+
+    cfg = make_config(index)
+    dev = torch.device("cuda:0")
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    coords, x = d(cfg.coords), d(cfg.features)
+    Ws = [None if w is None else d(w) for w in cfg.weights]
+    Bs = [None if b is None else d(b) for b in cfg.biases]
+    st = StackStep(cfg.layers, Ws, Bs)
+    dy_cache = {}
+
+    def dy_top(rows, ch):
+        if (rows, ch) not in dy_cache:
+            dy_cache[(rows, ch)] = d(make_dy(cfg.seed, rows, ch))
+        return dy_cache[(rows, ch)]
+
+    stream = torch.cuda.current_stream()
+    names = ("rulebook", "fwd", "bwd") if cfg.backward else ("rulebook", "fwd")
+
+    def one():
+        ev = {"start": torch.cuda.Event(enable_timing=True)}
+        ev["start"].record(stream)
+
+        def mark(name):
+            ev[name] = torch.cuda.Event(enable_timing=True)
+            ev[name].record(stream)
+
+        out, rec, _ = st.run(coords, cfg.grid, x, dy_top if cfg.backward else None, mark)
+        return ev, rec
+
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    walls, evs = [], []
+    rec = None
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        ev, rec = one()
+        torch.cuda.synchronize()
+        walls.append((time.perf_counter() - t0) * 1e3)
+        evs.append(ev)
+    ph = {}
+    prev = "start"
+    for nme in names:
+        ph[nme] = statistics.median(e[prev].elapsed_time(e[nme]) for e in evs)
+        prev = nme
+    ms = statistics.median(walls)
+    flops = conv_flops(rec, cfg.backward)
+    a_in = len(cfg.coords)
+    return {
+        "workload": CONFIG_WORKLOADS[index],
+        "a_in": a_in, "layers": len(cfg.layers),
+        "step": "fwd + bwd" if cfg.backward else "fwd",
+        "ms_per_step": round(ms, 4),
+        "phases_ms": {k: round(v, 4) for k, v in ph.items()},
+        "gflop_per_step": round(flops / 1e9, 3),
+        "gflops": round(flops / (ms / 1e3) / 1e9, 1),
+        "rulebook_chain_msites_per_s": round(a_in / (ph["rulebook"] / 1e3) / 1e6, 2),
+        "first_layer": {"a_out": rec[0][2], "pairs": rec[0][3]},
+        "reps": reps,
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -227,16 +467,24 @@ def main():
     if args.network:
         network_bench(args.batch, max(args.steps, 5), args.warmup)
         return
+    from gen import make_config, make_dy
+
+    log("generating the 1M-site workload")
+    cfg = make_config(3)
+    cpu = None
+    if not args.no_cpu:
+        # the CPU legs run before the GPU is touched (their worker processes
+        # start from a process without a GPU context)
+        log("timing the CPU oracle on bounded samples (one core, then all cores)")
+        cpu = cpu_baseline(cfg, args.cpu_sites, args.cpu_sites_each)
+
     import torch
 
     import paper_1505_02890_amd as scn
-    from gen import make_config, make_dy
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    log("generating the 1M-site workload")
-    cfg = make_config(3)
     L = cfg.layers[0]
     Cin, Cout = L.cin, L.cout
     d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
@@ -245,6 +493,7 @@ def main():
 
     rb = scn.build_rulebook(coords, cfg.grid, L.f, L.s)
     a_in, a_out, P = rb.a_in, rb.a_out, rb.n_pairs
+    dense_view = rb.dense_view
     dy = d(make_dy(cfg.seed, a_out, Cout))
     ws = scn.conv_bwd_workspace(rb, Cin, Cout, False)
     del rb
@@ -253,9 +502,12 @@ def main():
     stream = torch.cuda.current_stream()
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     phases = ("rulebook", "fwd", "bwd")
+    timer = KernelTimer(scn, stream, args.steps)
 
     def step(rec):
         e = [ev() for _ in range(4)]
+        if rec is not None:
+            timer.arm()
         e[0].record(stream)
         r = scn.build_rulebook(coords, cfg.grid, L.f, L.s)
         e[1].record(stream)
@@ -264,6 +516,7 @@ def main():
         scn.conv_bwd(r, x, g0, W, None, None, dy, None, ws=ws)
         e[3].record(stream)
         if rec is not None:
+            timer.disarm()
             rec.append(e)
         return r, y, g
 
@@ -287,37 +540,19 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     flop_pass = 2.0 * P * Cin * Cout
     value = 3 * flop_pass / (ms_per_step / 1e3) / 1e9
+    # the contraction kernels' own durations over the timed steps (HIP events
+    # the library records on the stream the kernels run on)
+    kern = {k: float(np.mean(timer.ms(k))) for k in ("fwd", "dx", "dw")}
+    log(f"ms/step={ms_per_step:.3f} phases(ms)={ {k: round(v, 4) for k, v in med.items()} } "
+        f"kernels(ms)={ {k: round(v, 4) for k, v in kern.items()} }")
 
     # dominant kernel: the forward contraction (dense blocks of mask-sorted
     # output rows: gather -> MFMA -> one store per row)
-    fwd_ms = med["fwd"]
-    achieved = flop_pass / (fwd_ms / 1e3) / 1e12
-    log(f"ms/step={ms_per_step:.3f} phases(ms)={ {k: round(v, 4) for k, v in med.items()} }")
-
-    # the two backward contractions timed on their own (outside the timed
-    # steps): input gradient alone, weight gradient alone; median of 10
-    r, y, g = step(None)
-
-    def time_need(need):
-        for _ in range(2):
-            scn.conv_bwd(r, x, g0, W, None, None, dy, None, need=need, ws=ws)
-        ts = []
-        for _ in range(10):
-            pe = [ev(), ev()]
-            pe[0].record(stream)
-            scn.conv_bwd(r, x, g0, W, None, None, dy, None, need=need, ws=ws)
-            pe[1].record(stream)
-            torch.cuda.synchronize()
-            ts.append(pe[0].elapsed_time(pe[1]))
-        return statistics.median(ts)
-
-    dx_ms, dw_ms = time_need(("dx",)), time_need(("dW",))
-    # the GEMM phase of a step: its forward and its backward call (one call
-    # computes dx, dW, dbias and dg_in; the column sums of dy are counted once)
-    gemm_ms = med["fwd"] + med["bwd"]
+    achieved = flop_pass / (kern["fwd"] / 1e3) / 1e12
 
     # max-pooling on the convolution output: 2x2x2 stride 2 (windows partition
     # the inputs) and 3x3x3 stride 2 (overlapping windows), median of 5 runs
+    r, y, g = step(None)
     C = Cout
 
     def time_pool(f, s):
@@ -351,14 +586,30 @@ def main():
 
     pool22 = time_pool(2, 2)
     pool32 = time_pool(3, 2)
+    del r, y, g, ws, dy
+    torch.cuda.empty_cache()
 
+    log("ceilings")
+    ceil = ceilings(scn, dev)
     # a plain device copy of known size (calibrates the HBM byte counters)
     cal = torch.full((64 << 20,), 1.0, dtype=torch.float32, device=dev)
     cal2 = torch.empty_like(cal)
-    cal2.copy_(cal)
+    import ctypes
+    assert scn.lib().scn_ceiling_copy(ctypes.c_void_p(cal.data_ptr()),
+                                      ctypes.c_void_p(cal2.data_ptr()), 256 << 20,
+                                      ctypes.c_void_p(stream.cuda_stream)) == 0
     torch.cuda.synchronize()
+    del cal, cal2
+
+    configs = {}
+    if not args.no_configs:
+        for i, reps in ((0, 20), (1, 10), (2, 10), (4, 5)):
+            log(f"workload {i}")
+            configs[str(i)] = config_bench(scn, i, reps, 2)
+            torch.cuda.empty_cache()
 
     rb_bytes = 16.0 * a_in + 16.0 * a_out + 8.0 * P
+    mf = lambda ms: round(flop_pass / (ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4)  # noqa: E731
     result = {
         "metric": "sparse-conv effective GFLOP/s (active sites only) + rulebook Msites/s, 1 GPU",
         "value": round(value, 2),
@@ -376,22 +627,23 @@ def main():
             "workload": "1M active sites (surface shells, 512^3 grid), one 3x3x3 stride-1 sparse "
                         "conv 64->64; step = rulebook + forward + input grad + weight grad",
             "a_in": a_in, "a_out": a_out, "pairs": P, "cin": Cin, "cout": Cout,
+            "dense_forward_view": dense_view,
         },
         "rulebook_msites_per_s": round(a_in / (med["rulebook"] / 1e3) / 1e6, 2),
         "phases_ms": {k: round(v, 4) for k, v in med.items()},
+        "kernels_ms": {k: round(v, 4) for k, v in kern.items()},
         "phase_gflops": {
             "fwd": round(flop_pass / (med["fwd"] / 1e3) / 1e9, 1),
             "bwd_dx_dw": round(2 * flop_pass / (med["bwd"] / 1e3) / 1e9, 1),
-            "dx_alone": round(flop_pass / (dx_ms / 1e3) / 1e9, 1),
-            "dw_alone": round(flop_pass / (dw_ms / 1e3) / 1e9, 1),
         },
-        # fraction of the fp32 MFMA peak per contraction (the two backward
-        # ones timed alone), and over the step's forward and backward calls
+        # fraction of the fp32 MFMA peak of each contraction kernel (its own
+        # duration), of the forward call, and of the step's forward and
+        # backward calls together (the GEMM phase)
         "mfma_frac": {
-            "fwd": round(flop_pass / (fwd_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
-            "dx": round(flop_pass / (dx_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
-            "dw": round(flop_pass / (dw_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
-            "gemm_phase": round(3 * flop_pass / (gemm_ms / 1e3) / 1e12 / MFMA_FP32_PEAK_TFLOPS, 4),
+            "fwd_kernel": mf(kern["fwd"]), "dx_kernel": mf(kern["dx"]),
+            "dw_kernel": mf(kern["dw"]), "fwd_call": mf(med["fwd"]),
+            "gemm_phase": round(3 * flop_pass / ((med["fwd"] + med["bwd"]) / 1e3) / 1e12
+                                / MFMA_FP32_PEAK_TFLOPS, 4),
         },
         "rulebook_alg_gbs": round(rb_bytes / (med["rulebook"] / 1e3) / 1e9, 1),
         "rulebook_hbm_frac": round(rb_bytes / (med["rulebook"] / 1e3) / 1e9 / HBM_PEAK_GBS, 3),
@@ -403,14 +655,15 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_FP32_PEAK_TFLOPS, 4),
             "traffic": measured_traffic(),
+            "frac_of_measured_ceiling": round(achieved / ceil["mfma_f32_loop"]["tflops"], 4),
         },
+        "ceilings": ceil,
         "pool": pool22,
         "pool_overlapping": pool32,
-        "cpu_baseline": None,
+        "configs": configs,
+        "cpu_baseline": cpu[0] if cpu else None,
+        "cpu_baseline_all_cores": cpu[1] if cpu else None,
     }
-    if not args.no_cpu:
-        log("timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sites)
     print(json.dumps(result), flush=True)
 
 

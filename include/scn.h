@@ -360,6 +360,33 @@ void scn_set_allocator(void* (*alloc)(size_t bytes, hipStream_t stream, void* ct
  */
 scn_status scn_set_dense_forward(int64_t min_rows, int32_t min_offsets);
 
+/*
+ * Measurement hook.  On the calling thread, later calls record the caller's
+ * events on their stream around their contraction kernels: events[0] before
+ * and events[1] after the forward's (scn_conv_fwd, scn_conv_fwd_noalloc),
+ * events[2] / events[3] around the input gradient's and events[4] / events[5]
+ * around the weight gradient's partial products (scn_conv_bwd).  A NULL entry
+ * records nothing; events = NULL (host array of 6) turns the hook off.  The
+ * events stay the caller's and must outlive the calls that record them.
+ * Errors: none (SCN_OK); a failing record makes that call return SCN_ERR_HIP.
+ */
+scn_status scn_set_kernel_timer(const hipEvent_t* events);
+
+/*
+ * Measured ceilings for roofline fractions (not part of the convolution):
+ * scn_ceiling_copy copies `bytes` (a multiple of 16, both pointers 16-byte
+ * aligned) from src to dst with a plain streaming kernel (the HBM ceiling and
+ * the reference of the memory counters); scn_ceiling_mfma_f32 runs
+ * `workgroups` work-groups of 4 waves, each wave issuing `iters` x 8
+ * independent v_mfma_f32_16x16x4f32 products on registers only (the fp32
+ * matrix-core ceiling), writes one value per wave to out (device float
+ * [4 * workgroups]) and stores its flop count in *flops (host).
+ * Errors: SCN_ERR_INVALID, SCN_ERR_HIP.
+ */
+scn_status scn_ceiling_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+scn_status scn_ceiling_mfma_f32(float* out, int64_t workgroups, int32_t iters, double* flops,
+                                hipStream_t stream);
+
 /* Message describing the last failing call on this thread ("" if none). */
 const char* scn_last_error(void);
 

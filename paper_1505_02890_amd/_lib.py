@@ -34,7 +34,8 @@ EXPORTED = (
     "scn_conv_bwd_workspace_bytes", "scn_conv_bwd", "scn_maxpool_fwd",
     "scn_maxpool_bwd_workspace_bytes", "scn_maxpool_bwd", "scn_set_allocator",
     "scn_set_dense_forward", "scn_last_error", "scn_version", "scn_conv_fwd_noalloc",
-    "scn_conv_fwd_noalloc_max_bytes",
+    "scn_conv_fwd_noalloc_max_bytes", "scn_set_kernel_timer", "scn_ceiling_copy",
+    "scn_ceiling_mfma_f32",
 )
 
 _ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
@@ -88,6 +89,9 @@ def lib() -> ctypes.CDLL:
         "scn_conv_fwd": (st, [P, P, P, P, P, i32, i32, u32, P, P, P]),
         "scn_conv_fwd_noalloc": (st, [P, P, P, P, P, i32, i32, u32, P, P, P]),
         "scn_conv_fwd_noalloc_max_bytes": (sz, []),
+        "scn_set_kernel_timer": (st, [P]),
+        "scn_ceiling_copy": (st, [P, P, sz, P]),
+        "scn_ceiling_mfma_f32": (st, [P, i64, i32, ctypes.POINTER(ctypes.c_double), P]),
         "scn_conv_bwd_workspace_bytes": (sz, [P, i32, i32, u32]),
         "scn_conv_bwd": (st, [P, P, P, P, P, P, P, P, i32, i32, u32, P, P, P, P, P, sz, P]),
         "scn_maxpool_fwd": (st, [P, P, P, i32, P, P, P, P]),

@@ -1346,6 +1346,19 @@ BwdLayout bwd_layout(const scn_rulebook* rb, int Cin, int Cout, uint32_t flags) 
 
 using namespace scn;
 
+// Measurement hook (scn_set_kernel_timer): per host thread, pairs of the
+// caller's events recorded on the call's stream around the contraction
+// kernels: [0, 1] the forward, [2, 3] the input gradient, [4, 5] the weight
+// gradient's partial products.
+enum TimedKernel { TK_FWD = 0, TK_DX = 1, TK_DW = 2 };
+static thread_local hipEvent_t g_kernel_timer[6] = {};
+
+static scn_status timer_mark(TimedKernel k, int end, hipStream_t st) {
+  hipEvent_t e = g_kernel_timer[2 * k + end];
+  if (e) SCN_HIP(hipEventRecord(e, st));
+  return SCN_OK;
+}
+
 // The forward's scratch: gw [K][NcP] and g_pre [NcP] (256-byte aligned),
 // then the packed weights [K][NcP][RkP].  Every element is written by the
 // forward's first kernels before any is read.
@@ -1414,7 +1427,9 @@ static scn_status fwd_run(const scn_rulebook* rb, const float* x, const float* g
     d.Cout = Cout;
     d.NcP = NcP;
     d.relu = relu;
-    return launch_dense(d, st);
+    scn_status rc;
+    if ((rc = timer_mark(TK_FWD, 0, st)) || (rc = launch_dense(d, st))) return rc;
+    return timer_mark(TK_FWD, 1, st);
   }
   GatherArgs a{};
   a.src = x;
@@ -1433,7 +1448,9 @@ static scn_status fwd_run(const scn_rulebook* rb, const float* x, const float* g
   a.wmap = nullptr;
   a.nrows = rb->a_out;
   a.K = rb->K;
-  return launch_gather(a, st);
+  scn_status rc;
+  if ((rc = timer_mark(TK_FWD, 0, st)) || (rc = launch_gather(a, st))) return rc;
+  return timer_mark(TK_FWD, 1, st);
 }
 
 // Scratch of scn_conv_fwd_noalloc: one array per GPU the library runs on,
@@ -1491,6 +1508,11 @@ scn_status scn_conv_fwd(const scn_rulebook* rb, const float* x, const float* g_i
 }
 
 size_t scn_conv_fwd_noalloc_max_bytes(void) { return NOALLOC_SCRATCH_BYTES; }
+
+scn_status scn_set_kernel_timer(const hipEvent_t* events) {
+  for (int i = 0; i < 6; ++i) g_kernel_timer[i] = events ? events[i] : nullptr;
+  return SCN_OK;
+}
 
 scn_status scn_conv_fwd_noalloc(const scn_rulebook* rb, const float* x, const float* g_in,
                                 const float* W, const float* bias, int32_t Cin, int32_t Cout,
@@ -1597,8 +1619,10 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
     a.wmap = rb->input_sorted ? nullptr : rb->perm;
     a.nrows = rb->a_in;
     a.K = K;
-    scn_status rc = launch_gather(a, st);
-    if (rc) return rc;
+    scn_status rc;
+    if ((rc = timer_mark(TK_DX, 0, st)) || (rc = launch_gather(a, st)) ||
+        (rc = timer_mark(TK_DX, 1, st)))
+      return rc;
   }
 
   // weight gradient partials (also the per-offset column sums T_k)
@@ -1624,11 +1648,13 @@ scn_status scn_conv_bwd(const scn_rulebook* rb, const float* x, const float* g_i
       const bool v4 = Cin % 4 == 0 && Cout % 4 == 0 &&
                       ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(dyb) |
                         reinterpret_cast<uintptr_t>(g_in)) & 15) == 0;
+      if (scn_status rc = timer_mark(TK_DW, 0, st)) return rc;
       if (v4)
         hipLaunchKernelGGL(dw_partial_kernel<true>, dim3((unsigned)nwg), dim3(NT), 0, st, d);
       else
         hipLaunchKernelGGL(dw_partial_kernel<false>, dim3((unsigned)nwg), dim3(NT), 0, st, d);
       SCN_LAUNCH_CHECK();
+      if (scn_status rc = timer_mark(TK_DW, 1, st)) return rc;
     }
     const int64_t nred = std::max<int64_t>((int64_t)K * Cin * Cout, (int64_t)K * Cout);
     hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)ceil_div(nred, RED_E)),
