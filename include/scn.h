@@ -331,8 +331,11 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
 /*
  * Device memory the library allocates for itself: rulebook storage and the
  * temporaries of scn_rulebook_build* and scn_conv_fwd (workspaces of the
- * backward passes are the caller's).  By default it comes from the device's
- * stream-ordered pool (hipMallocAsync / hipFreeAsync).  Callers that manage
+ * backward passes are the caller's).  By default it comes from the library's
+ * caching allocator: blocks from hipMalloc, kept by the library after they are
+ * freed (never returned to the driver before the process ends, except when
+ * hipMalloc fails) and reused in stream order, or on another stream once the
+ * work queued before their free has completed.  Callers that manage
  * device memory themselves (a framework's caching allocator) install
  *   alloc(bytes, stream, ctx) -> 256-byte-aligned device pointer or NULL
  *   free(ptr, stream, ctx)

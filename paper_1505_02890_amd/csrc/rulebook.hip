@@ -42,7 +42,6 @@
 // rulebook: they are H_out, and a build from this rulebook's output sites
 // (scn_rulebook_build_next) takes them as its H_in and skips phases 1-3.
 #include <hip/hip_runtime.h>
-#include <rocprim/device/device_radix_sort.hpp>
 
 #include <algorithm>
 #include <cstring>
@@ -51,25 +50,10 @@
 
 #include "scan.h"
 #include "scn_internal.h"
+#include "sort.h"
 
 namespace scn {
 namespace {
-
-// The dense forward's mask sort: a stable onesweep radix sort of (mask, row)
-// pairs over the K mask bits, 9 bits per pass (3 passes for the 27-offset
-// cube; 8-bit digits take 4 passes of the same length each).
-using MaskSortCfg = rocprim::radix_sort_config<
-    rocprim::default_config, rocprim::default_config,
-    rocprim::radix_sort_onesweep_config<rocprim::kernel_config<512, 16>,
-                                        rocprim::kernel_config<512, 16>, 9,
-                                        rocprim::block_radix_rank_algorithm::match>>;
-
-inline hipError_t mask_sort(void* tmp, size_t& bytes, const uint32_t* keys_in, uint32_t* keys_out,
-                            const int32_t* rows_in, int32_t* rows_out, int64_t n, int bits,
-                            hipStream_t st) {
-  return rocprim::radix_sort_pairs<MaskSortCfg>(tmp, bytes, keys_in, keys_out, rows_in, rows_out,
-                                                (size_t)n, 0u, (unsigned)bits, st);
-}
 
 enum : uint32_t { F_RANGE = 1, F_DUP = 2, F_UNSORTED = 4 };
 
@@ -164,7 +148,11 @@ __global__ void __launch_bounds__(256) mark_inputs_kernel(const int32_t* __restr
   __syncthreads();
   if (f) atomicOr(&sf, f);
   __syncthreads();
-  if (threadIdx.x == 0 && sf) atomicOr(flags, sf);
+  // every block of an unsorted list raises F_UNSORTED: read the word first,
+  // so the blocks do not all queue atomics on one address
+  if (threadIdx.x == 0 && sf &&
+      (__hip_atomic_load(flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & sf) != sf)
+    atomicOr(flags, sf);
 }
 
 struct PopcountLoad {
@@ -177,13 +165,6 @@ struct PopcountLoad {
   }
 };
 
-template <typename T>
-struct PlainLoad {
-  const T* v;
-  __device__ T operator()(int64_t i) const { return v[i]; }
-  __device__ void chunk(int64_t i, T (&x)[SCAN_ITEMS]) const { load16<T>(v + i, x); }
-};
-
 // ---- phase 3: rank -> caller row ------------------------------------------
 __global__ void __launch_bounds__(256) perm_kernel(const int32_t* __restrict__ coords, int64_t n,
                                                    GridDev g, const uint32_t* __restrict__ bm,
@@ -192,10 +173,15 @@ __global__ void __launch_bounds__(256) perm_kernel(const int32_t* __restrict__ c
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int4 c = reinterpret_cast<const int4*>(coords)[i];
+  // it runs before the list's errors are read back: sites outside the grid
+  // are skipped (the build then fails with SCN_ERR_RANGE)
+  if (c.x < 0 || c.x >= g.B || c.y < 0 || c.y >= g.mx || c.z < 0 || c.z >= g.my || c.w < 0 ||
+      c.w >= g.mz)
+    return;
   const int64_t w = row_base(g, c.x, c.z, c.w) + (c.y >> 5);
   const uint32_t below = (1u << (c.y & 31)) - 1u;
   const uint32_t rank = pref[w] + (uint32_t)__popc(bm[w] & below);
-  perm[rank] = (int32_t)i;
+  if (rank < n) perm[rank] = (int32_t)i;
 }
 
 // Output word wo of the output grid -> (b, z, y, word-in-row).  32-bit:
@@ -286,28 +272,36 @@ __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restri
   const int x0 = wp.wx * 32;
   uint32_t rank = opref[wo];
   if (S1) {
-    // E[k] bit j: input site (x0 + j + kx, y + ky, z + kz) of offset k is active
-    uint32_t E[K];
-    int k = 0;
+    // R[r] bit j + kx: input site (x0 + j + kx, y + ky, z + kz) of window row
+    // r = (ky, kz) is active; the row's offsets are consecutive mask bits
+    constexpr int NR = W::FZ * F;
+    uint64_t R[NR];
 #pragma unroll
     for (int kz = 0; kz < W::FZ; ++kz)
 #pragma unroll
       for (int ky = 0; ky < F; ++ky) {
+        R[kz * F + ky] = 0;
         if (W::row_len(ky, kz) <= 0) continue;
         const int64_t base = row_base(gi, wp.b, wp.y + ky, wp.z + kz);
         const int64_t w = x0 >> 5;
         const uint32_t lo = w < gi.rw ? inb[base + w] : 0u;
         const uint32_t hi = w + 1 < gi.rw ? inb[base + w + 1] : 0u;
-#pragma unroll
-        for (int kx = 0; kx < F; ++kx)
-          if (kx < W::row_len(ky, kz)) E[k++] = kx ? (lo >> kx) | (hi << (32 - kx)) : lo;
+        R[kz * F + ky] = (uint64_t)lo | ((uint64_t)hi << 32);
       }
     while (v) {
       const int j = __builtin_ctz(v);
       v &= v - 1;
       uint32_t m = 0;
+      int k = 0;
 #pragma unroll
-      for (int k = 0; k < K; ++k) m |= ((E[k] >> j) & 1u) << k;
+      for (int kz = 0; kz < W::FZ; ++kz)
+#pragma unroll
+        for (int ky = 0; ky < F; ++ky) {
+          const int len = W::row_len(ky, kz);
+          if (len <= 0) continue;
+          m |= (uint32_t)((R[kz * F + ky] >> j) & ((1u << len) - 1u)) << k;
+          k += len;
+        }
       reinterpret_cast<int4*>(out_coords)[rank] = make_int4(wp.b, x0 + j, wp.y, wp.z);
       masks[rank] = m;
       ++rank;
@@ -356,27 +350,24 @@ __global__ void __launch_bounds__(256) tile_count_kernel(const uint32_t* __restr
   if (lane < K && t < nt) cnt[lane * nt + t] = c;
 }
 
-// ---- phase 8b: list boundaries off[k] = position of (k, tile 0) -----------
-__global__ void list_offsets_kernel(const uint64_t* __restrict__ pos, int64_t nt, int K,
-                                    int64_t* __restrict__ off) {
-  const int k = threadIdx.x;
-  if (k <= K) off[k] = (int64_t)pos[(int64_t)k * nt];
-}
-
-// ---- phase 9: emit the pair lists ------------------------------------------
-// One thread per output, one wave per tile.  All K rank lookups are issued
-// before any dependent load so they overlap.
+// ---- phase 9: output-major tables --------------------------------------------
+// One thread per output, one wave per tile of 64 outputs: the window table
+// nbr[o][k] of a pooling rulebook, or the output-major neighbour list fnb of
+// the dense forward view (a stride-1 rulebook); the per-offset pair lists are
+// emitted input-major (emit_in_kernel).  The rows come from rank lookups in
+// the input bitmap and perm, which stay in L2 (reading them back from the
+// pair lists, long evicted, took 1.55 times as long).  All K rank lookups
+// are issued before any dependent load so they overlap.
+constexpr int EMIT_NB_STAGE = 12;  // staged neighbour-list entries per output
 template <int F, int LAT>
-__global__ void __launch_bounds__(256) emit_pairs_kernel(
+__global__ void __launch_bounds__(256) emit_out_kernel(
     const uint32_t* __restrict__ masks, const int32_t* __restrict__ out_coords, int64_t a_out,
-    int64_t nt, int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref,
-    GridDev gi, const int32_t* __restrict__ perm, const uint64_t* __restrict__ pos,
-    int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows, int32_t* __restrict__ in_rank,
-    int32_t* __restrict__ nbr, const uint32_t* __restrict__ fnb_off, int32_t* __restrict__ fnb) {
+    int s, const uint32_t* __restrict__ inb, const uint32_t* __restrict__ ipref, GridDev gi,
+    const int32_t* __restrict__ perm, int32_t* __restrict__ nbr,
+    const uint32_t* __restrict__ fnb_off, int32_t* __restrict__ fnb) {
   using W = Win<F, LAT>;
   constexpr int K = W::K;
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t t = o >> 6;
   const bool live = o < a_out;
   const uint32_t m = live ? masks[o] : 0u;
   int4 c = make_int4(0, 0, 0, 0);
@@ -418,36 +409,51 @@ __global__ void __launch_bounds__(256) emit_pairs_kernel(
         k += len;
       }
   }
-  // output-major neighbour list of the dense forward view
-  int32_t* nb = fnb && live ? fnb + fnb_off[o] : nullptr;
-  // Window table (rulebooks with stride >= 2): a lane's K entries are K words
-  // apart, so the wave stages its 64 rows in LDS (dynamic, 64*K words per
-  // wave) and writes them out as one contiguous run.  Stored straight from
-  // the lanes, every store instruction touched 64 cache lines.
+  // A lane's entries are up to K words apart, so the wave stages its 64
+  // outputs' entries in LDS (dynamic: 64*K words per wave for the table,
+  // 64*EMIT_NB_STAGE for the list) and writes them out as one contiguous run.
+  // Stored straight from the lanes, every store instruction touched up to 64
+  // cache lines, each only partly.  A wave whose list run is longer than its
+  // stage writes it directly.
   extern __shared__ int4 emit_lds[];
-  int32_t* stage = reinterpret_cast<int32_t*>(emit_lds) + (threadIdx.x >> 6) * (64 * K);
+  int32_t* stage = reinterpret_cast<int32_t*>(emit_lds) +
+                   (threadIdx.x >> 6) * (64 * (nbr ? K : EMIT_NB_STAGE));
+  const int lane = threadIdx.x & 63;
+  const int64_t o0 = o & ~(int64_t)63;  // the wave's first output
+  uint32_t nb_at = 0, nb0 = 0, nb_len = 0;
+  bool nb_lds = false;
+  if (fnb) {
+    // the wave's run of the neighbour list starts at fnb_off[o0]
+    nb_at = live ? fnb_off[o] : 0u;
+    nb0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)nb_at);
+    const int last = a_out - 1 - o0 < 63 ? (int)(a_out - 1 - o0) : 63;
+    nb_len = (uint32_t)__shfl((int)(nb_at + (uint32_t)__popc(m)), last < 0 ? 0 : last, 64) - nb0;
+    nb_lds = nb_len <= 64 * EMIT_NB_STAGE;
+    if (nb_lds) nb_at -= nb0;
+  }
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     const bool bit = (m >> k) & 1u;
-    const uint64_t bal = __ballot(bit);
     // sorted input: rank order is the caller's row order (no perm table)
     const int32_t row = bit ? (perm ? perm[rank[k]] : (int32_t)rank[k]) : -1;
-    if (bit) {
-      const uint64_t p = pos[(int64_t)k * nt + t] + lane_rank(bal);
-      in_rows[p] = row;
-      out_rows[p] = (int32_t)o;
-      if (in_rank) in_rank[p] = (int32_t)rank[k];
-      if (nb) *nb++ = row;
+    if (fnb && bit) {
+      if (nb_lds)
+        stage[nb_at++] = row;
+      else
+        fnb[nb_at++] = row;
     }
-    if (nbr) stage[(threadIdx.x & 63) * K + k] = row;
+    if (nbr) stage[lane * K + k] = row;
+  }
+  if (nb_lds && o0 < a_out) {
+    // the stage is this wave's alone: LDS accesses of one wave complete in order
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    for (uint32_t i = lane; i < nb_len; i += 64) fnb[nb0 + i] = stage[i];
   }
   if (nbr) {
     __syncthreads();
-    const int64_t o0 = o & ~(int64_t)63;  // the wave's first output
     if (o0 < a_out) {
       // 64-output runs start 256-byte aligned in nbr
       const int64_t n = ((o0 + 64 < a_out ? o0 + 64 : a_out) - o0) * K, n4 = n >> 2;
-      const int lane = threadIdx.x & 63;
       const int4* src = reinterpret_cast<const int4*>(stage);
       int4* dst = reinterpret_cast<int4*>(nbr + o0 * K);
       for (int64_t i = lane; i < n4; i += 64) dst[i] = src[i];
@@ -516,44 +522,189 @@ __global__ void __launch_bounds__(256) inv_windows_kernel(
   }
 }
 
-// ---- phase 9c (stride 1): row numbers for the mask sort -------------------
-__global__ void iota_kernel(int32_t* __restrict__ v, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) v[i] = (int32_t)i;
-}
-
-// flags[1] = number of active inputs, flags[2] = number of active outputs
+// The first read-back: flags[1] = number of active inputs, flags[2] =
+// number of active outputs and, when the lists are already emitted, their
+// boundaries off[k] = itile[k * nit] (also kept in the rulebook's off_dev).
 __global__ void pack_totals_kernel(uint32_t* __restrict__ flags, const uint32_t* __restrict__ a_in,
-                                   const uint32_t* __restrict__ a_out) {
-  flags[1] = *a_in;
-  flags[2] = *a_out;
+                                   const uint32_t* __restrict__ a_out,
+                                   const int64_t* __restrict__ itile, int64_t nit, int K,
+                                   int64_t* __restrict__ off, int64_t* __restrict__ off_dev) {
+  const int k = threadIdx.x;
+  if (k == 0) {
+    flags[1] = *a_in;
+    flags[2] = *a_out;
+  }
+  if (itile && k <= K) {
+    const int64_t v = itile[(int64_t)k * nit];
+    off[k] = v;
+    off_dev[k] = v;
+  }
 }
 
-// ---- phase 10: pair ranges per tile of input ranks -------------------------
-// itile[k * nit + t] = first position p in list k with rank[p] >= t * TILE;
-// ranks ascend along each list (the window map preserves key order).
-__global__ void __launch_bounds__(256) in_tiles_kernel(const int32_t* __restrict__ rank,
-                                                       const int64_t* __restrict__ off, int K,
-                                                       int64_t nit,
-                                                       int64_t* __restrict__ itile) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)K * nit + 1) return;
-  if (i == (int64_t)K * nit) {
-    itile[i] = off[K];
-    return;
+// list boundaries from the input tiles (lists emitted after the first wait)
+__global__ void list_offsets_kernel(const int64_t* __restrict__ itile, int64_t nit, int K,
+                                    int64_t* __restrict__ off) {
+  const int k = threadIdx.x;
+  if (k <= K) off[k] = itile[(int64_t)k * nit];
+}
+
+// ---- phase 10: pair counts per (offset, tile of input ranks) --------------
+// One wave per tile of 64 input ranks.  Input i pairs at offset k with the
+// output o = (i - k) / s when the division is exact and o lies in the output
+// grid: that output is active, since input i lies in its window.  So the
+// count needs only the input's coordinates, and the exclusive scan of
+// cnt[k * nit + t] gives itile[k * nit + t], the position in list k of the
+// first pair whose input rank is >= t * TILE (lists ascend by input rank).
+template <int F, int LAT, int SM>
+__global__ void __launch_bounds__(256) in_tile_count_kernel(
+    const int32_t* __restrict__ coords, const int32_t* __restrict__ perm, int64_t n,
+    int64_t nit, int s, GridDev go, uint64_t* __restrict__ cnt) {
+  using W = Win<F, LAT>;
+  constexpr int K = W::K;
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t t = r >> 6;
+  const int lane = threadIdx.x & 63;
+  int4 c = make_int4(0, 0, 0, 0);
+  bool live = r < n;
+  if (live) {
+    // a list with errors leaves ranks unwritten (the build then fails)
+    const int64_t row = perm ? perm[r] : r;
+    live = row >= 0 && row < n;
+    if (live) c = reinterpret_cast<const int4*>(coords)[row];
   }
-  const int k = (int)(i / nit);
-  const int64_t t = i % nit;
-  const int64_t target = t * TILE;
-  int64_t lo = off[k], hi = off[k + 1];
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    if ((int64_t)rank[mid] < target)
-      lo = mid + 1;
-    else
-      hi = mid;
+  uint64_t mine = 0;
+  int k = 0;
+#pragma unroll
+  for (int kz = 0; kz < W::FZ; ++kz)
+#pragma unroll
+    for (int ky = 0; ky < F; ++ky)
+#pragma unroll
+      for (int kx = 0; kx < F; ++kx) {
+        if (kx >= W::row_len(ky, kz)) continue;
+        const int dx = c.y - kx, dy = c.z - ky, dz = c.w - kz;
+        // SM: stride 1, stride 2, or any (a division)
+        bool ok = live && dx >= 0 && dy >= 0 && dz >= 0;
+        int ox = dx, oy = dy, oz = dz;
+        if (SM == 2) {
+          ok = ok && !((dx | dy | dz) & 1);
+          ox = dx >> 1;
+          oy = dy >> 1;
+          oz = dz >> 1;
+        } else if (SM != 1) {
+          ok = ok && dx % s == 0 && dy % s == 0 && dz % s == 0;
+          ox = dx / s;
+          oy = dy / s;
+          oz = dz / s;
+        }
+        ok = ok && ox < go.mx && oy < go.my && oz < go.mz;
+        if (W::SIMPLEX) ok = ok && ox + oy + oz < go.mx;
+        const uint64_t c_k = (uint64_t)__popcll(__ballot(ok));
+        if (lane == k) mine = c_k;
+        ++k;
+      }
+  if (lane < K && t < nit) cnt[lane * nit + t] = mine;
+}
+
+// ---- phase 10b: the pair lists, input-major ------------------------------
+// One thread per input rank r, one wave per tile of 64 ranks (the tiles of
+// in_tile_count_kernel).  Input i pairs at window offset k with output
+// o = (i - k) / s when that is exact and in the output grid; o's row is its
+// rank in the output bitmap.  The pair's place in list k is itile[k*nit + t]
+// plus the tile's earlier ranks that pair at offset k, so every list ascends
+// by input rank and, the window map keeping key order, by output row.  Where
+// every input of the tile pairs at k, the wave's stores of that list are one
+// contiguous 256-byte run.  The kernel tolerates an input list with errors
+// (out-of-grid sites and unwritten ranks are skipped; the build then fails),
+// and no store goes past the lists' capacity.
+template <int F, int LAT, int SM>
+__global__ void __launch_bounds__(256) emit_in_kernel(
+    const int32_t* __restrict__ coords, const int32_t* __restrict__ perm, int64_t n,
+    int64_t nit, int s, GridDev go, const uint32_t* __restrict__ outb,
+    const uint32_t* __restrict__ opref, const int64_t* __restrict__ itile, int64_t cap,
+    int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows,
+    int32_t* __restrict__ in_rank) {
+  using W = Win<F, LAT>;
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int tw = __builtin_amdgcn_readfirstlane((int)(r >> 6));
+  if (tw >= nit) return;  // a whole padding wave
+  int4 c = make_int4(0, 0, 0, 0);
+  int32_t row = 0;
+  bool live = r < n;
+  if (live) {
+    row = perm ? perm[r] : (int32_t)r;
+    live = row >= 0 && row < n;
+    if (live) {
+      c = reinterpret_cast<const int4*>(coords)[row];
+      live = c.x >= 0 && c.x < go.B;  // the other coordinates are checked per offset
+    }
   }
-  itile[i] = lo;
+  int k = 0;
+#pragma unroll
+  for (int kz = 0; kz < W::FZ; ++kz)
+#pragma unroll
+    for (int ky = 0; ky < F; ++ky) {
+      const int len = W::row_len(ky, kz);
+      if (len <= 0) continue;
+      // stride 1: the row's outputs x - len + 1 .. x lie in at most two words
+      // of one output x-row
+      uint32_t pa = 0, ba = 0, bb = 0;
+      int wa = 0;
+      if (SM == 1) {
+        const int oy = c.z - ky, oz = c.w - kz;
+        const int xl = c.y - (len - 1) > 0 ? c.y - (len - 1) : 0;
+        const bool row_ok = live && oy >= 0 && oz >= 0 && oy < go.my && oz < go.mz && xl < go.mx;
+        if (row_ok) {
+          const int64_t base = row_base(go, c.x, oy, oz);
+          wa = xl >> 5;
+          pa = opref[base + wa];
+          ba = outb[base + wa];
+          const int wb = c.y >> 5;
+          if (wb != wa && wb < go.rw) bb = outb[base + wb];
+        }
+      }
+#pragma unroll
+      for (int kx = 0; kx < F; ++kx) {
+        if (kx >= len) continue;
+        const int dx = c.y - kx, dy = c.z - ky, dz = c.w - kz;
+        bool ok = live && dx >= 0 && dy >= 0 && dz >= 0;
+        int ox = dx, oy = dy, oz = dz;
+        if (SM == 2) {
+          ok = ok && !((dx | dy | dz) & 1);
+          ox = dx >> 1;
+          oy = dy >> 1;
+          oz = dz >> 1;
+        } else if (SM != 1) {
+          ok = ok && dx % s == 0 && dy % s == 0 && dz % s == 0;
+          ox = dx / s;
+          oy = dy / s;
+          oz = dz / s;
+        }
+        ok = ok && ox < go.mx && oy < go.my && oz < go.mz;
+        if (W::SIMPLEX) ok = ok && ox + oy + oz < go.mx;
+        uint32_t orank = 0;
+        if (ok) {
+          const uint32_t below = (1u << (ox & 31)) - 1u;
+          if (SM == 1) {
+            orank = (ox >> 5) == wa ? pa + (uint32_t)__popc(ba & below)
+                                    : pa + (uint32_t)__popc(ba) + (uint32_t)__popc(bb & below);
+          } else {
+            const int64_t w = row_base(go, c.x, oy, oz) + (ox >> 5);
+            orank = opref[w] + (uint32_t)__popc(outb[w] & below);
+          }
+        }
+        const uint64_t bal = __ballot(ok);
+        const int64_t p0 = itile[(int64_t)k * nit + tw];
+        if (ok) {
+          const int64_t p = p0 + lane_rank(bal);
+          if (p < cap) {
+            in_rows[p] = row;
+            out_rows[p] = (int32_t)orank;
+            if (in_rank) in_rank[p] = (int32_t)r;
+          }
+        }
+        ++k;
+      }
+    }
 }
 
 inline unsigned blocks_for(int64_t n, int threads) {
@@ -635,8 +786,26 @@ struct Kernels {
     hipLaunchKernelGGL((tile_count_kernel<K>), g, dim3(256), 0, st, a...);
   }
   template <typename... A>
-  static void emit(dim3 g, size_t lds, hipStream_t st, A... a) {
-    hipLaunchKernelGGL((emit_pairs_kernel<F, LAT>), g, dim3(256), lds, st, a...);
+  static void emit_out(dim3 g, size_t lds, hipStream_t st, A... a) {
+    hipLaunchKernelGGL((emit_out_kernel<F, LAT>), g, dim3(256), lds, st, a...);
+  }
+  template <typename... A>
+  static void emit_in(int sm, dim3 g, hipStream_t st, A... a) {
+    if (sm == 1)
+      hipLaunchKernelGGL((emit_in_kernel<F, LAT, 1>), g, dim3(256), 0, st, a...);
+    else if (sm == 2)
+      hipLaunchKernelGGL((emit_in_kernel<F, LAT, 2>), g, dim3(256), 0, st, a...);
+    else
+      hipLaunchKernelGGL((emit_in_kernel<F, LAT, 0>), g, dim3(256), 0, st, a...);
+  }
+  template <typename... A>
+  static void in_tile_count(int sm, dim3 g, hipStream_t st, A... a) {
+    if (sm == 1)
+      hipLaunchKernelGGL((in_tile_count_kernel<F, LAT, 1>), g, dim3(256), 0, st, a...);
+    else if (sm == 2)
+      hipLaunchKernelGGL((in_tile_count_kernel<F, LAT, 2>), g, dim3(256), 0, st, a...);
+    else
+      hipLaunchKernelGGL((in_tile_count_kernel<F, LAT, 0>), g, dim3(256), 0, st, a...);
   }
   template <typename... A>
   static void inv_windows(int slots, dim3 g, hipStream_t st, A... a) {
@@ -700,14 +869,20 @@ scn_status copy_event(hipEvent_t* out) {
 // The build of one layer, in steps:
 //   check()   host only: arguments, output grid, bitmap sizes;
 //   phase1()  device: mark the caller's sites (first layer only), rank them,
-//             dilate, rank the outputs; queues the copy of the flags and
-//             totals to the layer's read-back slot;
+//             the input side (rank -> row, pair counts per tile of input
+//             ranks), dilate, rank the outputs, emit the pair lists; queues
+//             the copy of the flags, totals and list boundaries to the
+//             layer's read-back slot;
 //   sized()   after the host has waited for that copy: errors, a_out, the
-//             rulebook's storage;
-//   phase2()  device: output sites and masks, per-tile counts, list
-//             boundaries (copied out, then `copied` is recorded), emission,
-//             the mask sort, pooling windows, input tiles;
-//   finish()  after the host has waited for the boundary copy: pair count.
+//             rest of the rulebook's storage;
+//   phase2()  device: output sites and masks, per-tile pair ranges, the
+//             output-major tables (window table of a pooling rulebook, or the
+//             dense forward view and its mask sort), pooling windows;
+//   finish()  the pair count.
+// A layer of scn_rulebook_build_chain built from the previous layer's
+// outputs learns its sites only after the first wait: its input side and
+// lists move to sized() / phase2(), whose list boundaries are copied out
+// (then `copied` is recorded) for a second wait.
 // A layer built from the previous layer's outputs (`chained`) uses that
 // layer's output rank bitmap (its H_out) as its H_in and skips marking (its
 // sites are valid, distinct and in key order by construction).
@@ -740,7 +915,21 @@ struct LayerBuild {
       if (bits) dfree(bits, s, al);
     }
   } hout;
-  uint32_t *inb = nullptr, *ipref = nullptr, *flags = nullptr, *sc32 = nullptr;
+  uint32_t *inb = nullptr, *ipref = nullptr, *sc32 = nullptr;
+  // input side of the rulebook, built before the first wait (it needs only
+  // the input sites): rank -> caller row and the pair ranges per tile of
+  // input ranks, in one allocation the rulebook adopts
+  void* inblock = nullptr;
+  int32_t* perm = nullptr;
+  int64_t* itile = nullptr;
+  // the pair lists (capacity: inputs x windows per input) and their bounds,
+  // in the same allocation
+  int32_t *in_rows = nullptr, *out_rows = nullptr, *in_rank_arr = nullptr;
+  int64_t* off_dev = nullptr;
+  int64_t pcap = 0;
+  bool early = false;  // input side and lists before the first wait
+  const uint32_t *obits = nullptr, *orank = nullptr;  // this layer's H_out
+  Readback* drb = nullptr;                             // device side of the read-back
   // after phase 1
   int64_t a_out = 0, nt = 0, nit = 0, pmax = 0, nfb = 0;
   bool sorted = true, pool = false, dense = false;
@@ -756,9 +945,11 @@ struct LayerBuild {
     if (!keep && rb) {
       dfree(rb->block, st, rb->alloc);      // stream-ordered: after any queued kernel
       dfree(rb->hout_bits, st, rb->alloc);  // also holds hout_rank
+      dfree(rb->inblock, st, rb->alloc);
       if (rb->done) (void)hipEventDestroy(rb->done);
       delete rb;
     }
+    if (inblock) dfree(inblock, st, mem);  // not adopted by a rulebook
   }
 
   scn_status check() {
@@ -820,6 +1011,72 @@ struct LayerBuild {
     return SCN_OK;
   }
 
+  // The rulebook's input side, which needs only the input sites: perm
+  // (rank -> caller row; not for a chained layer, whose sites are in key
+  // order by construction) and itile (pair ranges per tile of input ranks:
+  // counts from the inputs' sites, then a scan), in one allocation the
+  // rulebook adopts.  Queued before the first wait when the sites are known;
+  // the kernels tolerate an input list with errors (the build then fails).
+  bool in_done = false;
+  scn_status input_side() {
+    scn_status rc;
+    nit = std::max<int64_t>(1, ceil_div(n, TILE));
+    // windows per input: at most ceil(f/s) per axis of the window
+    int per = 1;
+    for (int a = 0; a < (planar ? 2 : 3); ++a) per *= (f + s - 1) / s;
+    pcap = std::min<int64_t>((int64_t)n * std::min(per, K), INT32_MAX);
+    const size_t perm_bytes = chained ? 0 : Temps::round(std::max<int64_t>(n, 1) * 4);
+    const size_t list_bytes = Temps::round(std::max<int64_t>(pcap, 1) * 4);
+    if ((rc = dalloc(&inblock,
+                     perm_bytes + Temps::round((K * nit + 1) * 8) +
+                         (chained ? 2 : 3) * list_bytes + Temps::round((K + 1) * 8),
+                     st, mem)))
+      return rc;
+    char* cur = static_cast<char*>(inblock);
+    perm = chained ? nullptr : reinterpret_cast<int32_t*>(cur);
+    cur += perm_bytes;
+    itile = reinterpret_cast<int64_t*>(cur);
+    cur += Temps::round((K * nit + 1) * 8);
+    in_rows = reinterpret_cast<int32_t*>(cur);
+    cur += list_bytes;
+    out_rows = reinterpret_cast<int32_t*>(cur);
+    cur += list_bytes;
+    // a chained layer's sites are in key order: ranks are rows
+    in_rank_arr = chained ? nullptr : reinterpret_cast<int32_t*>(cur);
+    cur += chained ? 0 : list_bytes;
+    off_dev = reinterpret_cast<int64_t*>(cur);
+    if (!chained && n > 0) {
+      hipLaunchKernelGGL(perm_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n, gi,
+                         (const uint32_t*)inb, (const uint32_t*)ipref, perm);
+      SCN_LAUNCH_CHECK();
+    }
+    uint64_t *icnt = nullptr, *isc = nullptr;
+    if ((rc = tmp.get(&icnt, K * nit)) || (rc = tmp.get(&isc, scan_blocks(K * nit)))) return rc;
+    with_kernels(f, lattice, [&](auto k) {
+      k.in_tile_count(s == 1 ? 1 : (s == 2 ? 2 : 0), dim3(blocks_for(nit * TILE, 256)), st,
+                      coords, (const int32_t*)perm, n, nit, s, go, icnt);
+    });
+    SCN_LAUNCH_CHECK();
+    if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{icnt}, K * nit, (uint64_t*)itile,
+                                       (uint64_t*)itile + K * nit, isc, st)))
+      return rc;
+    in_done = true;
+    return SCN_OK;
+  }
+
+  // The pair lists, input-major, from the input side and this layer's H_out.
+  scn_status emit_lists() {
+    if (n > 0) {
+      with_kernels(f, lattice, [&](auto k) {
+        k.emit_in(s == 1 ? 1 : (s == 2 ? 2 : 0), dim3(blocks_for(nit * TILE, 256)), st, coords,
+                  (const int32_t*)perm, n, nit, s, go, obits, orank, (const int64_t*)itile, pcap,
+                  in_rows, out_rows, in_rank_arr);
+      });
+      SCN_LAUNCH_CHECK();
+    }
+    return SCN_OK;
+  }
+
   scn_status phase1() {
     mem = current_allocator();  // every array of this build comes from it
     tmp.s = st;
@@ -833,8 +1090,18 @@ struct LayerBuild {
     if ((rc = dalloc((void**)&hout.bits, hbits_bytes + Temps::round((nw_out + 1) * 4), st, mem)))
       return rc;
     hout.rank = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(hout.bits) + hbits_bytes);
+    obits = hout.bits;
+    orank = hout.rank;
+    // a chained layer of scn_rulebook_build_chain learns its sites only after
+    // the first wait; every other build has them now
+    const bool in_early = !(chained && !coords);
+    early = in_early;
+    const int64_t nit_early = std::max<int64_t>(1, ceil_div(n, TILE));
     if ((rc = tmp.reserve((chained ? 0 : Temps::round(nw_in * 4) + Temps::round((nw_in + 1) * 4)) +
-                          Temps::round(16) + Temps::round(nsb * 4))))
+                          Temps::round(sizeof(Readback)) + Temps::round(nsb * 4) +
+                          (in_early ? Temps::round(K * nit_early * 8) +
+                                          Temps::round(scan_blocks(K * nit_early) * 8)
+                                    : 0))))
       return rc;
     if (chained) {
       inb = const_cast<uint32_t*>(prev_bits);
@@ -843,8 +1110,11 @@ struct LayerBuild {
       if ((rc = tmp.get(&inb, nw_in)) || (rc = tmp.get(&ipref, nw_in + 1))) return rc;
       SCN_HIP(hipMemsetAsync(inb, 0, std::max<int64_t>(nw_in, 1) * 4, st));
     }
-    if ((rc = tmp.get(&flags, 4)) || (rc = tmp.get(&sc32, nsb))) return rc;
-    SCN_HIP(hipMemsetAsync(flags, 0, 16, st));
+    char* drb_bytes = nullptr;
+    if ((rc = tmp.get(&drb_bytes, sizeof(Readback))) || (rc = tmp.get(&sc32, nsb))) return rc;
+    drb = reinterpret_cast<Readback*>(drb_bytes);
+    uint32_t* const flags = &drb->flags;
+    SCN_HIP(hipMemsetAsync(drb, 0, sizeof(Readback), st));
     std::memset(hb, 0, sizeof(Readback));
     // phases 1-5 (1-2 only for the caller's sites)
     if (!chained) {
@@ -857,6 +1127,8 @@ struct LayerBuild {
                                          st)))
         return rc;
     }
+    // the input side overlaps the host's first wait
+    if (in_early && (rc = input_side())) return rc;
     {
       const int sm = s == 1 ? 1 : (s == 2 ? 2 : 0);
       with_kernels(f, lattice, [&](auto k) {
@@ -867,11 +1139,13 @@ struct LayerBuild {
     if ((rc = exclusive_scan<uint32_t>(PopcountLoad{hout.bits}, nw_out, hout.rank,
                                        hout.rank + nw_out, sc32, st)))
       return rc;
-    // flags and both totals in one read-back
-    hipLaunchKernelGGL(pack_totals_kernel, dim3(1), dim3(1), 0, st, flags, ipref + nw_in,
-                       hout.rank + nw_out);
+    if (in_early && (rc = emit_lists())) return rc;
+    // flags, both totals and (lists emitted) the list boundaries in one read-back
+    hipLaunchKernelGGL(pack_totals_kernel, dim3(1), dim3(64), 0, st, flags, ipref + nw_in,
+                       hout.rank + nw_out, in_early ? (const int64_t*)itile : nullptr, nit, K,
+                       drb->off, off_dev);
     SCN_LAUNCH_CHECK();
-    SCN_HIP(hipMemcpyAsync(&hb->flags, flags, 12, hipMemcpyDeviceToHost, st));
+    SCN_HIP(hipMemcpyAsync(hb, drb, sizeof(Readback), hipMemcpyDeviceToHost, st));
     return SCN_OK;
   }
 
@@ -888,12 +1162,12 @@ struct LayerBuild {
     }
     a_out = hb->a_out;
     sorted = !(hb->flags & F_UNSORTED);
+    if (!in_done && (rc = input_side())) return rc;
     // pooling tables (window rows per output, windows per input) for stride >= 2
     pool = s >= 2;
     inv_slots = pool ? (f > s ? 8 : 1) : 0;
     nt = std::max<int64_t>(1, ceil_div(a_out, TILE));
-    nit = std::max<int64_t>(1, ceil_div(n, TILE));
-    pmax = std::min<int64_t>(n, a_out) * K;
+    pmax = pcap;
     if (pool && a_out * K > INT32_MAX) {
       set_error("scn_rulebook_build: %lld pooling windows exceed the supported count",
                 (long long)a_out);
@@ -901,17 +1175,15 @@ struct LayerBuild {
     }
     // persistent rulebook storage in one block
     auto al = [](int64_t bytes) { return (bytes + 255) & ~int64_t(255); };
-    const int64_t sz_oc = al(a_out * 16), sz_pair = al(pmax * 4), sz_perm = al(n * 4),
-                  sz_off = al((K + 1) * 8), sz_ot = al((K * nt + 1) * 8),
-                  sz_it = al((K * nit + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
+    const int64_t sz_oc = al(a_out * 16), sz_ot = al((K * nt + 1) * 8),
+                  sz_nbr = pool ? al(a_out * K * 4) : 0,
                   sz_inv = pool ? al(n * 4 * inv_slots) : 0;
     // dense forward view for large stride-1 rulebooks (see scn_rulebook)
     dense = s == 1 && dense_forward_for(a_out, K);
     nfb = dense ? ceil_div(a_out, DENSE_ROWS) : 0;
     const int64_t sz_fnb = al((pmax + 1) * 4), sz_fnboff = al((a_out + 1) * 4),
                   sz_fperm = al(a_out * 4), sz_fmask = al(a_out * 4);
-    const int64_t total = sz_oc + 2 * sz_pair + (sorted ? 0 : sz_pair + sz_perm) + sz_off +
-                          sz_ot + sz_it + sz_nbr + sz_inv +
+    const int64_t total = sz_oc + sz_ot + sz_nbr + sz_inv +
                           (dense ? sz_fnb + sz_fnboff + sz_fperm + sz_fmask : 0);
     rb = new scn_rulebook();
     rb->alloc = mem;
@@ -924,13 +1196,15 @@ struct LayerBuild {
       return p;
     };
     rb->out_coords = (int32_t*)take(sz_oc);
-    rb->in_rows = (int32_t*)take(sz_pair);
-    rb->out_rows = (int32_t*)take(sz_pair);
-    rb->in_rank = sorted ? rb->in_rows : (int32_t*)take(sz_pair);
-    rb->perm = sorted ? nullptr : (int32_t*)take(sz_perm);  // identity when sorted
-    rb->off_dev = (int64_t*)take(sz_off);
+    rb->in_rows = in_rows;
+    rb->out_rows = out_rows;
+    rb->in_rank = sorted || !in_rank_arr ? in_rows : in_rank_arr;
+    rb->perm = sorted ? nullptr : perm;  // identity when sorted
+    rb->off_dev = off_dev;
     rb->otile = (int64_t*)take(sz_ot);
-    rb->itile = (int64_t*)take(sz_it);
+    rb->itile = itile;
+    rb->inblock = inblock;  // owned by rb from here (freed with it)
+    inblock = nullptr;
     rb->nbr = pool ? (int32_t*)take(sz_nbr) : nullptr;
     rb->inv = pool ? (int32_t*)take(sz_inv) : nullptr;
     rb->inv_slots = inv_slots;
@@ -958,13 +1232,12 @@ struct LayerBuild {
     rb->n_itiles = nit;
 
     ncnt = K * nt;
-    // the mask sort's scratch size (a query; no device work)
-    if (dense)
-      SCN_HIP(mask_sort(nullptr, sort_bytes, nullptr, nullptr, nullptr, nullptr, a_out, K, st));
+    // the mask sort's scratch
+    if (dense) sort_bytes = (size_t)radix_sort_words(a_out) * 4;
     if ((rc = tmp.reserve(Temps::round(a_out * 4) + Temps::round(ncnt * 8) +
                           Temps::round(scan_blocks(ncnt) * 8) +
                           (dense ? Temps::round(scan_blocks(a_out) * 4) +
-                                       Temps::round(a_out * 4) + Temps::round(sort_bytes)
+                                       Temps::round(sort_bytes)
                                  : 0))))
       return rc;
     if ((rc = tmp.get(&masks, a_out)) || (rc = tmp.get(&cnt, ncnt)) ||
@@ -977,10 +1250,15 @@ struct LayerBuild {
     scn_status rc;
     const uint32_t* outb = rb->hout_bits;
     const uint32_t* opref = rb->hout_rank;
-    if (n > 0 && !sorted) {
-      hipLaunchKernelGGL(perm_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n, gi,
-                         inb, ipref, rb->perm);
+    if (!early) {
+      // the lists of a layer whose sites arrived after the first wait; the
+      // host waits for their boundaries
+      if ((rc = emit_lists())) return rc;
+      hipLaunchKernelGGL(list_offsets_kernel, dim3(1), dim3(64), 0, st, (const int64_t*)itile,
+                         nit, K, off_dev);
       SCN_LAUNCH_CHECK();
+      SCN_HIP(hipMemcpyAsync(hb->off, off_dev, (K + 1) * 8, hipMemcpyDeviceToHost, st));
+      SCN_HIP(hipEventRecord(copied, st));
     }
     if (a_out > 0) {
       with_kernels(f, lattice, [&](auto k) {
@@ -997,14 +1275,6 @@ struct LayerBuild {
     if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, ncnt, (uint64_t*)rb->otile,
                                        (uint64_t*)rb->otile + ncnt, sc64, st)))
       return rc;
-    hipLaunchKernelGGL(list_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)rb->otile,
-                       nt, K, rb->off_dev);
-    SCN_LAUNCH_CHECK();
-    // From here the host needs only the list boundaries: copy them now and
-    // queue the rest of the build behind the copy, so the GPU keeps working
-    // while the caller waits for the copy alone.
-    SCN_HIP(hipMemcpyAsync(hb->off, rb->off_dev, (K + 1) * 8, hipMemcpyDeviceToHost, st));
-    SCN_HIP(hipEventRecord(copied, st));
     if (dense) {
       // start of each output's neighbour list: exclusive sum of mask popcounts
       uint32_t* sc_nb = nullptr;
@@ -1013,27 +1283,23 @@ struct LayerBuild {
                                          rb->fnb_off + a_out, sc_nb, st)))
         return rc;
     }
-    if (a_out > 0) {
+    if (a_out > 0 && (rb->nbr || rb->fnb)) {
       with_kernels(f, lattice, [&](auto k) {
-        // LDS stages the window table: 64*K words per wave of 256-thread blocks
-        k.emit(dim3(blocks_for(nt * TILE, 256)), rb->nbr ? (size_t)256 * K * 4 : 0, st,
-               (const uint32_t*)masks, (const int32_t*)rb->out_coords, a_out, nt, s,
-               (const uint32_t*)inb,
-               (const uint32_t*)ipref, gi, (const int32_t*)rb->perm, (const uint64_t*)rb->otile,
-               rb->in_rows, rb->out_rows, sorted ? nullptr : rb->in_rank, rb->nbr,
-               (const uint32_t*)rb->fnb_off, rb->fnb);
+        // LDS stages the window table or the neighbour list
+        k.emit_out(dim3(blocks_for(nt * TILE, 256)),
+                   rb->nbr ? (size_t)256 * K * 4 : (size_t)256 * EMIT_NB_STAGE * 4, st,
+                   (const uint32_t*)masks, (const int32_t*)rb->out_coords, a_out, s,
+                   (const uint32_t*)inb, (const uint32_t*)ipref, gi, (const int32_t*)rb->perm,
+                   rb->nbr, (const uint32_t*)rb->fnb_off, rb->fnb);
       });
       SCN_LAUNCH_CHECK();
     }
     if (dense) {
       // the output rows sorted by neighbour mask (a stable radix sort)
-      int32_t* iota = nullptr;
-      char* sort_tmp = nullptr;
-      if ((rc = tmp.get(&iota, a_out)) || (rc = tmp.get(&sort_tmp, sort_bytes))) return rc;
-      hipLaunchKernelGGL(iota_kernel, dim3(blocks_for(a_out, 256)), dim3(256), 0, st, iota,
-                         a_out);
-      SCN_LAUNCH_CHECK();
-      SCN_HIP(mask_sort(sort_tmp, sort_bytes, masks, rb->fmask, iota, rb->fperm, a_out, K, st));
+      uint32_t* sort_tmp = nullptr;
+      if ((rc = tmp.get(&sort_tmp, sort_bytes / 4)) ||
+          (rc = radix_sort_pairs(masks, rb->fmask, rb->fperm, a_out, K, sort_tmp, st)))
+        return rc;
     }
     if (pool && n > 0) {
       with_kernels(f, lattice, [&](auto k) {
@@ -1042,9 +1308,6 @@ struct LayerBuild {
       });
       SCN_LAUNCH_CHECK();
     }
-    hipLaunchKernelGGL(in_tiles_kernel, dim3(blocks_for(K * nit + 1, 256)), dim3(256), 0, st,
-                       rb->in_rank, rb->off_dev, K, nit, rb->itile);
-    SCN_LAUNCH_CHECK();
     SCN_HIP(hipEventCreateWithFlags(&rb->done, hipEventDisableTiming));
     SCN_HIP(hipEventRecord(rb->done, st));
     return SCN_OK;
@@ -1052,7 +1315,7 @@ struct LayerBuild {
 
   scn_status finish(scn_rulebook** out) {
     rb->n_pairs = hb->off[K];
-    if (rb->n_pairs > INT32_MAX || rb->n_pairs > pmax) {
+    if (rb->n_pairs > INT32_MAX || rb->n_pairs > pcap) {
       set_error("scn_rulebook_build: %lld pairs exceed the supported count",
                 (long long)rb->n_pairs);
       return SCN_ERR_OVERFLOW;
@@ -1104,7 +1367,7 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   // call returns.  prev is freed on its own stream, so that stream waits
   // for them: a free of prev after this call is then ordered after them.
   if (prev && prev->stream != st) SCN_HIP(hipStreamWaitEvent(prev->stream, L.rb->done, 0));
-  SCN_HIP(hipEventSynchronize(copied));
+  if (!L.early) SCN_HIP(hipEventSynchronize(copied));
   return L.finish(out);
 }
 
@@ -1165,7 +1428,10 @@ scn_status build_chain(const int32_t* coords, int64_t n, const int64_t* grid, in
     }
     if ((rc = L.sized()) || (rc = L.phase2(copied))) return rc;
   }
-  SCN_HIP(hipEventSynchronize(copied));  // the last layer's copy, so every layer's
+  // the last deferred layer's copy, so every layer's boundaries are known
+  bool deferred = false;
+  for (int i = 0; i < nl; ++i) deferred = deferred || !Ls[i]->early;
+  if (deferred) SCN_HIP(hipEventSynchronize(copied));
   std::vector<scn_rulebook*> res(nl, nullptr);
   for (int i = 0; i < nl; ++i)
     if ((rc = Ls[i]->finish(&res[i]))) {
@@ -1274,6 +1540,7 @@ void scn_rulebook_free(scn_rulebook* rb) {
   if (!rb) return;
   scn::dfree(rb->block, rb->stream, rb->alloc);
   scn::dfree(rb->hout_bits, rb->stream, rb->alloc);  // also holds hout_rank
+  scn::dfree(rb->inblock, rb->stream, rb->alloc);
   if (rb->done) (void)hipEventDestroy(rb->done);
   delete rb;
 }

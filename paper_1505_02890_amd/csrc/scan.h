@@ -83,6 +83,14 @@ __device__ inline void store16(T* p, const T (&v)[SCAN_ITEMS]) {
   }
 }
 
+// loader of a plain array
+template <typename T>
+struct PlainLoad {
+  const T* v;
+  __device__ T operator()(int64_t i) const { return v[i]; }
+  __device__ void chunk(int64_t i, T (&x)[SCAN_ITEMS]) const { load16<T>(v + i, x); }
+};
+
 template <typename T, class Load>
 __global__ void __launch_bounds__(SCAN_THREADS) scan_reduce_kernel(Load ld, int64_t n,
                                                                    T* block_sums) {

@@ -32,10 +32,10 @@ struct DeviceBuffer {
 };
 
 // Device allocation: the caller's hooks (scn_set_allocator) or, by default,
-// stream-ordered allocation from the device's default memory pool.  A value
+// the library's caching allocator (common.hip).  A value
 // is a snapshot: memory goes back through the allocator that produced it.
 struct Allocator {
-  void* (*alloc)(size_t bytes, hipStream_t s, void* ctx) = nullptr;  // null: default pool
+  void* (*alloc)(size_t bytes, hipStream_t s, void* ctx) = nullptr;  // null: the library's cache
   void (*free)(void* p, hipStream_t s, void* ctx) = nullptr;
   void* ctx = nullptr;
 };
@@ -126,7 +126,8 @@ struct scn_rulebook {
   // running; entry points called on another stream wait for this event.
   hipEvent_t done = nullptr;
 
-  void* block = nullptr;  // single allocation holding all arrays above
+  void* block = nullptr;    // one allocation holding the arrays above but perm and itile
+  void* inblock = nullptr;  // one allocation holding perm and itile
   scn::Allocator alloc;   // the allocator every array of the rulebook came from
 
   // The output layer's rank bitmap (H_out): occupancy words of the output grid
