@@ -1175,11 +1175,11 @@ struct LayerBuild {
     }
     // persistent rulebook storage in one block
     auto al = [](int64_t bytes) { return (bytes + 255) & ~int64_t(255); };
-    const int64_t sz_oc = al(a_out * 16), sz_ot = al((K * nt + 1) * 8),
-                  sz_nbr = pool ? al(a_out * K * 4) : 0,
-                  sz_inv = pool ? al(n * 4 * inv_slots) : 0;
     // dense forward view for large stride-1 rulebooks (see scn_rulebook)
     dense = s == 1 && dense_forward_for(a_out, K);
+    const int64_t sz_oc = al(a_out * 16), sz_ot = dense ? 0 : al((K * nt + 1) * 8),
+                  sz_nbr = pool ? al(a_out * K * 4) : 0,
+                  sz_inv = pool ? al(n * 4 * inv_slots) : 0;
     nfb = dense ? ceil_div(a_out, DENSE_ROWS) : 0;
     const int64_t sz_fnb = al((pmax + 1) * 4), sz_fnboff = al((a_out + 1) * 4),
                   sz_fperm = al(a_out * 4), sz_fmask = al(a_out * 4);
@@ -1201,7 +1201,7 @@ struct LayerBuild {
     rb->in_rank = sorted || !in_rank_arr ? in_rows : in_rank_arr;
     rb->perm = sorted ? nullptr : perm;  // identity when sorted
     rb->off_dev = off_dev;
-    rb->otile = (int64_t*)take(sz_ot);
+    rb->otile = dense ? nullptr : (int64_t*)take(sz_ot);  // the dense view replaces it
     rb->itile = itile;
     rb->inblock = inblock;  // owned by rb from here (freed with it)
     inblock = nullptr;
@@ -1231,7 +1231,7 @@ struct LayerBuild {
     rb->n_otiles = nt;
     rb->n_itiles = nit;
 
-    ncnt = K * nt;
+    ncnt = dense ? 0 : K * nt;  // tile counts only for the pair-list forward
     // the mask sort's scratch
     if (dense) sort_bytes = (size_t)radix_sort_words(a_out) * 4;
     if ((rc = tmp.reserve(Temps::round(a_out * 4) + Temps::round(ncnt * 8) +
@@ -1267,14 +1267,19 @@ struct LayerBuild {
       });
       SCN_LAUNCH_CHECK();
     }
-    with_kernels(f, lattice, [&](auto k) {
-      k.tile_count(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks, a_out, nt, cnt);
-    });
-    SCN_LAUNCH_CHECK();
-    // positions: otile[k*nt + t] = off[k] + pairs of list k in tiles < t
-    if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, ncnt, (uint64_t*)rb->otile,
-                                       (uint64_t*)rb->otile + ncnt, sc64, st)))
-      return rc;
+    if (!dense) {
+      // pair ranges per output tile, for the pair-list forward (a rulebook
+      // with the dense view forwards through it instead):
+      // otile[k*nt + t] = off[k] + pairs of list k in tiles < t
+      with_kernels(f, lattice, [&](auto k) {
+        k.tile_count(dim3(blocks_for(nt * TILE, 256)), st, (const uint32_t*)masks, a_out, nt,
+                     cnt);
+      });
+      SCN_LAUNCH_CHECK();
+      if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, ncnt, (uint64_t*)rb->otile,
+                                         (uint64_t*)rb->otile + ncnt, sc64, st)))
+        return rc;
+    }
     if (dense) {
       // start of each output's neighbour list: exclusive sum of mask popcounts
       uint32_t* sc_nb = nullptr;

@@ -92,6 +92,7 @@ struct scn_rulebook {
   // Pair ranges per tile.  otile[k*n_otiles + t] = global position of the first
   // pair of list k whose output row is >= t*TILE (t in [0, n_otiles]); the last
   // entry of list k equals the start of list k+1.  Length K*n_otiles + 1.
+  // Null in a rulebook with the dense forward view (its forward does not use it).
   int64_t n_otiles = 0;
   int64_t* otile = nullptr;
   // Same per tile of TILE input ranks (for the input-gradient pass).
