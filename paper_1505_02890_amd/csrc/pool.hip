@@ -77,6 +77,28 @@ __global__ void __launch_bounds__(256) maxpool_bwd_dx_kernel(const int32_t* __re
 // A block holds `per` sites with nc4 = C/4 threads each; argmax bytes of four
 // channels travel as one 32-bit word (byte e = channel 4*c4 + e).
 
+// The block's window-table rows are contiguous in nbr: the block loads them
+// into LDS with a few coalesced loads, instead of every lane of an output
+// loading each entry (for 64 channels, 16 lanes per output asked for the same
+// word, one load instruction per window position).
+template <int K>
+__device__ inline const int32_t* stage_rows(const int32_t* __restrict__ nbr, int64_t o_first,
+                                            int64_t a_out, int rows, int32_t* sh) {
+  const int64_t n = (o_first + rows < a_out ? (int64_t)rows : a_out - o_first) * K;
+  const int32_t* src = nbr + o_first * K;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) sh[i] = src[i];
+  __syncthreads();
+  return sh;
+}
+
+typedef float pool_v4f __attribute__((ext_vector_type(4)));
+
+// A streaming store, for rows nothing reads again soon (dx): 5-10% faster
+// than a plain store in the backward kernels.
+__device__ inline void store_stream(float4* p, float4 v) {
+  __builtin_nontemporal_store(pool_v4f{v.x, v.y, v.z, v.w}, reinterpret_cast<pool_v4f*>(p));
+}
+
 template <int K>
 __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __restrict__ x,
                                                               const float4* __restrict__ g_in,
@@ -84,11 +106,14 @@ __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __re
                                                               int64_t a_out, int nc4, int per,
                                                               float4* __restrict__ y,
                                                               uint32_t* __restrict__ argmax) {
+  extern __shared__ int32_t nsh[];  // per * K entries
   const int ol = threadIdx.x / nc4, c4 = threadIdx.x - ol * nc4;
-  const int64_t o = (int64_t)blockIdx.x * per + ol;
+  // overlapping windows share inputs with the windows of nearby blocks
+  const int64_t ob = (int64_t)blockIdx.x * per, o = ob + ol;
+  stage_rows<K>(nbr, ob, a_out, per, nsh);
   if (ol >= per || o >= a_out) return;
   const float4 g = g_in[c4];
-  const int32_t* nb = nbr + o * K;
+  const int32_t* nb = nsh + ol * K;
   // first strict maximum in ascending k, per channel
   // (the 27 positions of a 3-wide cube window a plane of 9 at a time;
   // smaller windows all at once)
@@ -97,14 +122,14 @@ __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __re
   uint32_t b0 = 0, b1 = 0, b2 = 0, b3 = 0;
 #pragma unroll 1
   for (int kz = 0; kz < NPL; ++kz) {
-    // branch-free: an inactive position reads row 0 (there is one: the
-    // output is active) and takes g, so all window loads are in flight together
+    // an inactive position takes g and loads nothing (its lanes are masked
+    // off); a plane's loads are all in flight together
     float4 v[PL];
 #pragma unroll
     for (int i = 0; i < PL; ++i) {
       const int32_t r = nb[kz * PL + i];
-      const float4 t = x[(int64_t)(r >= 0 ? r : 0) * nc4 + c4];
-      v[i] = r >= 0 ? t : g;
+      v[i] = g;
+      if (r >= 0) v[i] = x[(int64_t)r * nc4 + c4];
     }
 #pragma unroll
     for (int i = 0; i < PL; ++i) {
@@ -123,7 +148,7 @@ __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __re
   argmax[o * nc4 + c4] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
 }
 
-constexpr int PBV_ROWS = 256;  // outputs per block of the four-channel backward
+constexpr int PBV_ROWS = 64;  // outputs per block of the four-channel backward
 
 // Output-major backward: an input lies in at most one window, so each window
 // writes its inputs' dx rows (dy where the input won, else 0) and dx is
@@ -139,10 +164,12 @@ __global__ void __launch_bounds__(256) maxpool_bwd_vec_kernel(const int32_t* __r
                                                               float4* __restrict__ dx,
                                                               float4* __restrict__ part) {
   __shared__ float4 red[256];
+  __shared__ int32_t nsh[PBV_ROWS * K];
   const int rows = 256 / nc4;  // outputs in flight per block
   const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
   const int64_t o0 = (int64_t)blockIdx.x * PBV_ROWS;
   const int64_t o1 = min<int64_t>(o0 + PBV_ROWS, a_out);
+  stage_rows<K>(nbr, o0, a_out, PBV_ROWS, nsh);
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
   if (rl < rows)
     for (int64_t o = o0 + rl; o < o1; o += rows) {
@@ -150,14 +177,14 @@ __global__ void __launch_bounds__(256) maxpool_bwd_vec_kernel(const int32_t* __r
       const uint32_t am = argmax[j];
       const float4 d = dy[j];
       const uint32_t k0 = am & 255u, k1 = (am >> 8) & 255u, k2 = (am >> 16) & 255u, k3 = am >> 24;
-      const int32_t* nb = nbr + o * K;
+      const int32_t* nb = nsh + (o - o0) * K;
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         const int32_t r = nb[k];
         const float4 v = make_float4(k0 == (uint32_t)k ? d.x : 0.f, k1 == (uint32_t)k ? d.y : 0.f,
                                      k2 == (uint32_t)k ? d.z : 0.f, k3 == (uint32_t)k ? d.w : 0.f);
         if (r >= 0) {
-          if (dx) dx[(int64_t)r * nc4 + c4] = v;
+          if (dx) store_stream(dx + (int64_t)r * nc4 + c4, v);
         } else {
           s.x += v.x;
           s.y += v.y;
@@ -181,12 +208,41 @@ __global__ void __launch_bounds__(256) maxpool_bwd_vec_kernel(const int32_t* __r
   }
 }
 
-// Overlapping windows (filter > stride): an input lies in up to 8 windows.
-// dx[r][c] = sum over its windows (slot order 0..7, a fixed order) of
-// dy[o][c] where the input won channel c of window o.  win[r*8 + j] = o*K + k
-// or -1.  The window size K is a compile-time constant, so the slot
-// decodes are multiplications, and an empty slot loads nothing (its lanes
-// are masked off); every slot load is still issued before the first use.
+// dx[r] of one input over its (up to 8) windows: win8 = its slots (o*K + k
+// or -1), summed in slot order, a fixed order; nc4 lanes, channels 4*c4 ..
+template <int K>
+__device__ inline float4 input_grad(const int32_t (&t)[8], const uint32_t* __restrict__ argmax,
+                                    const float4* __restrict__ dy, int nc4, int c4) {
+  uint32_t am[8];
+  float4 d[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    am[j] = 0u;
+    d[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (t[j] >= 0) {  // an empty slot loads nothing: its lanes are masked off
+      const int64_t jj = (int64_t)((uint32_t)t[j] / K) * nc4 + c4;
+      am[j] = argmax[jj];
+      d[j] = dy[jj];
+    }
+  }
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    // 255: an empty slot, which no argmax byte holds
+    const uint32_t k = t[j] >= 0 ? (uint32_t)t[j] % K : 255u;
+    v.x += (am[j] & 255u) == k ? d[j].x : 0.f;
+    v.y += ((am[j] >> 8) & 255u) == k ? d[j].y : 0.f;
+    v.z += ((am[j] >> 16) & 255u) == k ? d[j].z : 0.f;
+    v.w += (am[j] >> 24) == k ? d[j].w : 0.f;
+  }
+  return v;
+}
+
+// Overlapping windows (filter > stride), input-major: an input lies in up to 8
+// windows, win[r*8 + j] = o*K + k or -1.  dx[r][c] = sum over its windows
+// (slot order) of dy[o][c] where the input won channel c of window o.  nc4
+// lanes per input.  (3-wide windows of stride 2 on the cubic lattice take the
+// cell-major kernel below instead, with about a third of the gathers.)
 template <int K>
 __global__ void __launch_bounds__(256) maxpool_bwd_overlap_vec_kernel(
     const int32_t* __restrict__ win, const uint32_t* __restrict__ argmax,
@@ -197,31 +253,125 @@ __global__ void __launch_bounds__(256) maxpool_bwd_overlap_vec_kernel(
   const int4 w0 = reinterpret_cast<const int4*>(win)[2 * r];
   const int4 w1 = reinterpret_cast<const int4*>(win)[2 * r + 1];
   const int32_t t[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-  uint32_t am[8];
-  float4 d[8];
-  uint32_t kk[8];
+  store_stream(dx + r * nc4 + c4, input_grad<K>(t, argmax, dy, nc4, c4));
+}
+
+// Inputs without a home window (3-wide windows of stride 2, cubic lattice):
+// the listed inputs, input-major as above (all slots empty: dx = 0).  A
+// grid-stride loop up to the count the rulebook build left on the device.
+__global__ void __launch_bounds__(256) maxpool_bwd_homeless_vec_kernel(
+    const int32_t* __restrict__ list, const int32_t* __restrict__ count,
+    const int32_t* __restrict__ win, const uint32_t* __restrict__ argmax,
+    const float4* __restrict__ dy, int nc4, int per, float4* __restrict__ dx) {
+  const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
+  if (rl >= per) return;
+  const int64_t n = *count;
+  for (int64_t i = (int64_t)blockIdx.x * per + rl; i < n; i += (int64_t)gridDim.x * per) {
+    const int64_t r = list[i];
+    const int4 w0 = reinterpret_cast<const int4*>(win)[2 * r];
+    const int4 w1 = reinterpret_cast<const int4*>(win)[2 * r + 1];
+    const int32_t t[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+    dx[r * nc4 + c4] = input_grad<27>(t, argmax, dy, nc4, c4);
+  }
+}
+
+// 3-wide windows of stride 2 on the cubic lattice, cell-major.  Window h's
+// home cell holds the inputs at its offsets w = (wx, wy, wz) in {0,1}^3
+// (position wx + 3wy + 9wz); such an input also lies in window h - b for each
+// b in {0,1}^3 with no bit where w has a 1 (low[h*8 + b]), at position
+// (wx + 2bx) + 3(wy + 2by) + 9(wz + 2bz), b being its slot there.  Each lane
+// group (nc4 lanes) takes a window, gathers dy and argmax of the windows h - b
+// its active home inputs need (avg about 5 for surfaces), and writes each
+// home input's dx row: the sum over its slots in slot order, the same sum
+// the input-major kernel forms.  Every input with a home window is written
+// exactly once (the others are listed as homeless).  The gathers per input
+// drop from 3.4 rows to about 1.2.  The window's own dy and argmax also give
+// the ground-state sums (dy where the winner is inactive), so no separate
+// pass reads them: part[blk][c] sums the block's windows in a fixed order
+// (part may be null).  PBV_ROWS windows per block: their home entries and
+// lower windows are staged in LDS once.
+__global__ void __launch_bounds__(256) maxpool_bwd_cells_kernel(
+    const int32_t* __restrict__ nbr, const int32_t* __restrict__ low,
+    const uint32_t* __restrict__ pmask, const uint32_t* __restrict__ argmax,
+    const float4* __restrict__ dy, int64_t a_out, int nc4, float4* __restrict__ dx,
+    float4* __restrict__ part) {
+  __shared__ int32_t home[PBV_ROWS * 8];
+  __shared__ int4 lows[PBV_ROWS * 2];
+  __shared__ float4 red[256];
+  const int64_t h0 = (int64_t)blockIdx.x * PBV_ROWS;
+  const int nh = (int)min<int64_t>(PBV_ROWS, a_out - h0);
+  if ((int)threadIdx.x < nh) {
+    const int t = threadIdx.x;
+    const int32_t* row = nbr + (h0 + t) * 27;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const bool ok = t[j] >= 0;
-    const uint32_t o = ok ? (uint32_t)t[j] / K : 0u;
-    kk[j] = ok ? (uint32_t)t[j] - o * K : 255u;  // 255: no argmax byte holds it
-    const int64_t jj = (int64_t)o * nc4 + c4;
-    am[j] = 0u;
-    d[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (ok) {
-      am[j] = argmax[jj];
-      d[j] = dy[jj];
+    for (int w = 0; w < 8; ++w) home[t * 8 + w] = row[(w & 1) + 3 * ((w >> 1) & 1) + 9 * (w >> 2)];
+  }
+  for (int i = threadIdx.x; i < 2 * nh; i += 256)
+    lows[i] = reinterpret_cast<const int4*>(low + h0 * 8)[i];
+  __syncthreads();
+  const int rows = 256 / nc4;
+  const int rl = threadIdx.x / nc4, c4 = threadIdx.x - rl * nc4;
+  float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (rl < rows)
+    for (int i = rl; i < nh; i += rows) {
+      const int32_t* hm = home + i * 8;
+      const int4 la = lows[2 * i], lb = lows[2 * i + 1];
+      const int32_t lw[8] = {la.x, la.y, la.z, la.w, lb.x, lb.y, lb.z, lb.w};
+      uint32_t act = 0u;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) act |= (hm[w] >= 0 ? 1u : 0u) << w;
+      uint32_t am[8];
+      float4 d[8];
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        // home offsets with no 1 along b's axes: these lie in window h - b
+        constexpr uint32_t ZX = 0x55u, ZY = 0x33u, ZZ = 0x0Fu;
+        const uint32_t zm = ((b & 1) ? ZX : 0xFFu) & ((b & 2) ? ZY : 0xFFu) & ((b & 4) ? ZZ : 0xFFu);
+        am[b] = 0u;
+        d[b] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (b == 0 || (lw[b] >= 0 && (act & zm))) {
+          const int64_t jj = (int64_t)lw[b] * nc4 + c4;
+          am[b] = argmax[jj];
+          d[b] = dy[jj];
+        }
+      }
+      // ground state: channels of window h whose winner is an inactive position
+      const uint32_t m = pmask[h0 + i];
+      if (!((m >> (am[0] & 255u)) & 1u)) g.x += d[0].x;
+      if (!((m >> ((am[0] >> 8) & 255u)) & 1u)) g.y += d[0].y;
+      if (!((m >> ((am[0] >> 16) & 255u)) & 1u)) g.z += d[0].z;
+      if (!((m >> (am[0] >> 24)) & 1u)) g.w += d[0].w;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        if (hm[w] < 0) continue;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          if (b & w) continue;  // not a window of this input
+          if (b != 0 && lw[b] < 0) continue;
+          const uint32_t k = ((w & 1) + 2 * (b & 1)) + 3 * (((w >> 1) & 1) + 2 * ((b >> 1) & 1)) +
+                             9 * ((w >> 2) + 2 * (b >> 2));
+          v.x += (am[b] & 255u) == k ? d[b].x : 0.f;
+          v.y += ((am[b] >> 8) & 255u) == k ? d[b].y : 0.f;
+          v.z += ((am[b] >> 16) & 255u) == k ? d[b].z : 0.f;
+          v.w += (am[b] >> 24) == k ? d[b].w : 0.f;
+        }
+        store_stream(dx + (int64_t)hm[w] * nc4 + c4, v);
+      }
     }
+  if (!part) return;
+  red[threadIdx.x] = g;
+  __syncthreads();
+  if (rl == 0) {
+    for (int i = 1; i < rows; ++i) {
+      const float4 t = red[i * nc4 + c4];
+      g.x += t.x;
+      g.y += t.y;
+      g.z += t.z;
+      g.w += t.w;
+    }
+    part[(int64_t)blockIdx.x * nc4 + c4] = g;
   }
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    v.x += (am[j] & 255u) == kk[j] ? d[j].x : 0.f;
-    v.y += ((am[j] >> 8) & 255u) == kk[j] ? d[j].y : 0.f;
-    v.z += ((am[j] >> 16) & 255u) == kk[j] ? d[j].z : 0.f;
-    v.w += (am[j] >> 24) == kk[j] ? d[j].w : 0.f;
-  }
-  dx[r * nc4 + c4] = v;
 }
 
 __global__ void __launch_bounds__(256) maxpool_bwd_overlap_kernel(const int32_t* __restrict__ win,
@@ -247,12 +397,12 @@ __global__ void __launch_bounds__(256) maxpool_bwd_overlap_kernel(const int32_t*
 
 // Ground-state partial sums alone (the overlapping case computes dx input-
 // major): part[blk][c] sums, over the block's outputs in a fixed order, dy[o][c]
-// where the winner of (o, c) is an inactive position.  Only the winners' window
-// entries are read.
-__global__ void __launch_bounds__(256) maxpool_ground_vec_kernel(const int32_t* __restrict__ nbr,
+// where the winner of (o, c) is an inactive position (bit am of pmask[o]
+// clear).  A stream over argmax and dy.
+__global__ void __launch_bounds__(256) maxpool_ground_vec_kernel(const uint32_t* __restrict__ pmask,
                                                                  const uint32_t* __restrict__ argmax,
                                                                  const float4* __restrict__ dy,
-                                                                 int64_t a_out, int nc4, int K,
+                                                                 int64_t a_out, int nc4,
                                                                  float4* __restrict__ part) {
   __shared__ float4 red[256];
   const int rows = 256 / nc4;
@@ -261,15 +411,15 @@ __global__ void __launch_bounds__(256) maxpool_ground_vec_kernel(const int32_t* 
   const int64_t o1 = min<int64_t>(o0 + PBV_ROWS, a_out);
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
   if (rl < rows)
+#pragma unroll 4
     for (int64_t o = o0 + rl; o < o1; o += rows) {
       const int64_t j = o * nc4 + c4;
-      const uint32_t am = argmax[j];
+      const uint32_t am = argmax[j], m = pmask[o];
       const float4 d = dy[j];
-      const int32_t* nb = nbr + o * K;
-      if (nb[am & 255u] < 0) s.x += d.x;
-      if (nb[(am >> 8) & 255u] < 0) s.y += d.y;
-      if (nb[(am >> 16) & 255u] < 0) s.z += d.z;
-      if (nb[am >> 24] < 0) s.w += d.w;
+      if (!((m >> (am & 255u)) & 1u)) s.x += d.x;
+      if (!((m >> ((am >> 8) & 255u)) & 1u)) s.y += d.y;
+      if (!((m >> ((am >> 16) & 255u)) & 1u)) s.z += d.z;
+      if (!((m >> (am >> 24)) & 1u)) s.w += d.w;
     }
   red[threadIdx.x] = s;
   __syncthreads();
@@ -300,10 +450,10 @@ constexpr int PB_ROWS = 1024;  // outputs per block of the one-channel ground gr
 // ---- any channel count (one channel per thread) -----------------------------
 
 // partial[blk][c] = sum over the block's outputs of dy[o][c] where the winner is inactive
-__global__ void __launch_bounds__(256) maxpool_bwd_ground_kernel(const int32_t* __restrict__ nbr,
+__global__ void __launch_bounds__(256) maxpool_bwd_ground_kernel(const uint32_t* __restrict__ pmask,
                                                                  const uint8_t* __restrict__ argmax,
                                                                  const float* __restrict__ dy,
-                                                                 int64_t a_out, int C, int K,
+                                                                 int64_t a_out, int C,
                                                                  float* __restrict__ part) {
   __shared__ float red[256];
   const int64_t o0 = (int64_t)blockIdx.x * PB_ROWS;
@@ -315,7 +465,7 @@ __global__ void __launch_bounds__(256) maxpool_bwd_ground_kernel(const int32_t* 
     if (c < C)
       for (int64_t o = o0 + rg; o < o1; o += 4) {
         const int64_t j = o * C + c;
-        if (nbr[o * K + argmax[j]] < 0) s += dy[j];
+        if (!((pmask[o] >> argmax[j]) & 1u)) s += dy[j];
       }
     red[threadIdx.x] = s;
     __syncthreads();
@@ -403,8 +553,9 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
       auto* y4 = reinterpret_cast<float4*>(y);
       auto* am4 = reinterpret_cast<uint32_t*>(argmax);
       with_window(rb->K, [&](auto k) {
-        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<decltype(k)::value>, grid, dim3(256), 0, st, x4,
-                           g4, rb->nbr, rb->a_out, nc4, per, y4, am4);
+        constexpr int K = decltype(k)::value;
+        hipLaunchKernelGGL(maxpool_fwd_vec_kernel<K>, grid, dim3(256), per * K * sizeof(int32_t),
+                           st, x4, g4, rb->nbr, rb->a_out, nc4, per, y4, am4);
       });
     } else {
       hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(nblocks(rb->a_out * C, 256)), dim3(256), 0, st,
@@ -447,18 +598,40 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
   const bool vec = pool_vec_ok(C, {dy, dx, part}, argmax);
   const bool overlap = rb->inv_slots == 8;
   int64_t nblk = 0;
-  if (overlap) {
+  if (overlap && vec && rb->lowwin) {
+    // cell-major (3-wide windows of stride 2, cubic lattice): the inputs
+    // without a home window, then every window's home cell and ground sums
+    const int nc4 = C / 4, per = 256 / nc4;
+    const auto* am4 = reinterpret_cast<const uint32_t*>(argmax);
+    const auto* dy4 = reinterpret_cast<const float4*>(dy);
+    auto* dx4 = reinterpret_cast<float4*>(dx);
+    if (rb->a_in > 0) {
+      hipLaunchKernelGGL(maxpool_bwd_homeless_vec_kernel,
+                         dim3(std::min<unsigned>(nblocks(rb->a_in, per), 1024)), dim3(256), 0, st,
+                         rb->homeless, rb->n_homeless, rb->inv, am4, dy4, nc4, per, dx4);
+      SCN_LAUNCH_CHECK();
+    }
+    nblk = std::max<int64_t>(1, ceil_div(rb->a_out, PBV_ROWS));
+    if (rb->a_out > 0) {
+      hipLaunchKernelGGL(maxpool_bwd_cells_kernel, dim3((unsigned)nblk), dim3(256), 0, st, rb->nbr,
+                         rb->lowwin, rb->pmask, am4, dy4, rb->a_out, nc4, dx4,
+                         reinterpret_cast<float4*>(part));
+      SCN_LAUNCH_CHECK();
+    }
+  } else if (overlap) {
     // dx per input over its (up to 8) windows, then the ground-state sums
     // output-major
     if (rb->a_in > 0) {
       if (vec) {
-        const int nc4 = C / 4, per = 256 / nc4;
+        const int nc4 = C / 4;
+        const auto* am4 = reinterpret_cast<const uint32_t*>(argmax);
+        const auto* dy4 = reinterpret_cast<const float4*>(dy);
+        auto* dx4 = reinterpret_cast<float4*>(dx);
+        const int per = 256 / nc4;
         with_window(rb->K, [&](auto k) {
           hipLaunchKernelGGL(maxpool_bwd_overlap_vec_kernel<decltype(k)::value>,
                              dim3(nblocks(rb->a_in, per)), dim3(256), 0, st, rb->inv,
-                             reinterpret_cast<const uint32_t*>(argmax),
-                             reinterpret_cast<const float4*>(dy), rb->a_in, nc4, per,
-                             reinterpret_cast<float4*>(dx));
+                             am4, dy4, rb->a_in, nc4, per, dx4);
         });
       } else {
         hipLaunchKernelGGL(maxpool_bwd_overlap_kernel, dim3(nblocks(rb->a_in * C, 256)), dim3(256),
@@ -471,12 +644,12 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
       if (rb->a_out > 0) {
         if (vec) {
           hipLaunchKernelGGL(maxpool_ground_vec_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
-                             rb->nbr, reinterpret_cast<const uint32_t*>(argmax),
-                             reinterpret_cast<const float4*>(dy), rb->a_out, C / 4, rb->K,
+                             rb->pmask, reinterpret_cast<const uint32_t*>(argmax),
+                             reinterpret_cast<const float4*>(dy), rb->a_out, C / 4,
                              reinterpret_cast<float4*>(part));
         } else {
           hipLaunchKernelGGL(maxpool_bwd_ground_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
-                             rb->nbr, argmax, dy, rb->a_out, C, rb->K, part);
+                             rb->pmask, argmax, dy, rb->a_out, C, part);
         }
         SCN_LAUNCH_CHECK();
       }
@@ -510,7 +683,7 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
     nblk = std::max<int64_t>(1, ceil_div(rb->a_out, PB_ROWS));
     if (dg_in && rb->a_out > 0) {
       hipLaunchKernelGGL(maxpool_bwd_ground_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
-                         rb->nbr, argmax, dy, rb->a_out, C, rb->K, part);
+                         rb->pmask, argmax, dy, rb->a_out, C, part);
       SCN_LAUNCH_CHECK();
     }
   }

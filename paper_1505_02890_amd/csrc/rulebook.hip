@@ -480,11 +480,15 @@ __device__ inline int window_index(int kx, int ky, int kz) {
   return k + kx;
 }
 
+// With `homeless` given, inputs outside their home window (slot 0 empty:
+// the window starting at s*floor(x/s) along each axis lies outside the output
+// grid) are appended to homeless[], counted in *n_homeless (in no particular
+// order).
 template <int F, int LAT, int SLOTS>
 __global__ void __launch_bounds__(256) inv_windows_kernel(
     const int32_t* __restrict__ coords, int64_t n, int s, GridDev go,
     const uint32_t* __restrict__ outb, const uint32_t* __restrict__ opref,
-    int32_t* __restrict__ inv) {
+    int32_t* __restrict__ inv, int32_t* __restrict__ homeless, int32_t* __restrict__ n_homeless) {
   using W = Win<F, LAT>;
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= n) return;
@@ -513,6 +517,7 @@ __global__ void __launch_bounds__(256) inv_windows_kernel(
       v[slot] = (int32_t)((int64_t)rank * W::K + window_index<F, LAT>(k[0], k[1], k[2]));
     }
   }
+  if (homeless && v[0] < 0) homeless[atomicAdd(n_homeless, 1)] = (int32_t)r;
   if (SLOTS == 8) {
     int4* d = reinterpret_cast<int4*>(inv + r * 8);
     d[0] = make_int4(v[0], v[1], v[2], v[3]);
@@ -520,6 +525,39 @@ __global__ void __launch_bounds__(256) inv_windows_kernel(
   } else {
     inv[r] = v[0];
   }
+}
+
+// ---- phase 9c (3-wide windows of stride 2, cubic lattice): the cells ------
+// Window h's home cell is the 2x2x2 block of inputs at offsets {0,1}^3 of
+// it.  Those inputs also lie in the windows h - b (b in {0,1}^3, bit a: one
+// step down along axis a, x y z), at offset +2 along the axes of b.  The
+// backward walks windows and computes the dx of each one's home cell from
+// the dy rows of these 8 windows.  low[h*8 + b] = row of window h - b, or -1
+// when it is outside the grid or inactive (low[h*8] = h).  Thread 0 also
+// zeroes the homeless count that inv_windows_kernel fills next.
+__global__ void __launch_bounds__(256) lower_windows_kernel(
+    const int32_t* __restrict__ out_coords, int64_t a_out, GridDev go,
+    const uint32_t* __restrict__ outb, const uint32_t* __restrict__ opref,
+    int32_t* __restrict__ low, int32_t* __restrict__ n_homeless) {
+  const int64_t h = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (h == 0) *n_homeless = 0;
+  if (h >= a_out) return;
+  const int4 c = reinterpret_cast<const int4*>(out_coords)[h];
+  int32_t v[8];
+  v[0] = (int32_t)h;
+#pragma unroll
+  for (int b = 1; b < 8; ++b) {
+    const int x = c.y - (b & 1), y = c.z - ((b >> 1) & 1), z = c.w - (b >> 2);
+    v[b] = -1;
+    if (x >= 0 && y >= 0 && z >= 0) {
+      const int64_t w = row_base(go, c.x, y, z) + (x >> 5);
+      const uint32_t bits = outb[w], bit = 1u << (x & 31);
+      if (bits & bit) v[b] = (int32_t)(opref[w] + (uint32_t)__popc(bits & (bit - 1u)));
+    }
+  }
+  int4* d = reinterpret_cast<int4*>(low + h * 8);
+  d[0] = make_int4(v[0], v[1], v[2], v[3]);
+  d[1] = make_int4(v[4], v[5], v[6], v[7]);
 }
 
 // The first read-back: flags[1] = number of active inputs, flags[2] =
@@ -932,7 +970,7 @@ struct LayerBuild {
   Readback* drb = nullptr;                             // device side of the read-back
   // after phase 1
   int64_t a_out = 0, nt = 0, nit = 0, pmax = 0, nfb = 0;
-  bool sorted = true, pool = false, dense = false;
+  bool sorted = true, pool = false, dense = false, cells = false;
   int inv_slots = 0;
   scn_rulebook* rb = nullptr;
   bool keep = false;
@@ -1179,11 +1217,16 @@ struct LayerBuild {
     dense = s == 1 && dense_forward_for(a_out, K);
     const int64_t sz_oc = al(a_out * 16), sz_ot = dense ? 0 : al((K * nt + 1) * 8),
                   sz_nbr = pool ? al(a_out * K * 4) : 0,
-                  sz_inv = pool ? al(n * 4 * inv_slots) : 0;
+                  sz_inv = pool ? al(n * 4 * inv_slots) : 0,
+                  sz_pmask = pool ? al(a_out * 4) : 0;
+    // cell tables of 3-wide windows of stride 2 on the cubic lattice
+    cells = pool && lattice == SCN_LATTICE_CUBIC && f == 3 && s == 2;
+    const int64_t sz_low = cells ? al(a_out * 8 * 4) : 0,
+                  sz_homeless = cells ? al(std::max<int64_t>(n, 1) * 4) + 256 : 0;
     nfb = dense ? ceil_div(a_out, DENSE_ROWS) : 0;
     const int64_t sz_fnb = al((pmax + 1) * 4), sz_fnboff = al((a_out + 1) * 4),
                   sz_fperm = al(a_out * 4), sz_fmask = al(a_out * 4);
-    const int64_t total = sz_oc + sz_ot + sz_nbr + sz_inv +
+    const int64_t total = sz_oc + sz_ot + sz_nbr + sz_inv + sz_pmask + sz_low + sz_homeless +
                           (dense ? sz_fnb + sz_fnboff + sz_fperm + sz_fmask : 0);
     rb = new scn_rulebook();
     rb->alloc = mem;
@@ -1208,6 +1251,10 @@ struct LayerBuild {
     rb->nbr = pool ? (int32_t*)take(sz_nbr) : nullptr;
     rb->inv = pool ? (int32_t*)take(sz_inv) : nullptr;
     rb->inv_slots = inv_slots;
+    rb->pmask = pool ? (uint32_t*)take(sz_pmask) : nullptr;
+    rb->lowwin = cells ? (int32_t*)take(sz_low) : nullptr;
+    rb->n_homeless = cells ? (int32_t*)take(256) : nullptr;
+    rb->homeless = cells ? (int32_t*)take(sz_homeless - 256) : nullptr;
     rb->n_fblocks = nfb;
     rb->fnb = dense ? (int32_t*)take(sz_fnb) : nullptr;
     rb->fnb_off = dense ? (uint32_t*)take(sz_fnboff) : nullptr;
@@ -1234,13 +1281,15 @@ struct LayerBuild {
     ncnt = dense ? 0 : K * nt;  // tile counts only for the pair-list forward
     // the mask sort's scratch
     if (dense) sort_bytes = (size_t)radix_sort_words(a_out) * 4;
-    if ((rc = tmp.reserve(Temps::round(a_out * 4) + Temps::round(ncnt * 8) +
+    // a pooling rulebook keeps its windows' masks (pmask); others use scratch
+    if ((rc = tmp.reserve((pool ? 0 : Temps::round(a_out * 4)) + Temps::round(ncnt * 8) +
                           Temps::round(scan_blocks(ncnt) * 8) +
                           (dense ? Temps::round(scan_blocks(a_out) * 4) +
                                        Temps::round(sort_bytes)
                                  : 0))))
       return rc;
-    if ((rc = tmp.get(&masks, a_out)) || (rc = tmp.get(&cnt, ncnt)) ||
+    if (pool) masks = rb->pmask;
+    if ((!pool && (rc = tmp.get(&masks, a_out))) || (rc = tmp.get(&cnt, ncnt)) ||
         (rc = tmp.get(&sc64, scan_blocks(ncnt))))
       return rc;
     return SCN_OK;
@@ -1306,10 +1355,18 @@ struct LayerBuild {
           (rc = radix_sort_pairs(masks, rb->fmask, rb->fperm, a_out, K, sort_tmp, st)))
         return rc;
     }
+    if (cells) {
+      // (also zeroes the homeless count before inv_windows fills it)
+      hipLaunchKernelGGL(lower_windows_kernel, dim3(blocks_for(std::max<int64_t>(a_out, 1), 256)),
+                         dim3(256), 0, st, (const int32_t*)rb->out_coords, a_out, go,
+                         (const uint32_t*)outb, (const uint32_t*)opref, rb->lowwin,
+                         rb->n_homeless);
+      SCN_LAUNCH_CHECK();
+    }
     if (pool && n > 0) {
       with_kernels(f, lattice, [&](auto k) {
         k.inv_windows(inv_slots, dim3(blocks_for(n, 256)), st, coords, n, s, go, outb, opref,
-                      rb->inv);
+                      rb->inv, rb->homeless, rb->n_homeless);
       });
       SCN_LAUNCH_CHECK();
     }

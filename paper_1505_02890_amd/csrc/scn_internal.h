@@ -104,9 +104,21 @@ struct scn_rulebook {
   // filter <= stride an input lies in at most one window (inv_slots = 1); with
   // filter > stride (3 over 2) in at most two per axis, slot j = sum over axes
   // of [k_axis >= s] << axis (inv_slots = 8).
+  // pmask[o] bit k: position k of window o holds an active input
+  // (nbr[o*K + k] >= 0), for the backward's ground-state test.
   int32_t* nbr = nullptr;
   int32_t* inv = nullptr;
   int inv_slots = 0;
+  uint32_t* pmask = nullptr;
+  // 3-wide windows of stride 2 on the cubic lattice: the backward goes cell by
+  // cell.  Window h's home cell is its 2x2x2 corner of inputs (offsets
+  // {0,1}^3); they also lie in the windows h - b, b in {0,1}^3 (bit a: one
+  // step down along axis a).  lowwin[h*8 + b] = row of window h - b or -1
+  // (lowwin[h*8] = h).  Inputs without a home window (at the upper grid edge)
+  // are listed in homeless[0 .. *n_homeless) (device count, any order).
+  int32_t* lowwin = nullptr;
+  int32_t* homeless = nullptr;
+  int32_t* n_homeless = nullptr;
 
   // Dense forward view (stride-1 rulebooks with outputs).  fnb holds, for
   // each output row o in key order, the caller rows of its active inputs in
