@@ -50,6 +50,9 @@ def lib():
         L.orc_rb_build.argtypes = [P, i64, P, i32, i32, ctypes.POINTER(P)]
         L.orc_rb_build.restype = ctypes.c_int
         L.orc_rb_build_lattice.argtypes = [P, i64, P, i32, i32, i32, ctypes.POINTER(P)]
+        L.orc_rb_build_nd.restype = ctypes.c_int
+        L.orc_rb_build_nd.argtypes = [P, i64, i32, P, i32, i32, ctypes.POINTER(P)]
+        L.orc_rb_info_nd.argtypes = [P, P]
         L.orc_rb_build_lattice.restype = ctypes.c_int
         L.orc_rb_free.argtypes = [P]
         L.orc_rb_info.argtypes = [P, P]
@@ -79,8 +82,8 @@ class RulebookArrays:
     a_out: int
     n_pairs: int
     K: int
-    out_grid: tuple            # (B, mx, my, mz) of the output layer
-    out_coords: np.ndarray     # int32[a_out][4]
+    out_grid: tuple            # (B, mx, my, mz) of the output layer ((B, m_1..m_d) in d dims)
+    out_coords: np.ndarray     # int32[a_out][4] (int32[a_out][d + 1] in d dims)
     in_rows: np.ndarray        # int32[n_pairs]
     out_rows: np.ndarray       # int32[n_pairs]
     offsets: np.ndarray        # int64[K+1]
@@ -88,23 +91,32 @@ class RulebookArrays:
 
 class Rulebook:
     """Owner of an oracle rulebook (H_in, H_out and the per-offset rule lists)
-    on one of the lattices of Figure 2."""
+    on one of the lattices of Figure 2, or (``ndim`` given) on the hypercubic
+    lattice over sites (b, x_1, .., x_ndim) with grid (B, m_1, .., m_ndim)."""
 
     def __init__(self, coords: np.ndarray, grid: Sequence[int], f: int, s: int,
-                 lattice: str = "cubic"):
-        c = np.ascontiguousarray(np.asarray(coords, dtype=np.int32).reshape(-1, 4))
+                 lattice: str = "cubic", ndim: Optional[int] = None):
         g = np.ascontiguousarray(np.asarray(grid, dtype=np.int64))
         h = ctypes.c_void_p()
-        rc = lib().orc_rb_build_lattice(_p(c), len(c), _p(g), int(f), int(s),
-                                        LATTICES[lattice], ctypes.byref(h))
+        if ndim is None:
+            c = np.ascontiguousarray(np.asarray(coords, dtype=np.int32).reshape(-1, 4))
+            rc = lib().orc_rb_build_lattice(_p(c), len(c), _p(g), int(f), int(s),
+                                            LATTICES[lattice], ctypes.byref(h))
+        else:
+            if lattice != "cubic":
+                raise ValueError("sites of ndim coordinates take the hypercubic lattice")
+            c = np.ascontiguousarray(np.asarray(coords, dtype=np.int32).reshape(-1, ndim + 1))
+            rc = lib().orc_rb_build_nd(_p(c), len(c), int(ndim), _p(g), int(f), int(s),
+                                       ctypes.byref(h))
         if rc != 0:
             raise OracleError(rc)
         self._h = h
         self.f, self.s, self.lattice = int(f), int(s), lattice
-        info = np.zeros(8, np.int64)
-        lib().orc_rb_info(self._h, _p(info))
+        info = np.zeros(10, np.int64)
+        lib().orc_rb_info_nd(self._h, _p(info))
         self.a_in, self.a_out, self.n_pairs, self.K = (int(v) for v in info[:4])
-        self.out_grid = tuple(int(v) for v in info[4:])
+        self.ndim = int(info[4])
+        self.out_grid = (int(info[5]),) + tuple(int(v) for v in info[6:6 + self.ndim])
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -113,7 +125,7 @@ class Rulebook:
             self._h = None
 
     def arrays(self) -> RulebookArrays:
-        oc = np.zeros((self.a_out, 4), np.int32)
+        oc = np.zeros((self.a_out, self.ndim + 1), np.int32)
         ir = np.zeros(self.n_pairs, np.int32)
         orr = np.zeros(self.n_pairs, np.int32)
         off = np.zeros(self.K + 1, np.int64)

@@ -31,6 +31,10 @@
 //  * an inactive input position inside a window contributes the ground state
 //    g_in, both to the convolution (the rows of Q) and to max-pooling;
 //  * max-pooling keeps the first strict maximum scanning k upwards;
+//  * the hypercubic lattice in d = 1..4 dimensions (section 1.2: the same
+//    construction in any dimension) takes sites (b, x_1, .., x_d) with key
+//    ((b*m_d + x_d)*m_(d-1) + ..)*m_1 + x_1 and the f^d offsets numbered
+//    k = sum_a k_a f^(a-1), k_1 fastest (in 3D the key and numbering above);
 //  * gradients are those of the dense-equivalent function, for the loss
 //    sum_active <dy[o], y[o]> + <dg_out, g_out>; ReLU'(0) = 0.
 #include <algorithm>
@@ -65,6 +69,11 @@ struct Rulebook {
   std::vector<int32_t> out_coords;  // [a_out][4] = (b, x, y, z)
   // per filter offset k: (input row, output row), ordered by output row
   std::vector<std::vector<std::pair<int32_t, int32_t>>> lists;
+  // hypercubic sites of D coordinates (orc_rb_build_nd): extents m_1..m_D of
+  // the input and output grids; out_coords then has D + 1 entries per row
+  bool nd = false;
+  int D = 3;
+  std::vector<int64_t> m_in, m_out;
 
   int64_t a_out() const { return static_cast<int64_t>(out_keys.size()); }
 
@@ -79,6 +88,7 @@ struct Rulebook {
   // Row of M_in at input site s*o + k for output row o, or -1 when that site
   // is not active (then the window sees the ground state there).
   int32_t input_row(int64_t o, int k) const {
+    if (nd) return input_row_nd(o, k);
     const int32_t* c = &out_coords[4 * o];
     int64_t kx, ky, kz;
     offset(k, &kx, &ky, &kz);
@@ -86,11 +96,36 @@ struct Rulebook {
     auto it = H_in.find(key);
     return it == H_in.end() ? -1 : it->second;
   }
+
+  // The same for the hypercubic sites of orc_rb_build_nd: input s*o + k.
+  int32_t input_row_nd(int64_t o, int k) const;
 };
 
 int64_t out_extent(int64_t m, int f, int s) { return m >= f ? (m - f) / s + 1 : 0; }
 
+// key of site (b, x_1..x_D) in extents m (x_1 fastest)
+uint64_t key_nd(int64_t b, const int64_t* x, const std::vector<int64_t>& m, int D) {
+  uint64_t key = static_cast<uint64_t>(b);
+  for (int a = D - 1; a >= 0; --a) key = key * static_cast<uint64_t>(m[a]) + static_cast<uint64_t>(x[a]);
+  return key;
+}
+
+// component a of offset k (k = sum_a k_a f^a)
+int64_t offset_nd(int k, int a, int f) {
+  int64_t v = k;
+  for (int i = 0; i < a; ++i) v /= f;
+  return v % f;
+}
+
 bool mul_ok(int64_t a, int64_t b, int64_t lim) { return a == 0 || b <= lim / a; }
+
+int32_t Rulebook::input_row_nd(int64_t o, int k) const {
+  const int32_t* c = &out_coords[(D + 1) * o];
+  int64_t x[4] = {0, 0, 0, 0};
+  for (int a = 0; a < D; ++a) x[a] = s * (int64_t)c[1 + a] + offset_nd(k, a, f);
+  auto it = H_in.find(key_nd(c[0], x, m_in, D));
+  return it == H_in.end() ? -1 : it->second;
+}
 
 }  // namespace
 
@@ -212,6 +247,128 @@ int orc_rb_build_lattice(const int32_t* coords, int64_t n, const int64_t* grid, 
 int orc_rb_build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f, int32_t s,
                  void** out) {
   return orc_rb_build_lattice(coords, n, grid, f, s, 0, out);
+}
+
+// Step 1 on the hypercubic lattice of D = 1..4 dimensions (section 1.2):
+// sites (b, x_1..x_D), coords int32[n][D + 1], grid (B, m_1..m_D), f^D
+// offsets.  The same three parts as above: H_in, the active outputs numbered
+// in key order, the rule lists in output order.
+int orc_rb_build_nd(const int32_t* coords, int64_t n, int32_t D, const int64_t* grid, int32_t f,
+                    int32_t s, void** out) {
+  *out = nullptr;
+  if (n < 0 || f < 1 || s < 1 || D < 1 || D > 4 || (n > 0 && coords == nullptr) ||
+      grid == nullptr)
+    return INVALID;
+  const int64_t B = grid[0];
+  if (B < 1) return INVALID;
+  const int64_t LIM = INT64_C(1) << 62;
+  int64_t sites = B;
+  for (int a = 0; a < D; ++a) {
+    if (grid[1 + a] < 1) return INVALID;
+    if (!mul_ok(sites, grid[1 + a], LIM)) return OVERFLOW_;
+    sites *= grid[1 + a];
+  }
+  if (n > INT32_MAX) return OVERFLOW_;
+  int64_t K = 1;
+  for (int a = 0; a < D; ++a) K *= f;
+  if (K > INT32_MAX) return OVERFLOW_;
+
+  Rulebook* rb = new Rulebook();
+  rb->nd = true;
+  rb->D = D;
+  rb->f = f;
+  rb->s = s;
+  rb->K = static_cast<int>(K);
+  for (int k = 0; k < rb->K; ++k) rb->offs.push_back(k);
+  for (int a = 0; a < D; ++a) {
+    rb->m_in.push_back(grid[1 + a]);
+    rb->m_out.push_back(out_extent(grid[1 + a], f, s));
+  }
+  rb->gin = Grid{B, 1, 1, 1};
+  rb->gout = Grid{B, 1, 1, 1};
+  rb->a_in = n;
+
+  for (int64_t r = 0; r < n; ++r) {
+    const int32_t* c = coords + (D + 1) * r;
+    int64_t x[4] = {0, 0, 0, 0};
+    bool ok = c[0] >= 0 && c[0] < B;
+    for (int a = 0; a < D; ++a) {
+      x[a] = c[1 + a];
+      ok = ok && x[a] >= 0 && x[a] < rb->m_in[a];
+    }
+    if (!ok) {
+      delete rb;
+      return RANGE;
+    }
+    if (!rb->H_in.emplace(key_nd(c[0], x, rb->m_in, D), static_cast<int32_t>(r)).second) {
+      delete rb;
+      return DUPLICATE;
+    }
+  }
+
+  // active outputs: every o with s*o + k an active input for some k
+  std::set<uint64_t> H_out;
+  for (int64_t r = 0; r < n; ++r) {
+    const int32_t* c = coords + (D + 1) * r;
+    for (int k = 0; k < rb->K; ++k) {
+      int64_t o[4] = {0, 0, 0, 0};
+      bool ok = true;
+      for (int a = 0; a < D; ++a) {
+        const int64_t d = c[1 + a] - offset_nd(k, a, f);
+        ok = ok && d >= 0 && d % s == 0 && d / s < rb->m_out[a];
+        o[a] = d / s;
+      }
+      if (ok) H_out.insert(key_nd(c[0], o, rb->m_out, D));
+    }
+  }
+  if (static_cast<int64_t>(H_out.size()) > INT32_MAX) {
+    delete rb;
+    return OVERFLOW_;
+  }
+  rb->out_keys.assign(H_out.begin(), H_out.end());
+  rb->out_coords.resize((D + 1) * rb->out_keys.size());
+  for (size_t o = 0; o < rb->out_keys.size(); ++o) {
+    uint64_t key = rb->out_keys[o];
+    int32_t* c = &rb->out_coords[(D + 1) * o];
+    for (int a = 0; a < D; ++a) {
+      c[1 + a] = static_cast<int32_t>(key % static_cast<uint64_t>(rb->m_out[a]));
+      key /= static_cast<uint64_t>(rb->m_out[a]);
+    }
+    c[0] = static_cast<int32_t>(key);
+  }
+
+  rb->lists.assign(rb->K, {});
+  int64_t total = 0;
+  for (int64_t o = 0; o < rb->a_out(); ++o)
+    for (int k = 0; k < rb->K; ++k) {
+      const int32_t r = rb->input_row(o, k);
+      if (r >= 0) {
+        rb->lists[k].push_back({r, static_cast<int32_t>(o)});
+        ++total;
+      }
+    }
+  if (total > INT32_MAX) {
+    delete rb;
+    return OVERFLOW_;
+  }
+  *out = rb;
+  return OK;
+}
+
+// info = {a_in, a_out, n_pairs, K, D, B, m_out_1 .. m_out_4 (0 past D)}
+void orc_rb_info_nd(const void* h, int64_t* info) {
+  const Rulebook* rb = static_cast<const Rulebook*>(h);
+  int64_t np = 0;
+  for (auto& l : rb->lists) np += (int64_t)l.size();
+  info[0] = rb->a_in;
+  info[1] = rb->a_out();
+  info[2] = np;
+  info[3] = rb->K;
+  info[4] = rb->nd ? rb->D : 3;
+  info[5] = rb->gout.B;
+  const int64_t m3[3] = {rb->gout.mx, rb->gout.my, rb->gout.mz};
+  for (int a = 0; a < 4; ++a)
+    info[6 + a] = rb->nd ? (a < rb->D ? rb->m_out[a] : 0) : (a < 3 ? m3[a] : 0);
 }
 
 void orc_rb_free(void* h) { delete static_cast<Rulebook*>(h); }

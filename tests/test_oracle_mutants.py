@@ -74,7 +74,28 @@ PLANAR_MUTANTS = [
      "const bool simplex = lattice == 1;"),
 ]
 
+# mistakes in the hypercubic lattice of d dimensions (section 1.2), caught by
+# its own pins
+ND_MUTANTS = [
+    ("nd_offset_digits_reversed",
+     "for (int a = 0; a < D; ++a) x[a] = s * (int64_t)c[1 + a] + offset_nd(k, a, f);",
+     "for (int a = 0; a < D; ++a) x[a] = s * (int64_t)c[1 + a] + offset_nd(k, D - 1 - a, f);"),
+    ("nd_key_axes_reversed",
+     "for (int a = D - 1; a >= 0; --a) key = key * static_cast<uint64_t>(m[a])",
+     "for (int a = 0; a < D; ++a) key = key * static_cast<uint64_t>(m[a])"),
+    ("nd_rules_not_ordered_by_output",
+     "rb->lists[k].push_back({r, static_cast<int32_t>(o)});",
+     "rb->lists[k].insert(rb->lists[k].begin(), {r, static_cast<int32_t>(o)});"),
+    ("nd_stride_divisibility_dropped",
+     "ok = ok && d >= 0 && d % s == 0 && d / s < rb->m_out[a];",
+     "ok = ok && d >= 0 && d / s < rb->m_out[a];"),
+    ("nd_last_axis_range_unchecked",
+     "ok = ok && x[a] >= 0 && x[a] < rb->m_in[a];",
+     "ok = ok && x[a] >= 0 && (a == D - 1 || x[a] < rb->m_in[a]);"),
+]
+
 CASES = [m + ("test_oracle_pins.py",) for m in MUTANTS] + \
+        [m + ("test_oracle_nd.py",) for m in ND_MUTANTS] + \
         [m + ("test_oracle_lattice.py",) for m in LATTICE_MUTANTS] + \
         [m + ("test_oracle_lattice2d.py",) for m in PLANAR_MUTANTS]
 
