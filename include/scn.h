@@ -95,6 +95,12 @@ typedef struct scn_rulebook_info {
   int32_t lattice;     /* SCN_LATTICE_* */
   int32_t dense_view;  /* 1 if the rulebook carries the dense forward view
                           (scn_set_dense_forward), else 0 */
+  int32_t ndim;        /* coordinates per site (3 but for scn_rulebook_build_nd);
+                          out_coords rows hold ndim + 1 int32 */
+  int32_t keyed;       /* 1 if built from sorted keys and hash tables (grids past
+                          the occupancy bitmaps, scn_rulebook_build_nd), else 0 */
+  int64_t in_grid_nd[5];  /* B, m_1 .. m_ndim (then 0) */
+  int64_t out_grid_nd[5]; /* B, floor((m_a - f)/s) + 1 (then 0) */
 } scn_rulebook_info;
 
 /*
@@ -122,14 +128,46 @@ typedef struct scn_rulebook_info {
  * Output ordering is canonical: output rows ascend by key, and each
  * per-offset pair list ascends by output row (hence also by input key), so the
  * result is deterministic and independent of the input row order.
+ * Grids whose occupancy bitmaps fit (2^26 32-bit words per grid, i.e.
+ * B*my*mz*ceil(mx/32) <= 2^26 for the input and the output grid) take the
+ * bitmap builder; larger ones the keyed builder of scn_rulebook_build_nd
+ * (same results; it needs B*mx*my*mz < 2^63, and one host wait).
  * Errors: SCN_ERR_INVALID, SCN_ERR_RANGE, SCN_ERR_DUPLICATE, SCN_ERR_OVERFLOW,
- * SCN_ERR_UNSUPPORTED (f > 3, or an occupancy bitmap of the input or output
- * grid above 2^26 32-bit words, i.e. B*my*mz*ceil(mx/32) > 2^26), SCN_ERR_NOMEM,
- * SCN_ERR_HIP.  coords must be 16-byte aligned.  On error *out is NULL.
+ * SCN_ERR_UNSUPPORTED (f > 3), SCN_ERR_NOMEM, SCN_ERR_HIP.  coords must be
+ * 16-byte aligned.  On error *out is NULL.
  */
 scn_status scn_rulebook_build(const int32_t* coords, int64_t n, const int64_t* grid,
                               int32_t filter, int32_t stride, hipStream_t stream,
                               scn_rulebook** out);
+
+/*
+ * The rulebook of a hypercubic lattice in ndim = 1 .. 4 dimensions (section
+ * 1.2: the method is the same in any dimension; its smallest filter has 2^d
+ * sites), built from sorted site keys and open-addressing hash tables
+ * (section 1.3 step 1 keeps H_in and H_out in "a map or hash table"), with
+ * no occupancy bitmap, so any grid with B * prod m_a < 2^63 is accepted.
+ *
+ *  coords  device int32[n][ndim + 1] rows (b, x_1, .., x_ndim), 4-byte
+ *          aligned; lifetime as for scn_rulebook_build.
+ *  grid    host int64[ndim + 1] = (B, m_1, .., m_ndim), all >= 1.
+ *  filter, stride   as for scn_rulebook_build, with f^ndim <= 27 offsets
+ *          (f <= 2 in 4D); offset k = sum_a k_a f^(a-1), k_1 fastest.
+ *
+ * The site key is ((b*m_ndim + x_ndim)*m_(ndim-1) + ..)*m_1 + x_1 (in 3D the
+ * key of scn_rulebook_build, whose results this reproduces); outputs are
+ * numbered and pairs ordered as there.  The out_coords rows have ndim + 1
+ * int32.  A rulebook with stride >= 2 serves pooling when filter <= stride,
+ * and on 3D sites also when filter > stride (other such rulebooks serve
+ * convolution only; scn_maxpool_* then return SCN_ERR_UNSUPPORTED).  The
+ * call waits for `stream` once.  Errors: SCN_ERR_INVALID (ndim outside 1..4,
+ * null or misaligned arguments), SCN_ERR_RANGE, SCN_ERR_DUPLICATE,
+ * SCN_ERR_OVERFLOW (n, a_out or the pair count above INT32_MAX, or a key
+ * above 63 bits), SCN_ERR_UNSUPPORTED (f > 3, or more than 27 offsets),
+ * SCN_ERR_NOMEM, SCN_ERR_HIP.  On error *out is NULL.
+ */
+scn_status scn_rulebook_build_nd(const int32_t* coords, int64_t n, int32_t ndim,
+                                 const int64_t* grid, int32_t filter, int32_t stride,
+                                 hipStream_t stream, scn_rulebook** out);
 
 /*
  * scn_rulebook_build on a chosen lattice (section 1.2, "CNNs on different
@@ -173,9 +211,12 @@ scn_status scn_rulebook_build_lattice(const int32_t* coords, int64_t n, const in
  * marking and ranking the sites again.  prev is only read, by kernels queued
  * on `stream` (some after the call returns).  If `stream` is not the stream
  * prev was built on, that stream is made to wait for them, so prev may be
- * freed (scn_rulebook_free, ordered on prev's stream) once this call returns.  Errors: SCN_ERR_INVALID (NULL, or prev's output
- * grid is empty), and as scn_rulebook_build.  It waits for stream as
- * scn_rulebook_build does, and orders stream after prev's build.
+ * freed (scn_rulebook_free, ordered on prev's stream) once this call
+ * returns.  A keyed prev (grids past the bitmaps, or scn_rulebook_build_nd)
+ * gives a keyed result over prev's ndim, built from prev's output sites.
+ * Errors: SCN_ERR_INVALID (NULL, or prev's output grid is empty), and as
+ * scn_rulebook_build.  It waits for stream as scn_rulebook_build does, and
+ * orders stream after prev's build.
  */
 scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int32_t stride,
                                    hipStream_t stream, scn_rulebook** out);
@@ -202,7 +243,7 @@ scn_status scn_rulebook_build_chain(const int32_t* coords, int64_t n, const int6
 /* Sizes and grids of a rulebook (host struct).  SCN_ERR_INVALID on null. */
 scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info);
 
-/* Device int32[a_out][4] (b, x, y, z) of the active output sites, ascending by
+/* Device int32[a_out][ndim + 1] (b, x, y, z for 3D) of the active output sites, ascending by
  * key: the input coordinates of the next layer.  Owned by rb. */
 const int32_t* scn_rulebook_out_coords(const scn_rulebook* rb);
 
@@ -215,7 +256,7 @@ const int32_t* scn_rulebook_out_rows(const scn_rulebook* rb);
 const int64_t* scn_rulebook_offsets(const scn_rulebook* rb);
 
 /* Copies the active output sites and the pair lists into caller device
- * buffers (each may be NULL): out_coords int32[a_out][4], in_rows and out_rows
+ * buffers (each may be NULL): out_coords int32[a_out][ndim + 1], in_rows and out_rows
  * int32[n_pairs].  Asynchronous on `stream`.  Errors: SCN_ERR_INVALID, SCN_ERR_HIP. */
 scn_status scn_rulebook_export(const scn_rulebook* rb, int32_t* out_coords, int32_t* in_rows,
                                int32_t* out_rows, hipStream_t stream);

@@ -12,6 +12,7 @@ from ._lib import (  # noqa: F401
     ScnError,
     build_chain,
     build_rulebook,
+    build_rulebook_nd,
     conv_bwd,
     conv_bwd_workspace,
     conv_fwd,

@@ -26,7 +26,8 @@ STATUS = {0: "ok", 1: "invalid", 2: "range", 3: "duplicate", 4: "overflow",
           5: "unsupported", 6: "workspace", 7: "hip", 8: "nomem"}
 
 EXPORTED = (
-    "scn_rulebook_build", "scn_rulebook_build_lattice", "scn_rulebook_build_next",
+    "scn_rulebook_build", "scn_rulebook_build_lattice", "scn_rulebook_build_nd",
+    "scn_rulebook_build_next",
     "scn_rulebook_build_chain",
     "scn_rulebook_get_info", "scn_rulebook_out_coords",
     "scn_rulebook_in_rows", "scn_rulebook_out_rows", "scn_rulebook_offsets",
@@ -55,7 +56,9 @@ class _Info(ctypes.Structure):
                 ("filter", ctypes.c_int32), ("stride", ctypes.c_int32),
                 ("input_sorted", ctypes.c_int32), ("in_grid", ctypes.c_int64 * 4),
                 ("out_grid", ctypes.c_int64 * 4), ("lattice", ctypes.c_int32),
-                ("dense_view", ctypes.c_int32)]
+                ("dense_view", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("keyed", ctypes.c_int32), ("in_grid_nd", ctypes.c_int64 * 5),
+                ("out_grid_nd", ctypes.c_int64 * 5)]
 
 
 _lib = None
@@ -77,6 +80,7 @@ def lib() -> ctypes.CDLL:
     sig = {
         "scn_rulebook_build": (st, [P, i64, P, i32, i32, P, ctypes.POINTER(P)]),
         "scn_rulebook_build_lattice": (st, [P, i64, P, i32, i32, i32, P, ctypes.POINTER(P)]),
+        "scn_rulebook_build_nd": (st, [P, i64, i32, P, i32, i32, P, ctypes.POINTER(P)]),
         "scn_rulebook_build_next": (st, [P, i32, i32, P, ctypes.POINTER(P)]),
         "scn_rulebook_build_chain": (st, [P, i64, P, i32, i32, P, P, P, ctypes.POINTER(P)]),
         "scn_rulebook_get_info": (st, [P, ctypes.POINTER(_Info)]),
@@ -137,17 +141,32 @@ def _dev_tensor(t: torch.Tensor, dtype, shape, name: str) -> torch.Tensor:
 
 
 class Rulebook:
-    """Owner of a device rulebook built by ``scn_rulebook_build_lattice``.
+    """Owner of a device rulebook built by ``scn_rulebook_build_lattice``
+    (or ``scn_rulebook_build_nd`` when ``ndim`` is given).
 
     ``coords`` is a device int32 [n, 4] tensor of (b, x, y, z) rows; ``grid``
     is (B, mx, my, mz); ``lattice`` is "cubic", "tetrahedral", "square" or
-    "triangular".  Attributes mirror ``scn_rulebook_info``.
+    "triangular".  With ``ndim``, coords is [n, ndim + 1] rows (b, x_1, ..)
+    and grid (B, m_1, .., m_ndim) on the hypercubic lattice.  Attributes
+    mirror ``scn_rulebook_info``.
     """
 
     def __init__(self, coords: Optional[torch.Tensor], grid: Sequence[int], filter: int,
-                 stride: int, lattice: str = "cubic", prev: Optional["Rulebook"] = None):
+                 stride: int, lattice: str = "cubic", prev: Optional["Rulebook"] = None,
+                 ndim: Optional[int] = None):
         h = ctypes.c_void_p()
-        if prev is not None:
+        if ndim is not None:
+            n = int(coords.shape[0]) if coords.dim() == 2 else -1
+            _dev_tensor(coords, torch.int32, (n, ndim + 1), "coords")
+            if lattice != "cubic":
+                raise ValueError("sites of ndim coordinates take the hypercubic lattice")
+            g = np.ascontiguousarray(np.asarray(grid, dtype=np.int64).reshape(ndim + 1))
+            _check(lib().scn_rulebook_build_nd(
+                _ptr(coords), n, int(ndim), g.ctypes.data_as(ctypes.c_void_p), int(filter),
+                int(stride), ctypes.c_void_p(_stream()), ctypes.byref(h)),
+                "scn_rulebook_build_nd")
+            device = coords.device
+        elif prev is not None:
             # the layer after prev: its sites are prev's active outputs
             _check(lib().scn_rulebook_build_next(prev.handle, int(filter), int(stride),
                                                  ctypes.c_void_p(_stream()), ctypes.byref(h)),
@@ -182,8 +201,9 @@ class Rulebook:
         self.input_sorted = bool(info.input_sorted)
         self.dense_view = bool(info.dense_view)
         self.lattice = {v: k for k, v in LATTICES.items()}[int(info.lattice)]
-        self.in_grid = tuple(int(v) for v in info.in_grid)
-        self.out_grid = tuple(int(v) for v in info.out_grid)
+        self.ndim, self.keyed = int(info.ndim), bool(info.keyed)
+        self.in_grid = tuple(int(v) for v in info.in_grid_nd[:self.ndim + 1])
+        self.out_grid = tuple(int(v) for v in info.out_grid_nd[:self.ndim + 1])
         off = lib().scn_rulebook_offsets(self._h)
         self.offsets = np.array([off[k] for k in range(self.K + 1)], dtype=np.int64)
 
@@ -204,8 +224,9 @@ class Rulebook:
             pass
 
     def export(self):
-        """(out_coords int32[a_out,4], in_rows int32[P], out_rows int32[P]) on the device."""
-        oc = torch.empty((self.a_out, 4), dtype=torch.int32, device=self.device)
+        """(out_coords int32[a_out, ndim+1], in_rows int32[P], out_rows int32[P]) on the
+        device."""
+        oc = torch.empty((self.a_out, self.ndim + 1), dtype=torch.int32, device=self.device)
         ir = torch.empty(self.n_pairs, dtype=torch.int32, device=self.device)
         orr = torch.empty(self.n_pairs, dtype=torch.int32, device=self.device)
         _check(lib().scn_rulebook_export(self._h, _ptr(oc), _ptr(ir), _ptr(orr),
@@ -213,7 +234,7 @@ class Rulebook:
         return oc, ir, orr
 
     def out_coords(self) -> torch.Tensor:
-        oc = torch.empty((self.a_out, 4), dtype=torch.int32, device=self.device)
+        oc = torch.empty((self.a_out, self.ndim + 1), dtype=torch.int32, device=self.device)
         _check(lib().scn_rulebook_export(self._h, _ptr(oc), None, None,
                                          ctypes.c_void_p(_stream())), "scn_rulebook_export")
         return oc
@@ -222,6 +243,13 @@ class Rulebook:
 def build_rulebook(coords: torch.Tensor, grid: Sequence[int], filter: int, stride: int,
                    lattice: str = "cubic") -> Rulebook:
     return Rulebook(coords, grid, filter, stride, lattice)
+
+
+def build_rulebook_nd(coords: torch.Tensor, grid: Sequence[int], filter: int,
+                      stride: int) -> Rulebook:
+    """Hypercubic rulebook over sites of ndim = len(grid) - 1 coordinates
+    (keyed builder: sorted keys and hash tables)."""
+    return Rulebook(coords, grid, filter, stride, ndim=len(grid) - 1)
 
 
 def next_rulebook(prev: Rulebook, filter: int, stride: int) -> Rulebook:

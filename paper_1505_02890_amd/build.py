@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libscn.so")
 ARCH = "gfx950"
 
-SOURCES = ["common.hip", "rulebook.hip", "conv.hip", "pool.hip", "ceiling.hip"]
+SOURCES = ["common.hip", "rulebook.hip", "keyed.hip", "conv.hip", "pool.hip", "ceiling.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

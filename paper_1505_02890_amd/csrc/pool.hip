@@ -498,19 +498,26 @@ inline unsigned nblocks(int64_t n, int t) { return (unsigned)std::max<int64_t>(1
 
 // calls fn(std::integral_constant<int, K>{}) for the window sizes of the
 // lattices: 1, 8, 27 (cube), 4, 10 (tetrahedron), 4, 9 (square), 3, 6
-// (triangle)
+// (triangle), 2, 3 (line) and 16 (the 4D hypercube of 2); false for others
 template <typename Fn>
-void with_window(int K, Fn fn) {
+bool with_window(int K, Fn fn) {
   switch (K) {
-    case 1: fn(std::integral_constant<int, 1>{}); break;
-    case 3: fn(std::integral_constant<int, 3>{}); break;
-    case 4: fn(std::integral_constant<int, 4>{}); break;
-    case 6: fn(std::integral_constant<int, 6>{}); break;
-    case 8: fn(std::integral_constant<int, 8>{}); break;
-    case 9: fn(std::integral_constant<int, 9>{}); break;
-    case 10: fn(std::integral_constant<int, 10>{}); break;
-    default: fn(std::integral_constant<int, 27>{}); break;
+    case 1: fn(std::integral_constant<int, 1>{}); return true;
+    case 2: fn(std::integral_constant<int, 2>{}); return true;
+    case 3: fn(std::integral_constant<int, 3>{}); return true;
+    case 4: fn(std::integral_constant<int, 4>{}); return true;
+    case 6: fn(std::integral_constant<int, 6>{}); return true;
+    case 8: fn(std::integral_constant<int, 8>{}); return true;
+    case 9: fn(std::integral_constant<int, 9>{}); return true;
+    case 10: fn(std::integral_constant<int, 10>{}); return true;
+    case 16: fn(std::integral_constant<int, 16>{}); return true;
+    case 27: fn(std::integral_constant<int, 27>{}); return true;
+    default: return false;
   }
+}
+
+inline bool window_size_ok(int K) {
+  return with_window(K, [](auto) {});
 }
 
 // four-channel path: C % 4 == 0, C <= 1024, float rows 16-byte aligned, argmax
@@ -541,7 +548,12 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
     return SCN_ERR_INVALID;
   }
   if (!rb->nbr) {
-    set_error("scn_maxpool_fwd: pooling needs a rulebook with stride >= 2");
+    set_error("scn_maxpool_fwd: the rulebook has no pooling tables (stride 1, or windows wider "
+              "than their stride on sites of other than 3 coordinates)");
+    return SCN_ERR_UNSUPPORTED;
+  }
+  if (!window_size_ok(rb->K)) {
+    set_error("scn_maxpool_fwd: windows of %d sites are not supported", rb->K);
     return SCN_ERR_UNSUPPORTED;
   }
   if (rb->a_out > 0) {
@@ -586,7 +598,12 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
     return SCN_ERR_INVALID;
   }
   if (!rb->nbr) {
-    set_error("scn_maxpool_bwd: pooling needs a rulebook with stride >= 2");
+    set_error("scn_maxpool_bwd: the rulebook has no pooling tables (stride 1, or windows wider "
+              "than their stride on sites of other than 3 coordinates)");
+    return SCN_ERR_UNSUPPORTED;
+  }
+  if (!window_size_ok(rb->K)) {
+    set_error("scn_maxpool_bwd: windows of %d sites are not supported", rb->K);
     return SCN_ERR_UNSUPPORTED;
   }
   const size_t need = scn_maxpool_bwd_workspace_bytes(rb, C);

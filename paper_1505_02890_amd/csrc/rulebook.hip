@@ -1269,8 +1269,8 @@ struct LayerBuild {
     rb->hout_words = nw_out;
     hout.bits = hout.rank = nullptr;  // owned by rb from here (freed with it)
     for (int a = 0; a < 4; ++a) {
-      rb->gin[a] = grid[a];
-      rb->gout[a] = go4[a];
+      rb->gin[a] = rb->gin_nd[a] = grid[a];
+      rb->gout[a] = rb->gout_nd[a] = go4[a];
     }
     rb->a_in = n;
     rb->a_out = a_out;
@@ -1392,6 +1392,21 @@ struct LayerBuild {
 // Builds from the caller's sites, or (prev != null) from the active output
 // sites of prev: then coords/n/grid/lattice are prev's output layer, whose
 // rank bitmap (prev's H_out) serves as this build's H_in.
+// Whether a cubic-lattice layer's occupancy bitmaps fit (at most 2^26 words
+// per grid); valid arguments assumed (others are reported by check()).
+bool bitmaps_fit(const int64_t* grid, int32_t f, int32_t s) {
+  for (int a = 0; a < 4; ++a)
+    if (grid[a] < 1 || grid[a] > INT32_MAX) return true;
+  if (f < 1 || s < 1) return true;
+  double words_in = (double)grid[0] * grid[2] * grid[3] * (double)ceil_div(grid[1], 32);
+  int64_t go[4] = {grid[0], 0, 0, 0};
+  for (int a = 1; a < 4; ++a) go[a] = grid[a] >= f ? (grid[a] - f) / s + 1 : 0;
+  double words_out =
+      (double)go[0] * go[2] * go[3] * (double)ceil_div(std::max<int64_t>(go[1], 1), 32);
+  const double LIMW = (double)(int64_t(1) << 26);
+  return words_in <= LIMW && words_out <= LIMW;
+}
+
 scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t f, int32_t s,
                  int32_t lattice, hipStream_t st, scn_rulebook** out,
                  const scn_rulebook* prev = nullptr) {
@@ -1404,6 +1419,9 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
     set_error("scn_rulebook_build: grid is NULL");
     return SCN_ERR_INVALID;
   }
+  // past the bitmaps' reach, the cubic lattice goes to the keyed builder
+  if (lattice == SCN_LATTICE_CUBIC && !bitmaps_fit(grid, f, s))
+    return keyed_build(coords, n, 3, grid, f, s, st, out);
   LayerBuild L;
   L.coords = coords;
   L.n = n;
@@ -1446,6 +1464,24 @@ scn_status build_chain(const int32_t* coords, int64_t n, const int64_t* grid, in
     return SCN_ERR_INVALID;
   }
   for (int i = 0; i < nl; ++i) out[i] = nullptr;
+  if (lattice == SCN_LATTICE_CUBIC && !bitmaps_fit(grid, filters[0], strides[0])) {
+    // keyed builds one after the other, each from the previous one's outputs
+    std::vector<scn_rulebook*> res(nl, nullptr);
+    scn_status rc = SCN_OK;
+    for (int i = 0; i < nl && rc == SCN_OK; ++i) {
+      if (i == 0)
+        rc = keyed_build(coords, n, 3, grid, filters[0], strides[0], st, &res[0]);
+      else
+        rc = keyed_build(res[i - 1]->out_coords, res[i - 1]->a_out, 3, res[i - 1]->gout_nd,
+                         filters[i], strides[i], st, &res[i]);
+    }
+    if (rc != SCN_OK) {
+      for (int i = 0; i < nl; ++i) scn_rulebook_free(res[i]);
+      return rc;
+    }
+    for (int i = 0; i < nl; ++i) out[i] = res[i];
+    return SCN_OK;
+  }
   std::vector<std::unique_ptr<LayerBuild>> Ls;
   Readback* hb = nullptr;
   hipEvent_t copied = nullptr;
@@ -1539,8 +1575,8 @@ scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int
     scn::set_error("scn_rulebook_build_next: NULL argument");
     return SCN_ERR_INVALID;
   }
-  for (int a = 1; a < 4; ++a)
-    if (prev->gout[a] < 1) {
+  for (int a = 1; a <= prev->ndim; ++a)
+    if (prev->gout_nd[a] < 1) {
       *out = nullptr;
       scn::set_error("scn_rulebook_build_next: the previous layer's output grid is empty");
       return SCN_ERR_INVALID;
@@ -1549,6 +1585,9 @@ scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int
     *out = nullptr;
     return rc;
   }
+  if (prev->keyed)
+    return scn::keyed_build(prev->out_coords, prev->a_out, prev->ndim, prev->gout_nd, filter,
+                            stride, stream, out);
   return scn::build(prev->out_coords, prev->a_out, prev->gout, filter, stride, prev->lattice,
                     stream, out, prev);
 }
@@ -1571,6 +1610,12 @@ scn_status scn_rulebook_get_info(const scn_rulebook* rb, scn_rulebook_info* info
     info->in_grid[a] = rb->gin[a];
     info->out_grid[a] = rb->gout[a];
   }
+  info->ndim = rb->ndim;
+  info->keyed = rb->keyed;
+  for (int a = 0; a < 5; ++a) {
+    info->in_grid_nd[a] = a <= rb->ndim ? rb->gin_nd[a] : 0;
+    info->out_grid_nd[a] = a <= rb->ndim ? rb->gout_nd[a] : 0;
+  }
   return SCN_OK;
 }
 
@@ -1588,8 +1633,8 @@ scn_status scn_rulebook_export(const scn_rulebook* rb, int32_t* out_coords, int3
   }
   if (scn_status rc = scn::after_build(rb, stream)) return rc;
   if (out_coords && rb->a_out > 0)
-    SCN_HIP(hipMemcpyAsync(out_coords, rb->out_coords, rb->a_out * 16, hipMemcpyDeviceToDevice,
-                           stream));
+    SCN_HIP(hipMemcpyAsync(out_coords, rb->out_coords, rb->a_out * (rb->ndim + 1) * 4,
+                           hipMemcpyDeviceToDevice, stream));
   if (in_rows && rb->n_pairs > 0)
     SCN_HIP(hipMemcpyAsync(in_rows, rb->in_rows, rb->n_pairs * 4, hipMemcpyDeviceToDevice, stream));
   if (out_rows && rb->n_pairs > 0)

@@ -16,6 +16,7 @@ namespace scn {
 // output rows) and per (offset, tile of TILE input ranks).
 constexpr int TILE = 64;
 constexpr int MAX_K = 27;  // f <= 3 (the tetrahedral lattice needs at most 10)
+constexpr int KD_MAX = 4;  // coordinates per site of the keyed builder (keyed.hip)
 constexpr int DENSE_ROWS = 32;  // output rows per block of the dense forward view
 // Default policy for the dense forward view (scn_set_dense_forward): stride-1
 // rulebooks with at least this many output rows and offsets.  Below them the
@@ -76,6 +77,13 @@ struct scn_rulebook {
   int32_t lattice = SCN_LATTICE_CUBIC;
   int64_t gin[4] = {0, 0, 0, 0};   // B, mx, my, mz
   int64_t gout[4] = {0, 0, 0, 0};
+  // Sites of ndim coordinates (out_coords rows of ndim + 1 int32: b, x_1 ..);
+  // the extents (B, m_1 .. m_ndim) in gin_nd / gout_nd.  keyed: built from
+  // sorted keys and hash tables (keyed.hip), without the occupancy bitmaps.
+  int32_t ndim = 3;
+  int32_t keyed = 0;
+  int64_t gin_nd[scn::KD_MAX + 1] = {0, 0, 0, 0, 0};
+  int64_t gout_nd[scn::KD_MAX + 1] = {0, 0, 0, 0, 0};
   int64_t a_in = 0, a_out = 0, n_pairs = 0;
   int32_t input_sorted = 0;
   hipStream_t stream = nullptr;    // stream the rulebook was built on (frees go there)
@@ -153,6 +161,11 @@ struct scn_rulebook {
 };
 
 namespace scn {
+// The keyed builder (keyed.hip): a rulebook of the hypercubic lattice over
+// sites of D coordinates, coords int32[n][D + 1], grid (B, m_1 .. m_D).
+scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* grid, int f, int s,
+                       hipStream_t st, scn_rulebook** out);
+
 // Orders work on stream st after the rulebook's build (a no-op on the build's
 // own stream, where the order already holds).
 inline scn_status after_build(const scn_rulebook* rb, hipStream_t st) {

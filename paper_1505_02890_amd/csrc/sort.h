@@ -1,6 +1,7 @@
-// Stable LSD radix sort of (uint32 key, int32 value) pairs by the low `bits`
-// bits of the key, 9 bits (512 digits) per pass.  The dense forward view
-// uses it to order output rows by their neighbour masks.
+// Stable LSD radix sort of (key, int32 value) pairs by the low `bits` bits of
+// the key (uint32 or uint64), 9 bits (512 digits) per pass.  The dense
+// forward view uses it to order output rows by their neighbour masks, the
+// keyed rulebook builder to order site keys.
 //
 // Each pass, over tiles of 2048 pairs:
 //   upsweep    digit histogram of every tile -> hist[digit][tile]
@@ -50,7 +51,8 @@ __device__ inline uint32_t rs_below(uint64_t m) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-__global__ void __launch_bounds__(RS_THREADS) rs_upsweep_kernel(const uint32_t* __restrict__ keys,
+template <typename KT>
+__global__ void __launch_bounds__(RS_THREADS) rs_upsweep_kernel(const KT* __restrict__ keys,
                                                                 int64_t n, int shift,
                                                                 int64_t ntiles,
                                                                 uint32_t* __restrict__ hist) {
@@ -59,16 +61,16 @@ __global__ void __launch_bounds__(RS_THREADS) rs_upsweep_kernel(const uint32_t* 
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * RS_TILE;
   const int lane = threadIdx.x & 63;
-  uint32_t k[RS_ROUNDS];
+  KT k[RS_ROUNDS];
 #pragma unroll
   for (int j = 0; j < RS_ROUNDS; ++j) {
     const int64_t i = base + (int64_t)j * RS_THREADS + threadIdx.x;
-    k[j] = i < n ? keys[i] : 0u;
+    k[j] = i < n ? keys[i] : KT(0);
   }
 #pragma unroll
   for (int j = 0; j < RS_ROUNDS; ++j) {
     const bool valid = base + (int64_t)j * RS_THREADS + threadIdx.x < n;
-    const uint32_t d = (k[j] >> shift) & (RS_DIGITS - 1);
+    const uint32_t d = (uint32_t)(k[j] >> shift) & (RS_DIGITS - 1);
     const uint64_t peers = rs_peers(d, valid);
     // one LDS add per digit group of the wave
     if (valid && lane == __builtin_ctzll(peers)) atomicAdd(&h[d], (uint32_t)__popcll(peers));
@@ -80,7 +82,7 @@ __global__ void __launch_bounds__(RS_THREADS) rs_upsweep_kernel(const uint32_t* 
 
 // One work-group per digit d: pre[d][t] = sum of hist[d][t'] for t' < t, and
 // tot[d] = the digit's count.
-__global__ void __launch_bounds__(RS_THREADS) rs_colscan_kernel(const uint32_t* __restrict__ hist,
+static __global__ void __launch_bounds__(RS_THREADS) rs_colscan_kernel(const uint32_t* __restrict__ hist,
                                                                 int64_t ntiles,
                                                                 uint32_t* __restrict__ pre,
                                                                 uint32_t* __restrict__ tot) {
@@ -98,33 +100,34 @@ __global__ void __launch_bounds__(RS_THREADS) rs_colscan_kernel(const uint32_t* 
 }
 
 // FIRST: the values are the pairs' input positions (vin is not read)
-template <bool FIRST>
+template <typename KT, bool FIRST>
 __global__ void __launch_bounds__(RS_THREADS) rs_downsweep_kernel(
-    const uint32_t* __restrict__ kin, const int32_t* __restrict__ vin,
-    uint32_t* __restrict__ kout, int32_t* __restrict__ vout, int64_t n, int shift,
+    const KT* __restrict__ kin, const int32_t* __restrict__ vin,
+    KT* __restrict__ kout, int32_t* __restrict__ vout, int64_t n, int shift,
     int64_t ntiles, const uint32_t* __restrict__ pre, const uint32_t* __restrict__ tot) {
   __shared__ uint32_t cnt[RS_WAVES][RS_DIGITS];  // per-wave running counts
   __shared__ uint32_t toff[RS_DIGITS];           // tile: pairs of smaller digits
   __shared__ uint32_t gbase[RS_DIGITS];          // output place of the tile's run, less toff
-  __shared__ uint32_t skey[RS_TILE];
+  __shared__ KT skey[RS_TILE];
   __shared__ int32_t sval[RS_TILE];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int i = lane; i < RS_DIGITS; i += 64) cnt[w][i] = 0;
   __builtin_amdgcn_wave_barrier();
   const int64_t tbase = (int64_t)blockIdx.x * RS_TILE;
   const int64_t base = tbase + (int64_t)w * (64 * RS_ROUNDS);
-  uint32_t key[RS_ROUNDS], rank[RS_ROUNDS];
+  KT key[RS_ROUNDS];
+  uint32_t rank[RS_ROUNDS];
   int32_t val[RS_ROUNDS];
 #pragma unroll
   for (int j = 0; j < RS_ROUNDS; ++j) {
     const int64_t i = base + j * 64 + lane;
-    key[j] = i < n ? kin[i] : 0u;
+    key[j] = i < n ? kin[i] : KT(0);
     val[j] = FIRST ? (int32_t)i : (i < n ? vin[i] : 0);
   }
 #pragma unroll
   for (int j = 0; j < RS_ROUNDS; ++j) {
     const bool valid = base + j * 64 + lane < n;
-    const uint32_t d = (key[j] >> shift) & (RS_DIGITS - 1);
+    const uint32_t d = (uint32_t)(key[j] >> shift) & (RS_DIGITS - 1);
     const uint64_t peers = rs_peers(d, valid);
     const int leader = valid ? __builtin_ctzll(peers) : lane;
     uint32_t c = 0;
@@ -177,7 +180,7 @@ __global__ void __launch_bounds__(RS_THREADS) rs_downsweep_kernel(
 #pragma unroll
   for (int j = 0; j < RS_ROUNDS; ++j) {
     if (base + j * 64 + lane < n) {
-      const uint32_t d = (key[j] >> shift) & (RS_DIGITS - 1);
+      const uint32_t d = (uint32_t)(key[j] >> shift) & (RS_DIGITS - 1);
       const uint32_t q = toff[d] + cnt[w][d] + rank[j];
       skey[q] = key[j];
       sval[q] = val[j];
@@ -191,8 +194,8 @@ __global__ void __launch_bounds__(RS_THREADS) rs_downsweep_kernel(
   for (int j = 0; j < RS_ROUNDS; ++j) {
     const int q = j * RS_THREADS + threadIdx.x;
     if (q < valid_n) {
-      const uint32_t k = skey[q];
-      const uint32_t dst = gbase[(k >> shift) & (RS_DIGITS - 1)] + (uint32_t)q;
+      const KT k = skey[q];
+      const uint32_t dst = gbase[(uint32_t)(k >> shift) & (RS_DIGITS - 1)] + (uint32_t)q;
       if (dst < n) {  // always, when histogram and ranks agree
         kout[dst] = k;
         vout[dst] = sval[q];
@@ -201,51 +204,54 @@ __global__ void __launch_bounds__(RS_THREADS) rs_downsweep_kernel(
   }
 }
 
-// Scratch of radix_sort_pairs, in 32-bit words: two key/value buffers of n,
-// the histogram, its column prefix and the digit totals.
+// Scratch of radix_sort_pairs, in 32-bit words: two key and two value
+// buffers of n, the histogram, its column prefix and the digit totals.
+template <typename KT = uint32_t>
 inline int64_t radix_sort_words(int64_t n) {
   const int64_t h = (int64_t)RS_DIGITS * rs_tiles(n);
   auto al = [](int64_t w) { return (w + 63) & ~int64_t(63); };  // 256-byte pieces
-  return 4 * al(std::max<int64_t>(n, 1)) + 2 * al(h) + al(RS_DIGITS);
+  const int64_t kw = (int64_t)(sizeof(KT) / 4);
+  return 2 * (kw + 1) * al(std::max<int64_t>(n, 1)) + 2 * al(h) + al(RS_DIGITS);
 }
 
 // Sorts (keys_in[i], i) by the low `bits` bits of keys_in into
 // (keys_out, vals_out), stably.  tmp: radix_sort_words(n) 32-bit words,
 // 256-byte aligned.  All arrays device, n < 2^31.
-inline scn_status radix_sort_pairs(const uint32_t* keys_in, uint32_t* keys_out,
-                                   int32_t* vals_out, int64_t n, int bits, uint32_t* tmp,
-                                   hipStream_t st) {
+template <typename KT>
+inline scn_status radix_sort_pairs(const KT* keys_in, KT* keys_out, int32_t* vals_out, int64_t n,
+                                   int bits, uint32_t* tmp, hipStream_t st) {
   if (n <= 0) return SCN_OK;
   const int64_t ntiles = rs_tiles(n), h = (int64_t)RS_DIGITS * ntiles;
   auto al = [](int64_t w) { return (w + 63) & ~int64_t(63); };
-  uint32_t* ka = tmp;
-  int32_t* va = reinterpret_cast<int32_t*>(ka + al(n));
-  uint32_t* kb = reinterpret_cast<uint32_t*>(va + al(n));
-  int32_t* vb = reinterpret_cast<int32_t*>(kb + al(n));
+  const int64_t kw = (int64_t)(sizeof(KT) / 4);  // 32-bit words per key
+  KT* ka = reinterpret_cast<KT*>(tmp);
+  int32_t* va = reinterpret_cast<int32_t*>(tmp + kw * al(n));
+  KT* kb = reinterpret_cast<KT*>(va + al(n));
+  int32_t* vb = reinterpret_cast<int32_t*>(tmp + (kw + 1) * al(n) + kw * al(n));
   uint32_t* hist = reinterpret_cast<uint32_t*>(vb + al(n));
   uint32_t* pre = hist + al(h);
   uint32_t* tot = pre + al(h);
   const int passes = rs_passes(bits);
-  const uint32_t* kin = keys_in;
+  const KT* kin = keys_in;
   const int32_t* vin = nullptr;
   for (int p = 0; p < passes; ++p) {
     const bool last = p == passes - 1;
     // passes ping-pong between the two buffers and end in the outputs
-    uint32_t* ko = last ? keys_out : ((passes - 1 - p) % 2 ? ka : kb);
+    KT* ko = last ? keys_out : ((passes - 1 - p) % 2 ? ka : kb);
     int32_t* vo = last ? vals_out : ((passes - 1 - p) % 2 ? va : vb);
     const int shift = p * RS_BITS;
-    hipLaunchKernelGGL(rs_upsweep_kernel, dim3((unsigned)ntiles), dim3(RS_THREADS), 0, st, kin, n,
+    hipLaunchKernelGGL(rs_upsweep_kernel<KT>, dim3((unsigned)ntiles), dim3(RS_THREADS), 0, st, kin, n,
                        shift, ntiles, hist);
     SCN_LAUNCH_CHECK();
     hipLaunchKernelGGL(rs_colscan_kernel, dim3(RS_DIGITS), dim3(RS_THREADS), 0, st,
                        (const uint32_t*)hist, ntiles, pre, tot);
     SCN_LAUNCH_CHECK();
     if (p == 0)
-      hipLaunchKernelGGL(rs_downsweep_kernel<true>, dim3((unsigned)ntiles), dim3(RS_THREADS), 0,
+      hipLaunchKernelGGL((rs_downsweep_kernel<KT, true>), dim3((unsigned)ntiles), dim3(RS_THREADS), 0,
                          st, kin, vin, ko, vo, n, shift, ntiles, (const uint32_t*)pre,
                          (const uint32_t*)tot);
     else
-      hipLaunchKernelGGL(rs_downsweep_kernel<false>, dim3((unsigned)ntiles), dim3(RS_THREADS), 0,
+      hipLaunchKernelGGL((rs_downsweep_kernel<KT, false>), dim3((unsigned)ntiles), dim3(RS_THREADS), 0,
                          st, kin, vin, ko, vo, n, shift, ntiles, (const uint32_t*)pre,
                          (const uint32_t*)tot);
     SCN_LAUNCH_CHECK();

@@ -1,5 +1,6 @@
 """GPU parity at the library's stated limits: the largest grid the occupancy
-bitmap accepts (B * my * mz * ceil(mx / 32) = 2^26 words), one word past it,
+bitmap accepts (B * my * mz * ceil(mx / 32) = 2^26 words), one word past it
+(the keyed builder),
 the widest convolution layers (256 channels) and pooling at 1024+ channels,
 against the oracle."""
 from __future__ import annotations
@@ -56,10 +57,17 @@ def test_largest_bitmap_grid(scn, grid, f, s):
 
 
 def test_one_word_past_the_bitmap_limit(scn):
-    coords = np.array([[0, 1, 1, 1]], np.int32)
-    with pytest.raises(scn.ScnError) as e:
-        scn.build_rulebook(dev(coords), (1, 2048, 2048, 513), 3, 1)
-    assert e.value.status == "unsupported"
+    """One word past the bitmaps' limit the build goes to the keyed builder
+    (sorted keys and hash tables), with the same result."""
+    grid = (1, 2048, 2048, 513)
+    rng = stream_rng(83, 0)
+    coords = random_sites(rng, 1, grid[1:], 3000)
+    corners = np.array([[0, 2047, 2047, 512], [0, 0, 0, 0]], np.int32)
+    keep = ~(coords[:, None, :] == corners[None]).all(axis=2).any(axis=1)
+    coords = np.concatenate([coords[keep], corners]).astype(np.int32)
+    g = scn.build_rulebook(dev(coords), grid, 3, 1)
+    assert g.keyed
+    _check(g, oracle.Rulebook(coords, grid, 3, 1))
 
 
 @pytest.mark.parametrize("f", [2, 3])

@@ -109,9 +109,9 @@ def test_rulebook_errors(scn):
     with pytest.raises(scn.ScnError) as e:
         scn.build_rulebook(dev(ok), grid, 2, 0)
     assert e.value.status == "invalid"
-    with pytest.raises(scn.ScnError) as e:
-        scn.build_rulebook(dev(ok), (1, 1 << 20, 1 << 10, 1 << 10), 2, 1)
-    assert e.value.status == "unsupported"
+    # a grid past the occupancy bitmaps builds through the keyed builder
+    big = scn.build_rulebook(dev(ok), (1, 1 << 20, 1 << 10, 1 << 10), 2, 1)
+    assert big.keyed and (big.a_in, big.a_out, big.n_pairs) == (1, 8, 8)
     # misaligned coordinate pointer (offset by one int32)
     flat = dev(np.zeros(9, np.int32))
     with pytest.raises(scn.ScnError) as e:
