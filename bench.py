@@ -249,10 +249,12 @@ def network_bench(batch: int, reps: int, warmup: int) -> None:
         planar = lattice in PLANAR
         convs = 2 if planar else 1
         m = input_size(levels, convs)
-        # the rulebook's occupancy bitmap holds at most 2^26 words per grid
-        # (the largest grid is the first convolution's output, m + 1 per axis)
+        # the occupancy bitmaps hold at most 2^26 words per grid (the largest
+        # grid is the first convolution's output, m + 1 per axis); past them
+        # the cubic lattice builds with sorted keys and hash tables, the
+        # other lattices cap the batch
         words = (m + 1) * (1 if planar else m + 1) * ((m + 1 + 31) // 32)
-        batch_n = min(batch, (1 << 26) // words)
+        batch_n = batch if lattice == "cubic" else min(batch, (1 << 26) // words)
         rows = []
         for b in range(batch_n):
             rng = stream_rng(150502890 + scale, b)
@@ -594,6 +596,22 @@ def main():
     del r, y, g, ws, dy
     torch.cuda.empty_cache()
 
+    # the same rulebook from the keyed builder (sorted keys and open-
+    # addressing hash tables: the path of grids past the bitmaps and of
+    # sites of other dimensions), median of 5 builds, each one call
+    log("keyed rulebook")
+    kt = []
+    for i in range(7):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        rk = scn.build_rulebook_nd(coords, cfg.grid, L.f, L.s)
+        torch.cuda.synchronize()
+        if i >= 2:
+            kt.append(time.perf_counter() - t0)
+        assert (rk.a_out, rk.n_pairs) == (a_out, P)
+        del rk
+    keyed_ms = statistics.median(kt) * 1e3
+
     log("ceilings")
     ceil = ceilings(scn, dev)
     # a plain device copy of known size (calibrates the HBM byte counters)
@@ -635,6 +653,8 @@ def main():
             "dense_forward_view": dense_view,
         },
         "rulebook_msites_per_s": round(a_in / (med["rulebook"] / 1e3) / 1e6, 2),
+        "rulebook_keyed": {"ms": round(keyed_ms, 4),
+                           "msites_per_s": round(a_in / (keyed_ms / 1e3) / 1e6, 2)},
         "phases_ms": {k: round(v, 4) for k, v in med.items()},
         "kernels_ms": {k: round(v, 4) for k, v in kern.items()},
         "phase_gflops": {

@@ -106,3 +106,37 @@ def test_planar_network_matches_oracle_chain(scn, lattice, levels, patch):
     assert_exact("final sites", host(oc), c)
     assert len(c) == batch
     assert_site("scores", host(out), xr)
+
+
+@pytest.mark.timeout(900)
+def test_scale80_cubic_network_at_batch_256(scn):
+    """The scale-80 cubic network (six C2-MP3/2 levels, input grid 254^3) at
+    batch 256: its first grids hold 256 * 255^2 * 8 bitmap words, past the
+    occupancy bitmaps, so the chain's rulebooks come from the keyed builder.
+    Samples do not interact: the final site and the class scores of sampled
+    samples equal the oracle chain run on each sample alone."""
+    from paper_1505_02890_amd.network import SparseNet, input_size
+
+    batch, levels, scale = 256, 6, 80.0
+    m = input_size(levels)
+    assert batch * (m + 1) ** 2 * ((m + 1 + 31) // 32) > 1 << 26
+    coords = _batch(batch, m, scale, 8080)
+    net = SparseNet(levels, classes=10, seed=80)
+    x = np.ones((len(coords), 1), np.float32)
+    out, oc, rec = net.forward(dev(coords, torch.int32), dev(x), batch)
+    out, oc = host(out), host(oc)
+    assert len(oc) == batch and np.array_equal(oc[:, 0], np.arange(batch))
+    for b in (0, 131, 255):
+        cb = coords[coords[:, 0] == b].copy()
+        cb[:, 0] = 0
+        c, grid, xr, g = cb, (1, m, m, m), np.ones((len(cb), 1)), np.zeros(1)
+        for L, p in zip(net.layers, net.params):
+            o = oracle.Rulebook(c, grid, L.f, L.s)
+            if L.kind == "conv":
+                W, bias = (host(t).astype(np.float64) for t in p)
+                xr, g = oracle.conv_fwd(o, xr, g, W, bias, relu=L.relu)
+            else:
+                xr, g, _, _ = oracle.maxpool_fwd(o, xr, g)
+            c, grid = o.arrays().out_coords, tuple(o.out_grid)
+        assert_exact(f"final site of sample {b}", oc[b, 1:], c[0, 1:])
+        assert_site(f"scores of sample {b}", out[b:b + 1], xr)
