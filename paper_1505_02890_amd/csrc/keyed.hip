@@ -20,17 +20,17 @@
 //   H_in       open-addressing table key -> rank, linear probing, capacity a
 //              power of two at least twice the sites
 //   outputs    one thread per (input, offset) candidate output site.  A wave
-//              takes 64 consecutive inputs at one offset, so its candidates
-//              are distinct and go straight to an atomicCAS insert into
-//              H_out; the lanes that inserted a new key append it to a list,
-//              placed by one ballot and one atomic add per wave (the pair
-//              count per offset comes from the same ballots)
-//   -- one host wait: the output count, the pair counts, the error flags --
-//   sort       the new keys, into canonical order; rank written into H_out
-//   pairs      per (offset, tile of 64 input ranks) one wave: a ballot over
-//              the tile's valid candidates gives counts, a scan gives each
-//              tile's place (the per-input-tile ranges), a second ballot each
-//              pair's place; output rows are looked up in H_out
+//              takes the 64 inputs of one tile of ranks at one offset, so its
+//              candidates are distinct and go straight to an insert into
+//              H_out (a read, then an atomicCAS if the slot is empty); a
+//              ballot over the wave's valid candidates gives the tile's pair
+//              count at that offset, and a scan of those counts each tile's
+//              place in the pair lists (the per-input-tile ranges)
+//   compact    the occupied slots of H_out, in slot order, by a prefix scan
+//   -- one host wait: the output count, the list boundaries, the flags --
+//   sort       the output keys, into canonical order; rank written into H_out
+//   pairs      per (offset, input tile) one wave: the ballot again places
+//              each pair; output rows are looked up in H_out
 //   tiles      per (offset, tile of output rows): a binary search in the list
 //   pooling    window tables from H_in lookups, each input's windows from
 //              H_out lookups
@@ -45,6 +45,11 @@ namespace scn {
 namespace {
 
 constexpr uint64_t HK_EMPTY = ~uint64_t(0);
+// Probe bound of the output table's inserts.  The table is first sized from
+// an estimate of the output count; an insert that finds no place within the
+// bound (or a table more than half full) sends the build back to insert into
+// a table sized for every candidate being distinct.
+constexpr int KD_PROBES = 256;
 enum : uint32_t { KF_RANGE = 1, KF_DUP = 2, KF_UNSORTED = 4 };
 
 struct KGeo {
@@ -176,46 +181,89 @@ __global__ void __launch_bounds__(256) kd_insert_kernel(const uint64_t* __restri
   }
 }
 
-// Candidate output sites: input rank r = 256 blockIdx.x + thread, offset k =
-// blockIdx.y.  counts[0] = new keys so far (their list), counts[1 + k] =
-// pairs at offset k.
-__global__ void __launch_bounds__(256) kd_candidates_kernel(
-    const int32_t* __restrict__ sb, const int4* __restrict__ sx, int64_t n, KGeo g,
-    uint64_t* __restrict__ hk, uint64_t mask, uint64_t* __restrict__ list,
-    unsigned long long* __restrict__ counts) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// Candidate output sites: input rank r = 64 blockIdx.x + lane (one wave per
+// tile of TILE = 64 ranks), offset k = blockIdx.y.  cnt[k*nit + tile] = the
+// tile's pairs at offset k; *full set when an insert found no place within
+// KD_PROBES slots.  Most candidates repeat a key already in the table (a
+// window holds several active inputs), so a slot is read before any atomic:
+// a slot changes once, from empty to its key, so a stale read can only show
+// it empty, and the atomicCAS then decides.
+__global__ void __launch_bounds__(64) kd_candidates_kernel(
+    const int32_t* __restrict__ sb, const int4* __restrict__ sx, int64_t n, KGeo g, int64_t nit,
+    uint64_t* __restrict__ hk, uint64_t mask, uint64_t* __restrict__ cnt,
+    uint32_t* __restrict__ full) {
+  const int64_t r = (int64_t)blockIdx.x * 64 + threadIdx.x;
   const int k = blockIdx.y;
   uint64_t key = 0;
   const bool valid = r < n && kd_out_site(sb[r], sx[r], k, g, &key);
-  bool fresh = false;
-  if (valid)
-    for (uint64_t i = hmix(key) & mask;; i = (i + 1) & mask) {
-      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(hk + i),
-                                      (unsigned long long)HK_EMPTY, (unsigned long long)key);
-      if (prev == HK_EMPTY) {
-        fresh = true;
+  bool placed = !valid;
+  if (valid) {
+    uint64_t i = hmix(key) & mask;
+    for (int t = 0; t < KD_PROBES; ++t, i = (i + 1) & mask) {
+      const uint64_t cur = hk[i];
+      if (cur == key) {
+        placed = true;
         break;
       }
-      if (prev == key) break;
-    }
-  const uint64_t vb = __ballot(valid), fb = __ballot(fresh);
-  const int lane = threadIdx.x & 63;
-  uint32_t lo = 0, hi = 0;
-  if (lane == 0) {
-    if (vb) atomicAdd(&counts[1 + k], (unsigned long long)__popcll(vb));
-    if (fb) {
-      const unsigned long long base = atomicAdd(&counts[0], (unsigned long long)__popcll(fb));
-      lo = (uint32_t)base;
-      hi = (uint32_t)(base >> 32);
+      if (cur != HK_EMPTY) continue;
+      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(hk + i),
+                                      (unsigned long long)HK_EMPTY, (unsigned long long)key);
+      if (prev == HK_EMPTY || prev == key) {
+        placed = true;
+        break;
+      }
     }
   }
-  // every lane takes part in the shuffles (lane 0 need not be fresh)
-  const uint64_t base = ((uint64_t)(uint32_t)__shfl((int)hi, 0, 64) << 32) |
-                        (uint32_t)__shfl((int)lo, 0, 64);
-  if (fresh) {
-    const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(fb >> 32),
-                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)fb, 0u));
-    list[base + below] = key;
+  const uint64_t vb = __ballot(valid);
+  const bool lost = __ballot(!placed) != 0;
+  if (threadIdx.x == 0) {
+    cnt[(int64_t)k * nit + blockIdx.x] = (uint64_t)__popcll(vb);
+    if (lost) atomicOr(full, 1u);
+  }
+}
+
+// Occupied slots of the output table per chunk of SCAN_BLOCK slots
+__global__ void __launch_bounds__(SCAN_THREADS) kd_occupied_kernel(const uint64_t* __restrict__ hk,
+                                                                   uint64_t cap,
+                                                                   uint32_t* __restrict__ bcnt) {
+  const uint64_t base = (uint64_t)blockIdx.x * SCAN_BLOCK;
+  uint32_t c = 0;
+  for (int j = threadIdx.x; j < SCAN_BLOCK; j += SCAN_THREADS)
+    c += (base + j < cap && hk[base + j] != HK_EMPTY) ? 1u : 0u;
+  uint32_t all;
+  block_exclusive_scan<uint32_t>(c, &all);
+  if (threadIdx.x == 0) bcnt[blockIdx.x] = all;
+}
+
+// The occupied slots' keys to list[], in slot order: chunk b starts at
+// bpre[b]; inside it, ballots place the wave's keys
+__global__ void __launch_bounds__(SCAN_THREADS) kd_compact_kernel(const uint64_t* __restrict__ hk,
+                                                                  uint64_t cap,
+                                                                  const uint32_t* __restrict__ bpre,
+                                                                  uint64_t* __restrict__ list) {
+  __shared__ uint32_t wsum[SCAN_THREADS / 64];
+  const uint64_t base = (uint64_t)blockIdx.x * SCAN_BLOCK;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t out = bpre[blockIdx.x];
+  for (int j0 = 0; j0 < SCAN_BLOCK; j0 += SCAN_THREADS) {
+    const uint64_t i = base + j0 + threadIdx.x;
+    const uint64_t key = i < cap ? hk[i] : HK_EMPTY;
+    const bool occ = key != HK_EMPTY;
+    const uint64_t bal = __ballot(occ);
+    if (lane == 0) wsum[w] = (uint32_t)__popcll(bal);
+    __syncthreads();
+    uint32_t before = 0, all = 0;
+#pragma unroll
+    for (int v = 0; v < SCAN_THREADS / 64; ++v) {
+      if (v < w) before += wsum[v];
+      all += wsum[v];
+    }
+    if (occ)
+      list[out + before + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))] =
+          key;
+    out += all;
+    __syncthreads();
   }
 }
 
@@ -241,19 +289,6 @@ __global__ void __launch_bounds__(256) kd_assign_kernel(const uint64_t* __restri
       key /= (uint64_t)g.mo[a];
     }
   c[0] = (int32_t)key;
-}
-
-// per (tile of 64 input ranks, offset): the tile's pairs at that offset
-__global__ void __launch_bounds__(64) kd_tile_count_kernel(const int32_t* __restrict__ sb,
-                                                           const int4* __restrict__ sx, int64_t n,
-                                                           KGeo g, int64_t nit,
-                                                           uint64_t* __restrict__ cnt) {
-  const int64_t r = (int64_t)blockIdx.x * 64 + threadIdx.x;
-  const int k = blockIdx.y;
-  uint64_t key;
-  const bool valid = r < n && kd_out_site(sb[r], sx[r], k, g, &key);
-  const uint64_t vb = __ballot(valid);
-  if (threadIdx.x == 0) cnt[(int64_t)k * nit + blockIdx.x] = (uint64_t)__popcll(vb);
 }
 
 // The pairs: list k holds, in input rank order, (caller row, output row) of
@@ -284,6 +319,12 @@ __global__ void kd_offsets_kernel(const uint64_t* __restrict__ itile, int64_t ni
                                   int64_t* __restrict__ off) {
   const int k = threadIdx.x;
   if (k <= K) off[k] = (int64_t)itile[(int64_t)k * nit];
+}
+
+// the output count: the compaction's total
+__global__ void kd_total_kernel(const uint32_t* __restrict__ bpre, int64_t nb,
+                                const uint32_t* __restrict__ bcnt, unsigned long long* out) {
+  *out = nb > 0 ? (unsigned long long)bpre[nb - 1] + bcnt[nb - 1] : 0ull;
 }
 
 // otile[k*nt + t] = place of the first pair of list k whose output row is at
@@ -392,8 +433,9 @@ inline int bits_for(uint64_t v) {  // bits of the largest key below v
 
 // Read-back of the host wait (pinned, one per host thread).
 struct KReadback {
-  uint32_t flags, pad;
-  unsigned long long counts[1 + MAX_K];
+  uint32_t flags, full;
+  unsigned long long a_out;
+  int64_t off[MAX_K + 1];
 };
 
 scn_status kd_readback(KReadback** out) {
@@ -511,39 +553,48 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   for (int a = 0; a < D; ++a) per_in *= (uint64_t)ceil_div(f, s);
   const uint64_t ucap = std::max<uint64_t>(
       1, std::min<uint64_t>((uint64_t)std::max<int64_t>(n, 1) * per_in, sites_out));
-  const uint64_t cap_out = pow2_at_least(2 * ucap);
+  // the output table: first sized for 8 outputs per input (a surface under a
+  // 3x3x3 filter gives about 4.4), at most for every candidate distinct
+  const uint64_t cap_full = pow2_at_least(2 * ucap);
+  uint64_t cap_out = std::min(cap_full, pow2_at_least(2 * std::min<uint64_t>(
+                                            ucap, 8 * (uint64_t)std::max<int64_t>(n, 1))));
   const int64_t nit = std::max<int64_t>(1, ceil_div(n, TILE));
   uint64_t *keys = nullptr, *skeys = nullptr, *hk_in = nullptr, *hk_out = nullptr,
-           *list = nullptr;
-  int32_t *perm = nullptr, *hv_in = nullptr, *hv_out = nullptr, *sb = nullptr;
+           *list = nullptr, *cnt = nullptr, *scan_tmp = nullptr;
+  int32_t *hv_in = nullptr, *hv_out = nullptr, *sb = nullptr;
   int4* sx = nullptr;
-  uint32_t *flags = nullptr, *sort_tmp = nullptr;
-  unsigned long long* counts = nullptr;
+  uint32_t *flags = nullptr, *sort_tmp = nullptr, *bcnt = nullptr, *bpre = nullptr,
+           *bscan = nullptr;
+  int64_t* off_tmp = nullptr;
+  unsigned long long* aout_dev = nullptr;
   const int bits_in = bits_for(sites_in);
   if ((rc = tmp.get(&keys, n)) || (rc = tmp.get(&skeys, n)) || (rc = tmp.get(&sb, n)) ||
       (rc = tmp.get(&sx, n)) || (rc = tmp.get(&hk_in, (int64_t)cap_in)) ||
-      (rc = tmp.get(&hv_in, (int64_t)cap_in)) || (rc = tmp.get(&hk_out, (int64_t)cap_out)) ||
-      (rc = tmp.get(&hv_out, (int64_t)cap_out)) || (rc = tmp.get(&list, (int64_t)ucap)) ||
-      (rc = tmp.get(&flags, 64)) || (rc = tmp.get(&counts, 1 + MAX_K)) ||
+      (rc = tmp.get(&hv_in, (int64_t)cap_in)) || (rc = tmp.get(&list, (int64_t)ucap)) ||
+      (rc = tmp.get(&flags, 64)) || (rc = tmp.get(&off_tmp, MAX_K + 1)) ||
+      (rc = tmp.get(&aout_dev, 1)) || (rc = tmp.get(&cnt, K * nit)) ||
+      (rc = tmp.get(&scan_tmp, scan_blocks(K * nit))) ||
       (rc = tmp.get(&sort_tmp, radix_sort_words<uint64_t>(n))))
     return rc;
-  // rank -> caller row; the rulebook adopts it when the rows were unsorted
-  void* perm_block = nullptr;
-  if ((rc = dalloc(&perm_block, (size_t)std::max<int64_t>(n, 1) * 4, st, mem))) return rc;
-  perm = static_cast<int32_t*>(perm_block);
-  struct PermGuard {
+  // The input block, adopted by the rulebook: rank -> caller row (perm, used
+  // when the rows were unsorted) and the per-input-tile pair ranges (itile,
+  // K*nit + 1 entries: the scan of the candidates' tile counts).
+  const size_t perm_bytes = (size_t)((std::max<int64_t>(n, 1) * 4 + 255) & ~int64_t(255));
+  void* in_block = nullptr;
+  if ((rc = dalloc(&in_block, perm_bytes + (size_t)(K * nit + 1) * 8, st, mem))) return rc;
+  int32_t* perm = static_cast<int32_t*>(in_block);
+  uint64_t* itile = reinterpret_cast<uint64_t*>(static_cast<char*>(in_block) + perm_bytes);
+  struct BlockGuard {
     void*& p;
     hipStream_t st;
     Allocator al;
-    ~PermGuard() {
+    ~BlockGuard() {
       if (p) dfree(p, st, al);
     }
-  } perm_guard{perm_block, st, mem};
+  } in_guard{in_block, st, mem};
 
-  SCN_HIP(hipMemsetAsync(flags, 0, 4, st));
-  SCN_HIP(hipMemsetAsync(counts, 0, (1 + MAX_K) * sizeof(unsigned long long), st));
+  SCN_HIP(hipMemsetAsync(flags, 0, 8, st));
   SCN_HIP(hipMemsetAsync(hk_in, 0xFF, cap_in * 8, st));
-  SCN_HIP(hipMemsetAsync(hk_out, 0xFF, cap_out * 8, st));
   if (n > 0) {
     hipLaunchKernelGGL(kd_keys_kernel, dim3(kd_blocks(n, 256)), dim3(256), 0, st, coords, n, g,
                        keys, flags);
@@ -555,15 +606,57 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
     hipLaunchKernelGGL(kd_insert_kernel, dim3(kd_blocks(n, 256)), dim3(256), 0, st,
                        (const uint64_t*)skeys, n, hk_in, hv_in, cap_in - 1);
     SCN_LAUNCH_CHECK();
-    hipLaunchKernelGGL(kd_candidates_kernel, dim3(kd_blocks(n, 256), (unsigned)K), dim3(256), 0,
-                       st, (const int32_t*)sb, (const int4*)sx, n, g, hk_out, cap_out - 1, list,
-                       counts);
-    SCN_LAUNCH_CHECK();
+  } else {
+    SCN_HIP(hipMemsetAsync(cnt, 0, K * nit * 8, st));
   }
-  SCN_HIP(hipMemcpyAsync(&hb->flags, flags, 4, hipMemcpyDeviceToHost, st));
-  SCN_HIP(hipMemcpyAsync(hb->counts, counts, (1 + K) * sizeof(unsigned long long),
-                         hipMemcpyDeviceToHost, st));
-  SCN_HIP(hipStreamSynchronize(st));
+  // the output table: the candidates' inserts, the tile counts and their
+  // scan, the compaction of the occupied slots and the read-back; again with
+  // the largest table when the first one overflowed
+  auto outputs = [&]() -> scn_status {
+    scn_status rc2;
+    const int64_t nb = (int64_t)ceil_div((int64_t)cap_out, SCAN_BLOCK);
+    if ((rc2 = tmp.get(&hk_out, (int64_t)cap_out)) ||
+        (rc2 = tmp.get(&hv_out, (int64_t)cap_out)) || (rc2 = tmp.get(&bcnt, nb)) ||
+        (rc2 = tmp.get(&bpre, nb + 1)) || (rc2 = tmp.get(&bscan, scan_blocks(nb))))
+      return rc2;
+    SCN_HIP(hipMemsetAsync(flags + 1, 0, 4, st));
+    SCN_HIP(hipMemsetAsync(hk_out, 0xFF, cap_out * 8, st));
+    if (n > 0) {
+      hipLaunchKernelGGL(kd_candidates_kernel, dim3((unsigned)nit, (unsigned)K), dim3(64), 0, st,
+                         (const int32_t*)sb, (const int4*)sx, n, g, nit, hk_out, cap_out - 1, cnt,
+                         flags + 1);
+      SCN_LAUNCH_CHECK();
+    }
+    if ((rc2 = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, K * nit, itile,
+                                        itile + K * nit, scan_tmp, st)))
+      return rc2;
+    hipLaunchKernelGGL(kd_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)itile, nit,
+                       (int)K, off_tmp);
+    SCN_LAUNCH_CHECK();
+    hipLaunchKernelGGL(kd_occupied_kernel, dim3((unsigned)nb), dim3(SCAN_THREADS), 0, st,
+                       (const uint64_t*)hk_out, cap_out, bcnt);
+    SCN_LAUNCH_CHECK();
+    if ((rc2 = exclusive_scan<uint32_t>(PlainLoad<uint32_t>{bcnt}, nb, bpre, bpre + nb, bscan,
+                                        st)))
+      return rc2;
+    hipLaunchKernelGGL(kd_compact_kernel, dim3((unsigned)nb), dim3(SCAN_THREADS), 0, st,
+                       (const uint64_t*)hk_out, cap_out, (const uint32_t*)bpre, list);
+    SCN_LAUNCH_CHECK();
+    hipLaunchKernelGGL(kd_total_kernel, dim3(1), dim3(1), 0, st, (const uint32_t*)bpre, nb,
+                       (const uint32_t*)bcnt, aout_dev);
+    SCN_LAUNCH_CHECK();
+    SCN_HIP(hipMemcpyAsync(&hb->flags, flags, 8, hipMemcpyDeviceToHost, st));
+    SCN_HIP(hipMemcpyAsync(&hb->a_out, aout_dev, 8, hipMemcpyDeviceToHost, st));
+    SCN_HIP(hipMemcpyAsync(hb->off, off_tmp, (K + 1) * 8, hipMemcpyDeviceToHost, st));
+    SCN_HIP(hipStreamSynchronize(st));
+    return SCN_OK;
+  };
+  if ((rc = outputs())) return rc;
+  if ((hb->full || hb->a_out > cap_out / 2) && !(hb->flags & (KF_RANGE | KF_DUP)) &&
+      cap_out < cap_full) {
+    cap_out = cap_full;
+    if ((rc = outputs())) return rc;
+  }
   if (hb->flags & KF_RANGE) {
     set_error("scn_rulebook_build_nd: a site lies outside the grid");
     return SCN_ERR_RANGE;
@@ -572,11 +665,15 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
     set_error("scn_rulebook_build_nd: duplicate site in the input list");
     return SCN_ERR_DUPLICATE;
   }
+  if (hb->full || hb->a_out > cap_out / 2) {  // cannot happen with the largest table
+    set_error("scn_rulebook_build_nd: output table overflow (%llu outputs)",
+              (unsigned long long)hb->a_out);
+    return SCN_ERR_HIP;
+  }
   const bool sorted = !(hb->flags & KF_UNSORTED);
-  const int64_t a_out = (int64_t)hb->counts[0];
+  const int64_t a_out = (int64_t)hb->a_out;
   int64_t off[MAX_K + 1];
-  off[0] = 0;
-  for (int k = 0; k < K; ++k) off[k + 1] = off[k] + (int64_t)hb->counts[1 + k];
+  for (int k = 0; k <= K; ++k) off[k] = hb->off[k];
   const int64_t P = off[K];
   if (a_out > INT32_MAX || P > INT32_MAX) {
     set_error("scn_rulebook_build_nd: %lld outputs / %lld pairs exceed INT32_MAX",
@@ -585,15 +682,14 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   }
   const int64_t nt = std::max<int64_t>(1, ceil_div(a_out, TILE));
 
-  // the rulebook: one block for everything but perm
+  // the rulebook: one block for everything but the input block
   auto al = [](int64_t bytes) { return (bytes + 255) & ~int64_t(255); };
   const int64_t sz_oc = al(a_out * (D + 1) * 4), sz_p = al(P * 4),
                 sz_rank = sorted ? 0 : al(P * 4), sz_off = al((K + 1) * 8),
-                sz_ot = al((K * nt + 1) * 8), sz_it = al((K * nit + 1) * 8),
-                sz_nbr = pool ? al(a_out * K * 4) : 0, sz_inv = pool ? al(n * slots * 4) : 0,
-                sz_pm = pool ? al(a_out * 4) : 0;
-  const int64_t total = sz_oc + 2 * sz_p + sz_rank + sz_off + sz_ot + sz_it + sz_nbr + sz_inv +
-                        sz_pm;
+                sz_ot = al((K * nt + 1) * 8), sz_nbr = pool ? al(a_out * K * 4) : 0,
+                sz_inv = pool ? al(n * slots * 4) : 0, sz_pm = pool ? al(a_out * 4) : 0;
+  const int64_t total =
+      sz_oc + 2 * sz_p + sz_rank + sz_off + sz_ot + sz_nbr + sz_inv + sz_pm;
   scn_rulebook* rb = new scn_rulebook();
   struct RbGuard {
     scn_rulebook*& rb;
@@ -604,6 +700,8 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   } rb_guard{rb};
   rb->alloc = mem;
   rb->stream = st;
+  rb->inblock = in_block;  // owned by rb from here
+  in_block = nullptr;
   if ((rc = dalloc(&rb->block, (size_t)total, st, mem))) return rc;
   char* cur = static_cast<char*>(rb->block);
   auto take = [&](int64_t bytes) {
@@ -618,17 +716,13 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   rb->in_rank = sorted ? rb->in_rows : in_rank_arr;
   rb->off_dev = (int64_t*)take(sz_off);
   rb->otile = (int64_t*)take(sz_ot);
-  rb->itile = (int64_t*)take(sz_it);
+  rb->itile = reinterpret_cast<int64_t*>(itile);
   rb->nbr = pool ? (int32_t*)take(sz_nbr) : nullptr;
   rb->inv = pool ? (int32_t*)take(sz_inv) : nullptr;
   rb->pmask = pool ? (uint32_t*)take(sz_pm) : nullptr;
   rb->inv_slots = slots;
-  if (!sorted) {
-    rb->inblock = perm_block;  // owned by rb from here
-    perm_block = nullptr;
-    rb->perm = perm;
-  }
-  const int32_t* perm_or_null = sorted ? nullptr : perm;
+  rb->perm = sorted ? nullptr : perm;
+  const int32_t* perm_or_null = rb->perm;
   rb->f = f;
   rb->s = s;
   rb->K = (int32_t)K;
@@ -651,6 +745,7 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   rb->n_otiles = nt;
   rb->n_itiles = nit;
   for (int k = 0; k <= K; ++k) rb->off_host[k] = off[k];
+  SCN_HIP(hipMemcpyAsync(rb->off_dev, off_tmp, (K + 1) * 8, hipMemcpyDeviceToDevice, st));
 
   // outputs in canonical order, their rows into H_out
   uint64_t* okeys = nullptr;
@@ -668,23 +763,6 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
                        cap_out - 1, rb->out_coords);
     SCN_LAUNCH_CHECK();
   }
-  // pairs: counts per (offset, input tile), their scan, the emission
-  uint64_t *cnt = nullptr, *scan_tmp = nullptr;
-  if ((rc = tmp.get(&cnt, K * nit)) || (rc = tmp.get(&scan_tmp, scan_blocks(K * nit)))) return rc;
-  if (n > 0) {
-    hipLaunchKernelGGL(kd_tile_count_kernel, dim3((unsigned)nit, (unsigned)K), dim3(64), 0, st,
-                       (const int32_t*)sb, (const int4*)sx, n, g, nit, cnt);
-    SCN_LAUNCH_CHECK();
-  } else {
-    SCN_HIP(hipMemsetAsync(cnt, 0, K * nit * 8, st));
-  }
-  uint64_t* itile = reinterpret_cast<uint64_t*>(rb->itile);
-  if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{cnt}, K * nit, itile, itile + K * nit,
-                                     scan_tmp, st)))
-    return rc;
-  hipLaunchKernelGGL(kd_offsets_kernel, dim3(1), dim3(64), 0, st, (const uint64_t*)itile, nit,
-                     (int)K, rb->off_dev);
-  SCN_LAUNCH_CHECK();
   if (n > 0 && P > 0) {
     hipLaunchKernelGGL(kd_emit_kernel, dim3((unsigned)nit, (unsigned)K), dim3(64), 0, st,
                        (const int32_t*)sb, (const int4*)sx, n, g, nit, (const uint64_t*)itile,
