@@ -904,6 +904,44 @@ scn_status copy_event(hipEvent_t* out) {
   return SCN_OK;
 }
 
+// A second stream per device and host thread, at the default priority like
+// the caller's, for build stages that do not depend on each other: fork()
+// orders it after the work queued so far on st, join() orders st after it.
+struct AuxStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+
+scn_status aux_stream(AuxStream** out) {
+  static thread_local AuxStream aux[64];
+  int dev = 0;
+  SCN_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) {
+    set_error("scn_rulebook_build: device %d out of range", dev);
+    return SCN_ERR_HIP;
+  }
+  AuxStream& a = aux[dev];
+  if (!a.s) {
+    SCN_HIP(hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking));
+    SCN_HIP(hipEventCreateWithFlags(&a.fork, hipEventDisableTiming));
+    SCN_HIP(hipEventCreateWithFlags(&a.join, hipEventDisableTiming));
+  }
+  *out = &a;
+  return SCN_OK;
+}
+
+scn_status fork(hipStream_t st, AuxStream* a) {
+  SCN_HIP(hipEventRecord(a->fork, st));
+  SCN_HIP(hipStreamWaitEvent(a->s, a->fork, 0));
+  return SCN_OK;
+}
+
+scn_status join(hipStream_t st, AuxStream* a) {
+  SCN_HIP(hipEventRecord(a->join, a->s));
+  SCN_HIP(hipStreamWaitEvent(st, a->join, 0));
+  return SCN_OK;
+}
+
 // The build of one layer, in steps:
 //   check()   host only: arguments, output grid, bitmap sizes;
 //   phase1()  device: mark the caller's sites (first layer only), rank them,
@@ -1056,7 +1094,9 @@ struct LayerBuild {
   // rulebook adopts.  Queued before the first wait when the sites are known;
   // the kernels tolerate an input list with errors (the build then fails).
   bool in_done = false;
-  scn_status input_side() {
+  AuxStream* aux = nullptr;
+  // xs: the stream its kernels run on (allocations stay tagged with st)
+  scn_status input_side(hipStream_t xs) {
     scn_status rc;
     nit = std::max<int64_t>(1, ceil_div(n, TILE));
     // windows per input: at most ceil(f/s) per axis of the window
@@ -1084,19 +1124,19 @@ struct LayerBuild {
     cur += chained ? 0 : list_bytes;
     off_dev = reinterpret_cast<int64_t*>(cur);
     if (!chained && n > 0) {
-      hipLaunchKernelGGL(perm_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, coords, n, gi,
+      hipLaunchKernelGGL(perm_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, xs, coords, n, gi,
                          (const uint32_t*)inb, (const uint32_t*)ipref, perm);
       SCN_LAUNCH_CHECK();
     }
     uint64_t *icnt = nullptr, *isc = nullptr;
     if ((rc = tmp.get(&icnt, K * nit)) || (rc = tmp.get(&isc, scan_blocks(K * nit)))) return rc;
     with_kernels(f, lattice, [&](auto k) {
-      k.in_tile_count(s == 1 ? 1 : (s == 2 ? 2 : 0), dim3(blocks_for(nit * TILE, 256)), st,
+      k.in_tile_count(s == 1 ? 1 : (s == 2 ? 2 : 0), dim3(blocks_for(nit * TILE, 256)), xs,
                       coords, (const int32_t*)perm, n, nit, s, go, icnt);
     });
     SCN_LAUNCH_CHECK();
     if ((rc = exclusive_scan<uint64_t>(PlainLoad<uint64_t>{icnt}, K * nit, (uint64_t*)itile,
-                                       (uint64_t*)itile + K * nit, isc, st)))
+                                       (uint64_t*)itile + K * nit, isc, xs)))
       return rc;
     in_done = true;
     return SCN_OK;
@@ -1166,7 +1206,11 @@ struct LayerBuild {
         return rc;
     }
     // the input side overlaps the host's first wait
-    if (in_early && (rc = input_side())) return rc;
+    // the input side (it needs only the input bitmap: every output of an
+    // active input is active) beside the output bitmap's dilation and scan
+    if (in_early &&
+        ((rc = aux_stream(&aux)) || (rc = fork(st, aux)) || (rc = input_side(aux->s))))
+      return rc;
     {
       const int sm = s == 1 ? 1 : (s == 2 ? 2 : 0);
       with_kernels(f, lattice, [&](auto k) {
@@ -1177,7 +1221,7 @@ struct LayerBuild {
     if ((rc = exclusive_scan<uint32_t>(PopcountLoad{hout.bits}, nw_out, hout.rank,
                                        hout.rank + nw_out, sc32, st)))
       return rc;
-    if (in_early && (rc = emit_lists())) return rc;
+    if (in_early && ((rc = join(st, aux)) || (rc = emit_lists()))) return rc;
     // flags, both totals and (lists emitted) the list boundaries in one read-back
     hipLaunchKernelGGL(pack_totals_kernel, dim3(1), dim3(64), 0, st, flags, ipref + nw_in,
                        hout.rank + nw_out, in_early ? (const int64_t*)itile : nullptr, nit, K,
@@ -1200,7 +1244,7 @@ struct LayerBuild {
     }
     a_out = hb->a_out;
     sorted = !(hb->flags & F_UNSORTED);
-    if (!in_done && (rc = input_side())) return rc;
+    if (!in_done && (rc = input_side(st))) return rc;
     // pooling tables (window rows per output, windows per input) for stride >= 2
     pool = s >= 2;
     inv_slots = pool ? (f > s ? 8 : 1) : 0;
@@ -1329,6 +1373,15 @@ struct LayerBuild {
                                          (uint64_t*)rb->otile + ncnt, sc64, st)))
         return rc;
     }
+    // the mask sort (it needs only the masks) beside the neighbour lists
+    const bool side_sort = dense && a_out > 0;
+    if (side_sort) {
+      uint32_t* sort_tmp = nullptr;
+      if ((rc = tmp.get(&sort_tmp, sort_bytes / 4)) || (rc = aux_stream(&aux)) ||
+          (rc = fork(st, aux)) ||
+          (rc = radix_sort_pairs(masks, rb->fmask, rb->fperm, a_out, K, sort_tmp, aux->s)))
+        return rc;
+    }
     if (dense) {
       // start of each output's neighbour list: exclusive sum of mask popcounts
       uint32_t* sc_nb = nullptr;
@@ -1348,13 +1401,7 @@ struct LayerBuild {
       });
       SCN_LAUNCH_CHECK();
     }
-    if (dense) {
-      // the output rows sorted by neighbour mask (a stable radix sort)
-      uint32_t* sort_tmp = nullptr;
-      if ((rc = tmp.get(&sort_tmp, sort_bytes / 4)) ||
-          (rc = radix_sort_pairs(masks, rb->fmask, rb->fperm, a_out, K, sort_tmp, st)))
-        return rc;
-    }
+    if (side_sort && (rc = join(st, aux))) return rc;
     if (cells) {
       // (also zeroes the homeless count before inv_windows fills it)
       hipLaunchKernelGGL(lower_windows_kernel, dim3(blocks_for(std::max<int64_t>(a_out, 1), 256)),
