@@ -61,8 +61,8 @@ def parse():
                         "networks (3D object recognition on the cubic and tetrahedral "
                         "lattices; 2D SquareNet / TriangLeNet), one JSON line each")
     p.add_argument("--batch", type=int, default=256,
-                   help="samples per batch for --network (capped per network by the "
-                        "rulebook's grid limit)")
+                   help="samples per batch for --network (the tetrahedral networks are "
+                        "capped by the occupancy bitmaps' grid limit)")
     return p.parse_args()
 
 

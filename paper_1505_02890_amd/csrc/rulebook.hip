@@ -1512,15 +1512,22 @@ scn_status build_chain(const int32_t* coords, int64_t n, const int64_t* grid, in
   }
   for (int i = 0; i < nl; ++i) out[i] = nullptr;
   if (lattice == SCN_LATTICE_CUBIC && !bitmaps_fit(grid, filters[0], strides[0])) {
-    // keyed builds one after the other, each from the previous one's outputs
+    // keyed builds one after the other, each from the previous one's
+    // outputs, until a layer's grids fit the bitmaps: the rest of the chain
+    // is then a bitmap chain (same results, faster)
     std::vector<scn_rulebook*> res(nl, nullptr);
     scn_status rc = SCN_OK;
     for (int i = 0; i < nl && rc == SCN_OK; ++i) {
-      if (i == 0)
+      if (i == 0) {
         rc = keyed_build(coords, n, 3, grid, filters[0], strides[0], st, &res[0]);
-      else
+      } else if (bitmaps_fit(res[i - 1]->gout_nd, filters[i], strides[i])) {
+        rc = build_chain(res[i - 1]->out_coords, res[i - 1]->a_out, res[i - 1]->gout_nd,
+                         lattice, nl - i, filters + i, strides + i, st, res.data() + i);
+        break;
+      } else {
         rc = keyed_build(res[i - 1]->out_coords, res[i - 1]->a_out, 3, res[i - 1]->gout_nd,
                          filters[i], strides[i], st, &res[i]);
+      }
     }
     if (rc != SCN_OK) {
       for (int i = 0; i < nl; ++i) scn_rulebook_free(res[i]);
@@ -1632,9 +1639,20 @@ scn_status scn_rulebook_build_next(const scn_rulebook* prev, int32_t filter, int
     *out = nullptr;
     return rc;
   }
-  if (prev->keyed)
+  if (prev->keyed) {
+    // 3D sites whose next grids fit the bitmaps take the bitmap builder
+    // (same result); the sites, in key order, are read by kernels queued here
+    if (prev->ndim == 3 && scn::bitmaps_fit(prev->gout_nd, filter, stride)) {
+      scn_status rc = scn::build(prev->out_coords, prev->a_out, prev->gout_nd, filter, stride,
+                                 SCN_LATTICE_CUBIC, stream, out);
+      if (rc == SCN_OK && prev->stream != stream)
+        rc = (hipStreamWaitEvent(prev->stream, (*out)->done, 0) == hipSuccess) ? SCN_OK
+                                                                              : SCN_ERR_HIP;
+      return rc;
+    }
     return scn::keyed_build(prev->out_coords, prev->a_out, prev->ndim, prev->gout_nd, filter,
                             stride, stream, out);
+  }
   return scn::build(prev->out_coords, prev->a_out, prev->gout, filter, stride, prev->lattice,
                     stream, out, prev);
 }

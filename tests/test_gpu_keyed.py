@@ -233,3 +233,29 @@ def test_nd_empty_and_errors(scn):
     with pytest.raises(scn.ScnError) as e:
         scn.maxpool_fwd(g2, dev(np.ones((2, 4), np.float32)), dev(np.zeros(4, np.float32)))
     assert e.value.status == "unsupported"
+
+
+def test_keyed_chain_switches_to_the_bitmaps(scn):
+    """A chain whose first grids are past the bitmaps and whose later grids fit
+    them: the later layers come from the bitmap builder, with the same
+    rulebooks as the oracle chain (and next_rulebook does the same)."""
+    grid = (2, 4096, 4096, 1024)
+    layers = [(3, 2), (3, 2), (2, 1), (3, 1)]
+    rng = stream_rng(672, 0)
+    centres = np.stack([rng.integers(0, 2, 50), rng.integers(0, grid[1] - 24, 50),
+                        rng.integers(0, grid[2] - 24, 50), rng.integers(0, grid[3] - 24, 50)], 1)
+    pts = centres[rng.integers(0, 50, 5000)] + np.concatenate(
+        [np.zeros((5000, 1), np.int64), rng.integers(0, 24, (5000, 3))], 1)
+    coords = np.unique(pts, axis=0).astype(np.int32)
+    chain = scn.build_chain(dev(coords), grid, layers)
+    assert [r.keyed for r in chain] == [True, True, False, False]
+    g = None
+    c, gr = coords, grid
+    for i, (f, s) in enumerate(layers):
+        g = scn.build_rulebook(dev(coords), grid, f, s) if i == 0 else scn.next_rulebook(g, f, s)
+        assert g.keyed == (i < 2)
+        o = oracle.Rulebook(c, gr, f, s)
+        check_rulebook(g, o)
+        check_rulebook(chain[i], o)
+        oa = o.arrays()
+        c, gr = oa.out_coords, tuple(oa.out_grid)
