@@ -249,11 +249,11 @@ def network_bench(batch: int, reps: int, warmup: int) -> None:
         planar = lattice in PLANAR
         convs = 2 if planar else 1
         m = input_size(levels, convs)
-        # the occupancy bitmaps hold at most 2^26 words per grid (the largest
-        # grid is the first convolution's output, m + 1 per axis); past them
-        # the cubic lattice builds with sorted keys and hash tables, the
-        # other lattices cap the batch
-        words = (m + 1) * (1 if planar else m + 1) * ((m + 1 + 31) // 32)
+        # the occupancy bitmaps hold at most 2^26 32-bit words per grid (the
+        # largest grid is the input, m per axis, rows padded to 32 sites);
+        # past them the cubic lattice builds with sorted keys and hash
+        # tables, the other lattices cap the batch
+        words = m * (1 if planar else m) * ((m + 31) // 32)
         batch_n = batch if lattice == "cubic" else min(batch, (1 << 26) // words)
         rows = []
         for b in range(batch_n):
