@@ -667,18 +667,29 @@ __global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
   const int64_t b = (int64_t)blockIdx.x * (NT / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (b >= a.nblk) return;
   const int cb = blockIdx.y;
+  // Two lane layouts.  MFMA layout: lane (n16, q) = n16 + 16q holds row n16
+  // (and 16 + n16), channels 4q .. 4q + 3 of each 16; the operand fixes it.
+  // Load layout: lane (rl, cq) = 4rl + cq loads row rl (and 16 + rl),
+  // channels 4cq .. 4cq + 3, so four adjacent lanes read one row's 64
+  // contiguous bytes (in the MFMA layout four adjacent lanes read four
+  // rows, and the L1 serves each 16-byte piece on its own).  The rows are
+  // gathered in the load layout and moved to the MFMA layout by ds_bpermute.
   const int n16 = lane & 15, q = lane >> 4;
+  const int rl = lane >> 2, cq = lane & 3;
+  const int from = (n16 * 4 + q) * 4;  // bpermute address: MFMA lane <- load lane 4 n16 + q
   const int ncb = a.NcP >> 6;
-  const int64_t pos0 = b * DENSE_ROWS + n16, pos1 = pos0 + 16;
+  const int64_t pos0 = b * DENSE_ROWS + n16, pos1 = pos0 + 16;      // MFMA layout
+  const int64_t lpos0 = b * DENSE_ROWS + rl, lpos1 = lpos0 + 16;    // load layout
   const int o0 = pos0 < a.a_out ? a.fperm[pos0] : 0, o1 = pos1 < a.a_out ? a.fperm[pos1] : 0;
+  const int lo0 = lpos0 < a.a_out ? a.fperm[lpos0] : 0, lo1 = lpos1 < a.a_out ? a.fperm[lpos1] : 0;
   DRow w0, w1;
-  w0.m = pos0 < a.a_out ? a.fmask[pos0] : 0u;
-  w1.m = pos1 < a.a_out ? a.fmask[pos1] : 0u;
-  w0.off = a.nb_off[o0];
-  w1.off = a.nb_off[o1];
+  w0.m = lpos0 < a.a_out ? a.fmask[lpos0] : 0u;
+  w1.m = lpos1 < a.a_out ? a.fmask[lpos1] : 0u;
+  w0.off = a.nb_off[lo0];
+  w1.off = a.nb_off[lo1];
   uint32_t u = w0.m | w1.m;
 #pragma unroll
-  for (int d = 1; d < 16; d <<= 1) u |= (uint32_t)__shfl_xor((int)u, d, 16);
+  for (int d = 4; d < 64; d <<= 1) u |= (uint32_t)__shfl_xor((int)u, d, 64);
   const uint32_t U = (uint32_t)__builtin_amdgcn_readfirstlane((int)u);
   v4f acc[2][4];
 #pragma unroll
@@ -709,7 +720,7 @@ __global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
     advance(nn);
     const int nit = __builtin_popcount(U) * NCH;
     int n0 = dense_src(a, w0, n.k), n1 = dense_src(a, w1, n.k);
-    DRows<TC> cur = dense_rows_i<NKT, VEC>(a, dense_src(a, w0, c.k), dense_src(a, w1, c.k), 0, q);
+    DRows<TC> cur = dense_rows_i<NKT, VEC>(a, dense_src(a, w0, c.k), dense_src(a, w1, c.k), 0, cq);
     DRows<TC> nxt;
     int nn0 = 0, nn1 = 0;
     for (int it = 0; it < nit; ++it) {
@@ -725,18 +736,25 @@ __global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
       // item's last weight load, so the waits for the weights leave them in
       // flight
       auto prefetch = [&]() {
-        nxt = dense_rows_i<NKT, VEC>(a, n0, n1, n.ch, q);
+        nxt = dense_rows_i<NKT, VEC>(a, n0, n1, n.ch, cq);
         nn0 = dense_src(a, w0, nn.k);
         nn1 = dense_src(a, w1, nn.k);
       };
       auto mult = [&](int t, const float4 (&A)[4]) {
         const int tg = 4 * ch + t;
-        const float4 gq = *reinterpret_cast<const float4*>(&gsh[16 * tg + 4 * q]);
+        // x - g_in, zero for an absent row, in the load layout; then to the
+        // MFMA layout
+        const float4 gq = *reinterpret_cast<const float4*>(&gsh[16 * tg + 4 * cq]);
         const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
         float4 d0 = cur.v[0][t], d1 = cur.v[1][t];
         d0.x -= gq.x; d0.y -= gq.y; d0.z -= gq.z; d0.w -= gq.w;
         d1.x -= gq.x; d1.y -= gq.y; d1.z -= gq.z; d1.w -= gq.w;
-        const float4 B0 = cur.r0 >= 0 ? d0 : z, B1 = cur.r1 >= 0 ? d1 : z;
+        const float4 L0 = cur.r0 >= 0 ? d0 : z, L1 = cur.r1 >= 0 ? d1 : z;
+        auto perm = [&](float v) {
+          return __int_as_float(__builtin_amdgcn_ds_bpermute(from, __float_as_int(v)));
+        };
+        const float4 B0 = make_float4(perm(L0.x), perm(L0.y), perm(L0.z), perm(L0.w));
+        const float4 B1 = make_float4(perm(L1.x), perm(L1.y), perm(L1.z), perm(L1.w));
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           acc[0][g] = mfma4(A[g].x, B0.x, acc[0][g]);
