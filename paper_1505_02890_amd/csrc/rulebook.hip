@@ -255,6 +255,12 @@ __global__ void __launch_bounds__(256) dilate_kernel(const uint32_t* __restrict_
 }
 
 // ---- phase 6: output coordinates and neighbour masks ----------------------
+// One thread per output word; its sites take consecutive ranks.  A block's
+// 256 words hold one contiguous rank range: when it fits OUT_STAGE entries
+// the sites are staged in LDS and written out as one coalesced run (stored
+// straight from the lanes, every store touched up to 64 lines, each only
+// partly); a denser block writes directly.
+constexpr int OUT_STAGE = 1024;
 template <int F, int LAT, bool S1>
 __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restrict__ inb, GridDev gi,
                                                         const uint32_t* __restrict__ outb,
@@ -263,71 +269,90 @@ __global__ void __launch_bounds__(256) out_sites_kernel(const uint32_t* __restri
                                                         int32_t* __restrict__ out_coords,
                                                         uint32_t* __restrict__ masks) {
   using W = Win<F, LAT>;
-  constexpr int K = W::K;
-  const int wo = blockIdx.x * blockDim.x + threadIdx.x;
-  if (wo >= nw_out) return;
-  uint32_t v = outb[wo];
-  if (!v) return;
-  const WordPos wp = word_pos(wo, go);
-  const int x0 = wp.wx * 32;
-  uint32_t rank = opref[wo];
-  if (S1) {
-    // R[r] bit j + kx: input site (x0 + j + kx, y + ky, z + kz) of window row
-    // r = (ky, kz) is active; the row's offsets are consecutive mask bits
-    constexpr int NR = W::FZ * F;
-    uint64_t R[NR];
-#pragma unroll
-    for (int kz = 0; kz < W::FZ; ++kz)
-#pragma unroll
-      for (int ky = 0; ky < F; ++ky) {
-        R[kz * F + ky] = 0;
-        if (W::row_len(ky, kz) <= 0) continue;
-        const int64_t base = row_base(gi, wp.b, wp.y + ky, wp.z + kz);
-        const int64_t w = x0 >> 5;
-        const uint32_t lo = w < gi.rw ? inb[base + w] : 0u;
-        const uint32_t hi = w + 1 < gi.rw ? inb[base + w + 1] : 0u;
-        R[kz * F + ky] = (uint64_t)lo | ((uint64_t)hi << 32);
-      }
-    while (v) {
-      const int j = __builtin_ctz(v);
-      v &= v - 1;
-      uint32_t m = 0;
-      int k = 0;
-#pragma unroll
-      for (int kz = 0; kz < W::FZ; ++kz)
-#pragma unroll
-        for (int ky = 0; ky < F; ++ky) {
-          const int len = W::row_len(ky, kz);
-          if (len <= 0) continue;
-          m |= (uint32_t)((R[kz * F + ky] >> j) & ((1u << len) - 1u)) << k;
-          k += len;
-        }
-      reinterpret_cast<int4*>(out_coords)[rank] = make_int4(wp.b, x0 + j, wp.y, wp.z);
+  __shared__ int4 st_c[OUT_STAGE];
+  __shared__ uint32_t st_m[OUT_STAGE];
+  const int wb0 = blockIdx.x * blockDim.x;
+  const int wb1 = min(nw_out, wb0 + (int)blockDim.x);
+  // opref[nw_out] is the total
+  const uint32_t first = opref[wb0], cnt = opref[wb1] - first;
+  const bool staged = cnt <= (uint32_t)OUT_STAGE;
+  const int wo = wb0 + threadIdx.x;
+  uint32_t v = wo < nw_out ? outb[wo] : 0u;
+  auto put = [&](uint32_t rank, int4 c, uint32_t m) {
+    if (staged) {
+      st_c[rank - first] = c;
+      st_m[rank - first] = m;
+    } else {
+      reinterpret_cast<int4*>(out_coords)[rank] = c;
       masks[rank] = m;
-      ++rank;
     }
-  } else {
-    while (v) {
-      const int j = __builtin_ctz(v);
-      v &= v - 1;
-      const int64_t xi = (int64_t)s * (x0 + j);
-      uint32_t m = 0;
-      int k = 0;
+  };
+  if (v) {
+    const WordPos wp = word_pos(wo, go);
+    const int x0 = wp.wx * 32;
+    uint32_t rank = opref[wo];
+    if (S1) {
+      // R[r] bit j + kx: input site (x0 + j + kx, y + ky, z + kz) of window row
+      // r = (ky, kz) is active; the row's offsets are consecutive mask bits
+      constexpr int NR = W::FZ * F;
+      uint64_t R[NR];
 #pragma unroll
       for (int kz = 0; kz < W::FZ; ++kz)
 #pragma unroll
         for (int ky = 0; ky < F; ++ky) {
+          R[kz * F + ky] = 0;
           if (W::row_len(ky, kz) <= 0) continue;
-          const int64_t base = row_base(gi, wp.b, (int64_t)s * wp.y + ky, (int64_t)s * wp.z + kz);
-          const uint32_t bits = extract32(inb, base, gi.rw, xi);
-#pragma unroll
-          for (int kx = 0; kx < F; ++kx)
-            if (kx < W::row_len(ky, kz)) m |= ((bits >> kx) & 1u) << k++;
+          const int64_t base = row_base(gi, wp.b, wp.y + ky, wp.z + kz);
+          const int64_t w = x0 >> 5;
+          const uint32_t lo = w < gi.rw ? inb[base + w] : 0u;
+          const uint32_t hi = w + 1 < gi.rw ? inb[base + w + 1] : 0u;
+          R[kz * F + ky] = (uint64_t)lo | ((uint64_t)hi << 32);
         }
-      reinterpret_cast<int4*>(out_coords)[rank] = make_int4(wp.b, x0 + j, wp.y, wp.z);
-      masks[rank] = m;
-      ++rank;
+      while (v) {
+        const int j = __builtin_ctz(v);
+        v &= v - 1;
+        uint32_t m = 0;
+        int k = 0;
+#pragma unroll
+        for (int kz = 0; kz < W::FZ; ++kz)
+#pragma unroll
+          for (int ky = 0; ky < F; ++ky) {
+            const int len = W::row_len(ky, kz);
+            if (len <= 0) continue;
+            m |= (uint32_t)((R[kz * F + ky] >> j) & ((1u << len) - 1u)) << k;
+            k += len;
+          }
+        put(rank++, make_int4(wp.b, x0 + j, wp.y, wp.z), m);
+      }
+    } else {
+      while (v) {
+        const int j = __builtin_ctz(v);
+        v &= v - 1;
+        const int64_t xi = (int64_t)s * (x0 + j);
+        uint32_t m = 0;
+        int k = 0;
+#pragma unroll
+        for (int kz = 0; kz < W::FZ; ++kz)
+#pragma unroll
+          for (int ky = 0; ky < F; ++ky) {
+            if (W::row_len(ky, kz) <= 0) continue;
+            const int64_t base =
+                row_base(gi, wp.b, (int64_t)s * wp.y + ky, (int64_t)s * wp.z + kz);
+            const uint32_t bits = extract32(inb, base, gi.rw, xi);
+#pragma unroll
+            for (int kx = 0; kx < F; ++kx)
+              if (kx < W::row_len(ky, kz)) m |= ((bits >> kx) & 1u) << k++;
+          }
+        put(rank++, make_int4(wp.b, x0 + j, wp.y, wp.z), m);
+      }
     }
+  }
+  if (!staged) return;  // block-uniform
+  __syncthreads();
+  int4* oc = reinterpret_cast<int4*>(out_coords) + first;
+  for (uint32_t i = threadIdx.x; i < cnt; i += blockDim.x) {
+    oc[i] = st_c[i];
+    masks[first + i] = st_m[i];
   }
 }
 
@@ -1373,15 +1398,16 @@ struct LayerBuild {
                                          (uint64_t*)rb->otile + ncnt, sc64, st)))
         return rc;
     }
-    // the mask sort (it needs only the masks) beside the neighbour lists
+    // the mask sort (it needs only the masks) beside the neighbour lists: the
+    // second stream waits for the masks here, but the sort's launches are
+    // queued after the main stream's, so the neighbour lists start while the
+    // host still queues the sort
     const bool side_sort = dense && a_out > 0;
-    if (side_sort) {
-      uint32_t* sort_tmp = nullptr;
-      if ((rc = tmp.get(&sort_tmp, sort_bytes / 4)) || (rc = aux_stream(&aux)) ||
-          (rc = fork(st, aux)) ||
-          (rc = radix_sort_pairs(masks, rb->fmask, rb->fperm, a_out, K, sort_tmp, aux->s)))
-        return rc;
-    }
+    uint32_t* sort_tmp = nullptr;
+    if (side_sort &&
+        ((rc = tmp.get(&sort_tmp, sort_bytes / 4)) || (rc = aux_stream(&aux)) ||
+         (rc = fork(st, aux))))
+      return rc;
     if (dense) {
       // start of each output's neighbour list: exclusive sum of mask popcounts
       uint32_t* sc_nb = nullptr;
@@ -1401,7 +1427,10 @@ struct LayerBuild {
       });
       SCN_LAUNCH_CHECK();
     }
-    if (side_sort && (rc = join(st, aux))) return rc;
+    if (side_sort &&
+        ((rc = radix_sort_pairs(masks, rb->fmask, rb->fperm, a_out, K, sort_tmp, aux->s)) ||
+         (rc = join(st, aux))))
+      return rc;
     if (cells) {
       // (also zeroes the homeless count before inv_windows fills it)
       hipLaunchKernelGGL(lower_windows_kernel, dim3(blocks_for(std::max<int64_t>(a_out, 1), 256)),
