@@ -350,6 +350,9 @@ __global__ void __launch_bounds__(256) kd_otile_kernel(const int32_t* __restrict
 
 // Pooling window table: nbr[o*K + k] = caller row of the input at s*o + k
 // (offset k = sum_a k_a f^a) or -1; pmask[o] bit k = that input is active.
+// A window per 32 lanes (lane k < K looks up offset k, K <= 27): the K hash
+// lookups of a window run side by side, its row of the table is one
+// contiguous store, and its mask is a ballot.
 __global__ void __launch_bounds__(256) kd_windows_kernel(const int32_t* __restrict__ out_coords,
                                                          int64_t a_out, KGeo g,
                                                          const uint64_t* __restrict__ hk,
@@ -358,30 +361,28 @@ __global__ void __launch_bounds__(256) kd_windows_kernel(const int32_t* __restri
                                                          const int32_t* __restrict__ perm,
                                                          int32_t* __restrict__ nbr,
                                                          uint32_t* __restrict__ pmask) {
-  const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (o >= a_out) return;
-  const int32_t* c = out_coords + o * (g.D + 1);
-  int32_t oc[KD_MAX] = {0, 0, 0, 0};
-#pragma unroll
-  for (int a = 0; a < KD_MAX; ++a)
-    if (a < g.D) oc[a] = c[1 + a];
-  uint32_t m = 0u;
-  for (int k = 0; k < g.K; ++k) {
+  const int64_t o = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 5;
+  const int k = threadIdx.x & 31;
+  const bool live = o < a_out && k < g.K;
+  int32_t row = -1;
+  if (live) {
+    const int32_t* c = out_coords + o * (g.D + 1);
     int32_t x[KD_MAX] = {0, 0, 0, 0};
 #pragma unroll
     for (int a = 0; a < KD_MAX; ++a)
-      if (a < g.D) x[a] = g.s * oc[a] + (k / g.fpow[a]) % g.f;
+      if (a < g.D) x[a] = g.s * c[1 + a] + (k / g.fpow[a]) % g.f;
     const int32_t rank = h_find(hk, hv, mask, kd_key(c[0], x, g.m, g.D));
-    const int32_t row = rank < 0 ? -1 : (perm ? perm[rank] : rank);
+    row = rank < 0 ? -1 : (perm ? perm[rank] : rank);
     nbr[o * g.K + k] = row;
-    if (row >= 0) m |= 1u << k;
   }
-  pmask[o] = m;
+  const uint64_t bal = __ballot(row >= 0);
+  if (live && k == 0) pmask[o] = (uint32_t)(bal >> (threadIdx.x & 32));
 }
 
 // Each input's windows: slot j (bit a: the window one step down along axis a,
 // used when f > s) of input rank r is window o_a = x_a / s - j_a at offset
-// k_a = x_a - s*o_a < f; inv[row*slots + j] = (output row)*K + k or -1.
+// k_a = x_a - s*o_a < f; inv[row*slots + j] = (output row)*K + k or -1.  A
+// thread per (input, slot), so an input's lookups run side by side.
 __global__ void __launch_bounds__(256) kd_inv_kernel(const int32_t* __restrict__ sb,
                                                      const int4* __restrict__ sx, int64_t n,
                                                      KGeo g, int slots,
@@ -389,30 +390,30 @@ __global__ void __launch_bounds__(256) kd_inv_kernel(const int32_t* __restrict__
                                                      const uint64_t* __restrict__ hk,
                                                      const int32_t* __restrict__ hv, uint64_t mask,
                                                      int32_t* __restrict__ inv) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = i / slots;
+  const int j = (int)(i - r * slots);
   if (r >= n) return;
   const int4 xv = sx[r];
   const int32_t x[KD_MAX] = {xv.x, xv.y, xv.z, xv.w};
   const int64_t row = perm ? perm[r] : r;
-  for (int j = 0; j < slots; ++j) {
-    int32_t o[KD_MAX] = {0, 0, 0, 0};
-    int kidx = 0;
-    bool ok = true;
+  int32_t o[KD_MAX] = {0, 0, 0, 0};
+  int kidx = 0;
+  bool ok = true;
 #pragma unroll
-    for (int a = 0; a < KD_MAX; ++a)
-      if (a < g.D) {
-        o[a] = x[a] / g.s - ((j >> a) & 1);
-        const int32_t ka = x[a] - g.s * o[a];
-        ok = ok && o[a] >= 0 && o[a] < g.mo[a] && ka < g.f;
-        kidx += ka * g.fpow[a];
-      }
-    int32_t v = -1;
-    if (ok) {
-      const int32_t orow = h_find(hk, hv, mask, kd_key(sb[r], o, g.mo, g.D));
-      if (orow >= 0) v = (int32_t)((int64_t)orow * g.K + kidx);
+  for (int a = 0; a < KD_MAX; ++a)
+    if (a < g.D) {
+      o[a] = x[a] / g.s - ((j >> a) & 1);
+      const int32_t ka = x[a] - g.s * o[a];
+      ok = ok && o[a] >= 0 && o[a] < g.mo[a] && ka < g.f;
+      kidx += ka * g.fpow[a];
     }
-    inv[row * slots + j] = v;
+  int32_t v = -1;
+  if (ok) {
+    const int32_t orow = h_find(hk, hv, mask, kd_key(sb[r], o, g.mo, g.D));
+    if (orow >= 0) v = (int32_t)((int64_t)orow * g.K + kidx);
   }
+  inv[row * slots + j] = v;
 }
 
 inline unsigned kd_blocks(int64_t n, int t) {
@@ -775,13 +776,13 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
                      rb->otile);
   SCN_LAUNCH_CHECK();
   if (pool && a_out > 0) {
-    hipLaunchKernelGGL(kd_windows_kernel, dim3(kd_blocks(a_out, 256)), dim3(256), 0, st,
+    hipLaunchKernelGGL(kd_windows_kernel, dim3(kd_blocks(a_out * 32, 256)), dim3(256), 0, st,
                        (const int32_t*)rb->out_coords, a_out, g, (const uint64_t*)hk_in,
                        (const int32_t*)hv_in, cap_in - 1, perm_or_null, rb->nbr, rb->pmask);
     SCN_LAUNCH_CHECK();
   }
   if (pool && n > 0) {
-    hipLaunchKernelGGL(kd_inv_kernel, dim3(kd_blocks(n, 256)), dim3(256), 0, st,
+    hipLaunchKernelGGL(kd_inv_kernel, dim3(kd_blocks(n * slots, 256)), dim3(256), 0, st,
                        (const int32_t*)sb, (const int4*)sx, n, g, slots, perm_or_null,
                        (const uint64_t*)hk_out, (const int32_t*)hv_out, cap_out - 1, rb->inv);
     SCN_LAUNCH_CHECK();
