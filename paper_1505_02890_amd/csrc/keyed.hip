@@ -78,13 +78,22 @@ __device__ inline uint64_t kd_key(int64_t b, const int32_t (&x)[KD_MAX], const i
   return k;
 }
 
+// A slot of a hash table: the key (HK_EMPTY when free) and the rank stored
+// with it, side by side, so a probe that finds its key reads one 16-byte
+// piece of memory.
+struct alignas(16) HSlot {
+  uint64_t key;
+  int32_t val;
+  int32_t pad;
+};
+
 // The rank stored with key k, or -1 when k is absent.  The table is at most
 // half full, so the probe meets an empty slot.
-__device__ inline int32_t h_find(const uint64_t* __restrict__ hk, const int32_t* __restrict__ hv,
-                                 uint64_t mask, uint64_t k) {
+__device__ inline int32_t h_find(const HSlot* __restrict__ h, uint64_t mask, uint64_t k) {
   for (uint64_t i = hmix(k) & mask;; i = (i + 1) & mask) {
-    const uint64_t t = hk[i];
-    if (t == k) return hv[i];
+    const uint4 v = *reinterpret_cast<const uint4*>(h + i);
+    const uint64_t t = ((uint64_t)v.y << 32) | v.x;
+    if (t == k) return (int32_t)v.z;
     if (t == HK_EMPTY) return -1;
   }
 }
@@ -166,16 +175,16 @@ __global__ void __launch_bounds__(256) kd_ranked_kernel(const int32_t* __restric
 
 // H_in: key -> rank, one thread per rank
 __global__ void __launch_bounds__(256) kd_insert_kernel(const uint64_t* __restrict__ skeys,
-                                                        int64_t n, uint64_t* __restrict__ hk,
-                                                        int32_t* __restrict__ hv, uint64_t mask) {
+                                                        int64_t n, HSlot* __restrict__ h,
+                                                        uint64_t mask) {
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= n) return;
   const uint64_t k = skeys[r];
   for (uint64_t i = hmix(k) & mask;; i = (i + 1) & mask) {
-    const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(hk + i),
+    const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(&h[i].key),
                                     (unsigned long long)HK_EMPTY, (unsigned long long)k);
     if (prev == HK_EMPTY || prev == k) {
-      hv[i] = (int32_t)r;
+      h[i].val = (int32_t)r;
       return;
     }
   }
@@ -190,7 +199,7 @@ __global__ void __launch_bounds__(256) kd_insert_kernel(const uint64_t* __restri
 // it empty, and the atomicCAS then decides.
 __global__ void __launch_bounds__(64) kd_candidates_kernel(
     const int32_t* __restrict__ sb, const int4* __restrict__ sx, int64_t n, KGeo g, int64_t nit,
-    uint64_t* __restrict__ hk, uint64_t mask, uint64_t* __restrict__ cnt,
+    HSlot* __restrict__ h, uint64_t mask, uint64_t* __restrict__ cnt,
     uint32_t* __restrict__ full) {
   const int64_t r = (int64_t)blockIdx.x * 64 + threadIdx.x;
   const int k = blockIdx.y;
@@ -200,13 +209,13 @@ __global__ void __launch_bounds__(64) kd_candidates_kernel(
   if (valid) {
     uint64_t i = hmix(key) & mask;
     for (int t = 0; t < KD_PROBES; ++t, i = (i + 1) & mask) {
-      const uint64_t cur = hk[i];
+      const uint64_t cur = h[i].key;
       if (cur == key) {
         placed = true;
         break;
       }
       if (cur != HK_EMPTY) continue;
-      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(hk + i),
+      const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long*>(&h[i].key),
                                       (unsigned long long)HK_EMPTY, (unsigned long long)key);
       if (prev == HK_EMPTY || prev == key) {
         placed = true;
@@ -223,13 +232,13 @@ __global__ void __launch_bounds__(64) kd_candidates_kernel(
 }
 
 // Occupied slots of the output table per chunk of SCAN_BLOCK slots
-__global__ void __launch_bounds__(SCAN_THREADS) kd_occupied_kernel(const uint64_t* __restrict__ hk,
+__global__ void __launch_bounds__(SCAN_THREADS) kd_occupied_kernel(const HSlot* __restrict__ h,
                                                                    uint64_t cap,
                                                                    uint32_t* __restrict__ bcnt) {
   const uint64_t base = (uint64_t)blockIdx.x * SCAN_BLOCK;
   uint32_t c = 0;
   for (int j = threadIdx.x; j < SCAN_BLOCK; j += SCAN_THREADS)
-    c += (base + j < cap && hk[base + j] != HK_EMPTY) ? 1u : 0u;
+    c += (base + j < cap && h[base + j].key != HK_EMPTY) ? 1u : 0u;
   uint32_t all;
   block_exclusive_scan<uint32_t>(c, &all);
   if (threadIdx.x == 0) bcnt[blockIdx.x] = all;
@@ -237,7 +246,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) kd_occupied_kernel(const uint64_
 
 // The occupied slots' keys to list[], in slot order: chunk b starts at
 // bpre[b]; inside it, ballots place the wave's keys
-__global__ void __launch_bounds__(SCAN_THREADS) kd_compact_kernel(const uint64_t* __restrict__ hk,
+__global__ void __launch_bounds__(SCAN_THREADS) kd_compact_kernel(const HSlot* __restrict__ h,
                                                                   uint64_t cap,
                                                                   const uint32_t* __restrict__ bpre,
                                                                   uint64_t* __restrict__ list) {
@@ -247,7 +256,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) kd_compact_kernel(const uint64_t
   uint32_t out = bpre[blockIdx.x];
   for (int j0 = 0; j0 < SCAN_BLOCK; j0 += SCAN_THREADS) {
     const uint64_t i = base + j0 + threadIdx.x;
-    const uint64_t key = i < cap ? hk[i] : HK_EMPTY;
+    const uint64_t key = i < cap ? h[i].key : HK_EMPTY;
     const bool occ = key != HK_EMPTY;
     const uint64_t bal = __ballot(occ);
     if (lane == 0) wsum[w] = (uint32_t)__popcll(bal);
@@ -270,15 +279,14 @@ __global__ void __launch_bounds__(SCAN_THREADS) kd_compact_kernel(const uint64_t
 // rank i of the sorted output keys: its row into H_out and its coordinates
 __global__ void __launch_bounds__(256) kd_assign_kernel(const uint64_t* __restrict__ okeys,
                                                         int64_t a_out, KGeo g,
-                                                        const uint64_t* __restrict__ hk,
-                                                        int32_t* __restrict__ hv, uint64_t mask,
+                                                        HSlot* __restrict__ h, uint64_t mask,
                                                         int32_t* __restrict__ out_coords) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a_out) return;
   uint64_t key = okeys[i];
   for (uint64_t j = hmix(key) & mask;; j = (j + 1) & mask)
-    if (hk[j] == key) {
-      hv[j] = (int32_t)i;
+    if (h[j].key == key) {
+      h[j].val = (int32_t)i;
       break;
     }
   int32_t* c = out_coords + i * (g.D + 1);
@@ -297,7 +305,7 @@ __global__ void __launch_bounds__(256) kd_assign_kernel(const uint64_t* __restri
 __global__ void __launch_bounds__(64) kd_emit_kernel(
     const int32_t* __restrict__ sb, const int4* __restrict__ sx, int64_t n, KGeo g, int64_t nit,
     const uint64_t* __restrict__ itile, const int32_t* __restrict__ perm,
-    const uint64_t* __restrict__ hk, const int32_t* __restrict__ hv, uint64_t mask,
+    const HSlot* __restrict__ h, uint64_t mask,
     int32_t* __restrict__ in_rows, int32_t* __restrict__ out_rows,
     int32_t* __restrict__ in_rank) {
   const int64_t r = (int64_t)blockIdx.x * 64 + threadIdx.x;
@@ -310,7 +318,7 @@ __global__ void __launch_bounds__(64) kd_emit_kernel(
                        __builtin_amdgcn_mbcnt_hi((uint32_t)(vb >> 32),
                                                  __builtin_amdgcn_mbcnt_lo((uint32_t)vb, 0u));
   in_rows[pos] = perm ? perm[r] : (int32_t)r;
-  out_rows[pos] = h_find(hk, hv, mask, key);
+  out_rows[pos] = h_find(h, mask, key);
   if (in_rank) in_rank[pos] = (int32_t)r;
 }
 
@@ -355,8 +363,7 @@ __global__ void __launch_bounds__(256) kd_otile_kernel(const int32_t* __restrict
 // contiguous store, and its mask is a ballot.
 __global__ void __launch_bounds__(256) kd_windows_kernel(const int32_t* __restrict__ out_coords,
                                                          int64_t a_out, KGeo g,
-                                                         const uint64_t* __restrict__ hk,
-                                                         const int32_t* __restrict__ hv,
+                                                         const HSlot* __restrict__ h,
                                                          uint64_t mask,
                                                          const int32_t* __restrict__ perm,
                                                          int32_t* __restrict__ nbr,
@@ -371,7 +378,7 @@ __global__ void __launch_bounds__(256) kd_windows_kernel(const int32_t* __restri
 #pragma unroll
     for (int a = 0; a < KD_MAX; ++a)
       if (a < g.D) x[a] = g.s * c[1 + a] + (k / g.fpow[a]) % g.f;
-    const int32_t rank = h_find(hk, hv, mask, kd_key(c[0], x, g.m, g.D));
+    const int32_t rank = h_find(h, mask, kd_key(c[0], x, g.m, g.D));
     row = rank < 0 ? -1 : (perm ? perm[rank] : rank);
     nbr[o * g.K + k] = row;
   }
@@ -387,8 +394,7 @@ __global__ void __launch_bounds__(256) kd_inv_kernel(const int32_t* __restrict__
                                                      const int4* __restrict__ sx, int64_t n,
                                                      KGeo g, int slots,
                                                      const int32_t* __restrict__ perm,
-                                                     const uint64_t* __restrict__ hk,
-                                                     const int32_t* __restrict__ hv, uint64_t mask,
+                                                     const HSlot* __restrict__ h, uint64_t mask,
                                                      int32_t* __restrict__ inv) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t r = i / slots;
@@ -410,7 +416,7 @@ __global__ void __launch_bounds__(256) kd_inv_kernel(const int32_t* __restrict__
     }
   int32_t v = -1;
   if (ok) {
-    const int32_t orow = h_find(hk, hv, mask, kd_key(sb[r], o, g.mo, g.D));
+    const int32_t orow = h_find(h, mask, kd_key(sb[r], o, g.mo, g.D));
     if (orow >= 0) v = (int32_t)((int64_t)orow * g.K + kidx);
   }
   inv[row * slots + j] = v;
@@ -560,9 +566,10 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   uint64_t cap_out = std::min(cap_full, pow2_at_least(2 * std::min<uint64_t>(
                                             ucap, 8 * (uint64_t)std::max<int64_t>(n, 1))));
   const int64_t nit = std::max<int64_t>(1, ceil_div(n, TILE));
-  uint64_t *keys = nullptr, *skeys = nullptr, *hk_in = nullptr, *hk_out = nullptr,
+  HSlot *h_in = nullptr, *h_out = nullptr;
+  uint64_t *keys = nullptr, *skeys = nullptr,
            *list = nullptr, *cnt = nullptr, *scan_tmp = nullptr;
-  int32_t *hv_in = nullptr, *hv_out = nullptr, *sb = nullptr;
+  int32_t* sb = nullptr;
   int4* sx = nullptr;
   uint32_t *flags = nullptr, *sort_tmp = nullptr, *bcnt = nullptr, *bpre = nullptr,
            *bscan = nullptr;
@@ -570,8 +577,8 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   unsigned long long* aout_dev = nullptr;
   const int bits_in = bits_for(sites_in);
   if ((rc = tmp.get(&keys, n)) || (rc = tmp.get(&skeys, n)) || (rc = tmp.get(&sb, n)) ||
-      (rc = tmp.get(&sx, n)) || (rc = tmp.get(&hk_in, (int64_t)cap_in)) ||
-      (rc = tmp.get(&hv_in, (int64_t)cap_in)) || (rc = tmp.get(&list, (int64_t)ucap)) ||
+      (rc = tmp.get(&sx, n)) || (rc = tmp.get(&h_in, (int64_t)cap_in)) ||
+      (rc = tmp.get(&list, (int64_t)ucap)) ||
       (rc = tmp.get(&flags, 64)) || (rc = tmp.get(&off_tmp, MAX_K + 1)) ||
       (rc = tmp.get(&aout_dev, 1)) || (rc = tmp.get(&cnt, K * nit)) ||
       (rc = tmp.get(&scan_tmp, scan_blocks(K * nit))) ||
@@ -595,7 +602,7 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   } in_guard{in_block, st, mem};
 
   SCN_HIP(hipMemsetAsync(flags, 0, 8, st));
-  SCN_HIP(hipMemsetAsync(hk_in, 0xFF, cap_in * 8, st));
+  SCN_HIP(hipMemsetAsync(h_in, 0xFF, cap_in * sizeof(HSlot), st));
   if (n > 0) {
     hipLaunchKernelGGL(kd_keys_kernel, dim3(kd_blocks(n, 256)), dim3(256), 0, st, coords, n, g,
                        keys, flags);
@@ -605,7 +612,7 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
                        (const uint64_t*)skeys, (const int32_t*)perm, n, g, sb, sx, flags);
     SCN_LAUNCH_CHECK();
     hipLaunchKernelGGL(kd_insert_kernel, dim3(kd_blocks(n, 256)), dim3(256), 0, st,
-                       (const uint64_t*)skeys, n, hk_in, hv_in, cap_in - 1);
+                       (const uint64_t*)skeys, n, h_in, cap_in - 1);
     SCN_LAUNCH_CHECK();
   } else {
     SCN_HIP(hipMemsetAsync(cnt, 0, K * nit * 8, st));
@@ -616,15 +623,14 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   auto outputs = [&]() -> scn_status {
     scn_status rc2;
     const int64_t nb = (int64_t)ceil_div((int64_t)cap_out, SCAN_BLOCK);
-    if ((rc2 = tmp.get(&hk_out, (int64_t)cap_out)) ||
-        (rc2 = tmp.get(&hv_out, (int64_t)cap_out)) || (rc2 = tmp.get(&bcnt, nb)) ||
+    if ((rc2 = tmp.get(&h_out, (int64_t)cap_out)) || (rc2 = tmp.get(&bcnt, nb)) ||
         (rc2 = tmp.get(&bpre, nb + 1)) || (rc2 = tmp.get(&bscan, scan_blocks(nb))))
       return rc2;
     SCN_HIP(hipMemsetAsync(flags + 1, 0, 4, st));
-    SCN_HIP(hipMemsetAsync(hk_out, 0xFF, cap_out * 8, st));
+    SCN_HIP(hipMemsetAsync(h_out, 0xFF, cap_out * sizeof(HSlot), st));
     if (n > 0) {
       hipLaunchKernelGGL(kd_candidates_kernel, dim3((unsigned)nit, (unsigned)K), dim3(64), 0, st,
-                         (const int32_t*)sb, (const int4*)sx, n, g, nit, hk_out, cap_out - 1, cnt,
+                         (const int32_t*)sb, (const int4*)sx, n, g, nit, h_out, cap_out - 1, cnt,
                          flags + 1);
       SCN_LAUNCH_CHECK();
     }
@@ -635,13 +641,13 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
                        (int)K, off_tmp);
     SCN_LAUNCH_CHECK();
     hipLaunchKernelGGL(kd_occupied_kernel, dim3((unsigned)nb), dim3(SCAN_THREADS), 0, st,
-                       (const uint64_t*)hk_out, cap_out, bcnt);
+                       (const HSlot*)h_out, cap_out, bcnt);
     SCN_LAUNCH_CHECK();
     if ((rc2 = exclusive_scan<uint32_t>(PlainLoad<uint32_t>{bcnt}, nb, bpre, bpre + nb, bscan,
                                         st)))
       return rc2;
     hipLaunchKernelGGL(kd_compact_kernel, dim3((unsigned)nb), dim3(SCAN_THREADS), 0, st,
-                       (const uint64_t*)hk_out, cap_out, (const uint32_t*)bpre, list);
+                       (const HSlot*)h_out, cap_out, (const uint32_t*)bpre, list);
     SCN_LAUNCH_CHECK();
     hipLaunchKernelGGL(kd_total_kernel, dim3(1), dim3(1), 0, st, (const uint32_t*)bpre, nb,
                        (const uint32_t*)bcnt, aout_dev);
@@ -760,14 +766,14 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
     if ((rc = radix_sort_pairs<uint64_t>(list, okeys, oval, a_out, bits_out, sort_tmp2, st)))
       return rc;
     hipLaunchKernelGGL(kd_assign_kernel, dim3(kd_blocks(a_out, 256)), dim3(256), 0, st,
-                       (const uint64_t*)okeys, a_out, g, (const uint64_t*)hk_out, hv_out,
+                       (const uint64_t*)okeys, a_out, g, h_out,
                        cap_out - 1, rb->out_coords);
     SCN_LAUNCH_CHECK();
   }
   if (n > 0 && P > 0) {
     hipLaunchKernelGGL(kd_emit_kernel, dim3((unsigned)nit, (unsigned)K), dim3(64), 0, st,
                        (const int32_t*)sb, (const int4*)sx, n, g, nit, (const uint64_t*)itile,
-                       perm_or_null, (const uint64_t*)hk_out, (const int32_t*)hv_out,
+                       perm_or_null, (const HSlot*)h_out,
                        cap_out - 1, rb->in_rows, rb->out_rows, sorted ? nullptr : in_rank_arr);
     SCN_LAUNCH_CHECK();
   }
@@ -777,14 +783,14 @@ scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* g
   SCN_LAUNCH_CHECK();
   if (pool && a_out > 0) {
     hipLaunchKernelGGL(kd_windows_kernel, dim3(kd_blocks(a_out * 32, 256)), dim3(256), 0, st,
-                       (const int32_t*)rb->out_coords, a_out, g, (const uint64_t*)hk_in,
-                       (const int32_t*)hv_in, cap_in - 1, perm_or_null, rb->nbr, rb->pmask);
+                       (const int32_t*)rb->out_coords, a_out, g, (const HSlot*)h_in,
+                       cap_in - 1, perm_or_null, rb->nbr, rb->pmask);
     SCN_LAUNCH_CHECK();
   }
   if (pool && n > 0) {
     hipLaunchKernelGGL(kd_inv_kernel, dim3(kd_blocks(n * slots, 256)), dim3(256), 0, st,
                        (const int32_t*)sb, (const int4*)sx, n, g, slots, perm_or_null,
-                       (const uint64_t*)hk_out, (const int32_t*)hv_out, cap_out - 1, rb->inv);
+                       (const HSlot*)h_out, cap_out - 1, rb->inv);
     SCN_LAUNCH_CHECK();
   }
   SCN_HIP(hipEventCreateWithFlags(&rb->done, hipEventDisableTiming));
