@@ -397,7 +397,7 @@ void scn_set_allocator(void* (*alloc)(size_t bytes, hipStream_t stream, void* ct
  * pays back when the layer is large and has many offsets.  A stride-1
  * rulebook built after this call carries the view when it has at least
  * min_rows output rows and at least min_offsets offsets (K).  Defaults:
- * min_rows = 1048576, min_offsets = 9 (set with negative arguments).
+ * min_rows = 524288, min_offsets = 8 (set with negative arguments).
  * Process-wide.  Results agree with the pair-list forward to rounding (each
  * output sums its active offsets in ascending order either way).
  * Errors: none (always SCN_OK).

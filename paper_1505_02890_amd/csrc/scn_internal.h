@@ -22,8 +22,8 @@ constexpr int DENSE_ROWS = 32;  // output rows per block of the dense forward vi
 // rulebooks with at least this many output rows and offsets.  Below them the
 // view's sort and extra launches cost more than the forward saves (measured
 // on the paper's networks, whose 2x2x2 layers never gain).
-constexpr int64_t DENSE_MIN_ROWS = int64_t(1) << 20;
-constexpr int DENSE_MIN_K = 9;
+constexpr int64_t DENSE_MIN_ROWS = int64_t(1) << 19;
+constexpr int DENSE_MIN_K = 8;
 
 void set_error(const char* fmt, ...);
 void clear_error();
