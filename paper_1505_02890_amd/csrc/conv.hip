@@ -201,7 +201,7 @@ __device__ inline WFrag<NKT> load_w(const GatherArgs& a, int k, int cb, int w, i
 template <int NKT>
 struct StageRegs {
   static constexpr int NQ = (4 * NKT + 7) / 8;  // float4 per thread
-  float4 v[NQ];
+  v4f v[NQ];  // (arrays of HIP's float4 struct were left in scratch memory)
   int acc_row;
 };
 
@@ -215,12 +215,10 @@ __device__ inline StageRegs<NKT> load_stage(const GatherArgs& a, int gi, int ai,
     const int c = 4 * (part + 8 * u);
     if (VEC) {
       const int cc = c < a.Rk ? c : 0;
-      R.v[u] = *reinterpret_cast<const float4*>(rp + cc);
+      R.v[u] = *reinterpret_cast<const v4f*>(rp + cc);
     } else {
-      float e[4];
 #pragma unroll
-      for (int z = 0; z < 4; ++z) e[z] = rp[c + z < a.Rk ? c + z : 0];
-      R.v[u] = make_float4(e[0], e[1], e[2], e[3]);
+      for (int z = 0; z < 4; ++z) R.v[u][z] = rp[c + z < a.Rk ? c + z : 0];
     }
   }
   R.acc_row = ai;
@@ -234,7 +232,7 @@ __device__ inline void store_stage(float* xs, int tid, const StageRegs<NKT>& R) 
 #pragma unroll
   for (int u = 0; u < StageRegs<NKT>::NQ; ++u) {
     const int quad = part + 8 * u;
-    if (quad < 4 * NKT) *reinterpret_cast<float4*>(xs + row * XLD + 4 * quad) = R.v[u];
+    if (quad < 4 * NKT) *reinterpret_cast<v4f*>(xs + row * XLD + 4 * quad) = R.v[u];
   }
   reinterpret_cast<int*>(xs)[row * XLD + 16 * NKT] = R.acc_row;  // same value from all 8
 }
@@ -487,17 +485,18 @@ __global__ void __launch_bounds__(NT, MINB) gather_mfma_kernel(GatherArgs a) {
 typedef void (*GatherFn)(GatherArgs);
 
 // Tile rows (TM * 64) and work-groups per CU: the accumulators and the two
-// stage buffers must fit the 160 KB of LDS.  Reductions over up to 64
-// channels use 128-row tiles (several work-groups per CU hide the gather
-// latency); longer reductions use 256-row tiles, one work-group per CU.
+// stage buffers must fit the 160 KB of LDS.  Reductions over up to 160
+// channels use 128-row tiles, three work-groups per CU up to 64 channels and
+// two past that (several work-groups per CU hide the gather latency); longer
+// reductions use 256-row tiles, one work-group per CU.
 template <int NKT>
 constexpr int gather_tm() {
-  return NKT > 4 ? 4 : 2;
+  return NKT > 10 ? 4 : 2;
 }
 
 template <int NKT>
 GatherFn pick_gather(bool vec) {
-  constexpr int TM = gather_tm<NKT>(), MINB = NKT > 4 ? 1 : 3;
+  constexpr int TM = gather_tm<NKT>(), MINB = NKT > 10 ? 1 : (NKT > 4 ? 2 : 3);
   return vec ? gather_mfma_kernel<NKT, true, TM, MINB> : gather_mfma_kernel<NKT, false, TM, MINB>;
 }
 
@@ -528,7 +527,7 @@ scn_status launch_gather(GatherArgs a, hipStream_t st) {
 
   a.dvec_ok = ((a.Nc & 3) == 0) && ((reinterpret_cast<uintptr_t>(a.dst) & 15) == 0);
   const int nkt = (int)ceil_div(a.Rk, 16);
-  const int TM = nkt > 4 ? gather_tm<5>() : gather_tm<1>();
+  const int TM = nkt > 10 ? gather_tm<11>() : gather_tm<1>();
   const int64_t nwg = ceil_div(a.ntile, TM);
   const unsigned ncb = (unsigned)ceil_div(a.Nc, CB);
   const size_t smem =
