@@ -5,7 +5,8 @@ four 64-channel chunks (including last chunks of a single 16-channel step:
 Cin = 80, 136, 200), several 64-column blocks, ragged last blocks, ReLU on and
 off, sorted and shuffled inputs.  The same layers with the view switched off
 (the per-offset pair-list forward) also match the oracle and give the same
-rulebook; repeated calls are bitwise identical."""
+rulebook; repeated calls are bitwise identical.  Single-channel layers with
+the view (a network's first layer) are checked forward and backward."""
 from __future__ import annotations
 
 import math
@@ -18,7 +19,7 @@ torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 from gen import random_sites, stream_rng, tetra_random_sites, tri_random_sites  # noqa: E402
 
-from helpers import assert_site, dev, host  # noqa: E402
+from helpers import assert_site, conv_parity, dev, host  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -68,6 +69,12 @@ CASES = [
     ("cubic", 2, 1, 16, 1000, 136, 64, False, True),
     ("cubic", 3, 1, 14, 600, 200, 48, True, True),
     ("tetrahedral", 3, 1, 24, 1500, 80, 72, False, True),
+    # one input channel: odd and wide column counts, every lattice's window
+    ("cubic", 2, 2, 20, 1800, 1, 7, False, True),
+    ("cubic", 3, 1, 20, 1500, 1, 130, True, False),
+    ("tetrahedral", 3, 1, 24, 1500, 1, 33, True, True),
+    ("square", 3, 2, 50, 2000, 1, 64, False, True),
+    ("triangular", 2, 1, 40, 600, 1, 256, True, True),
 ]
 
 
@@ -142,3 +149,32 @@ def test_dense_empty_and_strided(scn):
     y_ref, _ = oracle.conv_fwd(o, x, g_in, W, None)
     yd, _ = scn.conv_fwd(g, dev(x), dev(g_in), dev(W), None)
     assert_site("y strided", host(yd), y_ref)
+
+
+# single-channel layers with the view, forward and backward, across column
+# counts (odd, under and over 64) and lattices
+C1_CASES = [
+    ("cubic", 3, 1, 22, 1500, 64, True, True),
+    ("cubic", 2, 2, 18, 1600, 7, False, True),
+    ("tetrahedral", 3, 1, 24, 1500, 33, True, True),
+    ("square", 3, 2, 40, 1500, 64, False, False),
+    ("triangular", 3, 1, 50, 900, 20, True, True),
+    ("cubic", 3, 1, 20, 1200, 96, True, True),
+]
+
+
+@pytest.mark.parametrize("case", C1_CASES, ids=[f"{c[0]}{i}" for i, c in enumerate(C1_CASES)])
+def test_single_channel_fwd_bwd(scn, case):
+    lattice, f, B, m, n, Cout, relu, shuffle = case
+    i = C1_CASES.index(case)
+    rng = stream_rng(175, i)
+    coords, grid = _sites(lattice, rng, B, m, n, shuffle)
+    K = _K(lattice, f)
+    x = rng.standard_normal((len(coords), 1)).astype(np.float32)
+    g_in = (rng.standard_normal(1) * 0.5).astype(np.float32)
+    W = (rng.standard_normal((K, 1, Cout)) / np.sqrt(K)).astype(np.float32)
+    bias = (rng.standard_normal(Cout) * 0.1).astype(np.float32)
+    g = scn.build_rulebook(dev(coords), grid, f, 1, lattice=lattice)
+    o = oracle.Rulebook(coords, grid, f, 1, lattice=lattice)
+    assert g.dense_view
+    conv_parity(scn, g, o, x, g_in, W, bias, relu, 300 + i)
