@@ -115,13 +115,17 @@ __device__ inline bool kd_out_site(int32_t b, int4 xv, int k, const KGeo& g, uin
   return ok;
 }
 
-// wave-wide OR of f, one atomic per wave
+// wave-wide OR of f, at most one atomic per wave: the word is read first, so
+// the waves of an unsorted list (each of which raises the same flag) do not
+// all queue atomics on one address
 __device__ inline void flag_or(uint32_t* flags, uint32_t f) {
   uint32_t all = 0;
 #pragma unroll
   for (int bit = 0; bit < 3; ++bit)
     if (__ballot((f >> bit) & 1u)) all |= 1u << bit;
-  if (all && (threadIdx.x & 63) == 0) atomicOr(flags, all);
+  if (all && (threadIdx.x & 63) == 0 &&
+      (__hip_atomic_load(flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & all) != all)
+    atomicOr(flags, all);
 }
 
 // one thread per site in caller order: its key and the range check
