@@ -476,23 +476,59 @@ __global__ void __launch_bounds__(256) maxpool_bwd_ground_kernel(const uint32_t*
   }
 }
 
-// dg_in[c] = dg_out[c] + sum_b part[b][c]; one block per channel, each thread
-// a strided share of the blocks, then a fixed-shape tree
-__global__ void __launch_bounds__(256) maxpool_bwd_ground_finish(const float* __restrict__ part,
-                                                                 int64_t nblk, int C,
+// The ground-state sums dg_in[c] = dg_out[c] + sum_b part[b][c], in two
+// passes of fixed shape.  First GF_BLOCKS work-groups each add a contiguous
+// range of part's rows: rg = 256 / C row groups of C lanes, so a wave reads
+// whole rows (one work-group per channel took 22 us for 15k rows of 64
+// channels: every load touched 64 lines); the row groups' sums are added in
+// order.  Then each work-group of the second pass takes 64 channels: four
+// row groups of 64 lanes add every fourth of the GF_BLOCKS partial rows, and
+// their sums are added in order.
+constexpr int GF_BLOCKS = 256;
+__global__ void __launch_bounds__(256) maxpool_ground_rows_kernel(const float* __restrict__ part,
+                                                                  int64_t nblk, int C,
+                                                                  float* __restrict__ part2) {
+  __shared__ float red[256];
+  const int64_t per = (nblk + GF_BLOCKS - 1) / GF_BLOCKS;
+  const int64_t b0 = (int64_t)blockIdx.x * per, b1 = min<int64_t>(nblk, b0 + per);
+  if (C <= 256) {
+    const int rg_n = 256 / C, rg = threadIdx.x / C, c = threadIdx.x - rg * C;
+    float s = 0.f;
+    if (rg < rg_n) {
+#pragma unroll 4
+      for (int64_t b = b0 + rg; b < b1; b += rg_n) s += part[b * C + c];
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    if (rg == 0) {
+      for (int g = 1; g < rg_n; ++g) s += red[g * C + c];
+      part2[(int64_t)blockIdx.x * C + c] = s;
+    }
+  } else {
+    for (int c = threadIdx.x; c < C; c += 256) {
+      float s = 0.f;
+      for (int64_t b = b0; b < b1; ++b) s += part[b * C + c];
+      part2[(int64_t)blockIdx.x * C + c] = s;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) maxpool_bwd_ground_finish(const float* __restrict__ part2,
+                                                                 int C,
                                                                  const float* __restrict__ dg_out,
                                                                  float* __restrict__ dg_in) {
   __shared__ float red[256];
-  const int c = blockIdx.x;
+  const int rg = threadIdx.x >> 6, c = blockIdx.x * 64 + (threadIdx.x & 63);
   float s = 0.f;
-  for (int64_t b = threadIdx.x; b < nblk; b += 256) s += part[b * C + c];
+  if (c < C) {
+#pragma unroll 8
+    for (int g = rg; g < GF_BLOCKS; g += 4) s += part2[(int64_t)g * C + c];
+  }
   red[threadIdx.x] = s;
   __syncthreads();
-  for (int h = 128; h > 0; h >>= 1) {
-    if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) dg_in[c] = (dg_out ? dg_out[c] : 0.f) + red[0];
+  if (rg == 0 && c < C)
+    dg_in[c] = (dg_out ? dg_out[c] : 0.f) + (((s + red[64 + threadIdx.x]) + red[128 + threadIdx.x]) +
+                                             red[192 + threadIdx.x]);
 }
 
 inline unsigned nblocks(int64_t n, int t) { return (unsigned)std::max<int64_t>(1, ceil_div(n, t)); }
@@ -531,6 +567,13 @@ inline bool pool_vec_ok(int C, std::initializer_list<const void*> rows, const vo
 }
 
 
+
+// floats of the per-block ground-state partial sums, rounded to 16 bytes;
+// enough for every path (the four-channel path uses PBV_ROWS-output blocks)
+inline size_t part_floats(const scn_rulebook* rb, int C) {
+  const int64_t rows = C % 4 == 0 ? PBV_ROWS : PB_ROWS;
+  return ((size_t)std::max<int64_t>(1, ceil_div(rb->a_out, rows)) * C + 3) & ~size_t(3);
+}
 
 }  // namespace
 }  // namespace scn
@@ -583,10 +626,8 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
 
 size_t scn_maxpool_bwd_workspace_bytes(const scn_rulebook* rb, int32_t C) {
   if (!rb || C < 1) return 0;
-  // enough for either path (the four-channel path uses 256-output blocks)
-  const int64_t rows = C % 4 == 0 ? PBV_ROWS : PB_ROWS;
-  return ((size_t)std::max<int64_t>(1, ceil_div(rb->a_out, rows)) * C * sizeof(float) + 15) &
-         ~size_t(15);
+  // the per-block partial sums, then the GF_BLOCKS partial rows
+  return (part_floats(rb, C) + (size_t)GF_BLOCKS * C) * sizeof(float);
 }
 
 scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const float* dy,
@@ -706,8 +747,12 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
     }
   }
   if (dg_in) {
-    hipLaunchKernelGGL(maxpool_bwd_ground_finish, dim3((unsigned)C), dim3(256), 0, st, part,
-                       rb->a_out > 0 ? nblk : 0, C, dg_out, dg_in);
+    float* part2 = part + part_floats(rb, C);
+    hipLaunchKernelGGL(maxpool_ground_rows_kernel, dim3(GF_BLOCKS), dim3(256), 0, st, part,
+                       rb->a_out > 0 ? nblk : 0, C, part2);
+    SCN_LAUNCH_CHECK();
+    hipLaunchKernelGGL(maxpool_bwd_ground_finish, dim3(nblocks(C, 64)), dim3(256), 0, st, part2,
+                       C, dg_out, dg_in);
     SCN_LAUNCH_CHECK();
   }
   return SCN_OK;
