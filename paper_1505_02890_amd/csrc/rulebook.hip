@@ -971,11 +971,12 @@ scn_status join(hipStream_t st, AuxStream* a) {
 //   check()   host only: arguments, output grid, bitmap sizes;
 //   phase1()  device: mark the caller's sites (first layer only), rank them,
 //             the input side (rank -> row, pair counts per tile of input
-//             ranks), dilate, rank the outputs, emit the pair lists; queues
-//             the copy of the flags, totals and list boundaries to the
-//             layer's read-back slot;
-//   sized()   after the host has waited for that copy: errors, a_out, the
-//             rest of the rulebook's storage;
+//             ranks), dilate, rank the outputs; queues the copy of the
+//             flags, totals and list boundaries to the layer's read-back
+//             slot, then the pair lists;
+//   sized()   after the host has waited for that copy (a single build waits
+//             for the copy alone, so the pair lists run meanwhile): errors,
+//             a_out, the rest of the rulebook's storage;
 //   phase2()  device: output sites and masks, per-tile pair ranges, the
 //             output-major tables (window table of a pooling rulebook, or the
 //             dense forward view and its mask sort), pooling windows;
@@ -998,6 +999,7 @@ struct LayerBuild {
   const uint32_t* prev_bits = nullptr;
   const uint32_t* prev_rank = nullptr;
   Readback* hb = nullptr;
+  hipEvent_t ready = nullptr;  // when set: recorded once the first read-back has landed
   // derived
   bool planar = false, simplex = false;
   int K = 0;
@@ -1246,13 +1248,17 @@ struct LayerBuild {
     if ((rc = exclusive_scan<uint32_t>(PopcountLoad{hout.bits}, nw_out, hout.rank,
                                        hout.rank + nw_out, sc32, st)))
       return rc;
-    if (in_early && ((rc = join(st, aux)) || (rc = emit_lists()))) return rc;
-    // flags, both totals and (lists emitted) the list boundaries in one read-back
+    if (in_early && (rc = join(st, aux))) return rc;
+    // flags, both totals and (input side known) the list boundaries in one
+    // read-back; the lists are emitted after it, so a host that waits for
+    // `ready` (not for the stream) sizes the rest of the build while they run
     hipLaunchKernelGGL(pack_totals_kernel, dim3(1), dim3(64), 0, st, flags, ipref + nw_in,
                        hout.rank + nw_out, in_early ? (const int64_t*)itile : nullptr, nit, K,
                        drb->off, off_dev);
     SCN_LAUNCH_CHECK();
     SCN_HIP(hipMemcpyAsync(hb, drb, sizeof(Readback), hipMemcpyDeviceToHost, st));
+    if (ready) SCN_HIP(hipEventRecord(ready, st));
+    if (in_early && (rc = emit_lists())) return rc;
     return SCN_OK;
   }
 
@@ -1514,10 +1520,11 @@ scn_status build(const int32_t* coords, int64_t n, const int64_t* grid, int32_t 
   scn_status rc;
   hipEvent_t copied = nullptr;
   // arguments first: no device call before they are known to be valid
-  if ((rc = L.check()) || (rc = readback_slots(&L.hb)) || (rc = copy_event(&copied)) ||
-      (rc = L.phase1()))
+  if ((rc = L.check()) || (rc = readback_slots(&L.hb)) || (rc = copy_event(&copied)))
     return rc;
-  SCN_HIP(hipStreamSynchronize(st));
+  L.ready = copied;  // recorded after the read-back, ahead of the pair emission
+  if ((rc = L.phase1())) return rc;
+  SCN_HIP(hipEventSynchronize(copied));
   if ((rc = L.sized()) || (rc = L.phase2(copied))) return rc;
   // The build's last kernels read prev's output bitmap and sites after the
   // call returns.  prev is freed on its own stream, so that stream waits
