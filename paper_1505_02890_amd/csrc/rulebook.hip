@@ -1404,29 +1404,32 @@ struct LayerBuild {
                                          (uint64_t*)rb->otile + ncnt, sc64, st)))
         return rc;
     }
-    // the mask sort (it needs only the masks) beside the neighbour lists: the
-    // second stream waits for the masks here, but the sort's launches are
-    // queued after the main stream's, so the neighbour lists start while the
-    // host still queues the sort
+    // the mask sort (it needs only the masks) beside the neighbour lists:
+    // the lists go to the second stream, which waits for the masks here, and
+    // are queued first, so they start while the host still queues the sort;
+    // the sort, the longer of the two, stays on the main stream, which then
+    // seldom waits at the join (a wait for work still running there left the
+    // device idle for about 40 us)
     const bool side_sort = dense && a_out > 0;
     uint32_t* sort_tmp = nullptr;
     if (side_sort &&
         ((rc = tmp.get(&sort_tmp, sort_bytes / 4)) || (rc = aux_stream(&aux)) ||
          (rc = fork(st, aux))))
       return rc;
+    const hipStream_t ls = side_sort ? aux->s : st;  // the output-major tables' stream
     if (dense) {
       // start of each output's neighbour list: exclusive sum of mask popcounts
       uint32_t* sc_nb = nullptr;
       if ((rc = tmp.get(&sc_nb, scan_blocks(a_out))) ||
           (rc = exclusive_scan<uint32_t>(PopcountLoad{masks}, a_out, rb->fnb_off,
-                                         rb->fnb_off + a_out, sc_nb, st)))
+                                         rb->fnb_off + a_out, sc_nb, ls)))
         return rc;
     }
     if (a_out > 0 && (rb->nbr || rb->fnb)) {
       with_kernels(f, lattice, [&](auto k) {
         // LDS stages the window table or the neighbour list
         k.emit_out(dim3(blocks_for(nt * TILE, 256)),
-                   rb->nbr ? (size_t)256 * K * 4 : (size_t)256 * EMIT_NB_STAGE * 4, st,
+                   rb->nbr ? (size_t)256 * K * 4 : (size_t)256 * EMIT_NB_STAGE * 4, ls,
                    (const uint32_t*)masks, (const int32_t*)rb->out_coords, a_out, s,
                    (const uint32_t*)inb, (const uint32_t*)ipref, gi, (const int32_t*)rb->perm,
                    rb->nbr, (const uint32_t*)rb->fnb_off, rb->fnb);
@@ -1434,7 +1437,7 @@ struct LayerBuild {
       SCN_LAUNCH_CHECK();
     }
     if (side_sort &&
-        ((rc = radix_sort_pairs(masks, rb->fmask, rb->fperm, a_out, K, sort_tmp, aux->s)) ||
+        ((rc = radix_sort_pairs(masks, rb->fmask, rb->fperm, a_out, K, sort_tmp, st)) ||
          (rc = join(st, aux))))
       return rc;
     if (cells) {
