@@ -93,6 +93,30 @@ __device__ inline const int32_t* stage_rows(const int32_t* __restrict__ nbr, int
 
 typedef float pool_v4f __attribute__((ext_vector_type(4)));
 
+// Work-groups go to the eight XCDs in turn (work-group b to XCD b mod 8), and
+// each XCD has its own L2.  Overlapping windows share input rows with the
+// windows one row and one plane of windows away, so each XCD takes runs of
+// `chunk` consecutive blocks: launched block b, the (b / 8)-th on XCD b mod
+// 8, does block xcd_block(b) of the list.  The grid is rounded up to whole
+// rounds of 8 * chunk blocks; the blocks past the list return at once.
+// MP3/2 forward on 4.4M rows: 0.363 -> 0.337 ms with runs of 16 blocks;
+// 2x2x2 forward 0.257 -> 0.251 ms with runs of 128.
+__device__ inline int64_t xcd_block(int64_t b, int chunk) {
+  const int64_t x = b & 7, s = b >> 3;
+  return ((s / chunk) * 8 + x) * chunk + s % chunk;
+}
+
+// runs of at most `want` blocks, and at most an eighth of the list (else
+// the first XCDs would take every block of a short list)
+inline int xcd_chunk(int64_t nblk, int want) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>(want, nblk / 8));
+}
+
+inline unsigned xcd_grid(int64_t nblk, int chunk) {
+  const int64_t r = 8 * (int64_t)chunk;
+  return (unsigned)std::max<int64_t>(1, (nblk + r - 1) / r * r);
+}
+
 // A streaming store, for rows nothing reads again soon (dx): 5-10% faster
 // than a plain store in the backward kernels.
 __device__ inline void store_stream(float4* p, float4 v) {
@@ -105,11 +129,14 @@ __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __re
                                                               const int32_t* __restrict__ nbr,
                                                               int64_t a_out, int nc4, int per,
                                                               float4* __restrict__ y,
-                                                              uint32_t* __restrict__ argmax) {
+                                                              uint32_t* __restrict__ argmax,
+                                                              int chunk) {
   extern __shared__ int32_t nsh[];  // per * K entries
   const int ol = threadIdx.x / nc4, c4 = threadIdx.x - ol * nc4;
   // overlapping windows share inputs with the windows of nearby blocks
-  const int64_t ob = (int64_t)blockIdx.x * per, o = ob + ol;
+  const int64_t blk = xcd_block(blockIdx.x, chunk);
+  if (blk * per >= a_out) return;  // the whole block: a launch rounded up to whole runs
+  const int64_t ob = blk * per, o = ob + ol;
   stage_rows<K>(nbr, ob, a_out, per, nsh);
   if (ol >= per || o >= a_out) return;
   const float4 g = g_in[c4];
@@ -295,11 +322,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) m
     const int32_t* __restrict__ nbr, const int32_t* __restrict__ low,
     const uint32_t* __restrict__ pmask, const uint32_t* __restrict__ argmax,
     const float4* __restrict__ dy, int64_t a_out, int nc4, float4* __restrict__ dx,
-    float4* __restrict__ part) {
+    float4* __restrict__ part, int chunk) {
   __shared__ int32_t home[PBV_ROWS * 8];
   __shared__ int4 lows[PBV_ROWS * 2];
   __shared__ float4 red[256];
-  const int64_t h0 = (int64_t)blockIdx.x * PBV_ROWS;
+  const int64_t blk = xcd_block(blockIdx.x, chunk);
+  const int64_t h0 = blk * PBV_ROWS;
+  if (h0 >= a_out) return;  // the whole block: a launch rounded up to whole runs
   const int nh = (int)min<int64_t>(PBV_ROWS, a_out - h0);
   if ((int)threadIdx.x < nh) {
     const int t = threadIdx.x;
@@ -371,7 +400,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) m
       g.z += t.z;
       g.w += t.w;
     }
-    part[(int64_t)blockIdx.x * nc4 + c4] = g;
+    part[blk * nc4 + c4] = g;
   }
 }
 
@@ -603,7 +632,9 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
   if (rb->a_out > 0) {
     if (pool_vec_ok(C, {x, g_in, y}, argmax)) {
       const int nc4 = C / 4, per = 256 / nc4;
-      const dim3 grid(nblocks(rb->a_out, per));
+      const int64_t nb = nblocks(rb->a_out, per);
+      const int chunk = xcd_chunk(nb, rb->K == 27 ? 16 : (rb->K == 8 ? 128 : 1));
+      const dim3 grid(xcd_grid(nb, chunk));
       const auto* x4 = reinterpret_cast<const float4*>(x);
       const auto* g4 = reinterpret_cast<const float4*>(g_in);
       auto* y4 = reinterpret_cast<float4*>(y);
@@ -611,7 +642,7 @@ scn_status scn_maxpool_fwd(const scn_rulebook* rb, const float* x, const float* 
       with_window(rb->K, [&](auto k) {
         constexpr int K = decltype(k)::value;
         hipLaunchKernelGGL(maxpool_fwd_vec_kernel<K>, grid, dim3(256), per * K * sizeof(int32_t),
-                           st, x4, g4, rb->nbr, rb->a_out, nc4, per, y4, am4);
+                           st, x4, g4, rb->nbr, rb->a_out, nc4, per, y4, am4, chunk);
       });
     } else {
       hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(nblocks(rb->a_out * C, 256)), dim3(256), 0, st,
@@ -672,9 +703,10 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
     }
     nblk = std::max<int64_t>(1, ceil_div(rb->a_out, PBV_ROWS));
     if (rb->a_out > 0) {
-      hipLaunchKernelGGL(maxpool_bwd_cells_kernel, dim3((unsigned)nblk), dim3(256), 0, st, rb->nbr,
-                         rb->lowwin, rb->pmask, am4, dy4, rb->a_out, nc4, dx4,
-                         reinterpret_cast<float4*>(part));
+      const int chunk = xcd_chunk(nblk, 16);
+      hipLaunchKernelGGL(maxpool_bwd_cells_kernel, dim3(xcd_grid(nblk, chunk)), dim3(256), 0, st,
+                         rb->nbr, rb->lowwin, rb->pmask, am4, dy4, rb->a_out, nc4, dx4,
+                         reinterpret_cast<float4*>(part), chunk);
       SCN_LAUNCH_CHECK();
     }
   } else if (overlap) {
