@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <cstdio>
 #include <string>
@@ -165,6 +166,28 @@ namespace scn {
 // sites of D coordinates, coords int32[n][D + 1], grid (B, m_1 .. m_D).
 scn_status keyed_build(const int32_t* coords, int64_t n, int D, const int64_t* grid, int f, int s,
                        hipStream_t st, scn_rulebook** out);
+
+// Work-groups go to the eight XCDs in turn (work-group b to XCD b mod 8), and
+// each XCD has its own L2.  Kernels whose nearby blocks read the same lines
+// give each XCD runs of `chunk` consecutive blocks: launched block b, the
+// (b / 8)-th on XCD b mod 8, does block xcd_block(b, chunk) of the list.
+// The grid is rounded up to whole rounds of 8 * chunk blocks; the blocks past
+// the list return at once.
+__device__ inline int64_t xcd_block(int64_t b, int chunk) {
+  const int64_t x = b & 7, s = b >> 3;
+  return ((s / chunk) * 8 + x) * chunk + s % chunk;
+}
+
+// runs of at most `want` blocks, and at most an eighth of the list (else
+// the first XCDs would take every block of a short list)
+inline int xcd_chunk(int64_t nblk, int want) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>(want, nblk / 8));
+}
+
+inline unsigned xcd_grid(int64_t nblk, int chunk) {
+  const int64_t r = 8 * (int64_t)chunk;
+  return (unsigned)std::max<int64_t>(1, (nblk + r - 1) / r * r);
+}
 
 // Orders work on stream st after the rulebook's build (a no-op on the build's
 // own stream, where the order already holds).
