@@ -275,6 +275,34 @@ def test_maxpool_parity(scn, case):
     pool_parity(scn, g, o, x, g_in, rng, f > s)
 
 
+# Block counts around the runs of consecutive blocks that each XCD takes
+# (runs of up to 16 blocks for 3x3x3 windows, 128 for 2x2x2, at most an
+# eighth of the blocks; the launch is rounded up to whole rounds of 8 runs):
+# fully active boxes give exact window counts.  (f, s, box edge, channels)
+RUN_CASES = [
+    (3, 2, 7, 64),    # 27 windows: 2 blocks, runs of 1
+    (3, 2, 37, 64),   # 5832 windows: 365 blocks, runs of 16, a ragged last round
+    (3, 2, 35, 4),    # 4913 windows, 256 a block: 20 blocks, runs of 2
+    (2, 2, 32, 64),   # 4096 windows: 256 blocks, runs of 32, whole rounds
+    (2, 2, 66, 64),   # 35937 windows: 2247 blocks, runs of 128, a ragged last round
+]
+
+
+@pytest.mark.parametrize("case", RUN_CASES, ids=[str(i) for i in range(len(RUN_CASES))])
+def test_maxpool_block_runs(scn, case):
+    f, s, m, C = case
+    rng = stream_rng(420 + RUN_CASES.index(case), 0)
+    g3 = np.stack(np.meshgrid(np.arange(m), np.arange(m), np.arange(m), indexing="ij"), -1)
+    coords = np.concatenate([np.zeros((m ** 3, 1), np.int64), g3.reshape(-1, 3)], 1)
+    coords = np.ascontiguousarray(coords[rng.permutation(len(coords))].astype(np.int32))
+    x = rng.standard_normal((len(coords), C)).astype(np.float32)
+    g_in = (np.abs(rng.standard_normal(C)) * 0.3).astype(np.float32)
+    grid = (1, m, m, m)
+    g, o = _rb_pair(scn, coords, grid, f, s)
+    assert g.a_out == ((m - f) // s + 1) ** 3
+    pool_parity(scn, g, o, x, g_in, rng, f > s)
+
+
 def test_maxpool_needs_stride_two(scn):
     coords = random_sites(stream_rng(1, 1), 1, (8, 8, 8), 50)
     g = scn.build_rulebook(dev(coords), (1, 8, 8, 8), 2, 1)
