@@ -153,6 +153,8 @@ __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __re
 }
 
 constexpr int PBV_ROWS = 64;  // outputs per block of the four-channel backward
+constexpr int CELL_ROWS = 32;  // windows per block of the MP3/2 cell backward (0.347 -> 0.341 ms
+                                // against 64; 16: 0.385)
 
 // Output-major backward: an input lies in at most one window, so each window
 // writes its inputs' dx rows (dy where the input won, else 0) and dx is
@@ -292,7 +294,7 @@ __global__ void __launch_bounds__(256) maxpool_bwd_homeless_vec_kernel(
 // drop from 3.4 rows to about 1.2.  The window's own dy and argmax also give
 // the ground-state sums (dy where the winner is inactive), so no separate
 // pass reads them: part[blk][c] sums the block's windows in a fixed order
-// (part may be null).  PBV_ROWS windows per block: their home entries and
+// (part may be null).  CELL_ROWS windows per block: their home entries and
 // lower windows are staged in LDS once.  Five waves per SIMD (96 VGPRs; the
 // compiler's own choice, 98, allowed four): 0.373 -> 0.366 ms on 4.4M inputs.
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) maxpool_bwd_cells_kernel(
@@ -300,13 +302,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) m
     const uint32_t* __restrict__ pmask, const uint32_t* __restrict__ argmax,
     const float4* __restrict__ dy, int64_t a_out, int nc4, float4* __restrict__ dx,
     float4* __restrict__ part, int chunk) {
-  __shared__ int32_t home[PBV_ROWS * 8];
-  __shared__ int4 lows[PBV_ROWS * 2];
+  __shared__ int32_t home[CELL_ROWS * 8];
+  __shared__ int4 lows[CELL_ROWS * 2];
   __shared__ float4 red[256];
   const int64_t blk = xcd_block(blockIdx.x, chunk);
-  const int64_t h0 = blk * PBV_ROWS;
+  const int64_t h0 = blk * CELL_ROWS;
   if (h0 >= a_out) return;  // the whole block: a launch rounded up to whole runs
-  const int nh = (int)min<int64_t>(PBV_ROWS, a_out - h0);
+  const int nh = (int)min<int64_t>(CELL_ROWS, a_out - h0);
   if ((int)threadIdx.x < nh) {
     const int t = threadIdx.x;
     const int32_t* row = nbr + (h0 + t) * 27;
@@ -575,9 +577,10 @@ inline bool pool_vec_ok(int C, std::initializer_list<const void*> rows, const vo
 
 
 // floats of the per-block ground-state partial sums, rounded to 16 bytes;
-// enough for every path (the four-channel path uses PBV_ROWS-output blocks)
+// enough for every path (the four-channel paths use blocks of PBV_ROWS or
+// CELL_ROWS outputs)
 inline size_t part_floats(const scn_rulebook* rb, int C) {
-  const int64_t rows = C % 4 == 0 ? PBV_ROWS : PB_ROWS;
+  const int64_t rows = C % 4 == 0 ? (PBV_ROWS < CELL_ROWS ? PBV_ROWS : CELL_ROWS) : PB_ROWS;
   return ((size_t)std::max<int64_t>(1, ceil_div(rb->a_out, rows)) * C + 3) & ~size_t(3);
 }
 
@@ -680,9 +683,9 @@ scn_status scn_maxpool_bwd(const scn_rulebook* rb, const uint8_t* argmax, const 
                          rb->homeless, rb->n_homeless, rb->inv, am4, dy4, nc4, per, dx4);
       SCN_LAUNCH_CHECK();
     }
-    nblk = std::max<int64_t>(1, ceil_div(rb->a_out, PBV_ROWS));
+    nblk = std::max<int64_t>(1, ceil_div(rb->a_out, CELL_ROWS));
     if (rb->a_out > 0) {
-      const int chunk = xcd_chunk(nblk, 16);
+      const int chunk = xcd_chunk(nblk, 32);  // runs of 1024 windows per XCD
       hipLaunchKernelGGL(maxpool_bwd_cells_kernel, dim3(xcd_grid(nblk, chunk)), dim3(256), 0, st,
                          rb->nbr, rb->lowwin, rb->pmask, am4, dy4, rb->a_out, nc4, dx4,
                          reinterpret_cast<float4*>(part), chunk);

@@ -276,8 +276,9 @@ def test_maxpool_parity(scn, case):
 
 
 # Block counts around the runs of consecutive blocks that each XCD takes
-# (runs of up to 16 blocks for 3x3x3 windows, 128 for 2x2x2, at most an
-# eighth of the blocks; the launch is rounded up to whole rounds of 8 runs):
+# (3x3x3 windows: runs of up to 16 forward blocks and 32 cell-backward
+# blocks; 2x2x2: 128 forward blocks; at most an eighth of the blocks; the
+# launch is rounded up to whole rounds of 8 runs):
 # fully active boxes give exact window counts.  (f, s, box edge, channels)
 RUN_CASES = [
     (3, 2, 7, 64),    # 27 windows: 2 blocks, runs of 1
