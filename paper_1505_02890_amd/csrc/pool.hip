@@ -148,8 +148,11 @@ __global__ void __launch_bounds__(256) maxpool_fwd_vec_kernel(const float4* __re
       if (v[i].w > best.w) { best.w = v[i].w; b3 = k; }
     }
   }
-  y[o * nc4 + c4] = best;
-  argmax[o * nc4 + c4] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+  // streaming stores: the outputs are not read again here, and the input
+  // rows that nearby windows re-read keep the cache (2x2x2 forward on 4.4M
+  // rows 0.251 -> 0.241 ms)
+  store_stream(y + o * nc4 + c4, best);
+  __builtin_nontemporal_store(b0 | (b1 << 8) | (b2 << 16) | (b3 << 24), argmax + o * nc4 + c4);
 }
 
 // outputs per block of the four-channel backward: 2x2x2 windows on 4.4M rows
