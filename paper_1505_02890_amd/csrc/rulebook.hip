@@ -478,7 +478,7 @@ __global__ void __launch_bounds__(256) emit_out_kernel(
   if (nb_lds && o0 < a_out) {
     // the stage is this wave's alone: LDS accesses of one wave complete in order
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    for (uint32_t i = lane; i < nb_len; i += 64) fnb[nb0 + i] = stage[i];
+    for (uint32_t i = lane; i < nb_len; i += 64) __builtin_nontemporal_store(stage[i], fnb + nb0 + i);
   }
   if (nbr) {
     __syncthreads();
@@ -766,9 +766,12 @@ __global__ void __launch_bounds__(256) emit_in_kernel(
         if (ok) {
           const int64_t p = p0 + lane_rank(bal);
           if (p < cap) {
-            in_rows[p] = row;
-            out_rows[p] = (int32_t)orank;
-            if (in_rank) in_rank[p] = (int32_t)r;
+            // streaming stores: the lists are read only by later calls, and
+            // the bitmap words this build looks up keep the cache (build
+            // 0.657 -> 0.599 ms on 1M sites, with the neighbour lists')
+            __builtin_nontemporal_store(row, in_rows + p);
+            __builtin_nontemporal_store((int32_t)orank, out_rows + p);
+            if (in_rank) __builtin_nontemporal_store((int32_t)r, in_rank + p);
           }
         }
         ++k;
