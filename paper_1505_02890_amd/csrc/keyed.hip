@@ -321,9 +321,10 @@ __global__ void __launch_bounds__(64) kd_emit_kernel(
   const uint64_t pos = itile[(int64_t)k * nit + blockIdx.x] +
                        __builtin_amdgcn_mbcnt_hi((uint32_t)(vb >> 32),
                                                  __builtin_amdgcn_mbcnt_lo((uint32_t)vb, 0u));
-  in_rows[pos] = perm ? perm[r] : (int32_t)r;
-  out_rows[pos] = h_find(h, mask, key);
-  if (in_rank) in_rank[pos] = (int32_t)r;
+  // streaming stores, as for the bitmap builder's lists
+  __builtin_nontemporal_store(perm ? perm[r] : (int32_t)r, in_rows + pos);
+  __builtin_nontemporal_store(h_find(h, mask, key), out_rows + pos);
+  if (in_rank) __builtin_nontemporal_store((int32_t)r, in_rank + pos);
 }
 
 // list boundaries off[k] = itile[k*nit] (off[K] = the pair count)
