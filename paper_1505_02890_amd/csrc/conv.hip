@@ -817,7 +817,9 @@ __global__ void __launch_bounds__(NT) dense_fwd_kernel(DenseArgs a) {
         if (a.relu) e[u2] = e[u2] > 0.f ? e[u2] : 0.f;
       }
       if (a.dvec_ok && col + 3 < a.Cout) {
-        *reinterpret_cast<float4*>(dp + col) = make_float4(e[0], e[1], e[2], e[3]);
+        // a streaming store: y is read only by later calls (kernel 2.669 ->
+        // 2.653 ms on the 1M-site layer)
+        __builtin_nontemporal_store(v4f{e[0], e[1], e[2], e[3]}, reinterpret_cast<v4f*>(dp + col));
       } else {
 #pragma unroll
         for (int u2 = 0; u2 < 4; ++u2)
